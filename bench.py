@@ -1,0 +1,249 @@
+#!/usr/bin/env python3
+"""Benchmark of the quantised convolution path on one MI355X.
+
+A step is one pass of the whole hot path over one batch: relayout+pack of the
+int8 NCHW activations into channel-packed 4-bit NHWC (qconv_pack), then the
+implicit-GEMM convolution with the fused requantise/ReLU/clamp/repack
+epilogue (qconv2d).  Filters are packed once beforehand (offline, untimed).
+
+Default workload: N=8, 56x56, C=K=64, 3x3, stride 1, pad 1, 4-bit activations
+in [0,15], 4-bit filters in [-8,7], per-channel multipliers in [2^14, 2^15),
+shift 20, ReLU, clamp [0,15] -- the stage-2 convolution of the paper's
+Table 1 (1,849,688,064 ops).  All inputs are seeded synthetic data, resident
+in HBM before timing starts.
+
+Prints ONE JSON line.  `value` = effective TOP/s of the step
+(2*N*P*Q*K*C*R*S per step / time per step).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "effective int4/int8 conv TOPS per layer + % of int8 MFMA peak (1 GPU)"
+INT8_PEAK_TOPS = 5000.0      # MI355X dense int8 MFMA, 5.0 POP/s
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, 8 TB/s
+
+
+def log(msg: str) -> None:
+    print(msg, file=sys.stderr, flush=True)
+
+
+def time_loop(fn, reps: int) -> float:
+    """Average microseconds per call of fn() over reps back-to-back calls, from
+    HIP events on the current stream (where the library launches)."""
+    import torch
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1000.0 / reps
+
+
+def layer_setup(cfg: int, lid: int, L, dev):
+    import torch
+    import qconv_inputs as qi
+    from paper_2202_06819_amd import qconv
+    t = qi.layer_tensors(cfg, lid, L)
+    x = torch.from_numpy(t["x"]).to(dev)
+    w = torch.from_numpy(t["w"]).to(dev)
+    xp = qconv.pack(x, L.bits, L.x_signed)
+    wp = qconv.pack(w, L.bits, L.w_signed)
+    e = L.epilogue
+    mult = torch.from_numpy(t["mult"]).to(dev) if e else None
+    return x, xp, wp, mult
+
+
+def per_layer_table(cfg: int, layers, dev, reps: int) -> list[dict]:
+    from paper_2202_06819_amd import qconv
+    import qconv_inputs as qi
+    rows = []
+    for lid, L in enumerate(layers):
+        x, xp, wp, mult = layer_setup(cfg, lid, L, dev)
+        e = L.epilogue
+        call = qconv.Conv2dCall(L.desc(), xp, wp, requant=e is not None, mult=mult,
+                                shift=e.shift if e else 20, relu=e.relu if e else False,
+                                clamp=(e.lo, e.hi) if e else (0, 15))
+        for _ in range(5):
+            call()
+        us = time_loop(call, reps)
+        tops = L.ops / (us * 1e-6) / 1e12
+        rows.append({"layer": L.name, "tile": qconv.tiles()[call.tile]["name"], "us": round(us, 3),
+                     "tops": round(tops, 2), "pct_int8_peak": round(100 * tops / INT8_PEAK_TOPS, 2),
+                     "gops": round(L.ops / 1e9, 4)})
+        log(f"  {L.name:28s} {us:9.2f} us {tops:8.1f} TOP/s {100 * tops / INT8_PEAK_TOPS:5.1f}%  tile {rows[-1]['tile']}")
+    return rows
+
+
+def chain_time(cfg: int, layers, dev, reps: int) -> dict:
+    """End-to-end time of a chained network (each output feeds the next layer)."""
+    import torch
+    import qconv_inputs as qi
+    from paper_2202_06819_amd import nets, qconv
+    t0 = qi.layer_tensors(cfg, 0, layers[0])
+    x = torch.from_numpy(t0["x"]).to(dev)
+    xp = qconv.pack(x, layers[0].bits, layers[0].x_signed)
+    specs = []
+    for lid, L in enumerate(layers):
+        t = qi.layer_tensors(cfg, lid, L)
+        wp = qconv.pack(torch.from_numpy(t["w"]).to(dev), L.bits, L.w_signed)
+        e = L.epilogue
+        specs.append(nets.LayerSpec(L.desc(), wp, torch.from_numpy(t["mult"]).to(dev), e.shift, e.relu,
+                                    (e.lo, e.hi), src=L.src))
+    chain = nets.Chain(specs, xp)
+    for _ in range(3):
+        chain.forward()
+    eager = time_loop(chain.forward, reps)
+    out = {"layers": len(layers), "gops": round(sum(L.ops for L in layers) / 1e9, 3), "eager_us": round(eager, 2)}
+    try:
+        chain.capture()
+        for _ in range(3):
+            chain.replay()
+        out["graph_us"] = round(time_loop(chain.replay, reps), 2)
+    except Exception as exc:  # graph capture is an extra, report why it is missing
+        out["graph_error"] = str(exc)[:200]
+    best = min(out.get("graph_us", eager), eager)
+    out["tops"] = round(sum(L.ops for L in layers) / (best * 1e-6) / 1e12, 2)
+    return out
+
+
+def cpu_baseline(L, seconds: float) -> dict:
+    """The oracle, as it stands, on the host cores: pack + conv + requant + repack
+    of the same layer, repeated for about `seconds`."""
+    import oracle
+    import qconv_inputs as qi
+    t = qi.layer_tensors(1, 0, L)
+    threads = oracle.max_threads()
+    e = L.epilogue
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.qconv_layer(t["x"], t["w"], bits=L.bits, x_signed=L.x_signed, w_signed=L.w_signed,
+                           stride=(L.stride, L.stride), pad=(L.pad, L.pad), mult=t["mult"], shift=e.shift,
+                           relu=e.relu, lo=e.lo, hi=e.hi, threads=threads)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    return {"value": round(L.ops * reps / el / 1e12, 6), "unit": "TOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"{reps} full passes of the benchmark layer ({L.name}: relayout+pack, direct conv, "
+                      f"requant, repack) in {el:.1f} s on {threads} OpenMP threads"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2000)
+    ap.add_argument("--warmup", type=int, default=100)
+    ap.add_argument("--layer-reps", type=int, default=200, help="repetitions per layer in the per-layer tables")
+    ap.add_argument("--tables", default="2", help="comma list of workloads with per-layer tables (2,3,4) or 'none'")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--tile", type=int, default=-1)
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the quantised convolution path has no multi-GPU mode "
+              f"(--gpus {args.gpus} requested).", file=sys.stderr)
+        return 2
+
+    import torch
+    import qconv_inputs as qi
+    from paper_2202_06819_amd import build as hip_build
+    from paper_2202_06819_amd import qconv
+
+    if not os.path.exists(hip_build.LIB):
+        hip_build.build()
+    dev = torch.device("cuda:0")
+    L = qi.config1()[0]
+    e = L.epilogue
+    x, xp, wp, mult = layer_setup(1, 0, L, dev)
+    pack = qconv.PackCall(x, L.bits, L.x_signed, out=xp)
+    conv = qconv.Conv2dCall(L.desc(), xp, wp, requant=True, mult=mult, shift=e.shift, relu=e.relu,
+                            clamp=(e.lo, e.hi), tile=args.tile)
+
+    def step():
+        pack()
+        conv()
+
+    log(f"workload {L.name}: {L.ops / 1e9:.4f} GOP per step, tile {qconv.tiles()[conv.tile]['name']}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms_total = e0.elapsed_time(e1)
+    ms_per_step = ms_total / args.steps
+    value = L.ops / (ms_per_step * 1e-3) / 1e12
+    log(f"step: {ms_per_step * 1000:.2f} us  ({value:.1f} TOP/s), wall {t_wall:.3f} s for {args.steps} steps")
+
+    # per-kernel averages, same launch configuration, HIP events on the launch stream
+    conv_us = time_loop(conv, args.steps)
+    pack_us = time_loop(pack, args.steps)
+    conv_tops = L.ops / (conv_us * 1e-6) / 1e12
+    pack_bytes = L.n * L.c * L.h * L.w + L.n * L.h * L.w * L.c // 2
+    pack_gbs = pack_bytes / (pack_us * 1e-6) / 1e9
+    log(f"conv kernel {conv_us:.2f} us = {conv_tops:.1f} TOP/s ({100 * conv_tops / INT8_PEAK_TOPS:.1f}% of int8 peak); "
+        f"pack kernel {pack_us:.2f} us = {pack_gbs:.0f} GB/s")
+
+    result = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "TOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int4",
+        "data": "synthetic",
+        "config": {"workload": "resnet50-stage2 3x3 conv, 4-bit, fused requant (relayout+pack then conv)",
+                   "n": L.n, "h": L.h, "w": L.w, "c": L.c, "k": L.k, "r": L.r, "s": L.s, "stride": L.stride,
+                   "pad": L.pad, "bits": L.bits, "ops_per_step": L.ops, "tile": qconv.tiles()[conv.tile]["name"]},
+        "roofline": {"bound": "mfma", "achieved": round(conv_tops, 3), "peak": INT8_PEAK_TOPS, "unit": "TOP/s",
+                     "frac": round(conv_tops / INT8_PEAK_TOPS, 5), "traffic": None,
+                     "kernel": "conv_igemm", "avg_us": round(conv_us, 3),
+                     "algorithmic_ops_per_launch": L.ops},
+        "kernels": {"conv_us": round(conv_us, 3), "pack_us": round(pack_us, 3),
+                    "pack_gbs": round(pack_gbs, 1), "pack_frac_hbm": round(pack_gbs / HBM_PEAK_GBS, 4),
+                    "pack_algorithmic_bytes": pack_bytes},
+    }
+
+    tables = [] if args.tables == "none" else [int(v) for v in args.tables.split(",") if v]
+    for cfg in tables:
+        layers = qi.CONFIGS[cfg]()
+        log(f"workload {cfg}: per-layer ({len(qi.distinct(layers)) if cfg in (2, 3) else len(layers)} layers)")
+        rows = per_layer_table(cfg, qi.distinct(layers) if cfg in (2, 3) else layers, dev, args.layer_reps)
+        entry = {"per_layer": rows}
+        if cfg in (2, 3):
+            entry["chain"] = chain_time(cfg, layers, dev, max(20, args.layer_reps // 4))
+            log(f"  chained network: {entry['chain']}")
+        result[f"workload{cfg}"] = entry
+
+    if not args.no_cpu:
+        log(f"cpu baseline: oracle for ~{args.cpu_seconds:.0f} s ...")
+        result["cpu_baseline"] = cpu_baseline(L, args.cpu_seconds)
+        log(f"  {result['cpu_baseline']}")
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,209 @@
+/*
+ * qconv.h -- C ABI of libqconv: reduced-precision (4-bit / 8-bit) integer 2-D
+ * convolution on AMD Instinct MI355X (gfx950), run as an implicit GEMM on the
+ * int8 matrix cores with int32 accumulation.
+ *
+ * The operation is the one the paper "Learning from Distinctive Candidates to
+ * Optimize Reduced-Precision Convolution Program on Tensor Cores" schedules:
+ *   - Sec. 2.1: a convolution of an N x H x W x C input with K filters of
+ *     R x S is the GEMM (N*P*Q, C*R*S) x (C*R*S, K) of the lowered (im2col)
+ *     input with the filters;
+ *   - Sec. 1 and Sec. 3.3: operands are 4-bit values packed eight per 32-bit
+ *     word along the channel axis, in a layout whose output is already the
+ *     next layer's input layout;
+ *   - Sec. 3.2.2: an epilogue on the wide accumulator followed by clipping
+ *     to the low bit-width and packing.
+ *
+ * Conventions shared by every entry point
+ *   - All tensor pointers are DEVICE pointers owned by the caller; the library
+ *     never allocates, frees or retains them beyond the call.
+ *   - Calls enqueue work on `stream` (a hipStream_t; NULL = the default
+ *     stream) and return without waiting.  Argument errors are reported
+ *     before anything is enqueued; faults during execution surface at the
+ *     caller's next synchronisation.
+ *   - Return value: QCONV_OK or a negative status; qconv_strerror() names it
+ *     and qconv_last_error() gives the detail of the calling thread's most
+ *     recent failure.
+ *   - The library holds no mutable global state besides a per-thread error
+ *     message and a per-device attribute cache; calls on distinct streams may
+ *     run concurrently from any threads.
+ *
+ * Packed layouts (b = bits)
+ *   activations  N x H x W x C, channels innermost
+ *   filters      K x R x S x C, channels innermost
+ *   b = 4: each pixel (or filter tap) is C/8 uint32 words; channel 8j+i is
+ *          bits [4i, 4i+3] of word j; signed values are two's-complement
+ *          nibbles.
+ *   b = 8: each pixel is C int8 values.
+ */
+#ifndef QCONV_H
+#define QCONV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define QCONV_OK 0
+#define QCONV_EINVAL (-1)      /* NULL, bad sizes, window larger than padded input, bad epilogue, misaligned */
+#define QCONV_EUNSUPPORTED (-2) /* valid request outside what the kernels implement (bit-width, channel multiple,
+                                   accumulator bound, tile not usable for the shape) */
+#define QCONV_EWORKSPACE (-3)  /* workspace smaller than qconv_layout_info.workspace_bytes */
+#define QCONV_EHIP (-4)        /* the HIP runtime rejected a launch or attribute call */
+
+/* Epilogue modes. */
+#define QCONV_OUT_RAW_I32 0    /* y = int32 accumulators, N x P x Q x K */
+#define QCONV_OUT_REQUANT 1    /* y = requantised values, packed like the input (b-bit, N x P x Q x K) */
+
+/*
+ * One convolution.  n, h, w, c: input batch, height, width, channels;
+ * k: output channels; r, s: filter height and width; stride and zero padding
+ * per axis; bits: 4 or 8; x_signed / w_signed: 0 or 1 (8-bit needs both 1).
+ * Output extent P = (h + 2*pad_h - r)/stride_h + 1, Q likewise (Sec. 2.1; no
+ * dilation, no groups; cross-correlation, no filter flip).
+ */
+typedef struct qconv_desc {
+    int32_t n, h, w, c;
+    int32_t k, r, s;
+    int32_t stride_h, stride_w;
+    int32_t pad_h, pad_w;
+    int32_t bits;
+    int32_t x_signed, w_signed;
+} qconv_desc;
+
+/* Sizes derived from a qconv_desc (bytes unless stated). */
+typedef struct qconv_layout_info {
+    int32_t p, q;              /* output height and width */
+    int64_t m;                 /* GEMM rows = n*p*q */
+    int64_t gemm_k;            /* GEMM depth = c*r*s */
+    int64_t macs;              /* n*p*q*k*c*r*s; effective ops = 2*macs */
+    int64_t x_bytes;           /* packed input */
+    int64_t w_bytes;           /* packed filters */
+    int64_t y_raw_bytes;       /* int32 output */
+    int64_t y_packed_bytes;    /* requantised packed output */
+    int64_t workspace_bytes;   /* device scratch qconv2d needs (0 today) */
+    int64_t max_abs_acc;       /* worst-case |accumulator| over all inputs of the declared ranges */
+} qconv_layout_info;
+
+/*
+ * Epilogue (Sec. 3.2.2: the wide accumulator is processed first, then clipped
+ * and packed):
+ *   t = acc * mult[k]                         (exact, 64-bit)
+ *   t = floor((t + 2^(shift-1)) / 2^shift)    (round half up)
+ *   t = max(t, 0) if relu
+ *   t = min(max(t, clamp_lo), clamp_hi)
+ * The clamp range must fit the output type: 4-bit [0,15] (unsigned output)
+ * or [-8,7] (signed), 8-bit [-128,127].  The output is signed iff
+ * clamp_lo < 0.  mult: DEVICE pointer to k int32 values.
+ * In QCONV_OUT_RAW_I32 mode only `mode` is read.
+ */
+typedef struct qconv_epilogue {
+    int32_t mode;
+    const int32_t *mult;
+    int32_t shift;             /* 1 .. 62 */
+    int32_t relu;              /* 0 or 1 */
+    int32_t clamp_lo, clamp_hi;
+} qconv_epilogue;
+
+/*
+ * A compile-time tile configuration of the convolution kernel: the paper's
+ * schedule knobs (Sec. 4.1) restated for 64-wide waves and MFMA.
+ *   waves_p, waves_k   waves of a workgroup along output pixels / channels
+ *                      (BLK-ROW-WARPS, BLK-COL-WARPS)
+ *   frag_p, frag_k     16x16 MFMA tiles per wave along pixels / channels
+ *                      (WARP-ROW-TILES, WARP-COL-TILES)
+ *   chunk_c            input channels staged per main-loop step (CHUNK)
+ *   tile_p, tile_k     workgroup tile = 16*waves*frag along each axis
+ *   bits               4 or 8: operand width the kernel is built for
+ */
+typedef struct qconv_tile_info {
+    int32_t id;
+    int32_t bits;
+    int32_t waves_p, waves_k;
+    int32_t frag_p, frag_k;
+    int32_t chunk_c;
+    int32_t tile_p, tile_k;
+    int32_t threads;
+    char name[64];
+} qconv_tile_info;
+
+/*
+ * qconv_layout -- host only, no device work.  Validates `d` exactly as
+ * qconv2d does and fills `out` with the output extent and buffer sizes.
+ * Returns QCONV_EINVAL / QCONV_EUNSUPPORTED for a descriptor qconv2d would
+ * reject.  `out` may be NULL (validation only).
+ */
+int qconv_layout(const qconv_desc *d, qconv_layout_info *out);
+
+/*
+ * qconv_pack -- relayout and pack (Sec. 1: eight 4-bit values grouped per
+ * 32-bit word along the channel axis; Sec. 3.3: channels innermost so the
+ * tensor is read with coalesced accesses).
+ *   src  DEVICE int8, n x c x h x w (activations) -- or k x c x r x s for
+ *        filters, which gives the k x r x s x c filter layout
+ *   dst  DEVICE, the packed layout above (bits 4: n*h*w*c/8 uint32;
+ *        bits 8: n*h*w*c int8)
+ * Each value is saturated into the b-bit range of `is_signed` before packing.
+ * Needs c % 8 == 0 for bits 4; bits 8 needs is_signed == 1.  src and dst must
+ * not overlap.  Errors: QCONV_EINVAL (NULL, negative sizes),
+ * QCONV_EUNSUPPORTED (bits, channel multiple), QCONV_EHIP (launch).
+ * Zero-sized tensors are a no-op returning QCONV_OK.
+ */
+int qconv_pack(const int8_t *src, void *dst, int32_t n, int32_t c, int32_t h, int32_t w,
+               int32_t bits, int32_t is_signed, void *stream);
+
+/*
+ * qconv2d -- the convolution (Sec. 2.1) as an implicit GEMM with the
+ * epilogue of Sec. 3.2.2 fused into it.
+ *   x          DEVICE, packed activations, 16-byte aligned
+ *   w          DEVICE, packed filters, 16-byte aligned
+ *   epi        host struct; NULL means QCONV_OUT_RAW_I32
+ *   y          DEVICE output, 16-byte aligned: y_raw_bytes (raw mode) or
+ *              y_packed_bytes (requant mode); must not overlap x or w
+ *   workspace  DEVICE scratch of workspace_bytes (may be NULL when 0)
+ *   tile_id    a tile from qconv_tile_get, or -1 for the built-in choice
+ * Requirements beyond qconv_layout's: bits 4 needs c % 8 == 0 and
+ * k % 8 == 0; bits 8 needs c % 4 == 0 and k % 4 == 0 and both operands
+ * signed; the worst-case accumulator (max_abs_acc) must stay below 2^31
+ * (Sec. 3.2.1).  Every tile gives byte-identical results.
+ * Errors: QCONV_EINVAL, QCONV_EUNSUPPORTED, QCONV_EWORKSPACE, QCONV_EHIP.
+ */
+int qconv2d(const qconv_desc *d, const void *x, const void *w, const qconv_epilogue *epi, void *y,
+            void *workspace, size_t workspace_bytes, int32_t tile_id, void *stream);
+
+/* Number of compiled tile configurations; ids are 0 .. count-1. */
+int qconv_tile_count(void);
+
+/* Describe tile `tile_id`.  QCONV_EINVAL for an unknown id or NULL `out`. */
+int qconv_tile_get(int32_t tile_id, qconv_tile_info *out);
+
+/*
+ * qconv_tile_check -- host only: QCONV_OK if tile `tile_id` can run `d`
+ * (bit-width matches, staging fits in LDS), else the status qconv2d would
+ * return for it.
+ */
+int qconv_tile_check(const qconv_desc *d, int32_t tile_id);
+
+/* The tile qconv2d uses for tile_id = -1 (a static per-shape heuristic). */
+int qconv_default_tile(const qconv_desc *d);
+
+/* Static text for a status code. */
+const char *qconv_strerror(int status);
+
+/* Detail of the calling thread's most recent failure ("" if none). */
+const char *qconv_last_error(void);
+
+/*
+ * Host-only self-check of the index arithmetic the kernels use (run-time
+ * constant division); touches no device.  Returns 0 when it holds.
+ */
+int qconv_selftest(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QCONV_H */

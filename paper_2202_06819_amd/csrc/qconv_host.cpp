@@ -1,0 +1,379 @@
+// Host side of libqconv: argument validation, sizes, tile choice and launch.
+// Validation and sizing touch no device and run on any machine; only the
+// launch paths call the HIP runtime.
+#include <hip/hip_runtime.h>
+#include <stdarg.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <mutex>
+#include <string>
+#include <unordered_map>
+
+#include "qconv.h"
+#include "qconv_internal.h"
+
+using namespace qconv;
+
+namespace {
+
+thread_local char g_err[256] = "";
+
+int fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+constexpr int64_t kLdsBytes = 160 * 1024;   // LDS per workgroup on gfx950
+constexpr int64_t kMaxBytes = (int64_t)1 << 31;
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+int64_t out_dim(int64_t in, int64_t win, int64_t stride, int64_t pad) {
+    int64_t span = in + 2 * pad - win;
+    if (span < 0) return -1;
+    return span / stride + 1;
+}
+
+int64_t max_abs(int bits, int is_signed) {
+    if (bits == 4) return is_signed ? 8 : 15;
+    return is_signed ? 128 : 255;
+}
+
+// Full descriptor validation shared by every entry point.
+int check_desc(const qconv_desc *d, qconv_layout_info *info) {
+    if (!d) return fail(QCONV_EINVAL, "descriptor is NULL");
+    if (d->n <= 0 || d->h <= 0 || d->w <= 0 || d->c <= 0 || d->k <= 0 || d->r <= 0 || d->s <= 0)
+        return fail(QCONV_EINVAL, "sizes must be positive (n=%d h=%d w=%d c=%d k=%d r=%d s=%d)", d->n, d->h, d->w,
+                    d->c, d->k, d->r, d->s);
+    if (d->stride_h < 1 || d->stride_w < 1) return fail(QCONV_EINVAL, "strides must be >= 1");
+    if (d->pad_h < 0 || d->pad_w < 0) return fail(QCONV_EINVAL, "padding must be >= 0");
+    if ((d->x_signed != 0 && d->x_signed != 1) || (d->w_signed != 0 && d->w_signed != 1))
+        return fail(QCONV_EINVAL, "x_signed and w_signed must be 0 or 1");
+    int64_t p = out_dim(d->h, d->r, d->stride_h, d->pad_h);
+    int64_t q = out_dim(d->w, d->s, d->stride_w, d->pad_w);
+    if (p < 1 || q < 1) return fail(QCONV_EINVAL, "filter window larger than the padded input");
+    if (d->bits != 4 && d->bits != 8) return fail(QCONV_EUNSUPPORTED, "bits must be 4 or 8 (got %d)", d->bits);
+    if (d->bits == 4 && (d->c % 8 || d->k % 8))
+        return fail(QCONV_EUNSUPPORTED, "4-bit needs c %% 8 == 0 and k %% 8 == 0 (c=%d k=%d)", d->c, d->k);
+    if (d->bits == 8 && (d->c % 4 || d->k % 4))
+        return fail(QCONV_EUNSUPPORTED, "8-bit needs c %% 4 == 0 and k %% 4 == 0 (c=%d k=%d)", d->c, d->k);
+    if (d->bits == 8 && (!d->x_signed || !d->w_signed))
+        return fail(QCONV_EUNSUPPORTED, "8-bit operands must be signed (the int8 MFMA is signed)");
+    const int64_t bits = d->bits;
+    const int64_t m = (int64_t)d->n * p * q;
+    const int64_t x_bytes = (int64_t)d->n * d->h * d->w * d->c * bits / 8;
+    const int64_t w_bytes = (int64_t)d->k * d->r * d->s * d->c * bits / 8;
+    const int64_t y_raw = m * d->k * 4;
+    const int64_t y_packed = m * d->k * bits / 8;
+    if (x_bytes >= kMaxBytes || w_bytes >= kMaxBytes || y_raw >= kMaxBytes)
+        return fail(QCONV_EUNSUPPORTED, "tensors must stay below 2 GiB (32-bit indexing)");
+    const int64_t depth = (int64_t)d->c * d->r * d->s;
+    const int64_t worst = depth * max_abs(d->bits, d->x_signed) * max_abs(d->bits, d->w_signed);
+    if (worst >= ((int64_t)1 << 31))
+        return fail(QCONV_EUNSUPPORTED, "worst-case accumulator %lld does not fit int32", (long long)worst);
+    if (d->bits == 4) {
+        int64_t scaled = worst << (4 * (d->x_signed + d->w_signed));
+        if (scaled >= ((int64_t)1 << 31))
+            return fail(QCONV_EUNSUPPORTED, "worst-case accumulator %lld times the widening factor does not fit int32",
+                        (long long)worst);
+    }
+    if (info) {
+        info->p = (int32_t)p;
+        info->q = (int32_t)q;
+        info->m = m;
+        info->gemm_k = depth;
+        info->macs = m * d->k * depth;
+        info->x_bytes = x_bytes;
+        info->w_bytes = w_bytes;
+        info->y_raw_bytes = y_raw;
+        info->y_packed_bytes = y_packed;
+        info->workspace_bytes = 0;
+        info->max_abs_acc = worst;
+    }
+    return QCONV_OK;
+}
+
+int check_epilogue(const qconv_desc *d, const qconv_epilogue *e) {
+    if (!e || e->mode == QCONV_OUT_RAW_I32) return QCONV_OK;
+    if (e->mode != QCONV_OUT_REQUANT) return fail(QCONV_EINVAL, "unknown epilogue mode %d", e->mode);
+    if (!e->mult) return fail(QCONV_EINVAL, "requant epilogue needs a multiplier array");
+    if (e->shift < 1 || e->shift > 62) return fail(QCONV_EINVAL, "shift must be in [1, 62] (got %d)", e->shift);
+    if (e->relu != 0 && e->relu != 1) return fail(QCONV_EINVAL, "relu must be 0 or 1");
+    if (e->clamp_lo > e->clamp_hi) return fail(QCONV_EINVAL, "clamp_lo > clamp_hi");
+    const int lo = e->clamp_lo, hi = e->clamp_hi;
+    bool ok;
+    if (d->bits == 4)
+        ok = (lo >= 0 && hi <= 15) || (lo >= -8 && hi <= 7);
+    else
+        ok = lo >= -128 && hi <= 127;
+    if (!ok) return fail(QCONV_EINVAL, "clamp range [%d, %d] does not fit the %d-bit output", lo, hi, d->bits);
+    return QCONV_OK;
+}
+
+// Padded ("virtual") row of output pixel m's first tap.
+int64_t vrow_of(const qconv_desc *d, int64_t p, int64_t q, int64_t m) {
+    int64_t img = m / (p * q), rem = m % (p * q);
+    return img * (d->h + 2 * d->pad_h) + (rem / q) * d->stride_h;
+}
+
+// Largest number of padded rows any workgroup of tile_p pixels touches.
+int64_t band_rows(const qconv_desc *d, int64_t p, int64_t q, int64_t tile_p) {
+    static std::mutex mu;
+    static std::unordered_map<std::string, int64_t> cache;
+    char key[160];
+    snprintf(key, sizeof(key), "%d,%d,%d,%d,%d,%d,%d,%lld", d->n, d->h, d->w, d->r, d->s, d->stride_h, d->pad_h,
+             (long long)tile_p);
+    {
+        std::lock_guard<std::mutex> g(mu);
+        auto it = cache.find(key);
+        if (it != cache.end()) return it->second;
+    }
+    const int64_t m = (int64_t)d->n * p * q;
+    int64_t best = 0;
+    for (int64_t m0 = 0; m0 < m; m0 += tile_p) {
+        int64_t last = std::min(m0 + tile_p, m) - 1;
+        best = std::max(best, vrow_of(d, p, q, last) + d->r - vrow_of(d, p, q, m0));
+    }
+    std::lock_guard<std::mutex> g(mu);
+    if (cache.size() > 4096) cache.clear();
+    cache[key] = best;
+    return best;
+}
+
+int64_t pad_plane(int64_t bytes) { return (bytes + 255) / 256 * 256 + 128; }
+
+struct Plan {
+    int64_t rows, pstride_b, pstride_w, lds;
+};
+
+int plan_tile(const qconv_desc *d, const qconv_layout_info &li, const qconv_tile_info &t, Plan *out) {
+    if (t.bits != d->bits)
+        return fail(QCONV_EUNSUPPORTED, "tile %s is built for %d-bit operands", t.name, t.bits);
+    const int64_t gran = 2 * d->bits;
+    const int64_t ncols = d->w + 2 * d->pad_w;
+    Plan pl;
+    pl.rows = band_rows(d, li.p, li.q, t.tile_p);
+    pl.pstride_b = pad_plane(pl.rows * ncols * gran);
+    pl.pstride_w = pad_plane((int64_t)d->r * d->s * t.tile_k * gran);
+    pl.lds = (int64_t)(t.chunk_c / 16) * (pl.pstride_b + pl.pstride_w);
+    if (pl.lds > kLdsBytes)
+        return fail(QCONV_EUNSUPPORTED, "tile %s needs %lld bytes of LDS for this shape (limit %lld)", t.name,
+                    (long long)pl.lds, (long long)kLdsBytes);
+    if (out) *out = pl;
+    return QCONV_OK;
+}
+
+int pick_default(const qconv_desc *d, const qconv_layout_info &li) {
+    // Static heuristic: prefer the largest tile that still gives every CU
+    // work and fits in LDS; the sweep harness measures the alternatives.
+    const TileEntry *tab = tile_table();
+    const int nt = tile_table_size();
+    int best = -1;
+    double best_score = -1.0;
+    for (int i = 0; i < nt; ++i) {
+        const qconv_tile_info &t = tab[i].info;
+        if (t.bits != d->bits) continue;
+        Plan pl;
+        if (plan_tile(d, li, t, &pl) != QCONV_OK) continue;
+        const double wgs = (double)((li.m + t.tile_p - 1) / t.tile_p) * ((d->k + t.tile_k - 1) / t.tile_k);
+        const double util = (double)li.m * d->k /
+                            ((double)((li.m + t.tile_p - 1) / t.tile_p) * t.tile_p *
+                             (double)((d->k + t.tile_k - 1) / t.tile_k) * t.tile_k);
+        const double fill = std::min(1.0, wgs / 512.0);
+        const double reuse = (double)t.tile_p * t.tile_k / (t.tile_p + t.tile_k);
+        const double score = util * fill * reuse * (t.chunk_c <= d->c ? 1.0 : 0.5);
+        if (score > best_score) {
+            best_score = score;
+            best = i;
+        }
+    }
+    return best;
+}
+
+struct DevAttrCache {
+    std::mutex mu;
+    std::unordered_map<long long, bool> done;   // (device, tile) -> max LDS attribute set
+};
+DevAttrCache g_attr;
+
+}  // namespace
+
+extern "C" {
+
+const char *qconv_strerror(int status) {
+    switch (status) {
+        case QCONV_OK: return "ok";
+        case QCONV_EINVAL: return "invalid argument";
+        case QCONV_EUNSUPPORTED: return "unsupported configuration";
+        case QCONV_EWORKSPACE: return "workspace too small";
+        case QCONV_EHIP: return "HIP runtime error";
+        default: return "unknown status";
+    }
+}
+
+const char *qconv_last_error(void) { return g_err; }
+
+int qconv_layout(const qconv_desc *d, qconv_layout_info *out) {
+    g_err[0] = 0;
+    return check_desc(d, out);
+}
+
+int qconv_tile_count(void) { return tile_table_size(); }
+
+int qconv_tile_get(int32_t tile_id, qconv_tile_info *out) {
+    if (!out || tile_id < 0 || tile_id >= tile_table_size()) return fail(QCONV_EINVAL, "unknown tile %d", tile_id);
+    *out = tile_table()[tile_id].info;
+    return QCONV_OK;
+}
+
+int qconv_tile_check(const qconv_desc *d, int32_t tile_id) {
+    g_err[0] = 0;
+    qconv_layout_info li;
+    int rc = check_desc(d, &li);
+    if (rc) return rc;
+    if (tile_id < 0 || tile_id >= tile_table_size()) return fail(QCONV_EINVAL, "unknown tile %d", tile_id);
+    return plan_tile(d, li, tile_table()[tile_id].info, nullptr);
+}
+
+int qconv_default_tile(const qconv_desc *d) {
+    g_err[0] = 0;
+    qconv_layout_info li;
+    int rc = check_desc(d, &li);
+    if (rc) return rc;
+    int t = pick_default(d, li);
+    if (t < 0) return fail(QCONV_EUNSUPPORTED, "no compiled tile fits this shape");
+    return t;
+}
+
+int qconv_pack(const int8_t *src, void *dst, int32_t n, int32_t c, int32_t h, int32_t w, int32_t bits,
+               int32_t is_signed, void *stream) {
+    g_err[0] = 0;
+    if (n < 0 || c < 0 || h < 0 || w < 0) return fail(QCONV_EINVAL, "sizes must be non-negative");
+    if (is_signed != 0 && is_signed != 1) return fail(QCONV_EINVAL, "is_signed must be 0 or 1");
+    if (bits != 4 && bits != 8) return fail(QCONV_EUNSUPPORTED, "bits must be 4 or 8 (got %d)", bits);
+    if (bits == 4 && c % 8) return fail(QCONV_EUNSUPPORTED, "4-bit packing needs c %% 8 == 0 (c=%d)", c);
+    if (bits == 8 && !is_signed) return fail(QCONV_EUNSUPPORTED, "8-bit values are signed");
+    const int64_t count = (int64_t)n * c * h * w;
+    if (count == 0) return QCONV_OK;
+    if (count >= kMaxBytes) return fail(QCONV_EUNSUPPORTED, "tensor must stay below 2^31 values");
+    if (!src || !dst) return fail(QCONV_EINVAL, "src and dst must be non-NULL");
+    if (((uintptr_t)dst & 3u) != 0) return fail(QCONV_EINVAL, "dst must be 4-byte aligned");
+    const uintptr_t s0 = (uintptr_t)src, s1 = s0 + count;
+    const uintptr_t d0 = (uintptr_t)dst, d1 = d0 + count * bits / 8;
+    if (s0 < d1 && d0 < s1) return fail(QCONV_EINVAL, "src and dst overlap");
+    hipError_t e = launch_pack(src, dst, n, c, h, w, bits, is_signed, (hipStream_t)stream);
+    if (e != hipSuccess) return fail(QCONV_EHIP, "pack launch: %s", hipGetErrorString(e));
+    return QCONV_OK;
+}
+
+int qconv2d(const qconv_desc *d, const void *x, const void *w, const qconv_epilogue *epi, void *y, void *workspace,
+            size_t workspace_bytes, int32_t tile_id, void *stream) {
+    g_err[0] = 0;
+    (void)workspace;
+    qconv_layout_info li;
+    int rc = check_desc(d, &li);
+    if (rc) return rc;
+    rc = check_epilogue(d, epi);
+    if (rc) return rc;
+    if (!x || !w || !y) return fail(QCONV_EINVAL, "x, w and y must be non-NULL");
+    if (!aligned16(x) || !aligned16(w) || !aligned16(y)) return fail(QCONV_EINVAL, "x, w and y must be 16-byte aligned");
+    const bool requant = epi && epi->mode == QCONV_OUT_REQUANT;
+    const int64_t ybytes = requant ? li.y_packed_bytes : li.y_raw_bytes;
+    const uintptr_t y0 = (uintptr_t)y, y1 = y0 + ybytes;
+    if (((uintptr_t)x < y1 && y0 < (uintptr_t)x + li.x_bytes) || ((uintptr_t)w < y1 && y0 < (uintptr_t)w + li.w_bytes))
+        return fail(QCONV_EINVAL, "y overlaps x or w");
+    if ((int64_t)workspace_bytes < li.workspace_bytes)
+        return fail(QCONV_EWORKSPACE, "workspace of %zu bytes, need %lld", workspace_bytes,
+                    (long long)li.workspace_bytes);
+    if (tile_id == -1) {
+        tile_id = pick_default(d, li);
+        if (tile_id < 0) return fail(QCONV_EUNSUPPORTED, "no compiled tile fits this shape");
+    }
+    if (tile_id < 0 || tile_id >= tile_table_size()) return fail(QCONV_EINVAL, "unknown tile %d", tile_id);
+    const TileEntry &te = tile_table()[tile_id];
+    Plan pl;
+    rc = plan_tile(d, li, te.info, &pl);
+    if (rc) return rc;
+
+    ConvArgs a;
+    memset(&a, 0, sizeof(a));
+    a.xptr = static_cast<const uint8_t *>(x);
+    a.wptr = static_cast<const uint8_t *>(w);
+    a.yptr = static_cast<uint8_t *>(y);
+    a.mult = requant ? epi->mult : nullptr;
+    a.n = d->n; a.h = d->h; a.w = d->w; a.c = d->c; a.k = d->k; a.r = d->r; a.s = d->s;
+    a.sh = d->stride_h; a.sw = d->stride_w; a.ph = d->pad_h; a.pw = d->pad_w;
+    a.p = li.p; a.q = li.q;
+    a.m = (int32_t)li.m;
+    a.vh = d->h + 2 * d->pad_h;
+    a.ncols = d->w + 2 * d->pad_w;
+    a.xpix = d->c * d->bits / 8;
+    a.nchunks = (d->c + te.info.chunk_c - 1) / te.info.chunk_c;
+    a.vec16 = (d->c * d->bits) % 128 == 0;
+    a.band_rows = (int32_t)pl.rows;
+    a.pstride_b = (int32_t)pl.pstride_b;
+    a.pstride_w = (int32_t)pl.pstride_w;
+    a.ktiles = (d->k + te.info.tile_k - 1) / te.info.tile_k;
+    a.mtiles = (int32_t)((li.m + te.info.tile_p - 1) / te.info.tile_p);
+    a.div_pq = make_fastdiv((uint32_t)(li.p * li.q));
+    a.div_q = make_fastdiv((uint32_t)li.q);
+    a.div_vh = make_fastdiv((uint32_t)a.vh);
+    a.div_ncols = make_fastdiv((uint32_t)a.ncols);
+    a.div_rs = make_fastdiv((uint32_t)(d->r * d->s));
+    // widening: unsigned nibble -> low half of a byte; signed nibble -> high half (value * 16)
+    a.xmask = d->x_signed ? 0xF0F0F0F0u : 0x0F0F0F0Fu;
+    a.xsl = d->x_signed ? 4 : 0;
+    a.xsr = d->x_signed ? 0 : 4;
+    a.wmask = d->w_signed ? 0xF0F0F0F0u : 0x0F0F0F0Fu;
+    a.wsl = d->w_signed ? 4 : 0;
+    a.wsr = d->w_signed ? 0 : 4;
+    a.acc_shift = d->bits == 4 ? 4 * (d->x_signed + d->w_signed) : 0;
+    a.mode = requant ? QCONV_OUT_REQUANT : QCONV_OUT_RAW_I32;
+    if (requant) {
+        a.shift = epi->shift;
+        a.lo = epi->relu ? std::max(epi->clamp_lo, 0) : epi->clamp_lo;
+        a.hi = epi->clamp_hi;
+        if (a.lo > a.hi) a.lo = a.hi;   // relu with an all-negative clamp range: every value is clamp_hi
+    }
+    const long long blocks = (long long)a.mtiles * a.ktiles;
+    if (blocks <= 0 || blocks >= (1ll << 31)) return fail(QCONV_EUNSUPPORTED, "grid size out of range");
+
+    if (pl.lds > 64 * 1024) {
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess) return fail(QCONV_EHIP, "hipGetDevice failed");
+        const long long key = (long long)dev * 4096 + tile_id;
+        std::lock_guard<std::mutex> g(g_attr.mu);
+        if (!g_attr.done[key]) {
+            hipError_t e = hipFuncSetAttribute(te.kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
+            if (e != hipSuccess) return fail(QCONV_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
+            g_attr.done[key] = true;
+        }
+    }
+    hipError_t e = te.launch(a, dim3((unsigned)blocks), (size_t)pl.lds, (hipStream_t)stream);
+    if (e != hipSuccess) return fail(QCONV_EHIP, "conv launch (%s): %s", te.info.name, hipGetErrorString(e));
+    return QCONV_OK;
+}
+
+// Host-only consistency checks of the helpers the kernels rely on; returns 0
+// when they hold.  Exposed so CPU tests can run them without a device.
+int qconv_selftest(void) {
+    const uint32_t ds[] = {1, 2, 3, 5, 7, 9, 14, 28, 49, 56, 58, 196, 784, 3136, 12544, 65535, 100003};
+    for (uint32_t dv : ds) {
+        FastDiv f = make_fastdiv(dv);
+        for (uint32_t n = 0; n < 200000; n += 7)
+            if (fdiv(n, f) != n / dv) return 1;
+        const uint32_t big[] = {0x7fffffffu, 0x7ffffffeu, 0x40000000u, 123456789u};
+        for (uint32_t n : big)
+            if (fdiv(n, f) != n / dv) return 2;
+    }
+    return 0;
+}
+
+}  // extern "C"

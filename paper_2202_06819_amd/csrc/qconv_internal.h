@@ -1,0 +1,84 @@
+// Internal declarations shared by the host library and the HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "qconv.h"
+
+namespace qconv {
+
+// Unsigned division by a run-time constant d >= 1, exact for numerators below
+// 2^31: q = (umulhi(n, mul) + n) >> shr with shr = ceil(log2 d) and
+// mul = floor(2^32 * (2^shr - d) / d) + 1 (Granlund & Montgomery, 1994).
+struct FastDiv {
+    uint32_t d;
+    uint32_t mul;
+    uint32_t shr;
+};
+
+inline FastDiv make_fastdiv(uint32_t d) {
+    FastDiv f{d, 0u, 0u};
+    uint32_t l = 0;
+    while ((1ull << l) < d) ++l;
+    f.shr = l;
+    f.mul = (uint32_t)(((1ull << 32) * ((1ull << l) - d)) / d + 1);
+    return f;
+}
+
+__host__ __device__ inline uint32_t fdiv(uint32_t n, FastDiv f) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    uint32_t t = __umulhi(n, f.mul);
+#else
+    uint32_t t = (uint32_t)(((uint64_t)n * f.mul) >> 32);
+#endif
+    return (t + n) >> f.shr;
+}
+
+// Everything a convolution launch needs, passed by value as the kernel argument.
+struct ConvArgs {
+    const uint8_t *xptr;    // packed activations, N x H x W x C
+    const uint8_t *wptr;    // packed filters, K x R x S x C
+    uint8_t *yptr;          // output (raw int32 or packed)
+    const int32_t *mult;    // per-channel multipliers (requant mode)
+    int32_t n, h, w, c, k, r, s;
+    int32_t sh, sw, ph, pw, p, q;
+    int32_t m;              // n * p * q
+    int32_t vh;             // h + 2*ph: rows of one zero-padded image
+    int32_t ncols;          // w + 2*pw: columns of one zero-padded row
+    int32_t xpix;           // bytes per input pixel (and per filter tap)
+    int32_t nchunks;        // channel chunks of the main loop
+    int32_t vec16;          // 1: every 16-byte vector of a pixel is whole (C*bits % 128 == 0)
+    int32_t band_rows;      // padded rows the band buffer holds
+    int32_t pstride_b;      // bytes per granule plane of the band buffer
+    int32_t pstride_w;      // bytes per granule plane of the filter buffer
+    int32_t ktiles;         // workgroup tiles along output channels
+    int32_t mtiles;         // workgroup tiles along output pixels
+    FastDiv div_pq, div_q, div_vh, div_ncols, div_rs;
+    // operand widening of 4-bit nibbles to int8 lanes (see widen4)
+    uint32_t xmask, wmask;
+    int32_t xsl, xsr, wsl, wsr;
+    int32_t acc_shift;      // accumulators carry a factor 2^acc_shift from widening
+    // epilogue
+    int32_t mode;           // QCONV_OUT_RAW_I32 / QCONV_OUT_REQUANT
+    int32_t shift;
+    int32_t lo, hi;         // clamp bounds, ReLU already folded into lo
+};
+
+using ConvLauncher = hipError_t (*)(const ConvArgs &, dim3 grid, size_t lds_bytes, hipStream_t);
+
+struct TileEntry {
+    qconv_tile_info info;
+    ConvLauncher launch;
+    const void *kernel;     // for hipFuncSetAttribute
+};
+
+// Defined in qconv_conv.hip.
+const TileEntry *tile_table();
+int tile_table_size();
+
+// Defined in qconv_pack.hip.
+hipError_t launch_pack(const int8_t *src, void *dst, int32_t n, int32_t c, int32_t h, int32_t w, int32_t bits,
+                       int32_t is_signed, hipStream_t stream);
+
+}  // namespace qconv

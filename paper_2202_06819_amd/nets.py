@@ -1,0 +1,69 @@
+"""Chained layers: each layer's packed output buffer is the next layer's input.
+
+The requantising epilogue writes the output in the same channel-packed NHWC
+layout the next convolution reads (Sec. 3.3), so a network is a list of
+qconv2d calls on one stream with no relayout between them.  A forward pass can
+be replayed as a HIP graph to take host launch cost out of the loop.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import torch
+
+from . import qconv
+
+
+@dataclass
+class LayerSpec:
+    """One convolution of a chain.  ``src`` is the index of the layer whose output
+    it reads (-1: the network input)."""
+    desc: dict
+    w_packed: torch.Tensor
+    mult: torch.Tensor
+    shift: int
+    relu: bool
+    clamp: tuple
+    src: int = -1
+    tile: int = -1
+
+
+class Chain:
+    def __init__(self, layers: list[LayerSpec], x_packed: torch.Tensor, stream=None):
+        self.layers = layers
+        self.x = x_packed
+        self.calls = []
+        outs = []
+        for L in layers:
+            inp = self.x if L.src < 0 else outs[L.src]
+            call = qconv.Conv2dCall(L.desc, inp, L.w_packed, requant=True, mult=L.mult, shift=L.shift,
+                                    relu=L.relu, clamp=L.clamp, tile=L.tile, stream=stream)
+            outs.append(call.out)
+            self.calls.append(call)
+        self.outputs = outs
+        self.graph = None
+
+    def forward(self) -> list[torch.Tensor]:
+        for c in self.calls:
+            c()
+        return self.outputs
+
+    def capture(self) -> None:
+        """Record one forward pass as a graph (the library allocates and memsets nothing)."""
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            # calls marshal the stream at construction: rebuild them for the capture stream
+            calls = [qconv.Conv2dCall(c.desc, c.x, c.w, requant=True, mult=c.mult, shift=c.epi.shift,
+                                      relu=bool(c.epi.relu), clamp=(c.epi.clamp_lo, c.epi.clamp_hi), out=c.out,
+                                      tile=c.tile, stream=s) for c in self.calls]
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=s):
+                for c in calls:
+                    c()
+        torch.cuda.current_stream().wait_stream(s)
+        self.graph = g
+
+    def replay(self) -> list[torch.Tensor]:
+        self.graph.replay()
+        return self.outputs

@@ -1,0 +1,261 @@
+"""ctypes binding of libqconv: argument marshalling only.
+
+Every step of the path runs in the HIP kernels behind the C ABI
+(``include/qconv.h``).  PyTorch supplies device memory and the stream; this
+module turns tensors into pointers and sizes and status codes into
+exceptions.  There is no fallback: if ``libqconv.so`` is missing or a call
+fails, an exception is raised.
+
+Tensor conventions
+  4-bit packed tensors are torch.int32 with the last axis = channels / 8 (each
+  element holds eight nibbles, channel 8j+i in bits [4i, 4i+3]); 8-bit tensors
+  are torch.int8 with the last axis = channels; raw accumulators are
+  torch.int32 N x P x Q x K.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+import torch
+
+from .build import LIB as LIB_PATH
+
+OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP = 0, -1, -2, -3, -4
+OUT_RAW_I32, OUT_REQUANT = 0, 1
+
+_i32, _i64, _vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p
+
+
+class QConvDesc(ctypes.Structure):
+    _fields_ = [(f, _i32) for f in ("n", "h", "w", "c", "k", "r", "s", "stride_h", "stride_w", "pad_h", "pad_w",
+                                    "bits", "x_signed", "w_signed")]
+
+
+class QConvLayoutInfo(ctypes.Structure):
+    _fields_ = [("p", _i32), ("q", _i32)] + [(f, _i64) for f in (
+        "m", "gemm_k", "macs", "x_bytes", "w_bytes", "y_raw_bytes", "y_packed_bytes", "workspace_bytes",
+        "max_abs_acc")]
+
+
+class QConvEpilogue(ctypes.Structure):
+    _fields_ = [("mode", _i32), ("mult", _vp), ("shift", _i32), ("relu", _i32), ("clamp_lo", _i32),
+                ("clamp_hi", _i32)]
+
+
+class QConvTileInfo(ctypes.Structure):
+    _fields_ = [(f, _i32) for f in ("id", "bits", "waves_p", "waves_k", "frag_p", "frag_k", "chunk_c", "tile_p",
+                                    "tile_k", "threads")] + [("name", ctypes.c_char * 64)]
+
+
+class QConvError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(what)
+
+
+_lock = threading.Lock()
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libqconv.so; raises if it has not been built."""
+    global _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        if not os.path.exists(LIB_PATH):
+            raise QConvError(EHIP, f"{LIB_PATH} is not built; run `python -m paper_2202_06819_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P = ctypes.POINTER
+        L.qconv_layout.argtypes = [P(QConvDesc), P(QConvLayoutInfo)]
+        L.qconv_pack.argtypes = [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _vp]
+        L.qconv2d.argtypes = [P(QConvDesc), _vp, _vp, P(QConvEpilogue), _vp, _vp, ctypes.c_size_t, _i32, _vp]
+        L.qconv_tile_count.argtypes = []
+        L.qconv_tile_get.argtypes = [_i32, P(QConvTileInfo)]
+        L.qconv_tile_check.argtypes = [P(QConvDesc), _i32]
+        L.qconv_default_tile.argtypes = [P(QConvDesc)]
+        L.qconv_strerror.argtypes = [ctypes.c_int]
+        L.qconv_strerror.restype = ctypes.c_char_p
+        L.qconv_last_error.argtypes = []
+        L.qconv_last_error.restype = ctypes.c_char_p
+        L.qconv_selftest.argtypes = []
+        for f in ("qconv_layout", "qconv_pack", "qconv2d", "qconv_tile_count", "qconv_tile_get", "qconv_tile_check",
+                  "qconv_default_tile", "qconv_selftest"):
+            getattr(L, f).restype = ctypes.c_int
+        _lib = L
+        return L
+
+
+def _check(rc: int, what: str) -> int:
+    if rc < 0:
+        L = lib()
+        raise QConvError(rc, f"{what}: {L.qconv_strerror(rc).decode()} ({L.qconv_last_error().decode()})")
+    return rc
+
+
+def make_desc(d: dict | QConvDesc) -> QConvDesc:
+    if isinstance(d, QConvDesc):
+        return d
+    return QConvDesc(**{f: int(d[f]) for f, _ in QConvDesc._fields_})
+
+
+def layout(d: dict) -> dict:
+    """Output extent and buffer sizes of a descriptor (host only)."""
+    info = QConvLayoutInfo()
+    _check(lib().qconv_layout(ctypes.byref(make_desc(d)), ctypes.byref(info)), "qconv_layout")
+    return {f: getattr(info, f) for f, _ in QConvLayoutInfo._fields_}
+
+
+def tiles() -> list[dict]:
+    out = []
+    for i in range(lib().qconv_tile_count()):
+        t = QConvTileInfo()
+        _check(lib().qconv_tile_get(i, ctypes.byref(t)), "qconv_tile_get")
+        row = {f: getattr(t, f) for f, _ in QConvTileInfo._fields_ if f != "name"}
+        row["name"] = t.name.decode()
+        out.append(row)
+    return out
+
+
+def tile_status(d: dict, tile_id: int) -> int:
+    """QCONV_OK if the tile can run the shape, else the status qconv2d would return."""
+    return lib().qconv_tile_check(ctypes.byref(make_desc(d)), int(tile_id))
+
+
+def default_tile(d: dict) -> int:
+    return _check(lib().qconv_default_tile(ctypes.byref(make_desc(d))), "qconv_default_tile")
+
+
+def selftest() -> int:
+    return lib().qconv_selftest()
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _dev_ptr(t: torch.Tensor, name: str, min_bytes: int = 0) -> int:
+    if not t.is_cuda:
+        raise QConvError(EINVAL, f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise QConvError(EINVAL, f"{name} must be contiguous")
+    if t.numel() * t.element_size() < min_bytes:
+        raise QConvError(EINVAL, f"{name} holds {t.numel() * t.element_size()} bytes, needs {min_bytes}")
+    return t.data_ptr()
+
+
+def packed_shape(n: int, h: int, w: int, c: int, bits: int) -> tuple:
+    return (n, h, w, c // 8) if bits == 4 else (n, h, w, c)
+
+
+def packed_dtype(bits: int) -> torch.dtype:
+    return torch.int32 if bits == 4 else torch.int8
+
+
+def pack(src: torch.Tensor, bits: int, is_signed: bool, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """int8 N x C x H x W (or K x C x R x S) -> saturated channel-packed N x H x W x ... ."""
+    if src.dtype != torch.int8 or src.dim() != 4:
+        raise QConvError(EINVAL, "pack expects a 4-d int8 tensor")
+    n, c, h, w = src.shape
+    if out is None:
+        out = torch.empty(packed_shape(n, h, w, c, bits), dtype=packed_dtype(bits), device=src.device)
+    rc = lib().qconv_pack(_dev_ptr(src, "src"), _dev_ptr(out, "dst", n * c * h * w * bits // 8), n, c, h, w,
+                          int(bits), int(bool(is_signed)),
+                          _vp(_stream(stream)))
+    _check(rc, "qconv_pack")
+    return out
+
+
+def conv2d(d: dict, x: torch.Tensor, w: torch.Tensor, *, requant: bool = False, mult: torch.Tensor | None = None,
+           shift: int = 20, relu: bool = True, clamp: tuple = (0, 15), out: torch.Tensor | None = None,
+           tile: int = -1, workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """The convolution with its fused epilogue; returns the output tensor.
+
+    Raw mode: int32 N x P x Q x K accumulators.  Requant mode: the packed
+    b-bit output (the next layer's input layout).
+    """
+    desc = make_desc(d)
+    info = layout(d)
+    bits = desc.bits
+    if out is None:
+        if requant:
+            out = torch.empty(packed_shape(desc.n, info["p"], info["q"], desc.k, bits), dtype=packed_dtype(bits),
+                              device=x.device)
+        else:
+            out = torch.empty((desc.n, info["p"], info["q"], desc.k), dtype=torch.int32, device=x.device)
+    epi = QConvEpilogue()
+    if requant:
+        if mult is None or mult.dtype != torch.int32 or mult.numel() != desc.k:
+            raise QConvError(EINVAL, "requant needs an int32 multiplier per output channel")
+        epi.mode, epi.mult = OUT_REQUANT, _dev_ptr(mult, "mult", 4 * desc.k)
+        epi.shift, epi.relu, epi.clamp_lo, epi.clamp_hi = int(shift), int(bool(relu)), int(clamp[0]), int(clamp[1])
+    else:
+        epi.mode = OUT_RAW_I32
+    ws_ptr, ws_bytes = (None, 0) if workspace is None else (_dev_ptr(workspace, "workspace"),
+                                                           workspace.numel() * workspace.element_size())
+    y_bytes = info["y_packed_bytes"] if requant else info["y_raw_bytes"]
+    rc = lib().qconv2d(ctypes.byref(desc), _dev_ptr(x, "x", info["x_bytes"]), _dev_ptr(w, "w", info["w_bytes"]),
+                       ctypes.byref(epi), _dev_ptr(out, "y", y_bytes), ws_ptr, ws_bytes, int(tile),
+                       _vp(_stream(stream)))
+    _check(rc, "qconv2d")
+    return out
+
+
+class PackCall:
+    """A qconv_pack call with its arguments marshalled once; ``()`` enqueues it."""
+
+    def __init__(self, src: torch.Tensor, bits: int, is_signed: bool, out: torch.Tensor | None = None, stream=None):
+        if src.dtype != torch.int8 or src.dim() != 4:
+            raise QConvError(EINVAL, "pack expects a 4-d int8 tensor")
+        n, c, h, w = src.shape
+        if out is None:
+            out = torch.empty(packed_shape(n, h, w, c, bits), dtype=packed_dtype(bits), device=src.device)
+        self.src, self.out = src, out
+        self._args = (_dev_ptr(src, "src"), _dev_ptr(out, "dst", n * c * h * w * bits // 8), n, c, h, w, int(bits),
+                      int(bool(is_signed)), _vp(_stream(stream)))
+        self._fn = lib().qconv_pack
+
+    def __call__(self) -> torch.Tensor:
+        _check(self._fn(*self._args), "qconv_pack")
+        return self.out
+
+
+class Conv2dCall:
+    """A qconv2d call with its arguments marshalled once; ``()`` enqueues it.
+
+    Tensors are held so their memory outlives the call object.
+    """
+
+    def __init__(self, d: dict, x: torch.Tensor, w: torch.Tensor, *, requant: bool = False,
+                 mult: torch.Tensor | None = None, shift: int = 20, relu: bool = True, clamp: tuple = (0, 15),
+                 out: torch.Tensor | None = None, tile: int = -1, stream=None):
+        self.desc = make_desc(d)
+        info = layout(d)
+        bits = self.desc.bits
+        if out is None:
+            shape = (packed_shape(self.desc.n, info["p"], info["q"], self.desc.k, bits) if requant
+                     else (self.desc.n, info["p"], info["q"], self.desc.k))
+            out = torch.empty(shape, dtype=packed_dtype(bits) if requant else torch.int32, device=x.device)
+        self.epi = QConvEpilogue()
+        if requant:
+            if mult is None or mult.dtype != torch.int32 or mult.numel() != self.desc.k:
+                raise QConvError(EINVAL, "requant needs an int32 multiplier per output channel")
+            self.epi.mode, self.epi.mult = OUT_REQUANT, _dev_ptr(mult, "mult", 4 * self.desc.k)
+            self.epi.shift, self.epi.relu = int(shift), int(bool(relu))
+            self.epi.clamp_lo, self.epi.clamp_hi = int(clamp[0]), int(clamp[1])
+        else:
+            self.epi.mode = OUT_RAW_I32
+        y_bytes = info["y_packed_bytes"] if requant else info["y_raw_bytes"]
+        self.x, self.w, self.mult, self.out, self.info = x, w, mult, out, info
+        self.tile = default_tile(d) if tile == -1 else int(tile)
+        self._args = (ctypes.byref(self.desc), _dev_ptr(x, "x", info["x_bytes"]), _dev_ptr(w, "w", info["w_bytes"]),
+                      ctypes.byref(self.epi), _dev_ptr(out, "y", y_bytes), None, 0, self.tile, _vp(_stream(stream)))
+        self._fn = lib().qconv2d
+
+    def __call__(self) -> torch.Tensor:
+        _check(self._fn(*self._args), "qconv2d")
+        return self.out

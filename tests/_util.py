@@ -1,0 +1,83 @@
+"""Helpers shared by the GPU parity tests: run a layer through the HIP path and
+through the oracle on the same seeded inputs."""
+from __future__ import annotations
+
+import os
+import sys
+
+import numpy as np
+
+import oracle
+import qconv_inputs as qi
+
+
+def announce(msg: str) -> None:
+    """Name the case before a GPU step (a crash then still says which one)."""
+    print(f"\n[gpu-case] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+def oracle_threads() -> int:
+    return max(1, min(16, oracle.max_threads()))
+
+
+def stress_shift(L: qi.Layer, x_range, w_range, mult_mid: float = 2 ** 14.5, target: float = None) -> int:
+    """A shift that spreads requantised outputs over the clamp range for
+    zero-mean filters: the accumulator's spread is about sqrt(C*R*S) times the
+    spread of one product.  (Input statistics only; nothing of the method.)"""
+    xv = np.arange(x_range[0], x_range[1] + 1, dtype=np.float64)
+    wv = np.arange(w_range[0], w_range[1] + 1, dtype=np.float64)
+    spread = np.sqrt(L.c * L.r * L.s * (xv ** 2).mean() * (wv ** 2).mean())
+    target = target or (8.0 if L.bits == 4 else 64.0)
+    return int(max(1, min(62, round(np.log2(spread * mult_mid / target)))))
+
+
+def ref_layer(L: qi.Layer, t: dict, *, requant: bool, shift=None, relu=None, lo=None, hi=None, threads=None,
+              packed_x=None) -> dict:
+    e = L.epilogue or qi.Epilogue()
+    kw = {}
+    if requant:
+        kw = dict(mult=t["mult"], shift=e.shift if shift is None else shift, relu=e.relu if relu is None else relu,
+                  lo=e.lo if lo is None else lo, hi=e.hi if hi is None else hi)
+    return oracle.qconv_layer(t["x"], t["w"], bits=L.bits, x_signed=L.x_signed, w_signed=L.w_signed,
+                              stride=(L.stride, L.stride), pad=(L.pad, L.pad), threads=threads or oracle_threads(),
+                              packed_x=packed_x, **kw)
+
+
+def as_u32(a) -> np.ndarray:
+    return np.ascontiguousarray(a).view(np.uint32) if a.dtype in (np.int32, np.uint32) else np.ascontiguousarray(a)
+
+
+def gpu_layer(L: qi.Layer, t: dict, *, requant: bool, tile: int = -1, shift=None, relu=None, lo=None, hi=None,
+              x_packed_dev=None):
+    """Pack x and w on the GPU, run the conv; returns host numpy arrays."""
+    import torch
+    from paper_2202_06819_amd import qconv
+
+    dev = torch.device("cuda:0")
+    e = L.epilogue or qi.Epilogue()
+    if x_packed_dev is None:
+        x_dev = torch.from_numpy(t["x"]).to(dev)
+        xp = qconv.pack(x_dev, L.bits, L.x_signed)
+    else:
+        xp = x_packed_dev
+    w_dev = torch.from_numpy(t["w"]).to(dev)
+    wp = qconv.pack(w_dev, L.bits, L.w_signed)
+    kw = {}
+    if requant:
+        kw = dict(requant=True, mult=torch.from_numpy(t["mult"]).to(dev), shift=e.shift if shift is None else shift,
+                  relu=e.relu if relu is None else relu,
+                  clamp=(e.lo if lo is None else lo, e.hi if hi is None else hi))
+    y = qconv.conv2d(L.desc(), xp, wp, tile=tile, **kw)
+    torch.cuda.synchronize()
+    return {"x_packed": xp.cpu().numpy(), "w_packed": wp.cpu().numpy(), "y": y.cpu().numpy(), "y_dev": y}
+
+
+def assert_same(got: np.ndarray, ref: np.ndarray, what: str) -> None:
+    g = as_u32(got)
+    r = as_u32(ref)
+    assert g.shape == r.shape, f"{what}: shape {g.shape} vs {r.shape}"
+    if not np.array_equal(g, r):
+        bad = np.argwhere(g != r)
+        raise AssertionError(f"{what}: {len(bad)} of {g.size} elements differ; first at {bad[0].tolist()}: "
+                             f"got {g[tuple(bad[0])]} want {r[tuple(bad[0])]}")

@@ -1,0 +1,186 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+include/qconv.h declares, sizes match their closed forms, and every argument
+error is reported before anything is launched.
+
+Pointer arguments here are plain integers that are never dereferenced: every
+call below is rejected by host-side validation first.
+"""
+import ctypes
+import json
+import os
+import re
+
+import pytest
+
+import qconv_inputs as qi
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "qconv.h")
+
+
+@pytest.fixture(scope="module")
+def q():
+    from paper_2202_06819_amd import build, qconv
+    if not os.path.exists(build.LIB):
+        build.build()
+    return qconv
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(qconv\w*)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_boundary():
+    names = _declared_functions()
+    for must in ("qconv_layout", "qconv_pack", "qconv2d", "qconv_strerror"):
+        assert must in names
+
+
+def test_library_exports_every_declared_symbol(q):
+    lib = ctypes.CDLL(q.LIB_PATH)
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_selftest(q):
+    assert q.selftest() == 0
+
+
+def D(**kw):
+    base = dict(n=8, h=56, w=56, c=64, k=64, r=3, s=3, stride_h=1, stride_w=1, pad_h=1, pad_w=1, bits=4,
+                x_signed=0, w_signed=1)
+    base.update(kw)
+    return base
+
+
+def test_layout_matches_table1(q):
+    gold = json.load(open(os.path.join(ROOT, "tests", "golden", "table1_ops.json")))
+    for st in gold["stages"]:
+        info = q.layout(D(h=st["hw"], w=st["hw"], c=st["channels"], k=st["channels"]))
+        assert (info["p"], info["q"]) == (st["hw"], st["hw"])
+        assert 2 * info["macs"] == gold["ops_per_conv"]
+
+
+def test_layout_sizes(q):
+    info = q.layout(D())
+    assert info["m"] == 8 * 56 * 56
+    assert info["gemm_k"] == 576
+    assert info["x_bytes"] == 8 * 56 * 56 * 32
+    assert info["w_bytes"] == 64 * 9 * 32
+    assert info["y_raw_bytes"] == 8 * 56 * 56 * 64 * 4
+    assert info["y_packed_bytes"] == 8 * 56 * 56 * 32
+    assert info["max_abs_acc"] == 576 * 15 * 8
+    i8 = q.layout(D(bits=8, x_signed=1))
+    assert i8["x_bytes"] == 8 * 56 * 56 * 64 and i8["y_packed_bytes"] == 8 * 56 * 56 * 64
+    s2 = q.layout(D(stride_h=2, stride_w=2, r=1, s=1, pad_h=0, pad_w=0))
+    assert (s2["p"], s2["q"]) == (28, 28)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n=0), -1), (dict(h=-1), -1), (dict(c=0), -1), (dict(k=0), -1), (dict(r=0), -1),
+    (dict(stride_h=0), -1), (dict(pad_w=-1), -1), (dict(h=2, pad_h=0), -1), (dict(x_signed=2), -1),
+    (dict(bits=2), -2), (dict(bits=16), -2), (dict(c=12), -2), (dict(k=20), -2),
+    (dict(bits=8, x_signed=0), -2), (dict(bits=8, x_signed=1, c=6), -2),
+    (dict(c=4096, r=7, s=7, x_signed=1), -2),           # accumulator bound with the widening factor
+    (dict(bits=8, x_signed=1, c=131072, r=1, s=1), -2), # 128*128*2^17 = 2^31
+])
+def test_descriptor_errors(q, kw, status):
+    with pytest.raises(q.QConvError) as e:
+        q.layout(D(**kw))
+    assert e.value.status == status
+
+
+def test_null_descriptor(q):
+    assert q.lib().qconv_layout(None, None) == -1
+    assert q.lib().qconv2d(None, 16, 16, None, 64, None, 0, -1, None) == -1
+
+
+def _conv_call(q, d, x=1 << 32, w=1 << 33, y=1 << 34, epi=None, ws=None, wsb=0, tile=-1):
+    desc = q.make_desc(d)
+    return q.lib().qconv2d(ctypes.byref(desc), x, w, ctypes.byref(epi) if epi else None, y, ws, wsb, tile, None)
+
+
+def _epi(q, **kw):
+    e = q.QConvEpilogue()
+    e.mode, e.mult, e.shift, e.relu, e.clamp_lo, e.clamp_hi = 1, 1 << 35, 20, 1, 0, 15
+    for k, v in kw.items():
+        setattr(e, k, v)
+    return e
+
+
+@pytest.mark.parametrize("kw", [dict(shift=0), dict(shift=63), dict(relu=2), dict(clamp_lo=5, clamp_hi=4),
+                                dict(clamp_lo=0, clamp_hi=16), dict(clamp_lo=-8, clamp_hi=8),
+                                dict(clamp_lo=-9, clamp_hi=0), dict(mode=7), dict(mult=None)])
+def test_epilogue_errors(q, kw):
+    assert _conv_call(q, D(), epi=_epi(q, **kw)) == -1
+
+
+def test_int8_clamp_range(q):
+    assert _conv_call(q, D(bits=8, x_signed=1), epi=_epi(q, clamp_lo=-129, clamp_hi=0)) == -1
+    assert _conv_call(q, D(bits=8, x_signed=1), epi=_epi(q, clamp_lo=0, clamp_hi=128)) == -1
+
+
+def test_pointer_errors(q):
+    assert _conv_call(q, D(), x=0) == -1
+    assert _conv_call(q, D(), y=0) == -1
+    assert _conv_call(q, D(), x=(1 << 32) + 4) == -1    # misaligned
+    assert _conv_call(q, D(), w=(1 << 33) + 8) == -1
+    assert _conv_call(q, D(), y=(1 << 34) + 4) == -1
+    assert _conv_call(q, D(), y=(1 << 32) + 4096) == -1  # y overlaps x
+    assert _conv_call(q, D(), y=(1 << 33) - 64) == -1    # y overlaps w
+    assert _conv_call(q, D(), tile=10 ** 6) == -1
+
+
+def test_tile_errors(q):
+    # a 4-bit tile cannot run an 8-bit layer
+    t4 = [t["id"] for t in q.tiles() if t["bits"] == 4][0]
+    assert q.tile_status(D(bits=8, x_signed=1), t4) == -2
+    assert _conv_call(q, D(bits=8, x_signed=1), tile=t4) == -2
+    # a very wide image does not fit the LDS band of any tile
+    assert all(q.tile_status(D(w=20000, h=3), t["id"]) == -2 for t in q.tiles())
+    with pytest.raises(q.QConvError):
+        q.default_tile(D(w=20000, h=3))
+    assert q.tile_status(D(), -5) == -1
+
+
+def test_pack_errors(q):
+    L = q.lib()
+    assert L.qconv_pack(4096, 8192, 1, 12, 4, 4, 4, 0, None) == -2     # c % 8
+    assert L.qconv_pack(4096, 8192, 1, 16, 4, 4, 5, 0, None) == -2     # bits
+    assert L.qconv_pack(4096, 8192, 1, 16, 4, 4, 8, 0, None) == -2     # unsigned 8-bit
+    assert L.qconv_pack(4096, 8192, -1, 16, 4, 4, 4, 0, None) == -1
+    assert L.qconv_pack(0, 8192, 1, 16, 4, 4, 4, 0, None) == -1
+    assert L.qconv_pack(4096, 4096 + 64, 1, 16, 4, 4, 4, 0, None) == -1   # overlap
+    assert L.qconv_pack(4096, 8194, 1, 16, 4, 4, 4, 0, None) == -1        # dst misaligned
+    assert L.qconv_pack(0, 0, 0, 16, 4, 4, 4, 0, None) == 0               # empty: no-op
+
+
+def test_strerror_and_last_error(q):
+    L = q.lib()
+    assert L.qconv_strerror(0) == b"ok"
+    assert L.qconv_strerror(-2) == b"unsupported configuration"
+    with pytest.raises(q.QConvError):
+        q.layout(D(c=12))
+    assert b"c % 8" in L.qconv_last_error()
+
+
+def test_tile_table_is_consistent(q):
+    tiles = q.tiles()
+    assert len(tiles) == q.lib().qconv_tile_count() >= 8
+    for i, t in enumerate(tiles):
+        assert t["id"] == i
+        assert t["tile_p"] == 16 * t["waves_p"] * t["frag_p"]
+        assert t["tile_k"] == 16 * t["waves_k"] * t["frag_k"]
+        assert t["threads"] == 64 * t["waves_p"] * t["waves_k"]
+        assert t["chunk_c"] % 64 == 0
+        if t["bits"] == 4:
+            assert t["frag_k"] % 2 == 0
+
+
+def test_every_workload_layer_has_a_tile(q):
+    for cfg, make in qi.CONFIGS.items():
+        for L in make():
+            tid = q.default_tile(L.desc())
+            assert q.tile_status(L.desc(), tid) == 0

@@ -1,0 +1,221 @@
+"""GPU parity: the HIP path (qconv_pack + qconv2d through the C ABI) against the
+CPU oracle, bit for bit, on seeded inputs.
+
+Integer sums have exactly one value, so every tile, every shape and every
+run must reproduce the oracle's bytes: packed inputs, raw int32 accumulators
+and requantised packed outputs.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import qconv_inputs as qi
+from _util import announce, assert_same, gpu_layer, ref_layer, stress_shift
+
+pytestmark = pytest.mark.gpu
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _qconv():
+    from paper_2202_06819_amd import qconv
+    return qconv
+
+
+def _valid_tiles(L):
+    q = _qconv()
+    return [t["id"] for t in q.tiles() if q.tile_status(L.desc(), t["id"]) == 0]
+
+
+# ----------------------------------------------------------------- qconv_pack
+
+PACK_CASES = [
+    # n, c, h, w, bits, signed, value range
+    (8, 64, 56, 56, 4, False, (-128, 127)),
+    (1, 8, 5, 7, 4, False, (-20, 30)),
+    (2, 72, 3, 11, 4, True, (-128, 127)),
+    (3, 136, 9, 9, 4, True, (-9, 9)),
+    (64, 64, 3, 3, 4, True, (-8, 7)),           # filters K x C x R x S
+    (2, 64, 56, 56, 8, True, (-128, 127)),
+    (1, 20, 7, 5, 8, True, (-128, 127)),
+    (2, 100, 1, 1, 8, True, (-128, 127)),
+]
+
+
+@pytest.mark.parametrize("case", PACK_CASES, ids=lambda c: "n%d_c%d_%dx%d_b%d_%s" % (c[:5] + ("s" if c[5] else "u",)))
+def test_pack_matches_oracle(case):
+    torch, q = _torch(), _qconv()
+    n, c, h, w, bits, signed, (lo, hi) = case
+    src = np.random.default_rng([7, n, c, h, w, bits]).integers(lo, hi + 1, size=(n, c, h, w)).astype(np.int8)
+    ref = oracle.relayout_pack(src, bits, signed)
+    announce(f"qconv_pack {case}")
+    got = q.pack(torch.from_numpy(src).cuda(), bits, signed)
+    torch.cuda.synchronize()
+    assert_same(got.cpu().numpy(), ref, "pack")
+
+
+def test_pack_zero_size_is_noop():
+    torch, q = _torch(), _qconv()
+    src = torch.empty((0, 64, 4, 4), dtype=torch.int8, device="cuda")
+    out = q.pack(src, 4, False)
+    torch.cuda.synchronize()
+    assert out.numel() == 0
+
+
+# ----------------------------------------------------------------- configs 0 and 1 at full size
+
+def test_config0_raw_every_tile():
+    L = qi.config0()[0]
+    t = qi.layer_tensors(0, 0, L)
+    ref = ref_layer(L, t, requant=False)
+    for tid in _valid_tiles(L):
+        announce(f"config0 raw tile {tid}")
+        got = gpu_layer(L, t, requant=False, tile=tid)
+        assert_same(got["x_packed"], ref["x_packed"], "x packed")
+        assert_same(got["w_packed"], ref["w_packed"], "w packed")
+        assert_same(got["y"], ref["acc"], f"raw acc tile {tid}")
+
+
+def test_config1_requant_every_tile():
+    L = qi.config1()[0]
+    t = qi.layer_tensors(1, 0, L)
+    ref = ref_layer(L, t, requant=True)
+    for tid in _valid_tiles(L):
+        announce(f"config1 requant tile {tid}")
+        got = gpu_layer(L, t, requant=True, tile=tid)
+        assert_same(got["y"], ref["y_packed"], f"requant tile {tid}")
+
+
+def test_config1_raw_default_tile():
+    L = qi.config1()[0]
+    t = qi.layer_tensors(1, 0, L)
+    ref = ref_layer(L, t, requant=False)
+    announce("config1 raw default tile")
+    assert_same(gpu_layer(L, t, requant=False)["y"], ref["acc"], "raw acc")
+
+
+# ----------------------------------------------------------------- ragged random shapes
+
+def _random_layer(seed: int) -> qi.Layer:
+    g = np.random.default_rng([99, seed])
+    bits = 8 if seed % 4 == 3 else 4
+    r = int(g.choice([1, 2, 3, 5, 7]))
+    s = int(g.choice([1, 3, r]))
+    stride = int(g.choice([1, 1, 2, 3]))
+    pad = int(g.integers(0, (max(r, s) // 2) + 2))
+    h = int(g.integers(max(1, r - 2 * pad), 24))
+    w = int(g.integers(max(1, s - 2 * pad), 24))
+    if bits == 4:
+        c = 8 * int(g.integers(1, 26))
+        k = 8 * int(g.integers(1, 18))
+        xs = bool(seed % 5 == 1)
+        ws = not (seed % 7 == 2)
+        xr = qi.S4 if xs else qi.U4
+        wr = qi.S4 if ws else qi.U4
+        epi = qi.Epilogue(relu=bool(seed % 2), lo=-8 if seed % 3 == 0 else 0, hi=7 if seed % 3 == 0 else 15)
+        return qi.Layer(f"rand{seed}", int(g.integers(1, 4)), h, w, c, k, r, s, stride, pad, 4, xs, ws, xr, wr, epi)
+    c = 4 * int(g.integers(1, 50))
+    k = 4 * int(g.integers(1, 34))
+    epi = qi.Epilogue(relu=bool(seed % 2), lo=-128, hi=127)
+    return qi.Layer(f"rand{seed}", int(g.integers(1, 4)), h, w, c, k, r, s, stride, pad, 8, True, True, qi.S8, qi.S8,
+                    epi)
+
+
+@pytest.mark.parametrize("seed", range(32))
+def test_random_shape(seed):
+    L = _random_layer(seed)
+    if L.h + 2 * L.pad < L.r or L.w + 2 * L.pad < L.s:
+        pytest.skip("window larger than padded input")
+    t = qi.layer_tensors(100, seed, L)
+    sh = stress_shift(L, L.x_range, L.w_range)
+    ref_raw = ref_layer(L, t, requant=False)
+    ref_req = ref_layer(L, t, requant=True, shift=sh)
+    tiles = _valid_tiles(L)
+    assert tiles, "no tile fits"
+    pick = [-1, tiles[seed % len(tiles)], tiles[-1]]
+    for tid in pick:
+        announce(f"random seed={seed} {L} tile={tid} raw")
+        assert_same(gpu_layer(L, t, requant=False, tile=tid)["y"], ref_raw["acc"], f"raw tile {tid}")
+        announce(f"random seed={seed} tile={tid} requant shift={sh}")
+        assert_same(gpu_layer(L, t, requant=True, tile=tid, shift=sh)["y"], ref_req["y_packed"], f"requant tile {tid}")
+
+
+# ----------------------------------------------------------------- epilogue stress
+
+@pytest.mark.parametrize("bits", [4, 8])
+def test_epilogue_spread_and_ties(bits):
+    """Zero-mean filters and a shift that spreads outputs over the whole clamp
+    range; then mult = 2^14, shift = 20 makes every acc = 32 (mod 64) an exact
+    rounding tie."""
+    if bits == 4:
+        L = qi.Layer("stress4", 4, 28, 28, 128, 64, 3, 3, 1, 1, w_range=(-7, 7))
+    else:
+        L = qi.Layer("stress8", 2, 28, 28, 64, 64, 3, 3, 1, 1, 8, True, True, qi.S8, qi.S8,
+                     qi.Epilogue(relu=False, lo=-128, hi=127))
+    t = qi.layer_tensors(200, bits, L)
+    sh = stress_shift(L, L.x_range, L.w_range)
+    for relu, lo, hi in ((True, 0, 15), (False, -8, 7)) if bits == 4 else ((False, -128, 127), (True, -128, 127)):
+        ref = ref_layer(L, t, requant=True, shift=sh, relu=relu, lo=lo, hi=hi)
+        vals = ref["y"]
+        assert len(np.unique(vals)) >= (12 if bits == 4 else 100), "stress case does not spread"
+        announce(f"stress bits={bits} relu={relu} clamp=({lo},{hi}) shift={sh}")
+        got = gpu_layer(L, t, requant=True, shift=sh, relu=relu, lo=lo, hi=hi)
+        assert_same(got["y"], ref["y_packed"], "stress requant")
+    # exact ties
+    t2 = dict(t, mult=np.full(L.k, 1 << 14, dtype=np.int32))
+    ref = ref_layer(L, t2, requant=True, shift=20, relu=False, lo=lo, hi=hi)
+    ties = int(((ref["acc"].astype(np.int64) % 64) == 32).sum())
+    assert ties > 100
+    announce(f"ties bits={bits} count={ties}")
+    got = gpu_layer(L, t2, requant=True, shift=20, relu=False, lo=lo, hi=hi)
+    assert_same(got["y"], ref["y_packed"], "ties")
+
+
+# ----------------------------------------------------------------- buffers, determinism, chaining
+
+def test_every_output_written_and_nothing_past_the_end():
+    torch, q = _torch(), _qconv()
+    L = qi.Layer("canary", 3, 13, 11, 64, 40, 3, 3, 1, 1)
+    t = qi.layer_tensors(300, 0, L)
+    ref = ref_layer(L, t, requant=False)
+    xp = q.pack(torch.from_numpy(t["x"]).cuda(), 4, False)
+    wp = q.pack(torch.from_numpy(t["w"]).cuda(), 4, True)
+    n_out = ref["acc"].size
+    for sentinel in (0x5A5A5A5A, -1):
+        buf = torch.full((n_out + 4096,), sentinel, dtype=torch.int32, device="cuda")
+        announce(f"sentinel {sentinel:#x}")
+        q.conv2d(L.desc(), xp, wp, out=buf[:n_out].view(ref["acc"].shape))
+        torch.cuda.synchronize()
+        host = buf.cpu().numpy()
+        assert_same(host[:n_out].reshape(ref["acc"].shape), ref["acc"], "raw")
+        assert (host[n_out:] == sentinel).all(), "write past the end of y"
+
+
+def test_run_twice_identical():
+    L = qi.config1()[0]
+    t = qi.layer_tensors(1, 0, L)
+    announce("determinism")
+    a = gpu_layer(L, t, requant=True)["y"]
+    b = gpu_layer(L, t, requant=True)["y"]
+    assert np.array_equal(a, b)
+
+
+def test_chained_layers_need_no_relayout():
+    """Layer 1's packed output is layer 2's input as-is (Sec. 3.3)."""
+    L1 = qi.Layer("chain1", 2, 20, 20, 64, 128, 3, 3, 1, 1, w_range=(-7, 7))
+    L2 = qi.Layer("chain2", 2, 20, 20, 128, 64, 3, 3, 2, 1, w_range=(-7, 7))
+    t1 = qi.layer_tensors(400, 1, L1)
+    t2 = qi.layer_tensors(400, 2, L2)
+    s1 = stress_shift(L1, L1.x_range, L1.w_range)
+    s2 = stress_shift(L2, L2.x_range, L2.w_range)
+    r1 = ref_layer(L1, t1, requant=True, shift=s1)
+    r2 = ref_layer(L2, t2, requant=True, shift=s2, packed_x=r1["y_packed"])
+    announce("chain layer 1")
+    g1 = gpu_layer(L1, t1, requant=True, shift=s1)
+    assert_same(g1["y"], r1["y_packed"], "layer 1")
+    announce("chain layer 2")
+    g2 = gpu_layer(L2, t2, requant=True, shift=s2, x_packed_dev=g1["y_dev"])
+    assert_same(g2["y"], r2["y_packed"], "layer 2")
