@@ -68,11 +68,15 @@ def per_layer_table(cfg: int, layers, dev, reps: int) -> list[dict]:
     import qconv_inputs as qi
     rows = []
     for lid, L in enumerate(layers):
+        from paper_2202_06819_amd import sweep
         x, xp, wp, mult = layer_setup(cfg, lid, L, dev)
         e = L.epilogue
-        call = qconv.Conv2dCall(L.desc(), xp, wp, requant=e is not None, mult=mult,
+        tile = sweep.tuned_tile(L.desc(), e is not None)
+        tile = qconv.default_tile(L.desc()) if tile == -1 else tile
+        wprep = qconv.prepare_filters(L.desc(), wp, tile)
+        call = qconv.Conv2dCall(L.desc(), xp, wprep, requant=e is not None, mult=mult,
                                 shift=e.shift if e else 20, relu=e.relu if e else False,
-                                clamp=(e.lo, e.hi) if e else (0, 15))
+                                clamp=(e.lo, e.hi) if e else (0, 15), tile=tile, prepared=True)
         for _ in range(5):
             call()
         us = time_loop(call, reps)
@@ -158,7 +162,7 @@ def main() -> int:
     import torch
     import qconv_inputs as qi
     from paper_2202_06819_amd import build as hip_build
-    from paper_2202_06819_amd import qconv
+    from paper_2202_06819_amd import qconv, sweep
 
     if not os.path.exists(hip_build.LIB):
         hip_build.build()
@@ -167,8 +171,11 @@ def main() -> int:
     e = L.epilogue
     x, xp, wp, mult = layer_setup(1, 0, L, dev)
     pack = qconv.PackCall(x, L.bits, L.x_signed, out=xp)
-    conv = qconv.Conv2dCall(L.desc(), xp, wp, requant=True, mult=mult, shift=e.shift, relu=e.relu,
-                            clamp=(e.lo, e.hi), tile=args.tile)
+    tile = sweep.tuned_tile(L.desc()) if args.tile == -1 else args.tile
+    tile = qconv.default_tile(L.desc()) if tile == -1 else tile
+    wprep = qconv.prepare_filters(L.desc(), wp, tile)     # offline, like packing the filters
+    conv = qconv.Conv2dCall(L.desc(), xp, wprep, requant=True, mult=mult, shift=e.shift, relu=e.relu,
+                            clamp=(e.lo, e.hi), tile=tile, prepared=True)
 
     def step():
         pack()

@@ -118,7 +118,16 @@ typedef struct qconv_epilogue {
  *   chunk_c            input channels staged per main-loop step (CHUNK)
  *   tile_p, tile_k     workgroup tile = 16*waves*frag along each axis
  *   bits               4 or 8: operand width the kernel is built for
+ *   variant            QCONV_VARIANT_STAGED: global -> VGPR -> LDS staging, one
+ *                      stage at a time, any channel count;
+ *                      QCONV_VARIANT_WIDE: next stage prefetched into registers
+ *                      during the MFMAs, operands widened once and staged in
+ *                      LDS as int8, double buffered, persistent over output
+ *                      tiles; needs c*bits % 128 == 0
  */
+#define QCONV_VARIANT_STAGED 0
+#define QCONV_VARIANT_WIDE 2
+
 typedef struct qconv_tile_info {
     int32_t id;
     int32_t bits;
@@ -127,6 +136,8 @@ typedef struct qconv_tile_info {
     int32_t chunk_c;
     int32_t tile_p, tile_k;
     int32_t threads;
+    int32_t variant;
+    int32_t x_signed, w_signed;   /* operand signedness the kernel is built for; -1 = any */
     char name[64];
 } qconv_tile_info;
 
@@ -173,6 +184,30 @@ int qconv_pack(const int8_t *src, void *dst, int32_t n, int32_t c, int32_t h, in
  */
 int qconv2d(const qconv_desc *d, const void *x, const void *w, const qconv_epilogue *epi, void *y,
             void *workspace, size_t workspace_bytes, int32_t tile_id, void *stream);
+
+/*
+ * Prepared filters.  Filters are constant across calls, so their layout work
+ * can be done once, offline, like packing them (Sec. 3.3: keep operands in the
+ * layout the kernel consumes).  For a wide tile the prepared form is the
+ * int8 image of each (output-channel tile, channel chunk) block exactly as
+ * the kernel stages it in LDS, so staging filters becomes a contiguous copy;
+ * for other tiles it is the packed KRSC filters unchanged.
+ *
+ * qconv_prepared_filter_bytes -- host only: size of the prepared filters of
+ *   `tile_id` (-1 = the built-in choice for `d`) for this shape.
+ * qconv_prepare_filters -- device work on `stream`: w_packed (packed KRSC,
+ *   16-byte aligned) -> w_prepared (`bytes` >= the size above, 16-byte
+ *   aligned, not overlapping w_packed).  Errors: QCONV_EINVAL,
+ *   QCONV_EUNSUPPORTED, QCONV_EHIP.
+ * qconv2d_prepared -- qconv2d with prepared filters; `tile_id` must be the
+ *   one they were prepared for (-1 resolves the same way for the same
+ *   descriptor).  Results are identical to qconv2d.
+ */
+int qconv_prepared_filter_bytes(const qconv_desc *d, int32_t tile_id, size_t *bytes);
+int qconv_prepare_filters(const qconv_desc *d, const void *w_packed, int32_t tile_id, void *w_prepared,
+                          size_t bytes, void *stream);
+int qconv2d_prepared(const qconv_desc *d, const void *x, const void *w_prepared, size_t w_prepared_bytes,
+                     const qconv_epilogue *epi, void *y, int32_t tile_id, void *stream);
 
 /* Number of compiled tile configurations; ids are 0 .. count-1. */
 int qconv_tile_count(void);

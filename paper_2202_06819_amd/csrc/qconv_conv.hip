@@ -2,9 +2,9 @@
 // int32 accumulation.
 //
 // GEMM view (Sec. 2.1): rows = output pixels m = (n, p, q), columns = output
-// channels, depth = (r, s, c).  The MFMA's A operand is the filter block
-// (16 output channels x 64 depth values), B is the activation block (64 depth
-// values x 16 pixels); D = A * B holds 16 channels x 16 pixels.
+// channels, depth = (r, s, c).  The MFMA's A operand is a filter block (16
+// output channels x 64 depth values), B an activation block (64 depth values
+// x 16 pixels); D = A * B holds 16 channels x 16 pixels.
 //
 // Staging (the duplicate-aware load of Sec. 3.1 / Alg. 1, restated): a
 // workgroup owns TP consecutive output pixels.  Instead of loading the
@@ -13,84 +13,44 @@
 // pixels touch into LDS.  A lowered row is then pure address arithmetic: the
 // pixel's base offset in the band plus a per-tap offset that is the same for
 // every lane.  Padding rows and columns are materialised as zeros in the band,
-// so no lane ever tests a border.
-//
-// LDS layout: channels are split into 16-channel granules (8 bytes packed
-// 4-bit, 16 bytes int8).  Each granule index owns a plane; inside a plane a
-// pixel's granule sits at (band_row * ncols + col) * granule_bytes.  MFMA
-// lane l reads granule plane (l / 16) of pixel (l % 16): the 16 lanes of a
-// plane read consecutive addresses, and planes are padded by 128 mod 256
-// bytes so the four lane groups of a read fall into different banks.
+// so no lane tests a border in the main loop.
 //
 // Operands stay packed in HBM and LDS; 4-bit values are widened to int8 in
-// VGPRs right before the MFMA (see widen4).
+// VGPRs right before the MFMA (widen4).
 //
 // Output packing in registers (Sec. 3.2.3 and 3.3, restated for wave64): the
-// MFMA result lane layout gives lane l the rows 4*(l/16)+v of the D tile.
-// Filters are placed in A so that D row i of fragment tm is output channel
-// (i/4)*4*FK + 4*tm + i%4 of the wave's channel block; then each lane ends
-// with 4*FK consecutive channels of one pixel and packs them into whole
-// 32-bit words without any cross-lane exchange.  The epilogue (requantise,
-// ReLU, clamp, pack) runs on those registers and stores each pixel's
-// channels as one contiguous run (Sec. 3.2.2: epilogue before the store).
+// MFMA result layout gives lane l the rows 4*(l/16)+v of the D tile.  Filters
+// are placed in A so that D row i of fragment tm is output channel
+// row_channel(tm, i) of the wave's block; each lane then ends with 4*FK
+// consecutive channels of one pixel and packs whole 32-bit words without any
+// cross-lane exchange.  The epilogue (requantise, ReLU, clamp, pack) runs on
+// those registers and stores each pixel's channel run contiguously
+// (Sec. 3.2.2: epilogue before the store).
+//
+// Two kernels share this design:
+//   conv_staged  global -> VGPR -> LDS staging, one stage at a time; any
+//                C that is a multiple of the packing word.
+//   conv_wide    the packed operands of the next (tile, chunk) stage are
+//                fetched into VGPRs while the MFMAs consume the current stage,
+//                then widened once and written to LDS as int8, so the MFMA loop
+//                itself carries no VALU work (widening inside that loop halves
+//                MFMA throughput on gfx950); two stage buffers; a workgroup
+//                walks several output tiles and keeps its filter block
+//                resident in LDS when the whole depth fits one chunk.  Needs
+//                every 16-byte vector of a pixel to be whole
+//                (C*bits % 128 == 0).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "qconv_device.h"
 #include "qconv_internal.h"
 
 namespace qconv {
 
-typedef int v4i __attribute__((ext_vector_type(4)));
-
-// 4-bit nibbles -> int8 lanes.  Each 32-bit word holds channels 0..7 of a
-// group; lo keeps the even channels, hi the odd ones, one per byte:
-//   unsigned: lo = v & 0x0F0F0F0F,        hi = (v >> 4) & 0x0F0F0F0F
-//   signed:   lo = (v << 4) & 0xF0F0F0F0, hi = v & 0xF0F0F0F0   (value * 16)
-// The signed form is exact: the nibble in the high half of a byte is the
-// two's-complement int8 16*v.  Both operands use the same channel order, so
-// the dot product is unchanged; the factor 16 is removed from the int32
-// accumulator by an exact arithmetic shift.
-__device__ __forceinline__ v4i widen4(uint2 v, uint32_t mask, int sl, int sr) {
-    v4i o;
-    o[0] = (int)((v.x << sl) & mask);
-    o[1] = (int)((v.x >> sr) & mask);
-    o[2] = (int)((v.y << sl) & mask);
-    o[3] = (int)((v.y >> sr) & mask);
-    return o;
-}
-
-template <int BITS>
-struct Gran;
-template <>
-struct Gran<4> {
-    using raw = uint2;
-    __device__ static __forceinline__ v4i widen(raw v, uint32_t mask, int sl, int sr) { return widen4(v, mask, sl, sr); }
-};
-template <>
-struct Gran<8> {
-    using raw = uint4;
-    __device__ static __forceinline__ v4i widen(raw v, uint32_t, int, int) {
-        v4i o;
-        o[0] = (int)v.x;
-        o[1] = (int)v.y;
-        o[2] = (int)v.z;
-        o[3] = (int)v.w;
-        return o;
-    }
-};
-
-// Padded row ("virtual row") of output pixel m's first tap, and its column.
-__device__ __forceinline__ void pixel_origin(const ConvArgs &a, int m, int &vrow, int &col) {
-    int img = (int)fdiv((uint32_t)m, a.div_pq);
-    int rem = m - img * (a.p * a.q);
-    int pp = (int)fdiv((uint32_t)rem, a.div_q);
-    int qq = rem - pp * a.q;
-    vrow = img * a.vh + pp * a.sh;
-    col = qq * a.sw;
-}
+// ============================================================== conv_staged
 
 template <int BITS, int WP, int WK, int FP, int FK, int CK>
-__global__ void __launch_bounds__(WP * WK * 64) conv_igemm(ConvArgs a) {
+__global__ void __launch_bounds__(WP * WK * 64) conv_staged(ConvArgs a) {
     constexpr int NT = WP * WK * 64;
     constexpr int TP = WP * FP * 16;
     constexpr int TK = WK * FK * 16;
@@ -99,6 +59,7 @@ __global__ void __launch_bounds__(WP * WK * 64) conv_igemm(ConvArgs a) {
     constexpr int VPP = CK * BITS / 128;    // 16-byte vectors per pixel and chunk
     constexpr int GPV = 16 / GRAN;          // granules per 16-byte vector
     constexpr int CPW = 32 / BITS;          // channels per 32-bit word
+    constexpr int BATCH = 4;                // vectors in flight per thread while staging
     static_assert(BITS == 8 || FK % 2 == 0, "4-bit output packs 8 channels per word: FK must be even");
     using G = Gran<BITS>;
     using Raw = typename G::raw;
@@ -115,18 +76,16 @@ __global__ void __launch_bounds__(WP * WK * 64) conv_igemm(ConvArgs a) {
     const int l16 = lane & 15;
     const int gq = lane >> 4;
 
-    const int bid = blockIdx.x;
-    const int kt = bid % a.ktiles;
-    const int mt = bid / a.ktiles;
+    const int kt = blockIdx.x % a.ktiles;
+    const int mt = blockIdx.x / a.ktiles;
     const int m0 = mt * TP;
     const int k0 = kt * TK;
     const int rs = a.r * a.s;
 
-    // Band of padded rows this workgroup's pixels touch.
     int vlo, c_unused, vlast;
     pixel_origin(a, m0, vlo, c_unused);
     pixel_origin(a, min(m0 + TP, a.m) - 1, vlast, c_unused);
-    const int nrows = vlast + a.r - vlo;   // <= a.band_rows (checked on the host)
+    const int nrows = vlast + a.r - vlo;   // <= a.band_rows (host-checked)
 
     int pixoff[FP];
 #pragma unroll
@@ -142,6 +101,9 @@ __global__ void __launch_bounds__(WP * WK * 64) conv_igemm(ConvArgs a) {
     for (int tn = 0; tn < FP; ++tn)
 #pragma unroll
         for (int tm = 0; tm < FK; ++tm) acc[tn][tm] = v4i{0, 0, 0, 0};
+    const int cb = k0 + wk * FK * 16 + gq * 4 * FK;
+    EpiParams<FK> ep;
+    load_epilogue_params<FK>(a, cb, ep);
 
     const int nvec_band = nrows * a.ncols * VPP;
     const int nvec_w = TK * rs * VPP;
@@ -150,185 +112,573 @@ __global__ void __launch_bounds__(WP * WK * 64) conv_igemm(ConvArgs a) {
         const int cbyte = chunk * (CK * BITS / 8);
         const int cbase = chunk * CK;
         __syncthreads();
-        // ---- band: global -> LDS, every needed input pixel exactly once
-        for (int idx = tid; idx < nvec_band; idx += NT) {
-            const int part = idx % VPP;
-            const int pix = idx / VPP;
+        // ---- band: global -> VGPR -> LDS; BATCH loads are issued before any is waited on
+        for (int base = 0; base < nvec_band; base += NT * BATCH) {
+            uint32_t d[BATCH][4];
+#pragma unroll
+            for (int u = 0; u < BATCH; ++u) {
+                d[u][0] = d[u][1] = d[u][2] = d[u][3] = 0u;
+                const int idx = base + u * NT + tid;
+                if (idx >= nvec_band) continue;
+                const int part = idx % VPP;
+                const int pix = idx / VPP;
+                const int rowl = (int)fdiv((uint32_t)pix, a.div_ncols);
+                const int col = pix - rowl * a.ncols;
+                const int vrow = vlo + rowl;
+                const int img = (int)fdiv((uint32_t)vrow, a.div_vh);
+                const int hh = vrow - img * a.vh - a.ph;
+                const int ww = col - a.pw;
+                if (img < a.n && hh >= 0 && hh < a.h && ww >= 0 && ww < a.w) {
+                    const int ch0 = cbase + part * (128 / BITS);
+                    const uint8_t *src = a.xptr + ((size_t)(img * a.h + hh) * a.w + ww) * a.xpix + cbyte + part * 16;
+                    if (a.vec16 && ch0 + 128 / BITS <= a.c) {
+                        uint4 v = *reinterpret_cast<const uint4 *>(src);
+                        d[u][0] = v.x; d[u][1] = v.y; d[u][2] = v.z; d[u][3] = v.w;
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            if (ch0 + e * CPW < a.c) d[u][e] = reinterpret_cast<const uint32_t *>(src)[e];
+                    }
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < BATCH; ++u) {
+                const int idx = base + u * NT + tid;
+                if (idx >= nvec_band) continue;
+                const int part = idx % VPP;
+                const int off = (idx / VPP) * GRAN;
+                if constexpr (BITS == 4) {
+                    *reinterpret_cast<uint2 *>(band + (size_t)(part * GPV) * a.pstride_b + off) = uint2{d[u][0], d[u][1]};
+                    *reinterpret_cast<uint2 *>(band + (size_t)(part * GPV + 1) * a.pstride_b + off) = uint2{d[u][2], d[u][3]};
+                } else {
+                    *reinterpret_cast<uint4 *>(band + (size_t)part * a.pstride_b + off) =
+                        uint4{d[u][0], d[u][1], d[u][2], d[u][3]};
+                }
+            }
+        }
+        // ---- filters: TK channels x R*S taps of this chunk, in MFMA row order
+        for (int base = 0; base < nvec_w; base += NT * BATCH) {
+            uint32_t d[BATCH][4];
+#pragma unroll
+            for (int u = 0; u < BATCH; ++u) {
+                d[u][0] = d[u][1] = d[u][2] = d[u][3] = 0u;
+                const int idx = base + u * NT + tid;
+                if (idx >= nvec_w) continue;
+                const int part = idx % VPP;
+                const int t = idx / VPP;
+                const int slot = (int)fdiv((uint32_t)t, a.div_rs);
+                const int tap = t - slot * rs;
+                const int wkk = slot / (FK * 16);
+                const int rem = slot % (FK * 16);
+                const int kk = k0 + wkk * FK * 16 + row_channel<FK>(rem / 16, rem % 16);
+                if (kk < a.k) {
+                    const int ch0 = cbase + part * (128 / BITS);
+                    const uint8_t *src = a.wptr + ((size_t)kk * rs + tap) * a.xpix + cbyte + part * 16;
+                    if (a.vec16 && ch0 + 128 / BITS <= a.c) {
+                        uint4 v = *reinterpret_cast<const uint4 *>(src);
+                        d[u][0] = v.x; d[u][1] = v.y; d[u][2] = v.z; d[u][3] = v.w;
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            if (ch0 + e * CPW < a.c) d[u][e] = reinterpret_cast<const uint32_t *>(src)[e];
+                    }
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < BATCH; ++u) {
+                const int idx = base + u * NT + tid;
+                if (idx >= nvec_w) continue;
+                const int part = idx % VPP;
+                const int t = idx / VPP;
+                const int slot = (int)fdiv((uint32_t)t, a.div_rs);
+                const int tap = t - slot * rs;
+                const int off = (tap * TK + slot) * GRAN;
+                if constexpr (BITS == 4) {
+                    *reinterpret_cast<uint2 *>(wlds + (size_t)(part * GPV) * a.pstride_w + off) = uint2{d[u][0], d[u][1]};
+                    *reinterpret_cast<uint2 *>(wlds + (size_t)(part * GPV + 1) * a.pstride_w + off) = uint2{d[u][2], d[u][3]};
+                } else {
+                    *reinterpret_cast<uint4 *>(wlds + (size_t)part * a.pstride_w + off) =
+                        uint4{d[u][0], d[u][1], d[u][2], d[u][3]};
+                }
+            }
+        }
+        __syncthreads();
+
+        // ---- main loop over taps: LDS -> VGPR, widen, MFMA
+        for (int rr = 0; rr < a.r; ++rr)
+            for (int ss = 0; ss < a.s; ++ss) {
+                const int tap = rr * a.s + ss;
+                const int toff = (rr * a.ncols + ss) * GRAN;
+#pragma unroll
+                for (int ks = 0; ks < KSTEPS; ++ks) {
+                    const int g = ks * 4 + gq;
+                    const uint8_t *bp = band + (size_t)g * a.pstride_b + toff;
+                    const uint8_t *ap = wlds + (size_t)g * a.pstride_w + (tap * TK + wk * FK * 16 + l16) * GRAN;
+                    v4i A[FK], B[FP];
+#pragma unroll
+                    for (int tm = 0; tm < FK; ++tm)
+                        A[tm] = G::widen(*reinterpret_cast<const Raw *>(ap + tm * 16 * GRAN), a.wmask, a.wsl, a.wsr);
+#pragma unroll
+                    for (int tn = 0; tn < FP; ++tn)
+                        B[tn] = G::widen(*reinterpret_cast<const Raw *>(bp + pixoff[tn]), a.xmask, a.xsl, a.xsr);
+#pragma unroll
+                    for (int tn = 0; tn < FP; ++tn)
+#pragma unroll
+                        for (int tm = 0; tm < FK; ++tm)
+                            acc[tn][tm] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A[tm], B[tn], acc[tn][tm], 0, 0, 0);
+                }
+            }
+    }
+    epilogue<BITS, FP, FK>(a, acc, m0 + wp * FP * 16, cb, l16, ep);
+}
+
+// ============================================================== conv_wide
+
+// Widening of one packed 16-byte vector with the signedness fixed at compile
+// time: 4-bit -> two 16-byte int8 granules (16 channels each, even channels
+// then odd channels of every word, the same order for both operands), 8-bit ->
+// itself.  3 VALU ops per packed 32-bit word.
+template <int BITS, bool SIGNED>
+__device__ __forceinline__ void widen_vec(uint4 v, uint4 &g0, uint4 &g1) {
+    if constexpr (BITS == 8) {
+        g0 = v;
+        g1 = v;
+    } else if constexpr (SIGNED) {
+        g0 = uint4{(v.x << 4) & 0xF0F0F0F0u, v.x & 0xF0F0F0F0u, (v.y << 4) & 0xF0F0F0F0u, v.y & 0xF0F0F0F0u};
+        g1 = uint4{(v.z << 4) & 0xF0F0F0F0u, v.z & 0xF0F0F0F0u, (v.w << 4) & 0xF0F0F0F0u, v.w & 0xF0F0F0F0u};
+    } else {
+        g0 = uint4{v.x & 0x0F0F0F0Fu, (v.x >> 4) & 0x0F0F0F0Fu, v.y & 0x0F0F0F0Fu, (v.y >> 4) & 0x0F0F0F0Fu};
+        g1 = uint4{v.z & 0x0F0F0F0Fu, (v.z >> 4) & 0x0F0F0F0Fu, v.w & 0x0F0F0F0Fu, (v.w >> 4) & 0x0F0F0F0Fu};
+    }
+}
+
+constexpr int kWideMaxV = 4;   // packed 16-byte vectors a thread prefetches per stage (band and filters each)
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+constexpr uint32_t kRsrcWord3 = 0x00020000u;   // raw buffer, dword data format (gfx9 family)
+
+// Buffer resource for a read-only tensor of `bytes` bytes (wave-uniform).
+__device__ __forceinline__ u32x4 make_rsrc(const void *base, int32_t bytes) {
+    const uint64_t b = (uint64_t)base;
+    u32x4 r;
+    r[0] = __builtin_amdgcn_readfirstlane((uint32_t)b);
+    r[1] = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+    r[2] = __builtin_amdgcn_readfirstlane((uint32_t)bytes);
+    r[3] = kRsrcWord3;
+    return r;
+}
+
+// 16 bytes per lane from global memory (buffer offset `voff`) straight into LDS
+// at lds_dst + 16 * lane.  Inline assembly keeps the compiler from guarding
+// later LDS reads with waits on these loads; the kernel waits explicitly.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(const uint8_t *lds_dst, uint32_t voff, u32x4 rsrc) {
+    const uint32_t m0v = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void *)lds_dst);
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" : : "s"(m0v), "v"(voff), "s"(rsrc)
+                 : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS>
+__device__ __forceinline__ void wide_body(const ConvArgs &a) {
+    constexpr int NW = WP * WK;
+    constexpr int NT = NW * 64;
+    constexpr int TP = WP * FP * 16;
+    constexpr int TK = WK * FK * 16;
+    constexpr int KSTEPS = CK / 64;
+    constexpr int VPP = CK * BITS / 128;    // packed 16-byte vectors per pixel (or filter tap) and chunk
+    constexpr int GPV = 16 / (2 * BITS);    // 16-channel int8 granules per packed vector
+    constexpr int CPV = 128 / BITS;         // channels per packed vector
+    constexpr int MAXV = kWideMaxV;
+    static_assert(BITS == 8 || FK % 2 == 0, "4-bit output packs 8 channels per word: FK must be even");
+
+    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wp = wave % WP;
+    const int wk = wave / WP;
+    const int l16 = lane & 15;
+    const int gq = lane >> 4;
+
+    const int kt = blockIdx.x % a.ktiles;
+    const int j0 = blockIdx.x / a.ktiles;
+    const int gpk = gridDim.x / a.ktiles;                    // workgroups sharing this channel tile
+    const int my_tiles = (a.mtiles - j0 + gpk - 1) / gpk;    // tiles j0, j0 + gpk, ...
+    const int nst = my_tiles * a.nchunks;
+    const int k0 = kt * TK;
+    const int rs = a.r * a.s;
+
+    // ---- band staging: packed global -> VGPR (prefetch) -> widen -> int8 LDS planes.
+    // Plane g holds granule g (channels 16g .. 16g+15 of the chunk) of every band
+    // pixel, 16 bytes each.  Lanes run along pixels so each write instruction
+    // fills one plane contiguously (no bank conflicts).
+    struct Fetch {
+        uint4 v[MAXV];
+        int n, npix;
+    };
+    auto band_fetch = [&](int ti, int c, Fetch &f) {
+        const int m0 = (j0 + ti * gpk) * TP;
+        int vlo, vlast, cu;
+        pixel_origin(a, m0, vlo, cu);
+        pixel_origin(a, min(m0 + TP, a.m) - 1, vlast, cu);
+        f.npix = (vlast + a.r - vlo) * a.ncols;
+        f.n = f.npix * VPP;   // <= NT * MAXV (host-checked)
+        const int cbyte = c * (CK * BITS / 8);
+        const int cbase = c * CK;
+#pragma unroll
+        for (int u = 0; u < MAXV; ++u) {
+            f.v[u] = uint4{0u, 0u, 0u, 0u};
+            const int idx = u * NT + tid;
+            if (idx >= f.n) continue;
+            const int part = idx / f.npix;
+            const int pix = idx - part * f.npix;
             const int rowl = (int)fdiv((uint32_t)pix, a.div_ncols);
             const int col = pix - rowl * a.ncols;
             const int vrow = vlo + rowl;
             const int img = (int)fdiv((uint32_t)vrow, a.div_vh);
             const int hh = vrow - img * a.vh - a.ph;
             const int ww = col - a.pw;
-            uint32_t d[4] = {0u, 0u, 0u, 0u};
-            const bool inside = img < a.n && hh >= 0 && hh < a.h && ww >= 0 && ww < a.w;
-            if (inside) {
-                const int ch0 = cbase + part * (128 / BITS);
-                const uint8_t *src =
-                    a.xptr + ((size_t)(img * a.h + hh) * a.w + ww) * a.xpix + cbyte + part * 16;
-                if (a.vec16 && ch0 + 128 / BITS <= a.c) {
-                    uint4 v = *reinterpret_cast<const uint4 *>(src);
-                    d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
-                } else {
+            if (img < a.n && hh >= 0 && hh < a.h && ww >= 0 && ww < a.w && cbase + part * CPV < a.c)
+                f.v[u] = *reinterpret_cast<const uint4 *>(a.xptr + ((size_t)(img * a.h + hh) * a.w + ww) * a.xpix +
+                                                          cbyte + part * 16);
+        }
+    };
+    auto band_store = [&](const Fetch &f, int buf) {
+        uint8_t *bb = smem + (buf ? a.off_b1 : a.off_b0);
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        if (ch0 + e * CPW < a.c) d[e] = reinterpret_cast<const uint32_t *>(src)[e];
-                }
-            }
-            const int off = pix * GRAN;
-            if constexpr (BITS == 4) {
-                *reinterpret_cast<uint2 *>(band + (size_t)(part * GPV) * a.pstride_b + off) = uint2{d[0], d[1]};
-                *reinterpret_cast<uint2 *>(band + (size_t)(part * GPV + 1) * a.pstride_b + off) = uint2{d[2], d[3]};
-            } else {
-                *reinterpret_cast<uint4 *>(band + (size_t)part * a.pstride_b + off) = uint4{d[0], d[1], d[2], d[3]};
+        for (int u = 0; u < MAXV; ++u) {
+            const int idx = u * NT + tid;
+            if (idx >= f.n) continue;
+            const int part = idx / f.npix;
+            const int pix = idx - part * f.npix;
+            uint4 g0, g1;
+            widen_vec<BITS, XS>(f.v[u], g0, g1);
+            *reinterpret_cast<uint4 *>(bb + (size_t)(part * GPV) * a.pstride_b + pix * 16) = g0;
+            if constexpr (GPV == 2) *reinterpret_cast<uint4 *>(bb + (size_t)(part * GPV + 1) * a.pstride_b + pix * 16) = g1;
+        }
+    };
+
+    // ---- filter staging.  Prepared filters (a.w_image): the block of this
+    // channel tile and chunk is already the LDS image (int8, MFMA row order,
+    // planes of pstride_w bytes), copied with asynchronous LDS-DMA.  Otherwise
+    // the packed KRSC filters are gathered, widened and written here; lanes run
+    // along filter slots so LDS writes stay contiguous.
+    const u32x4 rimg = make_rsrc(a.wptr, a.wbytes);
+    auto w_dma = [&](int c, int buf) {
+        uint8_t *wb = smem + (buf ? a.off_w1 : a.off_w0);
+        const uint32_t base = (uint32_t)((kt * a.nchunks + c) * (CK / 16) * a.pstride_w);
+        const int nkb = (CK / 16) * a.pstride_w / 1024;
+        for (int i = wave; i < nkb; i += NW) dma16(wb + i * 1024, base + i * 1024 + lane * 16, rimg);
+    };
+    auto w_gather = [&](int c, int base, Fetch &f) {
+        f.n = TK * rs * VPP;
+        const int cbyte = c * (CK * BITS / 8);
+        const int cbase = c * CK;
+#pragma unroll
+        for (int u = 0; u < MAXV; ++u) {
+            f.v[u] = uint4{0u, 0u, 0u, 0u};
+            const int idx = base + u * NT + tid;
+            if (idx >= f.n) continue;
+            // idx = (part * rs + tap) * TK + slot
+            const int slot = idx % TK;
+            const int rest = idx / TK;
+            const int pt = (int)fdiv((uint32_t)rest, a.div_rs);
+            const int tap = rest - pt * rs;
+            const int kk = k0 + (slot / (FK * 16)) * FK * 16 + row_channel<FK>((slot % (FK * 16)) / 16, slot % 16);
+            if (kk < a.k && cbase + pt * CPV < a.c)
+                f.v[u] = *reinterpret_cast<const uint4 *>(a.wptr + ((size_t)kk * rs + tap) * a.xpix + cbyte + pt * 16);
+        }
+    };
+    auto w_gather_store = [&](const Fetch &f, int base, int buf) {
+        uint8_t *wb = smem + (buf ? a.off_w1 : a.off_w0);
+#pragma unroll
+        for (int u = 0; u < MAXV; ++u) {
+            const int idx = base + u * NT + tid;
+            if (idx >= f.n) continue;
+            const int slot = idx % TK;
+            const int rest = idx / TK;
+            const int pt = (int)fdiv((uint32_t)rest, a.div_rs);
+            const int tap = rest - pt * rs;
+            uint4 g0, g1;
+            widen_vec<BITS, WS>(f.v[u], g0, g1);
+            const int e = (tap * TK + slot) * 16;
+            *reinterpret_cast<uint4 *>(wb + (size_t)(pt * GPV) * a.pstride_w + e) = g0;
+            if constexpr (GPV == 2) *reinterpret_cast<uint4 *>(wb + (size_t)(pt * GPV + 1) * a.pstride_w + e) = g1;
+        }
+    };
+    auto w_load_all = [&](int c, int buf) {
+        const int n = TK * rs * VPP;
+        for (int base = 0; base < n; base += NT * MAXV) {
+            Fetch f;
+            w_gather(c, base, f);
+            w_gather_store(f, base, buf);
+        }
+    };
+
+    const int lane_b = gq * a.pstride_b;
+    const int lane_a = gq * a.pstride_w + (wk * FK * 16 + l16) * 16;
+    int pixoff[FP];
+    auto set_tile = [&](int ti) {
+        const int m0 = (j0 + ti * gpk) * TP;
+        int vlo, cu;
+        pixel_origin(a, m0, vlo, cu);
+#pragma unroll
+        for (int tn = 0; tn < FP; ++tn) {
+            int m = min(m0 + wp * FP * 16 + tn * 16 + l16, a.m - 1);
+            int vr, cl;
+            pixel_origin(a, m, vr, cl);
+            pixoff[tn] = ((vr - vlo) * a.ncols + cl) * 16 + lane_b;
+        }
+    };
+
+    v4i acc[FP][FK];
+#pragma unroll
+    for (int tn = 0; tn < FP; ++tn)
+#pragma unroll
+        for (int tm = 0; tm < FK; ++tm) acc[tn][tm] = v4i{0, 0, 0, 0};
+
+    const int cb = k0 + wk * FK * 16 + gq * 4 * FK;
+    // the workgroup's TK multipliers live in LDS (read back in the epilogue)
+    int32_t *mlds = reinterpret_cast<int32_t *>(smem + a.off_m);
+    if (a.mode == QCONV_OUT_REQUANT)
+        for (int e = tid; e < TK; e += NT) mlds[e] = a.mult[min(k0 + e, a.k - 1)];
+
+    // ---- prologue: stage 0
+    if (nst > 0) {
+        Fetch fb;
+        band_fetch(0, 0, fb);
+        if (a.w_image)
+            w_dma(0, 0);
+        else
+            w_load_all(0, 0);
+        __builtin_amdgcn_s_waitcnt(0);
+        band_store(fb, 0);
+    }
+    set_tile(0);
+    __syncthreads();
+
+    const int nit = rs * KSTEPS;
+
+    int ti = 0, c = 0;
+    for (int st = 0; st < nst; ++st) {
+        int nti = ti, nc = c + 1;
+        if (nc == a.nchunks) {
+            nc = 0;
+            ++nti;
+        }
+        const int cur = st & 1;
+        const bool more = st + 1 < nst;
+        // prefetch the next stage; it lands while the MFMAs run
+        Fetch fb, fw;
+        if (more) {
+            band_fetch(nti, nc, fb);
+            if (a.nchunks > 1) {
+                if (a.w_image)
+                    w_dma(nc, cur ^ 1);
+                else
+                    w_gather(nc, 0, fw);
             }
         }
-        // ---- filters: TK channels x R*S taps of this chunk, in MFMA row order
-        for (int idx = tid; idx < nvec_w; idx += NT) {
-            const int part = idx % VPP;
-            const int t = idx / VPP;
-            const int slot = (int)fdiv((uint32_t)t, a.div_rs);
-            const int tap = t - slot * rs;
-            // slot = wave_k * FK*16 + tm*16 + i  ->  channel (i/4)*4*FK + 4*tm + i%4 of that wave's block
-            const int wkk = slot / (FK * 16);
-            const int rem = slot % (FK * 16);
-            const int tm = rem / 16;
-            const int i = rem % 16;
-            const int kk = k0 + wkk * FK * 16 + (i / 4) * (4 * FK) + 4 * tm + (i % 4);
-            uint32_t d[4] = {0u, 0u, 0u, 0u};
-            if (kk < a.k) {
-                const int ch0 = cbase + part * (128 / BITS);
-                const uint8_t *src = a.wptr + ((size_t)kk * rs + tap) * a.xpix + cbyte + part * 16;
-                if (a.vec16 && ch0 + 128 / BITS <= a.c) {
-                    uint4 v = *reinterpret_cast<const uint4 *>(src);
-                    d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
-                } else {
+
+        // ---- MFMA loop: int8 fragments straight from LDS, one step of lookahead
+        const uint8_t *bb = smem + (cur ? a.off_b1 : a.off_b0);
+        const uint8_t *wb = smem + ((a.nchunks > 1 && cur) ? a.off_w1 : a.off_w0) + lane_a;
+        auto offs = [&](int it, int &ao, int &bo) {
+            const int tap = it / KSTEPS;
+            const int ks = it % KSTEPS;
+            const int rr = (int)fdiv((uint32_t)tap, a.div_s);
+            const int ss = tap - rr * a.s;
+            ao = ks * 4 * a.pstride_w + tap * TK * 16;
+            bo = ks * 4 * a.pstride_b + (rr * a.ncols + ss) * 16;
+        };
+        v4i A0[FK], B0[FP], A1[FK], B1[FP];
+        auto ld = [&](int it, v4i(&A)[FK], v4i(&B)[FP]) {
+            int ao, bo;
+            offs(it, ao, bo);
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        if (ch0 + e * CPW < a.c) d[e] = reinterpret_cast<const uint32_t *>(src)[e];
+            for (int tm = 0; tm < FK; ++tm) A[tm] = *reinterpret_cast<const v4i *>(wb + ao + tm * 256);
+#pragma unroll
+            for (int tn = 0; tn < FP; ++tn) B[tn] = *reinterpret_cast<const v4i *>(bb + bo + pixoff[tn]);
+        };
+        auto mm = [&](const v4i(&A)[FK], const v4i(&B)[FP]) {
+#pragma unroll
+            for (int tn = 0; tn < FP; ++tn)
+#pragma unroll
+                for (int tm = 0; tm < FK; ++tm)
+                    acc[tn][tm] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A[tm], B[tn], acc[tn][tm], 0, 0, 0);
+        };
+        ld(0, A0, B0);
+        int it = 0;
+        for (; it + 2 <= nit; it += 2) {
+            ld(it + 1, A1, B1);
+            mm(A0, B0);
+            ld(min(it + 2, nit - 1), A0, B0);   // clamped: re-reading the last step is harmless
+            mm(A1, B1);
+        }
+        if (it < nit) mm(A0, B0);
+
+        if (c == a.nchunks - 1) {
+            EpiParams<FK> ep;
+            if (a.mode == QCONV_OUT_REQUANT) {
+                int32_t mraw[4 * FK];
+#pragma unroll
+                for (int e = 0; e < 4 * FK; e += 4) {
+                    const int4 q = *reinterpret_cast<const int4 *>(mlds + cb - k0 + e);
+                    mraw[e] = q.x; mraw[e + 1] = q.y; mraw[e + 2] = q.z; mraw[e + 3] = q.w;
                 }
-            }
-            const int off = (tap * TK + slot) * GRAN;
-            if constexpr (BITS == 4) {
-                *reinterpret_cast<uint2 *>(wlds + (size_t)(part * GPV) * a.pstride_w + off) = uint2{d[0], d[1]};
-                *reinterpret_cast<uint2 *>(wlds + (size_t)(part * GPV + 1) * a.pstride_w + off) = uint2{d[2], d[3]};
+                make_epilogue_params<FK>(a, cb, mraw, ep);
             } else {
-                *reinterpret_cast<uint4 *>(wlds + (size_t)part * a.pstride_w + off) = uint4{d[0], d[1], d[2], d[3]};
+                ep.fast = false;
+            }
+            epilogue<BITS, FP, FK>(a, acc, (j0 + ti * gpk) * TP + wp * FP * 16, cb, l16, ep);
+#pragma unroll
+            for (int tn = 0; tn < FP; ++tn)
+#pragma unroll
+                for (int tm = 0; tm < FK; ++tm) acc[tn][tm] = v4i{0, 0, 0, 0};
+        }
+        if (more) {
+            __builtin_amdgcn_s_waitcnt(0);   // prefetched band (and filter DMA) have landed
+            band_store(fb, cur ^ 1);
+            if (a.nchunks > 1 && !a.w_image) {
+                w_gather_store(fw, 0, cur ^ 1);
+                for (int base = NT * MAXV; base < TK * rs * VPP; base += NT * MAXV) {
+                    Fetch f2;
+                    w_gather(nc, base, f2);
+                    w_gather_store(f2, base, cur ^ 1);
+                }
             }
         }
         __syncthreads();
-
-        // ---- main loop over taps: LDS -> VGPR, widen, MFMA
-        for (int tap = 0; tap < rs; ++tap) {
-            const int rr = tap / a.s;
-            const int ss = tap - rr * a.s;
-            const int toff = (rr * a.ncols + ss) * GRAN;
-#pragma unroll
-            for (int ks = 0; ks < KSTEPS; ++ks) {
-                const int g = ks * 4 + gq;
-                const uint8_t *bp = band + (size_t)g * a.pstride_b + toff;
-                const uint8_t *ap = wlds + (size_t)g * a.pstride_w + (tap * TK + wk * FK * 16 + l16) * GRAN;
-                v4i A[FK], B[FP];
-#pragma unroll
-                for (int tm = 0; tm < FK; ++tm)
-                    A[tm] = G::widen(*reinterpret_cast<const Raw *>(ap + tm * 16 * GRAN), a.wmask, a.wsl, a.wsr);
-#pragma unroll
-                for (int tn = 0; tn < FP; ++tn)
-                    B[tn] = G::widen(*reinterpret_cast<const Raw *>(bp + pixoff[tn]), a.xmask, a.xsl, a.xsr);
-#pragma unroll
-                for (int tn = 0; tn < FP; ++tn)
-#pragma unroll
-                    for (int tm = 0; tm < FK; ++tm)
-                        acc[tn][tm] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A[tm], B[tn], acc[tn][tm], 0, 0, 0);
-            }
-        }
-    }
-
-    // ---- epilogue in registers: this lane holds channels cb .. cb + 4*FK - 1 of
-    // pixel m for every pixel fragment tn.
-    const int cb = k0 + wk * FK * 16 + gq * 4 * FK;
-    if (a.mode == QCONV_OUT_RAW_I32) {
-#pragma unroll
-        for (int tn = 0; tn < FP; ++tn) {
-            const int m = m0 + wp * FP * 16 + tn * 16 + l16;
-            if (m >= a.m) continue;
-            int32_t *yrow = reinterpret_cast<int32_t *>(a.yptr) + (size_t)m * a.k;
-#pragma unroll
-            for (int tm = 0; tm < FK; ++tm) {
-                if (cb + 4 * tm < a.k) {
-                    v4i v = acc[tn][tm];
-                    int4 o{v[0] >> a.acc_shift, v[1] >> a.acc_shift, v[2] >> a.acc_shift, v[3] >> a.acc_shift};
-                    *reinterpret_cast<int4 *>(yrow + cb + 4 * tm) = o;
-                }
-            }
-        }
-        return;
-    }
-
-    int32_t mul[4 * FK];
-#pragma unroll
-    for (int e = 0; e < 4 * FK; ++e) mul[e] = (cb + e < a.k) ? a.mult[cb + e] : 0;
-    const int64_t rnd = (int64_t)1 << (a.shift - 1);
-#pragma unroll
-    for (int tn = 0; tn < FP; ++tn) {
-        const int m = m0 + wp * FP * 16 + tn * 16 + l16;
-        if (m >= a.m) continue;
-        uint32_t words[4 * FK / CPW];
-#pragma unroll
-        for (int wd = 0; wd < 4 * FK / CPW; ++wd) words[wd] = 0u;
-#pragma unroll
-        for (int tm = 0; tm < FK; ++tm)
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int e = 4 * tm + v;   // channel cb + e
-                int64_t t = (int64_t)(acc[tn][tm][v] >> a.acc_shift) * mul[e] + rnd;
-                t >>= a.shift;              // arithmetic: floor
-                t = t < a.lo ? a.lo : t;
-                t = t > a.hi ? a.hi : t;
-                words[e / CPW] |= ((uint32_t)t & ((1u << BITS) - 1u)) << (BITS * (e % CPW));
-            }
-        uint32_t *yw = reinterpret_cast<uint32_t *>(a.yptr + (size_t)m * (a.k * BITS / 8) + cb * BITS / 8);
-#pragma unroll
-        for (int wd = 0; wd < 4 * FK / CPW; ++wd)
-            if (cb + wd * CPW < a.k) yw[wd] = words[wd];
+        if (more && nti != ti) set_tile(nti);
+        ti = nti;
+        c = nc;
     }
 }
 
+// Build the filter image conv_wide stages directly: for channel tile kt and
+// chunk c, plane g (channels 16g..16g+15 of the chunk), element tap*TK + slot
+// holds the widened int8 granule of output channel row_channel(slot) at that
+// tap -- the same bytes the gather path writes into LDS.  One thread per
+// 16-byte element; padding elements are zero.
+template <int BITS, int FK, bool WS>
+__global__ void __launch_bounds__(256) build_filter_image(ConvArgs a, int TK, int CK, uint8_t *img, int64_t total) {
+    const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (e >= total) return;
+    const int rs = a.r * a.s;
+    const int ng = CK / 16;
+    const int64_t plane_elems = a.pstride_w / 16;
+    const int64_t blk = e / (ng * plane_elems);
+    const int64_t rem = e - blk * ng * plane_elems;
+    const int g = (int)(rem / plane_elems);
+    const int el = (int)(rem - (int64_t)g * plane_elems);
+    const int kt = (int)(blk / a.nchunks);
+    const int c = (int)(blk - (int64_t)kt * a.nchunks);
+    uint4 out = uint4{0u, 0u, 0u, 0u};
+    if (el < rs * TK) {
+        const int tap = el / TK;
+        const int slot = el - tap * TK;
+        const int kk = kt * TK + (slot / (FK * 16)) * FK * 16 + row_channel<FK>((slot % (FK * 16)) / 16, slot % 16);
+        const int ch = c * CK + 16 * g;
+        if (kk < a.k && ch < a.c) {
+            const uint8_t *src = a.wptr + ((size_t)kk * rs + tap) * a.xpix + (size_t)ch * BITS / 8;
+            if constexpr (BITS == 4) {
+                const uint2 v = *reinterpret_cast<const uint2 *>(src);
+                uint4 g0, g1;
+                widen_vec<4, WS>(uint4{v.x, v.y, 0u, 0u}, g0, g1);
+                out = g0;
+            } else {
+                out = *reinterpret_cast<const uint4 *>(src);
+            }
+        }
+    }
+    *reinterpret_cast<uint4 *>(img + e * 16) = out;
+}
+
+// One operand signedness per kernel (the widening is compiled for it); 8-bit
+// operands are always signed.
+template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS>
+__global__ void __launch_bounds__(WP * WK * 64) __attribute__((amdgpu_waves_per_eu(2))) conv_wide(ConvArgs a) {
+    wide_body<BITS, WP, WK, FP, FK, CK, XS, WS>(a);
+}
+
+// ============================================================== tile registry
+
 template <int BITS, int WP, int WK, int FP, int FK, int CK>
-static hipError_t launch_conv(const ConvArgs &a, dim3 grid, size_t lds, hipStream_t stream) {
-    hipLaunchKernelGGL((conv_igemm<BITS, WP, WK, FP, FK, CK>), grid, dim3(WP * WK * 64), lds, stream, a);
+static hipError_t launch_staged(const ConvArgs &a, dim3 grid, size_t lds, hipStream_t stream) {
+    hipLaunchKernelGGL((conv_staged<BITS, WP, WK, FP, FK, CK>), grid, dim3(WP * WK * 64), lds, stream, a);
+    return hipGetLastError();
+}
+
+template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS>
+static hipError_t launch_wide(const ConvArgs &a, dim3 grid, size_t lds, hipStream_t stream) {
+    hipLaunchKernelGGL((conv_wide<BITS, WP, WK, FP, FK, CK, XS, WS>), grid, dim3(WP * WK * 64), lds, stream, a);
+    return hipGetLastError();
+}
+
+template <int BITS, int WK, int FK, int CK, bool WS>
+static hipError_t launch_prep(const ConvArgs &a, uint8_t *img, int64_t elems, hipStream_t stream) {
+    const int64_t blocks = (elems + 255) / 256;
+    hipLaunchKernelGGL((build_filter_image<BITS, FK, WS>), dim3((unsigned)blocks), dim3(256), 0, stream, a, WK * FK * 16, CK,
+                       img, elems);
     return hipGetLastError();
 }
 
 // The compiled tile space: (bits, waves_p, waves_k, frag_p, frag_k, chunk_c).
-#define QCONV_TILE_LIST(X)   \
-    X(4, 4, 1, 4, 4, 64)     \
-    X(4, 4, 1, 2, 4, 64)     \
-    X(4, 4, 1, 1, 4, 64)     \
-    X(4, 2, 2, 4, 4, 64)     \
-    X(4, 2, 2, 2, 4, 64)     \
-    X(4, 1, 4, 4, 4, 64)     \
-    X(4, 4, 1, 4, 2, 64)     \
-    X(4, 2, 2, 4, 2, 64)     \
-    X(4, 4, 1, 4, 4, 128)    \
-    X(4, 2, 2, 4, 4, 128)    \
-    X(4, 2, 2, 2, 4, 128)    \
-    X(4, 1, 4, 4, 4, 128)    \
-    X(8, 4, 1, 4, 4, 64)     \
-    X(8, 4, 1, 2, 4, 64)     \
-    X(8, 2, 2, 4, 4, 64)     \
-    X(8, 2, 2, 2, 4, 64)     \
-    X(8, 1, 4, 4, 4, 64)     \
-    X(8, 4, 1, 4, 2, 64)     \
-    X(8, 2, 2, 4, 4, 128)
+#define QCONV_STAGED_TILES(X) \
+    X(4, 4, 1, 1, 4, 64)      \
+    X(4, 4, 1, 2, 4, 64)      \
+    X(4, 2, 2, 2, 4, 128)     \
+    X(4, 4, 1, 4, 2, 64)      \
+    X(4, 4, 1, 1, 2, 64)      \
+    X(8, 4, 1, 1, 4, 64)      \
+    X(8, 4, 1, 2, 4, 64)      \
+    X(8, 4, 1, 4, 2, 64)      \
+    X(8, 4, 1, 2, 1, 64)
 
-#define QCONV_TILE_ENTRY(B, WP, WK, FP, FK, CK)                                                              \
-    {{0, B, WP, WK, FP, FK, CK, WP * FP * 16, WK * FK * 16, WP * WK * 64,                                    \
-      "b" #B "_w" #WP "x" #WK "_f" #FP "x" #FK "_c" #CK},                                                    \
-     &launch_conv<B, WP, WK, FP, FK, CK>,                                                                    \
-     reinterpret_cast<const void *>(&conv_igemm<B, WP, WK, FP, FK, CK>)},
+#define QCONV_WIDE_TILES(X) \
+    X(4, 4, 1, 1, 4, 64)    \
+    X(4, 4, 1, 2, 4, 64)    \
+    X(4, 4, 1, 4, 4, 64)    \
+    X(4, 8, 1, 1, 4, 64)    \
+    X(4, 8, 1, 2, 4, 64)    \
+    X(4, 4, 2, 2, 4, 64)    \
+    X(4, 4, 2, 4, 4, 64)    \
+    X(4, 2, 2, 4, 4, 64)    \
+    X(4, 2, 4, 4, 4, 64)    \
+    X(4, 1, 4, 4, 4, 64)    \
+    X(4, 4, 1, 4, 2, 64)    \
+    X(4, 8, 1, 4, 2, 64)    \
+    X(4, 4, 2, 4, 4, 128)   \
+    X(4, 2, 2, 4, 4, 128)   \
+    X(4, 2, 4, 2, 4, 128)   \
+    X(4, 1, 4, 4, 4, 128)   \
+    X(8, 4, 1, 2, 4, 64)    \
+    X(8, 4, 1, 4, 4, 64)    \
+    X(8, 8, 1, 2, 4, 64)    \
+    X(8, 4, 2, 4, 4, 64)    \
+    X(8, 2, 2, 4, 4, 64)    \
+    X(8, 2, 4, 4, 4, 64)    \
+    X(8, 1, 4, 4, 4, 64)
 
-static TileEntry g_tiles[] = {QCONV_TILE_LIST(QCONV_TILE_ENTRY)};
+#define QCONV_TILE_INFO(V, PREFIX, B, WP, WK, FP, FK, CK, XS, WS)                                                 \
+    {0, B, WP, WK, FP, FK, CK, WP * FP * 16, WK * FK * 16, WP * WK * 64, V, XS, WS,                              \
+     PREFIX #B "_w" #WP "x" #WK "_f" #FP "x" #FK "_c" #CK}
+#define QCONV_STAGED_ENTRY(B, WP, WK, FP, FK, CK)                                                                 \
+    {QCONV_TILE_INFO(QCONV_VARIANT_STAGED, "staged_b", B, WP, WK, FP, FK, CK, -1, -1),                           \
+     &launch_staged<B, WP, WK, FP, FK, CK>,                                                                       \
+     reinterpret_cast<const void *>(&conv_staged<B, WP, WK, FP, FK, CK>), nullptr},
+// 4-bit: unsigned activations x signed filters; 8-bit: signed x signed.
+#define QCONV_WIDE_ENTRY(B, WP, WK, FP, FK, CK)                                                                   \
+    {QCONV_TILE_INFO(QCONV_VARIANT_WIDE, "wide_b", B, WP, WK, FP, FK, CK, (B == 8), 1),                         \
+     &launch_wide<B, WP, WK, FP, FK, CK, (B == 8), true>,                                                         \
+     reinterpret_cast<const void *>(&conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true>),                          \
+     &launch_prep<B, WK, FK, CK, true>},
+
+static TileEntry g_tiles[] = {QCONV_STAGED_TILES(QCONV_STAGED_ENTRY) QCONV_WIDE_TILES(QCONV_WIDE_ENTRY)};
 
 const TileEntry *tile_table() {
     static bool numbered = [] {

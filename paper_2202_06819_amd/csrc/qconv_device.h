@@ -1,0 +1,223 @@
+// Device helpers shared by the convolution kernels: operand widening, pixel
+// addressing and the fused requantise/ReLU/clamp/repack epilogue.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "qconv_internal.h"
+
+namespace qconv {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+// 4-bit nibbles -> int8 lanes.  Each 32-bit word holds channels 0..7 of a
+// group; lo keeps the even channels, hi the odd ones, one per byte:
+//   unsigned: lo = v & 0x0F0F0F0F,        hi = (v >> 4) & 0x0F0F0F0F
+//   signed:   lo = (v << 4) & 0xF0F0F0F0, hi = v & 0xF0F0F0F0   (value * 16)
+// The signed form is exact: the nibble in the high half of a byte is the
+// two's-complement int8 16*v.  Both MFMA operands use the same channel order,
+// so the dot product is unchanged; the factor 16 stays in the int32
+// accumulator and is removed exactly in the epilogue.
+__device__ __forceinline__ v4i widen4(uint2 v, uint32_t mask, int sl, int sr) {
+    v4i o;
+    o[0] = (int)((v.x << sl) & mask);
+    o[1] = (int)((v.x >> sr) & mask);
+    o[2] = (int)((v.y << sl) & mask);
+    o[3] = (int)((v.y >> sr) & mask);
+    return o;
+}
+
+template <int BITS>
+struct Gran;
+template <>
+struct Gran<4> {
+    using raw = uint2;   // 16 channels, 8 bytes
+    __device__ static __forceinline__ v4i widen(raw v, uint32_t mask, int sl, int sr) { return widen4(v, mask, sl, sr); }
+};
+template <>
+struct Gran<8> {
+    using raw = uint4;   // 16 channels, 16 bytes
+    __device__ static __forceinline__ v4i widen(raw v, uint32_t, int, int) {
+        v4i o;
+        o[0] = (int)v.x;
+        o[1] = (int)v.y;
+        o[2] = (int)v.z;
+        o[3] = (int)v.w;
+        return o;
+    }
+};
+
+// Padded row ("virtual row") of output pixel m's first tap, and its column.
+__device__ __forceinline__ void pixel_origin(const ConvArgs &a, int m, int &vrow, int &col) {
+    int img = (int)fdiv((uint32_t)m, a.div_pq);
+    int rem = m - img * (a.p * a.q);
+    int pp = (int)fdiv((uint32_t)rem, a.div_q);
+    int qq = rem - pp * a.q;
+    vrow = img * a.vh + pp * a.sh;
+    col = qq * a.sw;
+}
+
+// Output channel held by MFMA row i of fragment tm in a wave's channel block:
+// rows are permuted so that lane group g of the result holds the 4*FK
+// consecutive channels g*4*FK .. g*4*FK + 4*FK - 1.
+template <int FK>
+__device__ __forceinline__ int row_channel(int tm, int i) {
+    return (i / 4) * (4 * FK) + 4 * tm + (i % 4);
+}
+
+// Per-lane multipliers for the epilogue: channels cb .. cb + 4*FK - 1 of the
+// wave's block, loaded once at kernel start so their latency hides behind the
+// main loop.
+//
+// Requantisation t = floor((acc*mult + 2^(shift-1)) / 2^shift) has an exact
+// 32-bit form when |mult| < 2^(shift-2) and shift + acc_shift <= 33:
+// with m2 = mult * 2^(33 - shift - acc_shift) (accumulators carry 2^acc_shift),
+// u = mulhi(acc, m2) = floor(2*acc*mult / 2^shift) and
+// floor(x + 1/2) = floor((floor(2x) + 1) / 2), so t = (u + 1) >> 1.
+// `fast` is decided once per wave; otherwise the product is formed in 64 bits.
+template <int FK>
+struct EpiParams {
+    int32_t mul[4 * FK];
+    bool fast;
+};
+
+// From multipliers already in registers (mraw[e] for channel cb + e; lanes
+// past the last channel hold a repeat of a valid one and are never stored).
+template <int FK>
+__device__ __forceinline__ void make_epilogue_params(const ConvArgs &a, int cb, const int32_t (&mraw)[4 * FK],
+                                                     EpiParams<FK> &ep) {
+    bool ok = true;
+    const int fast_sh = 33 - a.shift - a.acc_shift;
+    const int lim_bits = a.shift - 2;
+#pragma unroll
+    for (int e = 0; e < 4 * FK; ++e) {
+        const int32_t m = (cb + e < a.k) ? mraw[e] : 0;
+        ep.mul[e] = m;
+        const bool fits = lim_bits >= 31 || (lim_bits >= 0 && m < (1 << lim_bits) && m > -(1 << lim_bits));
+        ok = ok && fast_sh >= 0 && fits;
+    }
+    ep.fast = __all(ok);
+    if (ep.fast) {
+#pragma unroll
+        for (int e = 0; e < 4 * FK; ++e) ep.mul[e] = ep.mul[e] * (1 << fast_sh);
+    }
+}
+
+template <int FK>
+__device__ __forceinline__ void load_epilogue_params(const ConvArgs &a, int cb, EpiParams<FK> &ep) {
+    bool ok = true;
+    const int fast_sh = 33 - a.shift - a.acc_shift;
+    const int lim_bits = a.shift - 2;
+    if (a.mode != QCONV_OUT_REQUANT) {
+        ep.fast = false;
+#pragma unroll
+        for (int e = 0; e < 4 * FK; ++e) ep.mul[e] = 0;
+        return;
+    }
+#pragma unroll
+    for (int e = 0; e < 4 * FK; ++e) {
+        const int32_t m = (cb + e < a.k) ? a.mult[cb + e] : 0;
+        ep.mul[e] = m;
+        const bool fits = lim_bits >= 31 || (lim_bits >= 0 && m < (1 << lim_bits) && m > -(1 << lim_bits));
+        ok = ok && fast_sh >= 0 && fits;
+    }
+    ep.fast = __all(ok);
+    if (ep.fast) {
+#pragma unroll
+        for (int e = 0; e < 4 * FK; ++e) ep.mul[e] = ep.mul[e] * (1 << fast_sh);
+    }
+}
+
+// Store one pixel's packed channel run (4*FK channels of `BITS` bits).
+template <int BITS, int FK>
+__device__ __forceinline__ void store_run(const ConvArgs &a, int m, int cb, const uint32_t *words) {
+    constexpr int CPW = 32 / BITS;
+    constexpr int NWD = 4 * FK / CPW;
+    uint32_t *yw = reinterpret_cast<uint32_t *>(a.yptr + (size_t)m * (a.k * BITS / 8) + cb * BITS / 8);
+    const bool vec_ok = ((a.k * BITS / 8) % (NWD * 4)) == 0;   // row pitch keeps the vector aligned
+    if constexpr (NWD == 2) {
+        if (vec_ok && cb + 2 * CPW <= a.k) {
+            *reinterpret_cast<uint2 *>(yw) = uint2{words[0], words[1]};
+            return;
+        }
+    } else if constexpr (NWD == 4) {
+        if (vec_ok && cb + 4 * CPW <= a.k) {
+            *reinterpret_cast<uint4 *>(yw) = uint4{words[0], words[1], words[2], words[3]};
+            return;
+        }
+    }
+#pragma unroll
+    for (int wd = 0; wd < NWD; ++wd)
+        if (cb + wd * CPW < a.k) yw[wd] = words[wd];
+}
+
+// The epilogue for one wave (Sec. 3.2.2: work on the wide accumulator, then
+// clip and pack before the store).  acc[tn][tm][v] is output channel
+// cb + 4*tm + v of pixel mbase + 16*tn + l16.
+template <int BITS, int FP, int FK>
+__device__ __forceinline__ void epilogue(const ConvArgs &a, v4i (&acc)[FP][FK], int mbase, int cb, int l16,
+                                         const EpiParams<FK> &ep) {
+    constexpr int CPW = 32 / BITS;   // channels per 32-bit word
+    constexpr int NWD = 4 * FK / CPW;
+    constexpr uint32_t VMASK = (1u << BITS) - 1u;
+    if (a.mode == QCONV_OUT_RAW_I32) {
+#pragma unroll
+        for (int tn = 0; tn < FP; ++tn) {
+            const int m = mbase + tn * 16 + l16;
+            if (m >= a.m) continue;
+            int32_t *yrow = reinterpret_cast<int32_t *>(a.yptr) + (size_t)m * a.k;
+#pragma unroll
+            for (int tm = 0; tm < FK; ++tm) {
+                if (cb + 4 * tm < a.k) {
+                    v4i v = acc[tn][tm];
+                    int4 o{v[0] >> a.acc_shift, v[1] >> a.acc_shift, v[2] >> a.acc_shift, v[3] >> a.acc_shift};
+                    *reinterpret_cast<int4 *>(yrow + cb + 4 * tm) = o;
+                }
+            }
+        }
+        return;
+    }
+    const int lo = a.lo, hi = a.hi;
+    if (ep.fast) {
+#pragma unroll
+        for (int tn = 0; tn < FP; ++tn) {
+            uint32_t words[NWD];
+#pragma unroll
+            for (int wd = 0; wd < NWD; ++wd) words[wd] = 0u;
+#pragma unroll
+            for (int tm = 0; tm < FK; ++tm)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int e = 4 * tm + v;
+                    int32_t t = (__mulhi(acc[tn][tm][v], ep.mul[e]) + 1) >> 1;
+                    t = min(max(t, lo), hi);
+                    words[e / CPW] |= ((uint32_t)t & VMASK) << (BITS * (e % CPW));
+                }
+            const int m = mbase + tn * 16 + l16;
+            if (m < a.m) store_run<BITS, FK>(a, m, cb, words);
+        }
+        return;
+    }
+    const int64_t rnd = (int64_t)1 << (a.shift - 1);
+#pragma unroll
+    for (int tn = 0; tn < FP; ++tn) {
+        uint32_t words[NWD];
+#pragma unroll
+        for (int wd = 0; wd < NWD; ++wd) words[wd] = 0u;
+#pragma unroll
+        for (int tm = 0; tm < FK; ++tm)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int e = 4 * tm + v;
+                int64_t t64 = (int64_t)(acc[tn][tm][v] >> a.acc_shift) * ep.mul[e] + rnd;
+                t64 >>= a.shift;   // arithmetic: floor
+                t64 = t64 < lo ? lo : (t64 > hi ? hi : t64);
+                words[e / CPW] |= ((uint32_t)(int32_t)t64 & VMASK) << (BITS * (e % CPW));
+            }
+        const int m = mbase + tn * 16 + l16;
+        if (m < a.m) store_run<BITS, FK>(a, m, cb, words);
+    }
+}
+
+}  // namespace qconv

@@ -149,30 +149,91 @@ int64_t band_rows(const qconv_desc *d, int64_t p, int64_t q, int64_t tile_p) {
 
 int64_t pad_plane(int64_t bytes) { return (bytes + 255) / 256 * 256 + 128; }
 
+constexpr int kNumCUs = 256;   // MI355X compute units
+
 struct Plan {
-    int64_t rows, pstride_b, pstride_w, lds;
+    int64_t rows = 0, pstride_b = 0, pstride_w = 0, lds = 0;
+    int64_t off_b0 = 0, off_b1 = 0, off_w0 = 0, off_w1 = 0, off_m = 0;
+    int64_t mtiles = 0, ktiles = 0, grid = 0;
 };
 
-int plan_tile(const qconv_desc *d, const qconv_layout_info &li, const qconv_tile_info &t, Plan *out) {
+constexpr int kWideMaxV = 4;   // packed vectors a thread prefetches per stage in conv_wide
+
+int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+
+// Workgroups of this tile that fit one CU, from LDS and wave slots only.
+int64_t per_cu_estimate(const qconv_tile_info &t, int64_t lds) {
+    const int64_t by_lds = lds > 0 ? kLdsBytes / lds : 16;
+    const int64_t by_waves = 32 / (t.threads / 64);
+    return std::max<int64_t>(1, std::min<int64_t>({by_lds, by_waves, 16}));
+}
+
+// per_cu: workgroups per CU to plan the persistent grid for (0 = estimate).
+int plan_tile(const qconv_desc *d, const qconv_layout_info &li, const qconv_tile_info &t, Plan *out,
+              int64_t per_cu = 0) {
     if (t.bits != d->bits)
         return fail(QCONV_EUNSUPPORTED, "tile %s is built for %d-bit operands", t.name, t.bits);
-    const int64_t gran = 2 * d->bits;
+    if ((t.x_signed >= 0 && t.x_signed != d->x_signed) || (t.w_signed >= 0 && t.w_signed != d->w_signed))
+        return fail(QCONV_EUNSUPPORTED, "tile %s is built for x_signed=%d, w_signed=%d", t.name, t.x_signed, t.w_signed);
     const int64_t ncols = d->w + 2 * d->pad_w;
+    const int64_t nchunks = (d->c + t.chunk_c - 1) / t.chunk_c;
     Plan pl;
     pl.rows = band_rows(d, li.p, li.q, t.tile_p);
-    pl.pstride_b = pad_plane(pl.rows * ncols * gran);
-    pl.pstride_w = pad_plane((int64_t)d->r * d->s * t.tile_k * gran);
-    pl.lds = (int64_t)(t.chunk_c / 16) * (pl.pstride_b + pl.pstride_w);
+    pl.mtiles = (li.m + t.tile_p - 1) / t.tile_p;
+    pl.ktiles = (d->k + t.tile_k - 1) / t.tile_k;
+    if (t.variant == QCONV_VARIANT_STAGED) {
+        const int64_t gran = 2 * d->bits;
+        pl.pstride_b = pad_plane(pl.rows * ncols * gran);
+        pl.pstride_w = pad_plane((int64_t)d->r * d->s * t.tile_k * gran);
+        pl.lds = (int64_t)(t.chunk_c / 16) * (pl.pstride_b + pl.pstride_w);
+        pl.grid = pl.mtiles * pl.ktiles;
+    } else {
+        if ((d->c * d->bits) % 128 != 0)
+            return fail(QCONV_EUNSUPPORTED, "tile %s needs c*bits %% 128 == 0 (whole 16-byte vectors)", t.name);
+        const int64_t vpp = (int64_t)t.chunk_c * d->bits / 128;
+        if (pl.rows * ncols * vpp > (int64_t)t.threads * kWideMaxV)
+            return fail(QCONV_EUNSUPPORTED, "tile %s: the input band of this shape exceeds one prefetch batch", t.name);
+        const int64_t planes = t.chunk_c / 16;
+        // plane strides: multiples of 256 bytes keep the four 16-lane groups of a
+        // 16-byte LDS read in distinct banks; filter planes are whole KiB so a
+        // prepared filter block is copied with 1 KiB LDS-DMA instructions
+        pl.pstride_b = round_up(pl.rows * ncols * 16, 256);
+        pl.pstride_w = round_up((int64_t)d->r * d->s * t.tile_k * 16, 1024);
+        const int64_t bbuf = planes * pl.pstride_b, wbuf = planes * pl.pstride_w;
+        const int64_t mbytes = round_up((int64_t)t.tile_k * 4, 16);
+        const int64_t single = bbuf + wbuf + mbytes;
+        const int64_t tiles = pl.mtiles * pl.ktiles;
+        if (nchunks == 1 && tiles <= kNumCUs * per_cu_estimate(t, single)) {
+            // every workgroup gets exactly one stage: one band buffer suffices
+            pl.off_b0 = pl.off_b1 = 0;
+            pl.off_w0 = pl.off_w1 = bbuf;
+            pl.off_m = bbuf + wbuf;
+            pl.lds = single;
+            pl.grid = tiles;
+        } else {
+            pl.off_b0 = 0;
+            pl.off_b1 = bbuf;
+            pl.off_w0 = 2 * bbuf;
+            pl.off_w1 = pl.off_w0 + (nchunks > 1 ? wbuf : 0);
+            pl.off_m = pl.off_w1 + wbuf;
+            pl.lds = pl.off_m + mbytes;
+            const int64_t pc = per_cu > 0 ? per_cu : per_cu_estimate(t, pl.lds);
+            const int64_t gpk = std::min<int64_t>(pl.mtiles, std::max<int64_t>(1, (kNumCUs * pc + pl.ktiles - 1) / pl.ktiles));
+            pl.grid = gpk * pl.ktiles;
+        }
+    }
     if (pl.lds > kLdsBytes)
         return fail(QCONV_EUNSUPPORTED, "tile %s needs %lld bytes of LDS for this shape (limit %lld)", t.name,
                     (long long)pl.lds, (long long)kLdsBytes);
+    if (pl.grid <= 0 || pl.grid >= (1ll << 31)) return fail(QCONV_EUNSUPPORTED, "grid size out of range");
     if (out) *out = pl;
     return QCONV_OK;
 }
 
 int pick_default(const qconv_desc *d, const qconv_layout_info &li) {
-    // Static heuristic: prefer the largest tile that still gives every CU
-    // work and fits in LDS; the sweep harness measures the alternatives.
+    // Static heuristic: favour 64x64 wave tiles (operand reuse), the pipelined
+    // kernel where it applies, and enough workgroups to cover every CU; the
+    // sweep harness measures the alternatives.
     const TileEntry *tab = tile_table();
     const int nt = tile_table_size();
     int best = -1;
@@ -182,13 +243,14 @@ int pick_default(const qconv_desc *d, const qconv_layout_info &li) {
         if (t.bits != d->bits) continue;
         Plan pl;
         if (plan_tile(d, li, t, &pl) != QCONV_OK) continue;
-        const double wgs = (double)((li.m + t.tile_p - 1) / t.tile_p) * ((d->k + t.tile_k - 1) / t.tile_k);
-        const double util = (double)li.m * d->k /
-                            ((double)((li.m + t.tile_p - 1) / t.tile_p) * t.tile_p *
-                             (double)((d->k + t.tile_k - 1) / t.tile_k) * t.tile_k);
-        const double fill = std::min(1.0, wgs / 512.0);
-        const double reuse = (double)t.tile_p * t.tile_k / (t.tile_p + t.tile_k);
-        const double score = util * fill * reuse * (t.chunk_c <= d->c ? 1.0 : 0.5);
+        const double tiles = (double)pl.mtiles * pl.ktiles;
+        const double util = (double)li.m * d->k / (tiles * t.tile_p * t.tile_k);
+        const double waves = tiles * t.threads / 64.0;
+        const double fill = std::min(1.0, waves / (4.0 * kNumCUs));
+        const double reuse = 2.0 * t.frag_p * t.frag_k / (t.frag_p + t.frag_k);
+        const double pipe = t.variant == QCONV_VARIANT_WIDE ? 1.5 : 1.0;
+        const double chunk = t.chunk_c <= d->c ? 1.0 : 0.5;
+        const double score = util * fill * reuse * pipe * chunk;
         if (score > best_score) {
             best_score = score;
             best = i;
@@ -273,41 +335,30 @@ int qconv_pack(const int8_t *src, void *dst, int32_t n, int32_t c, int32_t h, in
     return QCONV_OK;
 }
 
-int qconv2d(const qconv_desc *d, const void *x, const void *w, const qconv_epilogue *epi, void *y, void *workspace,
-            size_t workspace_bytes, int32_t tile_id, void *stream) {
-    g_err[0] = 0;
-    (void)workspace;
-    qconv_layout_info li;
-    int rc = check_desc(d, &li);
-    if (rc) return rc;
-    rc = check_epilogue(d, epi);
-    if (rc) return rc;
-    if (!x || !w || !y) return fail(QCONV_EINVAL, "x, w and y must be non-NULL");
-    if (!aligned16(x) || !aligned16(w) || !aligned16(y)) return fail(QCONV_EINVAL, "x, w and y must be 16-byte aligned");
-    const bool requant = epi && epi->mode == QCONV_OUT_REQUANT;
-    const int64_t ybytes = requant ? li.y_packed_bytes : li.y_raw_bytes;
-    const uintptr_t y0 = (uintptr_t)y, y1 = y0 + ybytes;
-    if (((uintptr_t)x < y1 && y0 < (uintptr_t)x + li.x_bytes) || ((uintptr_t)w < y1 && y0 < (uintptr_t)w + li.w_bytes))
-        return fail(QCONV_EINVAL, "y overlaps x or w");
-    if ((int64_t)workspace_bytes < li.workspace_bytes)
-        return fail(QCONV_EWORKSPACE, "workspace of %zu bytes, need %lld", workspace_bytes,
-                    (long long)li.workspace_bytes);
+}  // extern "C"
+
+namespace {
+
+int resolve_tile(const qconv_desc *d, const qconv_layout_info &li, int32_t tile_id) {
     if (tile_id == -1) {
         tile_id = pick_default(d, li);
         if (tile_id < 0) return fail(QCONV_EUNSUPPORTED, "no compiled tile fits this shape");
     }
     if (tile_id < 0 || tile_id >= tile_table_size()) return fail(QCONV_EINVAL, "unknown tile %d", tile_id);
-    const TileEntry &te = tile_table()[tile_id];
-    Plan pl;
-    rc = plan_tile(d, li, te.info, &pl);
-    if (rc) return rc;
+    return tile_id;
+}
 
-    ConvArgs a;
+// Bytes of the prepared filters of `tile` for this shape: the int8 image of
+// every (channel tile, chunk) block for wide tiles, the packed KRSC filters
+// themselves otherwise.
+int64_t prepared_bytes(const qconv_desc *d, const qconv_layout_info &li, const qconv_tile_info &t, const Plan &pl) {
+    if (t.variant != QCONV_VARIANT_WIDE) return li.w_bytes;
+    const int64_t nchunks = (d->c + t.chunk_c - 1) / t.chunk_c;
+    return pl.ktiles * nchunks * (t.chunk_c / 16) * pl.pstride_w;
+}
+
+void fill_args(ConvArgs &a, const qconv_desc *d, const qconv_layout_info &li, const TileEntry &te, const Plan &pl) {
     memset(&a, 0, sizeof(a));
-    a.xptr = static_cast<const uint8_t *>(x);
-    a.wptr = static_cast<const uint8_t *>(w);
-    a.yptr = static_cast<uint8_t *>(y);
-    a.mult = requant ? epi->mult : nullptr;
     a.n = d->n; a.h = d->h; a.w = d->w; a.c = d->c; a.k = d->k; a.r = d->r; a.s = d->s;
     a.sh = d->stride_h; a.sw = d->stride_w; a.ph = d->pad_h; a.pw = d->pad_w;
     a.p = li.p; a.q = li.q;
@@ -318,15 +369,25 @@ int qconv2d(const qconv_desc *d, const void *x, const void *w, const qconv_epilo
     a.nchunks = (d->c + te.info.chunk_c - 1) / te.info.chunk_c;
     a.vec16 = (d->c * d->bits) % 128 == 0;
     a.band_rows = (int32_t)pl.rows;
+    a.xbytes = (int32_t)li.x_bytes;
+    a.wbytes = (int32_t)li.w_bytes;
+    a.off_b0 = (int32_t)pl.off_b0;
+    a.off_b1 = (int32_t)pl.off_b1;
+    a.off_w0 = (int32_t)pl.off_w0;
+    a.off_w1 = (int32_t)pl.off_w1;
+    a.off_m = (int32_t)pl.off_m;
     a.pstride_b = (int32_t)pl.pstride_b;
     a.pstride_w = (int32_t)pl.pstride_w;
-    a.ktiles = (d->k + te.info.tile_k - 1) / te.info.tile_k;
-    a.mtiles = (int32_t)((li.m + te.info.tile_p - 1) / te.info.tile_p);
+    a.ktiles = (int32_t)pl.ktiles;
+    a.mtiles = (int32_t)pl.mtiles;
     a.div_pq = make_fastdiv((uint32_t)(li.p * li.q));
     a.div_q = make_fastdiv((uint32_t)li.q);
     a.div_vh = make_fastdiv((uint32_t)a.vh);
     a.div_ncols = make_fastdiv((uint32_t)a.ncols);
     a.div_rs = make_fastdiv((uint32_t)(d->r * d->s));
+    a.div_s = make_fastdiv((uint32_t)d->s);
+    a.x_signed = d->x_signed;
+    a.w_signed = d->w_signed;
     // widening: unsigned nibble -> low half of a byte; signed nibble -> high half (value * 16)
     a.xmask = d->x_signed ? 0xF0F0F0F0u : 0x0F0F0F0Fu;
     a.xsl = d->x_signed ? 4 : 0;
@@ -335,6 +396,74 @@ int qconv2d(const qconv_desc *d, const void *x, const void *w, const qconv_epilo
     a.wsl = d->w_signed ? 4 : 0;
     a.wsr = d->w_signed ? 0 : 4;
     a.acc_shift = d->bits == 4 ? 4 * (d->x_signed + d->w_signed) : 0;
+}
+
+int ensure_lds_attribute(const TileEntry &te, int tile_id, int64_t lds) {
+    if (lds <= 64 * 1024) return QCONV_OK;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return fail(QCONV_EHIP, "hipGetDevice failed");
+    const long long key = (long long)dev * 4096 + tile_id;
+    std::lock_guard<std::mutex> g(g_attr.mu);
+    if (!g_attr.done[key]) {
+        hipError_t e = hipFuncSetAttribute(te.kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
+        if (e != hipSuccess) return fail(QCONV_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
+        g_attr.done[key] = true;
+    }
+    return QCONV_OK;
+}
+
+// The convolution; w is packed KRSC filters (prepared == false) or the
+// prepared filters of tile_id (prepared == true, w_bytes_given bytes).
+int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, size_t w_bytes_given,
+             const qconv_epilogue *epi, void *y, void *workspace, size_t workspace_bytes, int32_t tile_id,
+             void *stream) {
+    (void)workspace;
+    qconv_layout_info li;
+    int rc = check_desc(d, &li);
+    if (rc) return rc;
+    rc = check_epilogue(d, epi);
+    if (rc) return rc;
+    if (!x || !w || !y) return fail(QCONV_EINVAL, "x, w and y must be non-NULL");
+    if (!aligned16(x) || !aligned16(w) || !aligned16(y)) return fail(QCONV_EINVAL, "x, w and y must be 16-byte aligned");
+    if ((int64_t)workspace_bytes < li.workspace_bytes)
+        return fail(QCONV_EWORKSPACE, "workspace of %zu bytes, need %lld", workspace_bytes,
+                    (long long)li.workspace_bytes);
+    rc = resolve_tile(d, li, tile_id);
+    if (rc < 0) return rc;
+    tile_id = rc;
+    const TileEntry &te = tile_table()[tile_id];
+    Plan pl;
+    rc = plan_tile(d, li, te.info, &pl);
+    if (rc) return rc;
+    const int64_t wb = prepared ? prepared_bytes(d, li, te.info, pl) : li.w_bytes;
+    if (prepared && (int64_t)w_bytes_given < wb)
+        return fail(QCONV_EINVAL, "prepared filters of %zu bytes, tile %s needs %lld", w_bytes_given, te.info.name,
+                    (long long)wb);
+    if (wb >= kMaxBytes) return fail(QCONV_EUNSUPPORTED, "filter image must stay below 2 GiB");
+    const bool requant = epi && epi->mode == QCONV_OUT_REQUANT;
+    const int64_t ybytes = requant ? li.y_packed_bytes : li.y_raw_bytes;
+    const uintptr_t y0 = (uintptr_t)y, y1 = y0 + ybytes;
+    if (((uintptr_t)x < y1 && y0 < (uintptr_t)x + li.x_bytes) || ((uintptr_t)w < y1 && y0 < (uintptr_t)w + wb))
+        return fail(QCONV_EINVAL, "y overlaps x or w");
+    if (te.info.variant == QCONV_VARIANT_WIDE && pl.off_b1 != pl.off_b0) {
+        // persistent grid: size it by the occupancy the runtime reports for this kernel
+        rc = ensure_lds_attribute(te, tile_id, pl.lds);
+        if (rc) return rc;
+        int occ = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, te.kernel, te.info.threads, (size_t)pl.lds) == hipSuccess &&
+            occ > 0) {
+            rc = plan_tile(d, li, te.info, &pl, occ);
+            if (rc) return rc;
+        }
+    }
+    ConvArgs a;
+    fill_args(a, d, li, te, pl);
+    a.xptr = static_cast<const uint8_t *>(x);
+    a.wptr = static_cast<const uint8_t *>(w);
+    a.yptr = static_cast<uint8_t *>(y);
+    a.mult = requant ? epi->mult : nullptr;
+    a.w_image = (prepared && te.info.variant == QCONV_VARIANT_WIDE) ? 1 : 0;
+    if (a.w_image) a.wbytes = (int32_t)wb;
     a.mode = requant ? QCONV_OUT_REQUANT : QCONV_OUT_RAW_I32;
     if (requant) {
         a.shift = epi->shift;
@@ -342,23 +471,76 @@ int qconv2d(const qconv_desc *d, const void *x, const void *w, const qconv_epilo
         a.hi = epi->clamp_hi;
         if (a.lo > a.hi) a.lo = a.hi;   // relu with an all-negative clamp range: every value is clamp_hi
     }
-    const long long blocks = (long long)a.mtiles * a.ktiles;
-    if (blocks <= 0 || blocks >= (1ll << 31)) return fail(QCONV_EUNSUPPORTED, "grid size out of range");
-
-    if (pl.lds > 64 * 1024) {
-        int dev = 0;
-        if (hipGetDevice(&dev) != hipSuccess) return fail(QCONV_EHIP, "hipGetDevice failed");
-        const long long key = (long long)dev * 4096 + tile_id;
-        std::lock_guard<std::mutex> g(g_attr.mu);
-        if (!g_attr.done[key]) {
-            hipError_t e = hipFuncSetAttribute(te.kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
-            if (e != hipSuccess) return fail(QCONV_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
-            g_attr.done[key] = true;
-        }
-    }
-    hipError_t e = te.launch(a, dim3((unsigned)blocks), (size_t)pl.lds, (hipStream_t)stream);
+    rc = ensure_lds_attribute(te, tile_id, pl.lds);
+    if (rc) return rc;
+    hipError_t e = te.launch(a, dim3((unsigned)pl.grid), (size_t)pl.lds, (hipStream_t)stream);
     if (e != hipSuccess) return fail(QCONV_EHIP, "conv launch (%s): %s", te.info.name, hipGetErrorString(e));
     return QCONV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int qconv2d(const qconv_desc *d, const void *x, const void *w, const qconv_epilogue *epi, void *y, void *workspace,
+            size_t workspace_bytes, int32_t tile_id, void *stream) {
+    g_err[0] = 0;
+    return run_conv(d, x, w, false, 0, epi, y, workspace, workspace_bytes, tile_id, stream);
+}
+
+int qconv_prepared_filter_bytes(const qconv_desc *d, int32_t tile_id, size_t *bytes) {
+    g_err[0] = 0;
+    qconv_layout_info li;
+    int rc = check_desc(d, &li);
+    if (rc) return rc;
+    if (!bytes) return fail(QCONV_EINVAL, "bytes must be non-NULL");
+    rc = resolve_tile(d, li, tile_id);
+    if (rc < 0) return rc;
+    Plan pl;
+    const TileEntry &te = tile_table()[rc];
+    int prc = plan_tile(d, li, te.info, &pl);
+    if (prc) return prc;
+    *bytes = (size_t)prepared_bytes(d, li, te.info, pl);
+    return QCONV_OK;
+}
+
+int qconv_prepare_filters(const qconv_desc *d, const void *w_packed, int32_t tile_id, void *w_prepared,
+                          size_t bytes, void *stream) {
+    g_err[0] = 0;
+    qconv_layout_info li;
+    int rc = check_desc(d, &li);
+    if (rc) return rc;
+    if (!w_packed || !w_prepared) return fail(QCONV_EINVAL, "filter pointers must be non-NULL");
+    if (!aligned16(w_packed) || !aligned16(w_prepared)) return fail(QCONV_EINVAL, "filters must be 16-byte aligned");
+    rc = resolve_tile(d, li, tile_id);
+    if (rc < 0) return rc;
+    tile_id = rc;
+    const TileEntry &te = tile_table()[tile_id];
+    Plan pl;
+    rc = plan_tile(d, li, te.info, &pl);
+    if (rc) return rc;
+    const int64_t need = prepared_bytes(d, li, te.info, pl);
+    if ((int64_t)bytes < need)
+        return fail(QCONV_EINVAL, "prepared filter buffer of %zu bytes, need %lld", bytes, (long long)need);
+    const uintptr_t s0 = (uintptr_t)w_packed, s1 = s0 + li.w_bytes, d0 = (uintptr_t)w_prepared, d1 = d0 + need;
+    if (s0 < d1 && d0 < s1) return fail(QCONV_EINVAL, "packed and prepared filters overlap");
+    hipError_t e;
+    if (te.info.variant == QCONV_VARIANT_WIDE) {
+        ConvArgs a;
+        fill_args(a, d, li, te, pl);
+        a.wptr = static_cast<const uint8_t *>(w_packed);
+        e = te.prep(a, static_cast<uint8_t *>(w_prepared), need / 16, (hipStream_t)stream);
+    } else {
+        e = hipMemcpyAsync(w_prepared, w_packed, (size_t)li.w_bytes, hipMemcpyDeviceToDevice, (hipStream_t)stream);
+    }
+    if (e != hipSuccess) return fail(QCONV_EHIP, "prepare filters (%s): %s", te.info.name, hipGetErrorString(e));
+    return QCONV_OK;
+}
+
+int qconv2d_prepared(const qconv_desc *d, const void *x, const void *w_prepared, size_t w_prepared_bytes,
+                     const qconv_epilogue *epi, void *y, int32_t tile_id, void *stream) {
+    g_err[0] = 0;
+    return run_conv(d, x, w_prepared, true, w_prepared_bytes, epi, y, nullptr, 0, tile_id, stream);
 }
 
 // Host-only consistency checks of the helpers the kernels rely on; returns 0

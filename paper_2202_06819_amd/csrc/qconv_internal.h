@@ -50,11 +50,18 @@ struct ConvArgs {
     int32_t nchunks;        // channel chunks of the main loop
     int32_t vec16;          // 1: every 16-byte vector of a pixel is whole (C*bits % 128 == 0)
     int32_t band_rows;      // padded rows the band buffer holds
+    int32_t xbytes;         // packed activation bytes (buffer-load range)
+    int32_t wbytes;         // packed filter bytes (buffer-load range)
+    int32_t off_b0, off_b1; // LDS byte offsets of the two band buffers (pipelined kernel)
+    int32_t off_w0, off_w1; // LDS byte offsets of the two filter buffers (equal when one chunk)
+    int32_t off_m;          // LDS byte offset of the workgroup's multipliers (wide kernel)
+    int32_t w_image;        // 1: wptr is a prepared filter image (wide kernel), 0: packed KRSC filters
     int32_t pstride_b;      // bytes per granule plane of the band buffer
     int32_t pstride_w;      // bytes per granule plane of the filter buffer
     int32_t ktiles;         // workgroup tiles along output channels
     int32_t mtiles;         // workgroup tiles along output pixels
-    FastDiv div_pq, div_q, div_vh, div_ncols, div_rs;
+    FastDiv div_pq, div_q, div_vh, div_ncols, div_rs, div_s;
+    int32_t x_signed, w_signed;
     // operand widening of 4-bit nibbles to int8 lanes (see widen4)
     uint32_t xmask, wmask;
     int32_t xsl, xsr, wsl, wsr;
@@ -66,11 +73,13 @@ struct ConvArgs {
 };
 
 using ConvLauncher = hipError_t (*)(const ConvArgs &, dim3 grid, size_t lds_bytes, hipStream_t);
+using PrepLauncher = hipError_t (*)(const ConvArgs &, uint8_t *image, int64_t elems, hipStream_t);
 
 struct TileEntry {
     qconv_tile_info info;
     ConvLauncher launch;
     const void *kernel;     // for hipFuncSetAttribute
+    PrepLauncher prep;      // builds the filter image (wide tiles), else null
 };
 
 // Defined in qconv_conv.hip.

@@ -29,15 +29,21 @@ class LayerSpec:
 
 
 class Chain:
+    """Layers on one stream; filters are prepared once for each layer's tile."""
+
     def __init__(self, layers: list[LayerSpec], x_packed: torch.Tensor, stream=None):
         self.layers = layers
         self.x = x_packed
         self.calls = []
+        self.filters = []
         outs = []
         for L in layers:
             inp = self.x if L.src < 0 else outs[L.src]
-            call = qconv.Conv2dCall(L.desc, inp, L.w_packed, requant=True, mult=L.mult, shift=L.shift,
-                                    relu=L.relu, clamp=L.clamp, tile=L.tile, stream=stream)
+            tile = qconv.default_tile(L.desc) if L.tile == -1 else L.tile
+            wprep = qconv.prepare_filters(L.desc, L.w_packed, tile)
+            self.filters.append(wprep)
+            call = qconv.Conv2dCall(L.desc, inp, wprep, requant=True, mult=L.mult, shift=L.shift,
+                                    relu=L.relu, clamp=L.clamp, tile=tile, stream=stream, prepared=True)
             outs.append(call.out)
             self.calls.append(call)
         self.outputs = outs
@@ -56,7 +62,7 @@ class Chain:
             # calls marshal the stream at construction: rebuild them for the capture stream
             calls = [qconv.Conv2dCall(c.desc, c.x, c.w, requant=True, mult=c.mult, shift=c.epi.shift,
                                       relu=bool(c.epi.relu), clamp=(c.epi.clamp_lo, c.epi.clamp_hi), out=c.out,
-                                      tile=c.tile, stream=s) for c in self.calls]
+                                      tile=c.tile, stream=s, prepared=c.prepared) for c in self.calls]
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g, stream=s):
                 for c in calls:

@@ -46,7 +46,7 @@ class QConvEpilogue(ctypes.Structure):
 
 class QConvTileInfo(ctypes.Structure):
     _fields_ = [(f, _i32) for f in ("id", "bits", "waves_p", "waves_k", "frag_p", "frag_k", "chunk_c", "tile_p",
-                                    "tile_k", "threads")] + [("name", ctypes.c_char * 64)]
+                                    "tile_k", "threads", "variant", "x_signed", "w_signed")] + [("name", ctypes.c_char * 64)]
 
 
 class QConvError(RuntimeError):
@@ -81,8 +81,12 @@ def lib() -> ctypes.CDLL:
         L.qconv_last_error.argtypes = []
         L.qconv_last_error.restype = ctypes.c_char_p
         L.qconv_selftest.argtypes = []
+        L.qconv_prepared_filter_bytes.argtypes = [P(QConvDesc), _i32, P(ctypes.c_size_t)]
+        L.qconv_prepare_filters.argtypes = [P(QConvDesc), _vp, _i32, _vp, ctypes.c_size_t, _vp]
+        L.qconv2d_prepared.argtypes = [P(QConvDesc), _vp, _vp, ctypes.c_size_t, P(QConvEpilogue), _vp, _i32, _vp]
         for f in ("qconv_layout", "qconv_pack", "qconv2d", "qconv_tile_count", "qconv_tile_get", "qconv_tile_check",
-                  "qconv_default_tile", "qconv_selftest"):
+                  "qconv_default_tile", "qconv_selftest", "qconv_prepared_filter_bytes", "qconv_prepare_filters",
+                  "qconv2d_prepared"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
         return L
@@ -132,6 +136,29 @@ def selftest() -> int:
     return lib().qconv_selftest()
 
 
+def prepared_filter_bytes(d: dict, tile: int = -1) -> int:
+    """Bytes of the prepared filters of `tile` for this shape (host only)."""
+    n = ctypes.c_size_t(0)
+    _check(lib().qconv_prepared_filter_bytes(ctypes.byref(make_desc(d)), int(tile), ctypes.byref(n)),
+           "qconv_prepared_filter_bytes")
+    return int(n.value)
+
+
+def prepare_filters(d: dict, w_packed: torch.Tensor, tile: int = -1, out: torch.Tensor | None = None,
+                    stream=None) -> torch.Tensor:
+    """Packed KRSC filters -> the layout `tile` stages directly (done once, offline)."""
+    desc = make_desc(d)
+    nbytes = prepared_filter_bytes(d, tile)
+    info = layout(d)
+    if out is None:
+        out = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=w_packed.device)
+    rc = lib().qconv_prepare_filters(ctypes.byref(desc), _dev_ptr(w_packed, "w_packed", info["w_bytes"]), int(tile),
+                                     _dev_ptr(out, "w_prepared", nbytes), out.numel() * out.element_size(),
+                                     _vp(_stream(stream)))
+    _check(rc, "qconv_prepare_filters")
+    return out
+
+
 def _stream(stream) -> int:
     if stream is None:
         return torch.cuda.current_stream().cuda_stream
@@ -172,11 +199,13 @@ def pack(src: torch.Tensor, bits: int, is_signed: bool, out: torch.Tensor | None
 
 def conv2d(d: dict, x: torch.Tensor, w: torch.Tensor, *, requant: bool = False, mult: torch.Tensor | None = None,
            shift: int = 20, relu: bool = True, clamp: tuple = (0, 15), out: torch.Tensor | None = None,
-           tile: int = -1, workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+           tile: int = -1, workspace: torch.Tensor | None = None, stream=None,
+           prepared: bool = False) -> torch.Tensor:
     """The convolution with its fused epilogue; returns the output tensor.
 
     Raw mode: int32 N x P x Q x K accumulators.  Requant mode: the packed
-    b-bit output (the next layer's input layout).
+    b-bit output (the next layer's input layout).  With ``prepared`` the
+    filters `w` come from :func:`prepare_filters` for the same `tile`.
     """
     desc = make_desc(d)
     info = layout(d)
@@ -198,6 +227,13 @@ def conv2d(d: dict, x: torch.Tensor, w: torch.Tensor, *, requant: bool = False, 
     ws_ptr, ws_bytes = (None, 0) if workspace is None else (_dev_ptr(workspace, "workspace"),
                                                            workspace.numel() * workspace.element_size())
     y_bytes = info["y_packed_bytes"] if requant else info["y_raw_bytes"]
+    if prepared:
+        wb = prepared_filter_bytes(d, tile)
+        rc = lib().qconv2d_prepared(ctypes.byref(desc), _dev_ptr(x, "x", info["x_bytes"]), _dev_ptr(w, "w", wb),
+                                    w.numel() * w.element_size(), ctypes.byref(epi), _dev_ptr(out, "y", y_bytes),
+                                    int(tile), _vp(_stream(stream)))
+        _check(rc, "qconv2d_prepared")
+        return out
     rc = lib().qconv2d(ctypes.byref(desc), _dev_ptr(x, "x", info["x_bytes"]), _dev_ptr(w, "w", info["w_bytes"]),
                        ctypes.byref(epi), _dev_ptr(out, "y", y_bytes), ws_ptr, ws_bytes, int(tile),
                        _vp(_stream(stream)))
@@ -232,7 +268,7 @@ class Conv2dCall:
 
     def __init__(self, d: dict, x: torch.Tensor, w: torch.Tensor, *, requant: bool = False,
                  mult: torch.Tensor | None = None, shift: int = 20, relu: bool = True, clamp: tuple = (0, 15),
-                 out: torch.Tensor | None = None, tile: int = -1, stream=None):
+                 out: torch.Tensor | None = None, tile: int = -1, stream=None, prepared: bool = False):
         self.desc = make_desc(d)
         info = layout(d)
         bits = self.desc.bits
@@ -252,9 +288,18 @@ class Conv2dCall:
         y_bytes = info["y_packed_bytes"] if requant else info["y_raw_bytes"]
         self.x, self.w, self.mult, self.out, self.info = x, w, mult, out, info
         self.tile = default_tile(d) if tile == -1 else int(tile)
-        self._args = (ctypes.byref(self.desc), _dev_ptr(x, "x", info["x_bytes"]), _dev_ptr(w, "w", info["w_bytes"]),
-                      ctypes.byref(self.epi), _dev_ptr(out, "y", y_bytes), None, 0, self.tile, _vp(_stream(stream)))
-        self._fn = lib().qconv2d
+        self.prepared = prepared
+        if prepared:
+            wb = prepared_filter_bytes(d, self.tile)
+            self._args = (ctypes.byref(self.desc), _dev_ptr(x, "x", info["x_bytes"]), _dev_ptr(w, "w", wb),
+                          w.numel() * w.element_size(), ctypes.byref(self.epi), _dev_ptr(out, "y", y_bytes),
+                          self.tile, _vp(_stream(stream)))
+            self._fn = lib().qconv2d_prepared
+        else:
+            self._args = (ctypes.byref(self.desc), _dev_ptr(x, "x", info["x_bytes"]), _dev_ptr(w, "w", info["w_bytes"]),
+                          ctypes.byref(self.epi), _dev_ptr(out, "y", y_bytes), None, 0, self.tile,
+                          _vp(_stream(stream)))
+            self._fn = lib().qconv2d
 
     def __call__(self) -> torch.Tensor:
         _check(self._fn(*self._args), "qconv2d")

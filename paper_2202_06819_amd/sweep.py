@@ -1,0 +1,166 @@
+"""Tile-configuration sweep: the schedule search space of Sec. 4.1, measured
+exhaustively on the GPU (the "Exhaustive" row of Table 1, restated for the
+compiled gfx950 tile space).
+
+For each convolution shape and every compiled tile that can run it:
+  1. run it and check that its output bytes equal those of a reference tile
+     (integer sums have one value, so every tile must agree);
+  2. time it with HIP events over back-to-back launches (median of rounds);
+  3. append one JSON line to the results file (the run is resumable: pairs
+     already in the file are skipped).
+The fastest tile per shape goes into the tuned table that qconv2d callers use
+when they pass tile -1 through :func:`tuned_tile`.
+
+    python -m paper_2202_06819_amd.sweep --workload 4 --out sweep_w4.jsonl
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+
+import torch
+
+from . import qconv
+
+TUNED_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "tuned_tiles.json")
+INT8_PEAK_TOPS = 5000.0
+
+
+def shape_key(d: dict, requant: bool = True) -> str:
+    return ("n{n}_h{h}_w{w}_c{c}_k{k}_r{r}_s{s}_st{stride_h}x{stride_w}_p{pad_h}x{pad_w}_b{bits}_xs{x_signed}"
+            "_ws{w_signed}".format(**d) + ("_rq" if requant else "_raw"))
+
+
+_tuned_cache = None
+
+
+def tuned_table() -> dict:
+    global _tuned_cache
+    if _tuned_cache is None:
+        _tuned_cache = json.load(open(TUNED_PATH)) if os.path.exists(TUNED_PATH) else {}
+    return _tuned_cache
+
+
+def tuned_tile(d: dict, requant: bool = True) -> int:
+    """The swept best tile id for this shape, else the library's built-in choice (-1)."""
+    name = tuned_table().get(shape_key(d, requant))
+    if name:
+        for t in qconv.tiles():
+            if t["name"] == name and qconv.tile_status(d, t["id"]) == 0:
+                return t["id"]
+    return -1
+
+
+def _time(call, reps: int, rounds: int) -> float:
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    res = []
+    for _ in range(rounds):
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            call()
+        e1.record()
+        torch.cuda.synchronize()
+        res.append(e0.elapsed_time(e1) * 1000.0 / reps)
+    return statistics.median(res)
+
+
+def sweep_layer(d: dict, x: torch.Tensor, w: torch.Tensor, mult: torch.Tensor | None, *, shift=20, relu=True,
+                clamp=(0, 15), reps=100, rounds=5, done=frozenset(), log=print) -> list[dict]:
+    """Measure every valid tile on one shape; returns result rows."""
+    requant = mult is not None
+    key = shape_key(d, requant)
+    info = qconv.layout(d)
+    ops = 2 * info["macs"]
+    default = qconv.default_tile(d)
+    ref_call = qconv.Conv2dCall(d, x, w, requant=requant, mult=mult, shift=shift, relu=relu, clamp=clamp,
+                                tile=default)
+    ref = ref_call().clone()   # packed filters, default tile
+    rows = []
+    for t in qconv.tiles():
+        if qconv.tile_status(d, t["id"]) != 0 or (key, t["name"]) in done:
+            continue
+        wprep = qconv.prepare_filters(d, w, t["id"])   # offline filter layout for this tile
+        call = qconv.Conv2dCall(d, x, wprep, requant=requant, mult=mult, shift=shift, relu=relu, clamp=clamp,
+                                tile=t["id"], prepared=True)
+        out = call()
+        torch.cuda.synchronize()
+        same = bool(torch.equal(out, ref))
+        us = _time(call, reps, rounds)
+        tops = ops / (us * 1e-6) / 1e12
+        row = {"shape": key, "tile": t["name"], "tile_id": t["id"], "default": t["id"] == default,
+               "us": round(us, 3), "tops": round(tops, 2), "pct_int8_peak": round(100 * tops / INT8_PEAK_TOPS, 3),
+               "identical": same}
+        rows.append(row)
+        log(json.dumps(row))
+        if not same:
+            raise RuntimeError(f"tile {t['name']} output differs from tile {default} on {key}")
+    return rows
+
+
+def best_per_shape(rows: list[dict]) -> dict:
+    best = {}
+    for r in rows:
+        if r["shape"] not in best or r["us"] < best[r["shape"]]["us"]:
+            best[r["shape"]] = r
+    return best
+
+
+def main(argv=None) -> int:
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    import qconv_inputs as qi
+
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--workload", type=int, action="append", required=True, help="workload id (repeatable)")
+    ap.add_argument("--out", required=True, help="JSONL results file (appended; resumable)")
+    ap.add_argument("--reps", type=int, default=100)
+    ap.add_argument("--rounds", type=int, default=5)
+    ap.add_argument("--write-tuned", action="store_true", help="merge the best tiles into tuned_tiles.json")
+    args = ap.parse_args(argv)
+
+    done = set()
+    rows = []
+    if os.path.exists(args.out):
+        for line in open(args.out):
+            if line.strip():
+                r = json.loads(line)
+                rows.append(r)
+                done.add((r["shape"], r["tile"]))
+    dev = torch.device("cuda:0")
+    with open(args.out, "a") as fh:
+        def log(s):
+            print(s, flush=True)
+            fh.write(s + "\n")
+            fh.flush()
+        for cfg in args.workload:
+            layers = qi.CONFIGS[cfg]()
+            if cfg in (2, 3):
+                layers = qi.distinct(layers)
+            for lid, L in enumerate(layers):
+                t = qi.layer_tensors(cfg, lid, L)
+                x = qconv.pack(torch.from_numpy(t["x"]).to(dev), L.bits, L.x_signed)
+                w = qconv.pack(torch.from_numpy(t["w"]).to(dev), L.bits, L.w_signed)
+                e = L.epilogue
+                mult = torch.from_numpy(t["mult"]).to(dev) if e else None
+                print(f"# workload {cfg} layer {L.name}", flush=True)
+                rows += sweep_layer(L.desc(), x, w, mult, shift=e.shift if e else 20, relu=e.relu if e else False,
+                                    clamp=(e.lo, e.hi) if e else (0, 15), reps=args.reps, rounds=args.rounds,
+                                    done=frozenset(done), log=log)
+    best = best_per_shape(rows)
+    for key, r in sorted(best.items()):
+        dflt = [x for x in rows if x["shape"] == key and x["default"]]
+        speed = f" ({dflt[0]['us'] / r['us']:.2f}x vs default {dflt[0]['tile']})" if dflt else ""
+        print(f"best {key}: {r['tile']} {r['us']} us {r['tops']} TOP/s{speed}", flush=True)
+    if args.write_tuned:
+        table = json.load(open(TUNED_PATH)) if os.path.exists(TUNED_PATH) else {}
+        table.update({k: r["tile"] for k, r in best.items()})
+        with open(TUNED_PATH, "w") as fh:
+            json.dump(table, fh, indent=1, sort_keys=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -49,8 +49,9 @@ def as_u32(a) -> np.ndarray:
 
 
 def gpu_layer(L: qi.Layer, t: dict, *, requant: bool, tile: int = -1, shift=None, relu=None, lo=None, hi=None,
-              x_packed_dev=None):
-    """Pack x and w on the GPU, run the conv; returns host numpy arrays."""
+              x_packed_dev=None, prepared: bool = False):
+    """Pack x and w on the GPU, run the conv (from packed filters, or from
+    filters prepared for `tile`); returns host numpy arrays."""
     import torch
     from paper_2202_06819_amd import qconv
 
@@ -68,7 +69,12 @@ def gpu_layer(L: qi.Layer, t: dict, *, requant: bool, tile: int = -1, shift=None
         kw = dict(requant=True, mult=torch.from_numpy(t["mult"]).to(dev), shift=e.shift if shift is None else shift,
                   relu=e.relu if relu is None else relu,
                   clamp=(e.lo if lo is None else lo, e.hi if hi is None else hi))
-    y = qconv.conv2d(L.desc(), xp, wp, tile=tile, **kw)
+    if prepared:
+        tile = qconv.default_tile(L.desc()) if tile == -1 else tile
+        wprep = qconv.prepare_filters(L.desc(), wp, tile)
+        y = qconv.conv2d(L.desc(), xp, wprep, tile=tile, prepared=True, **kw)
+    else:
+        y = qconv.conv2d(L.desc(), xp, wp, tile=tile, **kw)
     torch.cuda.synchronize()
     return {"x_packed": xp.cpu().numpy(), "w_packed": wp.cpu().numpy(), "y": y.cpu().numpy(), "y_dev": y}
 

@@ -184,3 +184,51 @@ def test_every_workload_layer_has_a_tile(q):
         for L in make():
             tid = q.default_tile(L.desc())
             assert q.tile_status(L.desc(), tid) == 0
+
+
+def test_prepared_filter_bytes(q):
+    d = D()
+    info = q.layout(d)
+    for t in q.tiles():
+        if q.tile_status(d, t["id"]) != 0:
+            continue
+        n = q.prepared_filter_bytes(d, t["id"])
+        if t["variant"] == 2:       # wide tiles: padded per-(K tile, chunk) images
+            assert n >= info["gemm_k"] * d["k"]      # at least one int8 byte per filter weight
+            assert n % 1024 == 0
+        else:
+            assert n == info["w_bytes"]
+    assert q.prepared_filter_bytes(d, -1) == q.prepared_filter_bytes(d, q.default_tile(d))
+    with pytest.raises(q.QConvError):
+        q.prepared_filter_bytes(d, 10 ** 6)
+
+
+def test_prepare_filters_errors(q):
+    L = q.lib()
+    d = D()
+    desc = q.make_desc(d)
+    tid = q.default_tile(d)
+    need = q.prepared_filter_bytes(d, tid)
+    ref = ctypes.byref(desc)
+    assert L.qconv_prepare_filters(ref, 0, tid, 1 << 34, need, None) == -1            # NULL source
+    assert L.qconv_prepare_filters(ref, 1 << 33, tid, 0, need, None) == -1            # NULL destination
+    assert L.qconv_prepare_filters(ref, (1 << 33) + 4, tid, 1 << 34, need, None) == -1  # misaligned
+    assert L.qconv_prepare_filters(ref, 1 << 33, tid, 1 << 34, need - 16, None) == -1   # too small
+    assert L.qconv_prepare_filters(ref, 1 << 33, tid, (1 << 33) + 64, need, None) == -1  # overlap
+    assert L.qconv_prepare_filters(ref, 1 << 33, 10 ** 6, 1 << 34, need, None) == -1    # unknown tile
+    assert L.qconv_prepare_filters(None, 1 << 33, tid, 1 << 34, need, None) == -1
+
+
+def test_conv_prepared_errors(q):
+    L = q.lib()
+    d = D()
+    desc = q.make_desc(d)
+    tid = q.default_tile(d)
+    need = q.prepared_filter_bytes(d, tid)
+    ref = ctypes.byref(desc)
+    ok_epi = _epi(q)
+    # prepared buffer smaller than the tile's layout
+    assert L.qconv2d_prepared(ref, 1 << 32, 1 << 33, need - 16, ctypes.byref(ok_epi), 1 << 34, tid, None) == -1
+    assert L.qconv2d_prepared(ref, 0, 1 << 33, need, ctypes.byref(ok_epi), 1 << 34, tid, None) == -1
+    assert L.qconv2d_prepared(ref, 1 << 32, 1 << 33, need, ctypes.byref(_epi(q, shift=0)), 1 << 34, tid, None) == -1
+    assert L.qconv2d_prepared(None, 1 << 32, 1 << 33, need, None, 1 << 34, tid, None) == -1

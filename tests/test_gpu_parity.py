@@ -77,6 +77,8 @@ def test_config0_raw_every_tile():
         assert_same(got["x_packed"], ref["x_packed"], "x packed")
         assert_same(got["w_packed"], ref["w_packed"], "w packed")
         assert_same(got["y"], ref["acc"], f"raw acc tile {tid}")
+        announce(f"config0 raw tile {tid} prepared filters")
+        assert_same(gpu_layer(L, t, requant=False, tile=tid, prepared=True)["y"], ref["acc"], f"prepared tile {tid}")
 
 
 def test_config1_requant_every_tile():
@@ -87,6 +89,9 @@ def test_config1_requant_every_tile():
         announce(f"config1 requant tile {tid}")
         got = gpu_layer(L, t, requant=True, tile=tid)
         assert_same(got["y"], ref["y_packed"], f"requant tile {tid}")
+        announce(f"config1 requant tile {tid} prepared filters")
+        got = gpu_layer(L, t, requant=True, tile=tid, prepared=True)
+        assert_same(got["y"], ref["y_packed"], f"requant tile {tid} prepared")
 
 
 def test_config1_raw_default_tile():
@@ -141,6 +146,9 @@ def test_random_shape(seed):
         assert_same(gpu_layer(L, t, requant=False, tile=tid)["y"], ref_raw["acc"], f"raw tile {tid}")
         announce(f"random seed={seed} tile={tid} requant shift={sh}")
         assert_same(gpu_layer(L, t, requant=True, tile=tid, shift=sh)["y"], ref_req["y_packed"], f"requant tile {tid}")
+        announce(f"random seed={seed} tile={tid} requant shift={sh} prepared filters")
+        assert_same(gpu_layer(L, t, requant=True, tile=tid, shift=sh, prepared=True)["y"], ref_req["y_packed"],
+                    f"requant tile {tid} prepared")
 
 
 # ----------------------------------------------------------------- epilogue stress
