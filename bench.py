@@ -18,6 +18,8 @@ Prints ONE JSON line.  `value` = effective TOP/s of the step
 from __future__ import annotations
 
 import argparse
+import glob
+import hashlib
 import json
 import os
 import sys
@@ -33,6 +35,55 @@ HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, 8 TB/s
 
 def log(msg: str) -> None:
     print(msg, file=sys.stderr, flush=True)
+
+
+KERNEL_SOURCES = ("qconv_conv.hip", "qconv_device.h", "qconv_internal.h", "qconv_host.cpp", "qconv_pack.hip")
+
+
+def kernel_digest(tile_name: str) -> str:
+    """Digest of the kernel sources and the tile: HBM traffic counters taken
+    for another digest describe another kernel and are not reported."""
+    h = hashlib.sha256(tile_name.encode())
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2202_06819_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str, tile_name: str):
+    """HBM bytes per launch of the conv kernel from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE summary of this workload (each counter divided by
+    what it reads per byte of a plain copy kernel), or None when there is no
+    summary for the current kernel sources and tile."""
+    digest = kernel_digest(tile_name)
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*_traffic.md"))):
+        kv = {}
+        for line in open(path):
+            if line.startswith("- ") and ": " in line:
+                k, v = line[2:].split(": ", 1)
+                kv[k.strip()] = v.strip().strip("`")
+        if kv.get("workload") == workload and kv.get("kernel_digest") == digest:
+            try:
+                return int(float(kv["hbm_bytes_per_launch"]))
+            except (KeyError, ValueError):
+                return None
+    return None
+
+
+def copy_calibration(mib: int, reps: int) -> int:
+    """A plain one-to-one copy kernel over `mib` MiB of int32 (read once,
+    written once): the reference that scales FETCH_SIZE / WRITE_SIZE to bytes."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.arange(n, dtype=torch.int32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        torch.bitwise_not(src, out=dst)
+    torch.cuda.synchronize()
+    ok = bool(torch.equal(torch.bitwise_not(dst), src))
+    print(json.dumps({"copy_calibration": {"bytes_read": 4 * n, "bytes_written": 4 * n, "reps": reps,
+                                           "kernel": "bitwise_not int32", "verified": ok}}), flush=True)
+    return 0 if ok else 1
 
 
 def time_loop(fn, reps: int) -> float:
@@ -152,12 +203,17 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--tile", type=int, default=-1)
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain copy kernel over MIB MiB (counter calibration) and exit")
     args = ap.parse_args()
 
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the quantised convolution path has no multi-GPU mode "
               f"(--gpus {args.gpus} requested).", file=sys.stderr)
         return 2
+
+    if args.copy_calibration:
+        return copy_calibration(args.copy_calibration, max(1, min(args.steps, 50)))
 
     import torch
     import qconv_inputs as qi
@@ -204,10 +260,18 @@ def main() -> int:
     pack_us = time_loop(pack, args.steps)
     conv_tops = L.ops / (conv_us * 1e-6) / 1e12
     pack_bytes = L.n * L.c * L.h * L.w + L.n * L.h * L.w * L.c // 2
+    p_out = (L.h + 2 * L.pad - L.r) // L.stride + 1
+    q_out = (L.w + 2 * L.pad - L.s) // L.stride + 1
+    conv_bytes = (L.n * L.h * L.w * L.c * L.bits // 8 + L.k * L.r * L.s * L.c * L.bits // 8
+                  + L.n * p_out * q_out * L.k * L.bits // 8 + 4 * L.k)
     pack_gbs = pack_bytes / (pack_us * 1e-6) / 1e9
     log(f"conv kernel {conv_us:.2f} us = {conv_tops:.1f} TOP/s ({100 * conv_tops / INT8_PEAK_TOPS:.1f}% of int8 peak); "
         f"pack kernel {pack_us:.2f} us = {pack_gbs:.0f} GB/s")
 
+    tile_name = qconv.tiles()[conv.tile]["name"]
+    workload = (f"conv2d n{L.n} {L.h}x{L.w} {L.c}->{L.k} {L.r}x{L.s} stride {L.stride} pad {L.pad}, "
+                f"{L.bits}-bit, fused requant+repack")
+    traffic = measured_traffic(workload, tile_name)
     result = {
         "metric": METRIC,
         "value": round(value, 3),
@@ -221,13 +285,14 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "int4",
         "data": "synthetic",
-        "config": {"workload": "resnet50-stage2 3x3 conv, 4-bit, fused requant (relayout+pack then conv)",
+        "config": {"workload": workload, "step": "qconv_pack (int8 NCHW -> packed 4-bit NHWC) + qconv2d",
                    "n": L.n, "h": L.h, "w": L.w, "c": L.c, "k": L.k, "r": L.r, "s": L.s, "stride": L.stride,
-                   "pad": L.pad, "bits": L.bits, "ops_per_step": L.ops, "tile": qconv.tiles()[conv.tile]["name"]},
+                   "pad": L.pad, "bits": L.bits, "ops_per_step": L.ops, "tile": tile_name},
         "roofline": {"bound": "mfma", "achieved": round(conv_tops, 3), "peak": INT8_PEAK_TOPS, "unit": "TOP/s",
-                     "frac": round(conv_tops / INT8_PEAK_TOPS, 5), "traffic": None,
-                     "kernel": "conv_igemm", "avg_us": round(conv_us, 3),
-                     "algorithmic_ops_per_launch": L.ops},
+                     "frac": round(conv_tops / INT8_PEAK_TOPS, 5), "traffic": traffic,
+                     "kernel": "conv_wide" if tile_name.startswith("wide") else "conv_staged",
+                     "avg_us": round(conv_us, 3), "algorithmic_ops_per_launch": L.ops,
+                     "algorithmic_bytes_per_launch": conv_bytes, "kernel_digest": kernel_digest(tile_name)},
         "kernels": {"conv_us": round(conv_us, 3), "pack_us": round(pack_us, 3),
                     "pack_gbs": round(pack_gbs, 1), "pack_frac_hbm": round(pack_gbs / HBM_PEAK_GBS, 4),
                     "pack_algorithmic_bytes": pack_bytes},
