@@ -252,13 +252,14 @@ __device__ __forceinline__ void widen_vec(uint4 v, uint4 &g0, uint4 &g1) {
     }
 }
 
-constexpr int kWideMaxV = 4;   // packed 16-byte vectors a thread prefetches per stage (band and filters each)
+constexpr int kWideMaxV = 4;   // packed 16-byte band vectors a thread prefetches per stage
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 constexpr uint32_t kRsrcWord3 = 0x00020000u;   // raw buffer, dword data format (gfx9 family)
 
 // Buffer resource for a read-only tensor of `bytes` bytes (wave-uniform).
+// Loads at offsets >= bytes return zeros.
 __device__ __forceinline__ u32x4 make_rsrc(const void *base, int32_t bytes) {
     const uint64_t b = (uint64_t)base;
     u32x4 r;
@@ -269,9 +270,21 @@ __device__ __forceinline__ u32x4 make_rsrc(const void *base, int32_t bytes) {
     return r;
 }
 
-// 16 bytes per lane from global memory (buffer offset `voff`) straight into LDS
-// at lds_dst + 16 * lane.  Inline assembly keeps the compiler from guarding
-// later LDS reads with waits on these loads; the kernel waits explicitly.
+constexpr uint32_t kOutOfRange = 0x80000000u;   // a buffer offset past every tensor: loads return 0
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_brsrc(const void *base, int32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, bytes, (int)kRsrcWord3);
+}
+
+__device__ __forceinline__ uint4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+    return uint4{v[0], v[1], v[2], v[3]};
+}
+
+// Global memory straight into LDS (no VGPR round trip): lane i's 16 bytes
+// (dma16) or 4 bytes (dma4) from buffer offset `voff` land at lds_dst + 16*i
+// (or 4*i).  Inline assembly keeps the compiler from guarding later LDS reads
+// with waits on these loads; the kernel waits explicitly.
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void dma16(const uint8_t *lds_dst, uint32_t voff, u32x4 rsrc) {
@@ -279,10 +292,30 @@ __device__ __forceinline__ void dma16(const uint8_t *lds_dst, uint32_t voff, u32
     asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" : : "s"(m0v), "v"(voff), "s"(rsrc)
                  : "memory", "m0");
 }
+__device__ __forceinline__ void dma4(const uint8_t *lds_dst, uint32_t voff, u32x4 rsrc) {
+    const uint32_t m0v = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void *)lds_dst);
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds" : : "s"(m0v), "v"(voff), "s"(rsrc)
+                 : "memory", "m0");
+}
 #pragma clang diagnostic pop
 
-template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS>
+// Workgroups are dispatched round-robin over the 8 XCDs, each with its own L2:
+// block b runs on XCD b % 8.  Renumber them so that every XCD gets one
+// contiguous range of logical blocks; neighbouring output tiles share halo
+// rows, which then meet in the same L2.  A bijection for any grid size.
+__device__ __forceinline__ int xcd_block(int b, int g) {
+    constexpr int X = 8;
+    const int x = b % X, i = b / X;
+    const int q = g / X, r = g % X;
+    return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + i;
+}
+
+// RC, SC: filter height and width fixed at compile time (0: taken from the
+// descriptor).  A fixed-size instance always reads prepared filters and runs a
+// fully unrolled MFMA loop with immediate LDS offsets.
+template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC>
 __device__ __forceinline__ void wide_body(const ConvArgs &a) {
+    constexpr bool FIXED = RC > 0 && SC > 0;
     constexpr int NW = WP * WK;
     constexpr int NT = NW * 64;
     constexpr int TP = WP * FP * 16;
@@ -291,8 +324,10 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     constexpr int VPP = CK * BITS / 128;    // packed 16-byte vectors per pixel (or filter tap) and chunk
     constexpr int GPV = 16 / (2 * BITS);    // 16-channel int8 granules per packed vector
     constexpr int CPV = 128 / BITS;         // channels per packed vector
+    constexpr int PJ = kWideMaxV / VPP;     // band pixels a thread stages per chunk
     constexpr int MAXV = kWideMaxV;
     static_assert(BITS == 8 || FK % 2 == 0, "4-bit output packs 8 channels per word: FK must be even");
+    static_assert(VPP >= 1 && kWideMaxV % VPP == 0, "a pixel's vectors must divide the per-thread budget");
 
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
@@ -304,61 +339,76 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     const int l16 = lane & 15;
     const int gq = lane >> 4;
 
-    const int kt = blockIdx.x % a.ktiles;
-    const int j0 = blockIdx.x / a.ktiles;
+    const int lb = xcd_block(blockIdx.x, gridDim.x);
+    const int kt = lb % a.ktiles;
+    const int j0 = lb / a.ktiles;
     const int gpk = gridDim.x / a.ktiles;                    // workgroups sharing this channel tile
     const int my_tiles = (a.mtiles - j0 + gpk - 1) / gpk;    // tiles j0, j0 + gpk, ...
     const int nst = my_tiles * a.nchunks;
     const int k0 = kt * TK;
-    const int rs = a.r * a.s;
+    const int R = FIXED ? RC : a.r;
+    const int S = FIXED ? SC : a.s;
+    const int rs = R * S;
+    const bool w_image = FIXED || a.w_image;
 
-    // ---- band staging: packed global -> VGPR (prefetch) -> widen -> int8 LDS planes.
-    // Plane g holds granule g (channels 16g .. 16g+15 of the chunk) of every band
-    // pixel, 16 bytes each.  Lanes run along pixels so each write instruction
-    // fills one plane contiguously (no bank conflicts).
-    struct Fetch {
-        uint4 v[MAXV];
-        int n, npix;
-    };
-    auto band_fetch = [&](int ti, int c, Fetch &f) {
+    const __amdgpu_buffer_rsrc_t rx = make_brsrc(a.xptr, a.xbytes);
+
+    // ---- band staging.  The band of a tile is the run of zero-padded input
+    // rows its pixels touch; thread tid stages band pixels tid, tid + NT, ...
+    // Their byte offsets in x (or kOutOfRange for padding, which loads as
+    // zeros) are computed once per tile and reused for every channel chunk.
+    // Plane g of the LDS band holds granule g (channels 16g .. 16g+15 of the
+    // chunk) of every band pixel, 16 bytes each: one write instruction fills
+    // one plane contiguously.
+    uint32_t poff[PJ];
+    int npix = 0;
+    auto set_band = [&](int ti) {
         const int m0 = (j0 + ti * gpk) * TP;
         int vlo, vlast, cu;
         pixel_origin(a, m0, vlo, cu);
         pixel_origin(a, min(m0 + TP, a.m) - 1, vlast, cu);
-        f.npix = (vlast + a.r - vlo) * a.ncols;
-        f.n = f.npix * VPP;   // <= NT * MAXV (host-checked)
-        const int cbyte = c * (CK * BITS / 8);
-        const int cbase = c * CK;
+        npix = (vlast + R - vlo) * a.ncols;   // <= NT * PJ (host-checked)
 #pragma unroll
-        for (int u = 0; u < MAXV; ++u) {
-            f.v[u] = uint4{0u, 0u, 0u, 0u};
-            const int idx = u * NT + tid;
-            if (idx >= f.n) continue;
-            const int part = idx / f.npix;
-            const int pix = idx - part * f.npix;
+        for (int j = 0; j < PJ; ++j) {
+            const int pix = j * NT + tid;
             const int rowl = (int)fdiv((uint32_t)pix, a.div_ncols);
             const int col = pix - rowl * a.ncols;
             const int vrow = vlo + rowl;
             const int img = (int)fdiv((uint32_t)vrow, a.div_vh);
             const int hh = vrow - img * a.vh - a.ph;
             const int ww = col - a.pw;
-            if (img < a.n && hh >= 0 && hh < a.h && ww >= 0 && ww < a.w && cbase + part * CPV < a.c)
-                f.v[u] = *reinterpret_cast<const uint4 *>(a.xptr + ((size_t)(img * a.h + hh) * a.w + ww) * a.xpix +
-                                                          cbyte + part * 16);
+            const bool in = pix < npix && img < a.n && hh >= 0 && hh < a.h && ww >= 0 && ww < a.w;
+            poff[j] = in ? (uint32_t)(((img * a.h + hh) * a.w + ww) * a.xpix) : kOutOfRange;
         }
+    };
+    struct Fetch {
+        uint4 v[PJ][VPP];
+    };
+    auto band_fetch = [&](int c, Fetch &f) {
+        const uint32_t cbyte = (uint32_t)c * (CK * BITS / 8);
+        const int cbase = c * CK;
+#pragma unroll
+        for (int j = 0; j < PJ; ++j)
+#pragma unroll
+            for (int p = 0; p < VPP; ++p) {
+                const bool ok = poff[j] != kOutOfRange && cbase + p * CPV < a.c;
+                f.v[j][p] = buffer_load16(rx, ok ? poff[j] + cbyte + p * 16 : kOutOfRange);
+            }
     };
     auto band_store = [&](const Fetch &f, int buf) {
         uint8_t *bb = smem + (buf ? a.off_b1 : a.off_b0);
 #pragma unroll
-        for (int u = 0; u < MAXV; ++u) {
-            const int idx = u * NT + tid;
-            if (idx >= f.n) continue;
-            const int part = idx / f.npix;
-            const int pix = idx - part * f.npix;
-            uint4 g0, g1;
-            widen_vec<BITS, XS>(f.v[u], g0, g1);
-            *reinterpret_cast<uint4 *>(bb + (size_t)(part * GPV) * a.pstride_b + pix * 16) = g0;
-            if constexpr (GPV == 2) *reinterpret_cast<uint4 *>(bb + (size_t)(part * GPV + 1) * a.pstride_b + pix * 16) = g1;
+        for (int j = 0; j < PJ; ++j) {
+            const int pix = j * NT + tid;
+            if (pix >= npix) continue;
+#pragma unroll
+            for (int p = 0; p < VPP; ++p) {
+                uint4 g0, g1;
+                widen_vec<BITS, XS>(f.v[j][p], g0, g1);
+                *reinterpret_cast<uint4 *>(bb + (size_t)(p * GPV) * a.pstride_b + pix * 16) = g0;
+                if constexpr (GPV == 2)
+                    *reinterpret_cast<uint4 *>(bb + (size_t)(p * GPV + 1) * a.pstride_b + pix * 16) = g1;
+            }
         }
     };
 
@@ -374,15 +424,18 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         const int nkb = (CK / 16) * a.pstride_w / 1024;
         for (int i = wave; i < nkb; i += NW) dma16(wb + i * 1024, base + i * 1024 + lane * 16, rimg);
     };
-    auto w_gather = [&](int c, int base, Fetch &f) {
-        f.n = TK * rs * VPP;
+    struct WFetch {
+        uint4 v[MAXV];
+    };
+    auto w_gather = [&](int c, int base, WFetch &f) {
+        const int n = TK * rs * VPP;
         const int cbyte = c * (CK * BITS / 8);
         const int cbase = c * CK;
 #pragma unroll
         for (int u = 0; u < MAXV; ++u) {
             f.v[u] = uint4{0u, 0u, 0u, 0u};
             const int idx = base + u * NT + tid;
-            if (idx >= f.n) continue;
+            if (idx >= n) continue;
             // idx = (part * rs + tap) * TK + slot
             const int slot = idx % TK;
             const int rest = idx / TK;
@@ -393,12 +446,13 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                 f.v[u] = *reinterpret_cast<const uint4 *>(a.wptr + ((size_t)kk * rs + tap) * a.xpix + cbyte + pt * 16);
         }
     };
-    auto w_gather_store = [&](const Fetch &f, int base, int buf) {
+    auto w_gather_store = [&](const WFetch &f, int base, int buf) {
+        const int n = TK * rs * VPP;
         uint8_t *wb = smem + (buf ? a.off_w1 : a.off_w0);
 #pragma unroll
         for (int u = 0; u < MAXV; ++u) {
             const int idx = base + u * NT + tid;
-            if (idx >= f.n) continue;
+            if (idx >= n) continue;
             const int slot = idx % TK;
             const int rest = idx / TK;
             const int pt = (int)fdiv((uint32_t)rest, a.div_rs);
@@ -411,11 +465,13 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         }
     };
     auto w_load_all = [&](int c, int buf) {
-        const int n = TK * rs * VPP;
-        for (int base = 0; base < n; base += NT * MAXV) {
-            Fetch f;
-            w_gather(c, base, f);
-            w_gather_store(f, base, buf);
+        if constexpr (!FIXED) {
+            const int n = TK * rs * VPP;
+            for (int base = 0; base < n; base += NT * MAXV) {
+                WFetch f;
+                w_gather(c, base, f);
+                w_gather_store(f, base, buf);
+            }
         }
     };
 
@@ -442,19 +498,22 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         for (int tm = 0; tm < FK; ++tm) acc[tn][tm] = v4i{0, 0, 0, 0};
 
     const int cb = k0 + wk * FK * 16 + gq * 4 * FK;
-    // the workgroup's TK multipliers live in LDS (read back in the epilogue)
+    // the workgroup's TK multipliers go to LDS by DMA (read back in the epilogue)
     int32_t *mlds = reinterpret_cast<int32_t *>(smem + a.off_m);
-    if (a.mode == QCONV_OUT_REQUANT)
-        for (int e = tid; e < TK; e += NT) mlds[e] = a.mult[min(k0 + e, a.k - 1)];
+    if (a.mode == QCONV_OUT_REQUANT && wave == 0) {
+        const u32x4 rm = make_rsrc(a.mult, 4 * a.k);
+        for (int e = 0; e < TK; e += 64)
+            if (e + lane < TK)   // TK may be 32: only the lanes of the buffer write
+                dma4(reinterpret_cast<const uint8_t *>(mlds + e), (uint32_t)min(k0 + e + lane, a.k - 1) * 4u, rm);
+    }
 
-    // ---- prologue: stage 0
+    // ---- prologue: stage 0 (every load in flight before the first wait)
     if (nst > 0) {
+        if (w_image) w_dma(0, 0);
+        set_band(0);
         Fetch fb;
-        band_fetch(0, 0, fb);
-        if (a.w_image)
-            w_dma(0, 0);
-        else
-            w_load_all(0, 0);
+        band_fetch(0, fb);
+        if (!w_image) w_load_all(0, 0);
         __builtin_amdgcn_s_waitcnt(0);
         band_store(fb, 0);
     }
@@ -473,13 +532,15 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         const int cur = st & 1;
         const bool more = st + 1 < nst;
         // prefetch the next stage; it lands while the MFMAs run
-        Fetch fb, fw;
+        Fetch fb;
+        WFetch fw;
         if (more) {
-            band_fetch(nti, nc, fb);
+            if (nti != ti) set_band(nti);
+            band_fetch(nc, fb);
             if (a.nchunks > 1) {
-                if (a.w_image)
+                if (w_image)
                     w_dma(nc, cur ^ 1);
-                else
+                else if constexpr (!FIXED)
                     w_gather(nc, 0, fw);
             }
         }
@@ -495,31 +556,76 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
             ao = ks * 4 * a.pstride_w + tap * TK * 16;
             bo = ks * 4 * a.pstride_b + (rr * a.ncols + ss) * 16;
         };
-        v4i A0[FK], B0[FP], A1[FK], B1[FP];
-        auto ld = [&](int it, v4i(&A)[FK], v4i(&B)[FP]) {
-            int ao, bo;
-            offs(it, ao, bo);
-#pragma unroll
-            for (int tm = 0; tm < FK; ++tm) A[tm] = *reinterpret_cast<const v4i *>(wb + ao + tm * 256);
-#pragma unroll
-            for (int tn = 0; tn < FP; ++tn) B[tn] = *reinterpret_cast<const v4i *>(bb + bo + pixoff[tn]);
-        };
-        auto mm = [&](const v4i(&A)[FK], const v4i(&B)[FP]) {
+        if constexpr (FIXED) {
+            // every step's LDS offsets are known: filter reads use immediate
+            // offsets from one base; band reads from one base per (fragment,
+            // filter row, depth step) plus the column as an immediate
+            constexpr int PSW = (RC * SC * TK * 16 + 1023) / 1024 * 1024;   // filter plane stride
+            constexpr int NIT = RC * SC * KSTEPS;
+            const uint8_t *wa = wb;
+            const uint8_t *brow[FP][RC][KSTEPS];
 #pragma unroll
             for (int tn = 0; tn < FP; ++tn)
 #pragma unroll
+                for (int rr = 0; rr < RC; ++rr)
+#pragma unroll
+                    for (int ks = 0; ks < KSTEPS; ++ks)
+                        brow[tn][rr][ks] = bb + pixoff[tn] + rr * a.ncols * 16 + ks * 4 * a.pstride_b;
+            v4i A[2][FK], B[2][FP];
+            auto ld = [&](int it, int set) {
+                const int tap = it / KSTEPS, ks = it % KSTEPS, rr = tap / SC, ss = tap % SC;
+#pragma unroll
                 for (int tm = 0; tm < FK; ++tm)
-                    acc[tn][tm] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A[tm], B[tn], acc[tn][tm], 0, 0, 0);
-        };
-        ld(0, A0, B0);
-        int it = 0;
-        for (; it + 2 <= nit; it += 2) {
-            ld(it + 1, A1, B1);
-            mm(A0, B0);
-            ld(min(it + 2, nit - 1), A0, B0);   // clamped: re-reading the last step is harmless
-            mm(A1, B1);
+                    A[set][tm] = *reinterpret_cast<const v4i *>(wa + ks * 4 * PSW + tap * TK * 16 + tm * 256);
+#pragma unroll
+                for (int tn = 0; tn < FP; ++tn)
+                    B[set][tn] = *reinterpret_cast<const v4i *>(brow[tn][rr][ks] + ss * 16);
+            };
+            ld(0, 0);
+#pragma unroll
+            for (int it = 0; it < NIT; ++it) {
+                if (it + 1 < NIT) ld(it + 1, (it + 1) & 1);
+#pragma unroll
+                for (int tn = 0; tn < FP; ++tn)
+#pragma unroll
+                    for (int tm = 0; tm < FK; ++tm)
+                        acc[tn][tm] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A[it & 1][tm], B[it & 1][tn], acc[tn][tm],
+                                                                            0, 0, 0);
+            }
+        } else {
+            // three fragment sets in rotation: the LDS reads of step it+2 are in
+            // flight while the MFMAs of step it run
+            v4i A0[FK], B0[FP], A1[FK], B1[FP], A2[FK], B2[FP];
+            auto ld = [&](int it, v4i(&A)[FK], v4i(&B)[FP]) {
+                int ao, bo;
+                offs(it, ao, bo);
+    #pragma unroll
+                for (int tm = 0; tm < FK; ++tm) A[tm] = *reinterpret_cast<const v4i *>(wb + ao + tm * 256);
+    #pragma unroll
+                for (int tn = 0; tn < FP; ++tn) B[tn] = *reinterpret_cast<const v4i *>(bb + bo + pixoff[tn]);
+            };
+            auto mm = [&](const v4i(&A)[FK], const v4i(&B)[FP]) {
+    #pragma unroll
+                for (int tn = 0; tn < FP; ++tn)
+    #pragma unroll
+                    for (int tm = 0; tm < FK; ++tm)
+                        acc[tn][tm] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A[tm], B[tn], acc[tn][tm], 0, 0, 0);
+            };
+            // clamped step indices: re-reading the last step is harmless
+            ld(0, A0, B0);
+            ld(min(1, nit - 1), A1, B1);
+            int it = 0;
+            for (; it + 3 <= nit; it += 3) {
+                ld(min(it + 2, nit - 1), A2, B2);
+                mm(A0, B0);
+                ld(min(it + 3, nit - 1), A0, B0);
+                mm(A1, B1);
+                ld(min(it + 4, nit - 1), A1, B1);
+                mm(A2, B2);
+            }
+            if (it < nit) mm(A0, B0);
+            if (it + 1 < nit) mm(A1, B1);
         }
-        if (it < nit) mm(A0, B0);
 
         if (c == a.nchunks - 1) {
             EpiParams<FK> ep;
@@ -530,7 +636,7 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                     const int4 q = *reinterpret_cast<const int4 *>(mlds + cb - k0 + e);
                     mraw[e] = q.x; mraw[e + 1] = q.y; mraw[e + 2] = q.z; mraw[e + 3] = q.w;
                 }
-                make_epilogue_params<FK>(a, cb, mraw, ep);
+                make_epilogue_params<FK>(a, mraw, ep);
             } else {
                 ep.fast = false;
             }
@@ -543,17 +649,17 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         if (more) {
             __builtin_amdgcn_s_waitcnt(0);   // prefetched band (and filter DMA) have landed
             band_store(fb, cur ^ 1);
-            if (a.nchunks > 1 && !a.w_image) {
+            if constexpr (!FIXED) if (a.nchunks > 1 && !w_image) {
                 w_gather_store(fw, 0, cur ^ 1);
                 for (int base = NT * MAXV; base < TK * rs * VPP; base += NT * MAXV) {
-                    Fetch f2;
+                    WFetch f2;
                     w_gather(nc, base, f2);
                     w_gather_store(f2, base, cur ^ 1);
                 }
             }
+            __syncthreads();
+            if (nti != ti) set_tile(nti);
         }
-        __syncthreads();
-        if (more && nti != ti) set_tile(nti);
         ti = nti;
         c = nc;
     }
@@ -600,9 +706,9 @@ __global__ void __launch_bounds__(256) build_filter_image(ConvArgs a, int TK, in
 
 // One operand signedness per kernel (the widening is compiled for it); 8-bit
 // operands are always signed.
-template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS>
+template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC>
 __global__ void __launch_bounds__(WP * WK * 64) __attribute__((amdgpu_waves_per_eu(2))) conv_wide(ConvArgs a) {
-    wide_body<BITS, WP, WK, FP, FK, CK, XS, WS>(a);
+    wide_body<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC>(a);
 }
 
 // ============================================================== tile registry
@@ -613,9 +719,9 @@ static hipError_t launch_staged(const ConvArgs &a, dim3 grid, size_t lds, hipStr
     return hipGetLastError();
 }
 
-template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS>
+template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC>
 static hipError_t launch_wide(const ConvArgs &a, dim3 grid, size_t lds, hipStream_t stream) {
-    hipLaunchKernelGGL((conv_wide<BITS, WP, WK, FP, FK, CK, XS, WS>), grid, dim3(WP * WK * 64), lds, stream, a);
+    hipLaunchKernelGGL((conv_wide<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC>), grid, dim3(WP * WK * 64), lds, stream, a);
     return hipGetLastError();
 }
 
@@ -670,13 +776,19 @@ static hipError_t launch_prep(const ConvArgs &a, uint8_t *img, int64_t elems, hi
 #define QCONV_STAGED_ENTRY(B, WP, WK, FP, FK, CK)                                                                 \
     {QCONV_TILE_INFO(QCONV_VARIANT_STAGED, "staged_b", B, WP, WK, FP, FK, CK, -1, -1),                           \
      &launch_staged<B, WP, WK, FP, FK, CK>,                                                                       \
-     reinterpret_cast<const void *>(&conv_staged<B, WP, WK, FP, FK, CK>), nullptr},
+     reinterpret_cast<const void *>(&conv_staged<B, WP, WK, FP, FK, CK>), nullptr, {}},
 // 4-bit: unsigned activations x signed filters; 8-bit: signed x signed.
+// Each wide tile also has fixed-size instances for 3x3 and 1x1 filters, used
+// with prepared filters.
 #define QCONV_WIDE_ENTRY(B, WP, WK, FP, FK, CK)                                                                   \
     {QCONV_TILE_INFO(QCONV_VARIANT_WIDE, "wide_b", B, WP, WK, FP, FK, CK, (B == 8), 1),                         \
-     &launch_wide<B, WP, WK, FP, FK, CK, (B == 8), true>,                                                         \
-     reinterpret_cast<const void *>(&conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true>),                          \
-     &launch_prep<B, WK, FK, CK, true>},
+     &launch_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 0, 0>,                                                   \
+     reinterpret_cast<const void *>(&conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 0, 0>),                    \
+     &launch_prep<B, WK, FK, CK, true>,                                                                           \
+     {{3, 3, &launch_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3>,                                           \
+       reinterpret_cast<const void *>(&conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3>)},                 \
+      {1, 1, &launch_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 1, 1>,                                           \
+       reinterpret_cast<const void *>(&conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 1, 1>)}}},
 
 static TileEntry g_tiles[] = {QCONV_STAGED_TILES(QCONV_STAGED_ENTRY) QCONV_WIDE_TILES(QCONV_WIDE_ENTRY)};
 

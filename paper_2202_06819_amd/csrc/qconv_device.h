@@ -67,66 +67,67 @@ __device__ __forceinline__ int row_channel(int tm, int i) {
 }
 
 // Per-lane multipliers for the epilogue: channels cb .. cb + 4*FK - 1 of the
-// wave's block, loaded once at kernel start so their latency hides behind the
-// main loop.
+// wave's block.
 //
-// Requantisation t = floor((acc*mult + 2^(shift-1)) / 2^shift) has an exact
-// 32-bit form when |mult| < 2^(shift-2) and shift + acc_shift <= 33:
-// with m2 = mult * 2^(33 - shift - acc_shift) (accumulators carry 2^acc_shift),
-// u = mulhi(acc, m2) = floor(2*acc*mult / 2^shift) and
-// floor(x + 1/2) = floor((floor(2x) + 1) / 2), so t = (u + 1) >> 1.
-// `fast` is decided once per wave; otherwise the product is formed in 64 bits.
+// Requantisation t = floor((A*mult + 2^(shift-1)) / 2^shift) of an accumulator
+// acc = A * 2^acc_shift (the widening factor) has an exact one-instruction
+// form: with m2 = mult * 2^e, e = 32 - shift - acc_shift,
+//   acc*m2 + 2^31 = (A*mult + 2^(shift-1)) * 2^(32 - shift),
+// so t is the high word of that 64-bit sum (v_mad_i64_i32).  It needs e >= 0
+// and m2 to fit in int32; `fast` is decided once per wave, otherwise the
+// epilogue forms the product and the shift in 64 bits.
 template <int FK>
 struct EpiParams {
     int32_t mul[4 * FK];
     bool fast;
 };
 
-// From multipliers already in registers (mraw[e] for channel cb + e; lanes
-// past the last channel hold a repeat of a valid one and are never stored).
 template <int FK>
-__device__ __forceinline__ void make_epilogue_params(const ConvArgs &a, int cb, const int32_t (&mraw)[4 * FK],
-                                                     EpiParams<FK> &ep) {
-    bool ok = true;
-    const int fast_sh = 33 - a.shift - a.acc_shift;
-    const int lim_bits = a.shift - 2;
+__device__ __forceinline__ void finish_epilogue_params(const ConvArgs &a, EpiParams<FK> &ep) {
+    const int e = 32 - a.shift - a.acc_shift;
+    bool ok = e >= 0;
+    if (ok && e > 0) {
+        // |m| < 2^(31-e)  <=>  (uint32)(m + 2^(31-e)) < 2^(32-e)
+        const uint32_t lim = 1u << (31 - e);
 #pragma unroll
-    for (int e = 0; e < 4 * FK; ++e) {
-        const int32_t m = (cb + e < a.k) ? mraw[e] : 0;
-        ep.mul[e] = m;
-        const bool fits = lim_bits >= 31 || (lim_bits >= 0 && m < (1 << lim_bits) && m > -(1 << lim_bits));
-        ok = ok && fast_sh >= 0 && fits;
+        for (int i = 0; i < 4 * FK; ++i) ok = ok && (uint32_t)ep.mul[i] + lim < 2u * lim;
     }
     ep.fast = __all(ok);
     if (ep.fast) {
 #pragma unroll
-        for (int e = 0; e < 4 * FK; ++e) ep.mul[e] = ep.mul[e] * (1 << fast_sh);
+        for (int i = 0; i < 4 * FK; ++i) ep.mul[i] = (int32_t)((uint32_t)ep.mul[i] << e);
     }
+}
+
+// From multipliers already in registers (mraw[i] for channel cb + i, every
+// entry a valid multiplier: channels past k repeat the last one and are never
+// stored).
+template <int FK>
+__device__ __forceinline__ void make_epilogue_params(const ConvArgs &a, const int32_t (&mraw)[4 * FK],
+                                                     EpiParams<FK> &ep) {
+#pragma unroll
+    for (int i = 0; i < 4 * FK; ++i) ep.mul[i] = mraw[i];
+    finish_epilogue_params<FK>(a, ep);
 }
 
 template <int FK>
 __device__ __forceinline__ void load_epilogue_params(const ConvArgs &a, int cb, EpiParams<FK> &ep) {
-    bool ok = true;
-    const int fast_sh = 33 - a.shift - a.acc_shift;
-    const int lim_bits = a.shift - 2;
     if (a.mode != QCONV_OUT_REQUANT) {
         ep.fast = false;
 #pragma unroll
-        for (int e = 0; e < 4 * FK; ++e) ep.mul[e] = 0;
+        for (int i = 0; i < 4 * FK; ++i) ep.mul[i] = 0;
         return;
     }
 #pragma unroll
-    for (int e = 0; e < 4 * FK; ++e) {
-        const int32_t m = (cb + e < a.k) ? a.mult[cb + e] : 0;
-        ep.mul[e] = m;
-        const bool fits = lim_bits >= 31 || (lim_bits >= 0 && m < (1 << lim_bits) && m > -(1 << lim_bits));
-        ok = ok && fast_sh >= 0 && fits;
-    }
-    ep.fast = __all(ok);
-    if (ep.fast) {
-#pragma unroll
-        for (int e = 0; e < 4 * FK; ++e) ep.mul[e] = ep.mul[e] * (1 << fast_sh);
-    }
+    for (int i = 0; i < 4 * FK; ++i) ep.mul[i] = (cb + i < a.k) ? a.mult[cb + i] : 0;
+    finish_epilogue_params<FK>(a, ep);
+}
+
+// Clamp to [lo, hi] in one instruction (lo <= hi is checked on the host).
+__device__ __forceinline__ int32_t clamp_med3(int32_t x, int32_t lo, int32_t hi) {
+    int32_t r;
+    asm("v_med3_i32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "v"(lo), "v"(hi));
+    return r;
 }
 
 // Store one pixel's packed channel run (4*FK channels of `BITS` bits).
@@ -150,6 +151,35 @@ __device__ __forceinline__ void store_run(const ConvArgs &a, int m, int cb, cons
 #pragma unroll
     for (int wd = 0; wd < NWD; ++wd)
         if (cb + wd * CPW < a.k) yw[wd] = words[wd];
+}
+
+// Fast requantisation (see EpiParams): one v_mad_i64_i32, one v_med3_i32 and
+// one shift-or per value.  A non-negative clamp range needs no mask: the
+// clamped value already fits its field.
+template <int BITS, int FP, int FK, bool UNSIGNED_OUT>
+__device__ __forceinline__ void epilogue_fast(const ConvArgs &a, v4i (&acc)[FP][FK], int mbase, int cb, int l16,
+                                              const EpiParams<FK> &ep) {
+    constexpr int CPW = 32 / BITS;
+    constexpr int NWD = 4 * FK / CPW;
+    constexpr uint32_t VMASK = (1u << BITS) - 1u;
+    const int lo = a.lo, hi = a.hi;
+#pragma unroll
+    for (int tn = 0; tn < FP; ++tn) {
+        uint32_t words[NWD];
+#pragma unroll
+        for (int wd = 0; wd < NWD; ++wd) words[wd] = 0u;
+#pragma unroll
+        for (int tm = 0; tm < FK; ++tm)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int e = 4 * tm + v;
+                const int64_t s64 = (int64_t)acc[tn][tm][v] * ep.mul[e] + ((int64_t)1 << 31);
+                const uint32_t t = (uint32_t)clamp_med3((int32_t)(s64 >> 32), lo, hi);
+                words[e / CPW] |= (UNSIGNED_OUT ? t : (t & VMASK)) << (BITS * (e % CPW));
+            }
+        const int m = mbase + tn * 16 + l16;
+        if (m < a.m) store_run<BITS, FK>(a, m, cb, words);
+    }
 }
 
 // The epilogue for one wave (Sec. 3.2.2: work on the wide accumulator, then
@@ -180,23 +210,10 @@ __device__ __forceinline__ void epilogue(const ConvArgs &a, v4i (&acc)[FP][FK], 
     }
     const int lo = a.lo, hi = a.hi;
     if (ep.fast) {
-#pragma unroll
-        for (int tn = 0; tn < FP; ++tn) {
-            uint32_t words[NWD];
-#pragma unroll
-            for (int wd = 0; wd < NWD; ++wd) words[wd] = 0u;
-#pragma unroll
-            for (int tm = 0; tm < FK; ++tm)
-#pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    const int e = 4 * tm + v;
-                    int32_t t = (__mulhi(acc[tn][tm][v], ep.mul[e]) + 1) >> 1;
-                    t = min(max(t, lo), hi);
-                    words[e / CPW] |= ((uint32_t)t & VMASK) << (BITS * (e % CPW));
-                }
-            const int m = mbase + tn * 16 + l16;
-            if (m < a.m) store_run<BITS, FK>(a, m, cb, words);
-        }
+        if (lo >= 0)
+            epilogue_fast<BITS, FP, FK, true>(a, acc, mbase, cb, l16, ep);
+        else
+            epilogue_fast<BITS, FP, FK, false>(a, acc, mbase, cb, l16, ep);
         return;
     }
     const int64_t rnd = (int64_t)1 << (a.shift - 1);

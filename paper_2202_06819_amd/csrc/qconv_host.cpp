@@ -200,6 +200,9 @@ int plan_tile(const qconv_desc *d, const qconv_layout_info &li, const qconv_tile
         pl.pstride_b = round_up(pl.rows * ncols * 16, 256);
         pl.pstride_w = round_up((int64_t)d->r * d->s * t.tile_k * 16, 1024);
         const int64_t bbuf = planes * pl.pstride_b, wbuf = planes * pl.pstride_w;
+        // buffer loads take 32-bit offsets, and offset 2^31 marks padding
+        if (li.x_bytes >= (1ll << 31) || pl.ktiles * nchunks * wbuf >= (1ll << 31))
+            return fail(QCONV_EUNSUPPORTED, "tile %s addresses operands with 31-bit buffer offsets", t.name);
         const int64_t mbytes = round_up((int64_t)t.tile_k * 4, 16);
         const int64_t single = bbuf + wbuf + mbytes;
         const int64_t tiles = pl.mtiles * pl.ktiles;
@@ -398,14 +401,15 @@ void fill_args(ConvArgs &a, const qconv_desc *d, const qconv_layout_info &li, co
     a.acc_shift = d->bits == 4 ? 4 * (d->x_signed + d->w_signed) : 0;
 }
 
-int ensure_lds_attribute(const TileEntry &te, int tile_id, int64_t lds) {
+// inst: 0 = the tile's generic kernel, 1 + i = its fixed-size instance i.
+int ensure_lds_attribute(const void *kernel, int tile_id, int inst, int64_t lds) {
     if (lds <= 64 * 1024) return QCONV_OK;
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return fail(QCONV_EHIP, "hipGetDevice failed");
-    const long long key = (long long)dev * 4096 + tile_id;
+    const long long key = ((long long)dev * 4096 + tile_id) * 4 + inst;
     std::lock_guard<std::mutex> g(g_attr.mu);
     if (!g_attr.done[key]) {
-        hipError_t e = hipFuncSetAttribute(te.kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
+        hipError_t e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
         if (e != hipSuccess) return fail(QCONV_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
         g_attr.done[key] = true;
     }
@@ -445,12 +449,23 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
     const uintptr_t y0 = (uintptr_t)y, y1 = y0 + ybytes;
     if (((uintptr_t)x < y1 && y0 < (uintptr_t)x + li.x_bytes) || ((uintptr_t)w < y1 && y0 < (uintptr_t)w + wb))
         return fail(QCONV_EINVAL, "y overlaps x or w");
+    // prepared filters of a 3x3 or 1x1 layer run the tile's fixed-size instance
+    ConvLauncher launch = te.launch;
+    const void *kernel = te.kernel;
+    int inst = 0;
+    if (prepared && te.info.variant == QCONV_VARIANT_WIDE)
+        for (int i = 0; i < 2; ++i)
+            if (te.fixed[i].launch && te.fixed[i].r == d->r && te.fixed[i].s == d->s) {
+                launch = te.fixed[i].launch;
+                kernel = te.fixed[i].kernel;
+                inst = 1 + i;
+            }
     if (te.info.variant == QCONV_VARIANT_WIDE && pl.off_b1 != pl.off_b0) {
         // persistent grid: size it by the occupancy the runtime reports for this kernel
-        rc = ensure_lds_attribute(te, tile_id, pl.lds);
+        rc = ensure_lds_attribute(kernel, tile_id, inst, pl.lds);
         if (rc) return rc;
         int occ = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, te.kernel, te.info.threads, (size_t)pl.lds) == hipSuccess &&
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, te.info.threads, (size_t)pl.lds) == hipSuccess &&
             occ > 0) {
             rc = plan_tile(d, li, te.info, &pl, occ);
             if (rc) return rc;
@@ -471,9 +486,9 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
         a.hi = epi->clamp_hi;
         if (a.lo > a.hi) a.lo = a.hi;   // relu with an all-negative clamp range: every value is clamp_hi
     }
-    rc = ensure_lds_attribute(te, tile_id, pl.lds);
+    rc = ensure_lds_attribute(kernel, tile_id, inst, pl.lds);
     if (rc) return rc;
-    hipError_t e = te.launch(a, dim3((unsigned)pl.grid), (size_t)pl.lds, (hipStream_t)stream);
+    hipError_t e = launch(a, dim3((unsigned)pl.grid), (size_t)pl.lds, (hipStream_t)stream);
     if (e != hipSuccess) return fail(QCONV_EHIP, "conv launch (%s): %s", te.info.name, hipGetErrorString(e));
     return QCONV_OK;
 }

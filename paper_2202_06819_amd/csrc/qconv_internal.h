@@ -75,11 +75,19 @@ struct ConvArgs {
 using ConvLauncher = hipError_t (*)(const ConvArgs &, dim3 grid, size_t lds_bytes, hipStream_t);
 using PrepLauncher = hipError_t (*)(const ConvArgs &, uint8_t *image, int64_t elems, hipStream_t);
 
+// A compiled instance of a tile for one fixed filter size (prepared filters).
+struct FixedInstance {
+    int r, s;
+    ConvLauncher launch;
+    const void *kernel;
+};
+
 struct TileEntry {
     qconv_tile_info info;
     ConvLauncher launch;
     const void *kernel;     // for hipFuncSetAttribute
     PrepLauncher prep;      // builds the filter image (wide tiles), else null
+    FixedInstance fixed[2]; // wide tiles: 3x3 and 1x1 instances; empty (r == 0) otherwise
 };
 
 // Defined in qconv_conv.hip.

@@ -94,6 +94,31 @@ def test_config1_requant_every_tile():
         assert_same(got["y"], ref["y_packed"], f"requant tile {tid} prepared")
 
 
+@pytest.mark.parametrize("shape", [
+    # name, n, h, c, k, r, stride, pad -- the strided and 1x1 layers of the ResNet stacks
+    ("ds1x1_s2_64to128", 2, 56, 64, 128, 1, 2, 0),
+    ("conv3x3_s2_64to128", 2, 56, 64, 128, 3, 2, 1),
+    ("conv1x1_s1_256to64", 2, 28, 256, 64, 1, 1, 0),
+    ("conv3x3_s1_512to512", 2, 7, 512, 512, 3, 1, 1),
+], ids=lambda v: v[0])
+def test_resnet_shapes_every_tile_prepared(shape):
+    """Every tile that runs the shape, from packed and from prepared filters
+    (prepared 3x3 and 1x1 layers run the fixed-size kernel instances)."""
+    name, n, h, c, k, r, stride, pad = shape
+    L = qi.Layer(name, n, h, h, c, k, r, r, stride, pad, w_range=(-7, 7))
+    t = qi.layer_tensors(500, r * 10 + stride, L)
+    sh = stress_shift(L, L.x_range, L.w_range)
+    ref = ref_layer(L, t, requant=True, shift=sh)
+    ref_raw = ref_layer(L, t, requant=False)
+    for tid in _valid_tiles(L):
+        announce(f"{name} tile {tid} prepared requant shift={sh}")
+        assert_same(gpu_layer(L, t, requant=True, tile=tid, shift=sh, prepared=True)["y"], ref["y_packed"],
+                    f"{name} tile {tid} prepared")
+        announce(f"{name} tile {tid} prepared raw")
+        assert_same(gpu_layer(L, t, requant=False, tile=tid, prepared=True)["y"], ref_raw["acc"],
+                    f"{name} tile {tid} prepared raw")
+
+
 def test_config1_raw_default_tile():
     L = qi.config1()[0]
     t = qi.layer_tensors(1, 0, L)
