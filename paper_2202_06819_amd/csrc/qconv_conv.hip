@@ -299,6 +299,12 @@ __device__ __forceinline__ void dma4(const uint8_t *lds_dst, uint32_t voff, u32x
 }
 #pragma clang diagnostic pop
 
+// Scheduling groups, in program order, for the instruction scheduler.
+template <int N>
+__device__ __forceinline__ void sched_lds_reads() { __builtin_amdgcn_sched_group_barrier(0x100, N, 0); }
+template <int N>
+__device__ __forceinline__ void sched_mfmas() { __builtin_amdgcn_sched_group_barrier(0x008, N, 0); }
+
 // Workgroups are dispatched round-robin over the 8 XCDs, each with its own L2:
 // block b runs on XCD b % 8.  Renumber them so that every XCD gets one
 // contiguous range of logical blocks; neighbouring output tiles share halo
@@ -592,6 +598,15 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                         acc[tn][tm] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A[it & 1][tm], B[it & 1][tn], acc[tn][tm],
                                                                             0, 0, 0);
             }
+            // Pin the issue order (the scheduler otherwise reuses one register
+            // set and waits on every read): the LDS reads of step it+1 go out
+            // before the MFMAs of step it.
+            sched_lds_reads<FK + FP>();
+#pragma unroll
+            for (int it = 0; it < NIT; ++it) {
+                if (it + 1 < NIT) sched_lds_reads<FK + FP>();
+                sched_mfmas<FP * FK>();
+            }
         } else {
             // three fragment sets in rotation: the LDS reads of step it+2 are in
             // flight while the MFMAs of step it run
@@ -622,6 +637,11 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                 mm(A1, B1);
                 ld(min(it + 4, nit - 1), A1, B1);
                 mm(A2, B2);
+#pragma unroll
+                for (int g = 0; g < 3; ++g) {
+                    sched_lds_reads<FK + FP>();
+                    sched_mfmas<FP * FK>();
+                }
             }
             if (it < nit) mm(A0, B0);
             if (it + 1 < nit) mm(A1, B1);
