@@ -4,7 +4,13 @@
 A step is one pass of the whole hot path over one batch: relayout+pack of the
 int8 NCHW activations into channel-packed 4-bit NHWC (qconv_pack), then the
 implicit-GEMM convolution with the fused requantise/ReLU/clamp/repack
-epilogue (qconv2d).  Filters are packed once beforehand (offline, untimed).
+epilogue (qconv2d_prepared).  Filters are packed and laid out for the tile
+once beforehand (offline, untimed).
+
+The K timed steps run as replays of a captured HIP graph of G steps (one host
+launch per G steps), so the figure is the GPU's time per step, not the host's
+kernel-launch rate; the eager time per step (one host launch per kernel) is
+reported beside it.
 
 Default workload: N=8, 56x56, C=K=64, 3x3, stride 1, pad 1, 4-bit activations
 in [0,15], 4-bit filters in [-8,7], per-channel multipliers in [2^14, 2^15),
@@ -100,6 +106,41 @@ def time_loop(fn, reps: int) -> float:
     return e0.elapsed_time(e1) * 1000.0 / reps
 
 
+def captured(make_calls, passes: int):
+    """A graph holding `passes` back-to-back runs of the calls make_calls(stream)
+    returns (built for the capture stream).  Replaying it costs one launch for
+    all of them, so its timing is the GPU's and not the host's launch rate."""
+    import torch
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        calls = make_calls(s)
+        for c in calls:
+            c()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            for _ in range(passes):
+                for c in calls:
+                    c()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    return g, calls
+
+
+def time_graph(g, replays: int) -> float:
+    """Milliseconds for `replays` replays of graph g, from HIP events on the
+    stream that launches it."""
+    import torch
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(replays):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1)
+
+
 def layer_setup(cfg: int, lid: int, L, dev):
     import torch
     import qconv_inputs as qi
@@ -125,14 +166,21 @@ def per_layer_table(cfg: int, layers, dev, reps: int) -> list[dict]:
         tile = sweep.tuned_tile(L.desc(), e is not None)
         tile = qconv.default_tile(L.desc()) if tile == -1 else tile
         wprep = qconv.prepare_filters(L.desc(), wp, tile)
-        call = qconv.Conv2dCall(L.desc(), xp, wprep, requant=e is not None, mult=mult,
-                                shift=e.shift if e else 20, relu=e.relu if e else False,
-                                clamp=(e.lo, e.hi) if e else (0, 15), tile=tile, prepared=True)
+
+        def make(stream=None):
+            return qconv.Conv2dCall(L.desc(), xp, wprep, requant=e is not None, mult=mult,
+                                    shift=e.shift if e else 20, relu=e.relu if e else False,
+                                    clamp=(e.lo, e.hi) if e else (0, 15), tile=tile, prepared=True, stream=stream)
+
+        call = make()
         for _ in range(5):
             call()
-        us = time_loop(call, reps)
+        eager_us = time_loop(call, reps)
+        g, _ = captured(lambda s: [make(s)], reps)
+        us = time_graph(g, 3) * 1000.0 / (3 * reps)
         tops = L.ops / (us * 1e-6) / 1e12
         rows.append({"layer": L.name, "tile": qconv.tiles()[call.tile]["name"], "us": round(us, 3),
+                     "eager_us": round(eager_us, 3),
                      "tops": round(tops, 2), "pct_int8_peak": round(100 * tops / INT8_PEAK_TOPS, 2),
                      "gops": round(L.ops / 1e9, 4)})
         log(f"  {L.name:28s} {us:9.2f} us {tops:8.1f} TOP/s {100 * tops / INT8_PEAK_TOPS:5.1f}%  tile {rows[-1]['tile']}")
@@ -226,38 +274,58 @@ def main() -> int:
     L = qi.config1()[0]
     e = L.epilogue
     x, xp, wp, mult = layer_setup(1, 0, L, dev)
-    pack = qconv.PackCall(x, L.bits, L.x_signed, out=xp)
     tile = sweep.tuned_tile(L.desc()) if args.tile == -1 else args.tile
     tile = qconv.default_tile(L.desc()) if tile == -1 else tile
     wprep = qconv.prepare_filters(L.desc(), wp, tile)     # offline, like packing the filters
-    conv = qconv.Conv2dCall(L.desc(), xp, wprep, requant=True, mult=mult, shift=e.shift, relu=e.relu,
-                            clamp=(e.lo, e.hi), tile=tile, prepared=True)
+    y = torch.empty(qconv.packed_shape(L.n, L.p, L.q, L.k, L.bits), dtype=qconv.packed_dtype(L.bits), device=dev)
+
+    def make_pack(stream=None):
+        return qconv.PackCall(x, L.bits, L.x_signed, out=xp, stream=stream)
+
+    def make_conv(stream=None):
+        return qconv.Conv2dCall(L.desc(), xp, wprep, requant=True, mult=mult, shift=e.shift, relu=e.relu,
+                                clamp=(e.lo, e.hi), tile=tile, prepared=True, out=y, stream=stream)
+
+    pack, conv = make_pack(), make_conv()
 
     def step():
         pack()
         conv()
 
-    log(f"workload {L.name}: {L.ops / 1e9:.4f} GOP per step, tile {qconv.tiles()[conv.tile]['name']}")
+    tile_name = qconv.tiles()[conv.tile]["name"]
+    log(f"workload {L.name}: {L.ops / 1e9:.4f} GOP per step, tile {tile_name}")
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ref_out = y.clone()
+
+    # eager: one host launch per kernel (bounded by the host's launch rate)
+    eager_ms = time_loop(step, args.steps) / 1000.0
+
+    # timed region: the K steps as replays of a captured graph of G steps
+    G = max(d for d in range(1, min(args.steps, 100) + 1) if args.steps % d == 0)
+    g_step, _ = captured(lambda s: [make_pack(s), make_conv(s)], G)
+    for _ in range(max(1, args.warmup // G)):
+        g_step.replay()
     torch.cuda.synchronize()
+    y.zero_()
     t_wall = time.perf_counter()
-    e0.record()
-    for _ in range(args.steps):
-        step()
-    e1.record()
-    torch.cuda.synchronize()
+    ms_total = time_graph(g_step, args.steps // G)
     t_wall = time.perf_counter() - t_wall
-    ms_total = e0.elapsed_time(e1)
+    if not torch.equal(y, ref_out):
+        raise RuntimeError("graph replay output differs from the eager output")
     ms_per_step = ms_total / args.steps
     value = L.ops / (ms_per_step * 1e-3) / 1e12
-    log(f"step: {ms_per_step * 1000:.2f} us  ({value:.1f} TOP/s), wall {t_wall:.3f} s for {args.steps} steps")
+    log(f"step: {ms_per_step * 1000:.2f} us ({value:.1f} TOP/s) from {args.steps // G} replays of a {G}-step graph, "
+        f"wall {t_wall:.3f} s; eager {eager_ms * 1000:.2f} us per step")
 
-    # per-kernel averages, same launch configuration, HIP events on the launch stream
-    conv_us = time_loop(conv, args.steps)
-    pack_us = time_loop(pack, args.steps)
+    # per-kernel averages in the same launch configuration: graphs of back-to-back
+    # launches of one kernel, HIP events on the launching stream
+    reps = 200
+    g_conv, _ = captured(lambda s: [make_conv(s)], reps)
+    g_pack, _ = captured(lambda s: [make_pack(s)], reps)
+    conv_us = time_graph(g_conv, 5) * 1000.0 / (5 * reps)
+    pack_us = time_graph(g_pack, 5) * 1000.0 / (5 * reps)
     conv_tops = L.ops / (conv_us * 1e-6) / 1e12
     pack_bytes = L.n * L.c * L.h * L.w + L.n * L.h * L.w * L.c // 2
     p_out = (L.h + 2 * L.pad - L.r) // L.stride + 1
@@ -268,7 +336,6 @@ def main() -> int:
     log(f"conv kernel {conv_us:.2f} us = {conv_tops:.1f} TOP/s ({100 * conv_tops / INT8_PEAK_TOPS:.1f}% of int8 peak); "
         f"pack kernel {pack_us:.2f} us = {pack_gbs:.0f} GB/s")
 
-    tile_name = qconv.tiles()[conv.tile]["name"]
     workload = (f"conv2d n{L.n} {L.h}x{L.w} {L.c}->{L.k} {L.r}x{L.s} stride {L.stride} pad {L.pad}, "
                 f"{L.bits}-bit, fused requant+repack")
     traffic = measured_traffic(workload, tile_name)
@@ -280,6 +347,7 @@ def main() -> int:
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 6),
+        "eager_ms_per_step": round(eager_ms, 6),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

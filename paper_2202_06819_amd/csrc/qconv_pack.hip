@@ -3,13 +3,13 @@
 // axis; Sec. 3.3: channels innermost so consumers read it coalesced).
 //
 // The operation is a transpose of each image's C x (H*W) plane.  A workgroup
-// owns a tile of 64 channels x 64 pixels.  It reads the tile row by row
-// (each channel's 64 pixels are contiguous in NCHW, 16 bytes per lane),
-// saturates every value into the target range, and parks it in LDS; it then
-// reads the tile column-wise (one pixel's channels), packs, and writes each
-// pixel's run of channels contiguously.  Both HBM streams are therefore
-// coalesced; the LDS tile row has a 4-byte pad so the column reads spread
-// over banks.  The kernel is HBM-bound: every input byte is read once and
+// owns a tile of 64 channels x 128 pixels.  It reads the tile row by row
+// (each channel's pixels are contiguous in NCHW: 32 bytes per lane, whole
+// 128-byte lines per row), saturates every value into the target range and
+// parks it in LDS; it then reads 8 channels x 4 pixels per lane as dwords,
+// transposes the bytes in registers, packs nibbles and writes each pixel's
+// words.  The LDS row pitch of 33 dwords keeps the column reads free of bank
+// conflicts.  The kernel is HBM-bound: every input byte is read once and
 // every output byte written once.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -19,80 +19,114 @@
 namespace qconv {
 
 constexpr int PK_C = 64;          // channels per tile
-constexpr int PK_P = 64;          // pixels per tile
-constexpr int PK_ROW = PK_P + 4;  // LDS row pitch in bytes
+constexpr int PK_P = 128;         // pixels per tile: whole 128-byte lines of each channel row
+constexpr int PK_PITCH = 132;     // LDS row pitch in bytes (33 dwords: conflict-free column reads)
 constexpr int PK_THREADS = 256;
 
-__device__ __forceinline__ int sat(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
+// Same renumbering as the convolution kernels: block b runs on XCD b % 8;
+// give every XCD a contiguous range so neighbouring pixel tiles (which share
+// cache lines at row ends) meet in one L2.
+__device__ __forceinline__ int pack_xcd_block(int b, int g) {
+    const int x = b % 8, i = b / 8, q = g / 8, r = g % 8;
+    return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + i;
+}
 
-template <int BITS>
+__device__ __forceinline__ uint32_t byte_of(uint32_t v, int j) { return (v >> (8 * j)) & 0xFFu; }
+
+// 4x4 byte transpose: byte k of result j is byte j of t[k].
+__device__ __forceinline__ uint32_t gather_byte(const uint32_t (&t)[4], int j) {
+    return byte_of(t[0], j) | (byte_of(t[1], j) << 8) | (byte_of(t[2], j) << 16) | (byte_of(t[3], j) << 24);
+}
+
+template <int BITS, bool SIGNED>
 __global__ void __launch_bounds__(PK_THREADS)
-    pack_nchw(const int8_t *__restrict__ src, uint8_t *__restrict__ dst, int c, int hw, int ptiles, int ctiles,
-              int lo, int hi) {
-    __shared__ int8_t tile[PK_C * PK_ROW];
+    pack_nchw(const int8_t *__restrict__ src, uint8_t *__restrict__ dst, int c, int hw, int ptiles, int ctiles) {
+    constexpr int LO = SIGNED ? -(1 << (BITS - 1)) : 0;
+    constexpr int HI = SIGNED ? (1 << (BITS - 1)) - 1 : (1 << BITS) - 1;
+    __shared__ __attribute__((aligned(16))) uint8_t tile[PK_C * PK_PITCH];
     const int tid = threadIdx.x;
-    int bid = blockIdx.x;
-    const int ct = bid % ctiles;
-    bid /= ctiles;
+    int bid = pack_xcd_block(blockIdx.x, gridDim.x);
     const int pt = bid % ptiles;
-    const int img = bid / ptiles;
+    bid /= ptiles;
+    const int ct = bid % ctiles;
+    const int img = bid / ctiles;
     const int c0 = ct * PK_C;
     const int p0 = pt * PK_P;
     const int8_t *plane = src + (size_t)img * c * hw;
 
-    // ---- load: 64 channel rows x 64 pixels; lane covers 16 consecutive pixels of one row
+    // ---- phase 1: 64 channel rows x 128 pixels; a lane reads 32 consecutive
+    // pixels of one row, saturates them and parks them in LDS
     {
-        const int row = tid >> 2;            // channel within tile
-        const int seg = (tid & 3) * 16;      // first pixel of this lane's segment
+        const int row = tid >> 2;
+        const int seg = (tid & 3) * 32;
         const int ch = c0 + row;
-        int8_t vals[16];
-        if (ch < c && p0 + seg + 16 <= hw && ((((size_t)img * c + ch) * hw + p0 + seg) & 15) == 0) {
-            int4 v = *reinterpret_cast<const int4 *>(plane + (size_t)ch * hw + p0 + seg);
-            const int8_t *b = reinterpret_cast<const int8_t *>(&v);
-#pragma unroll
-            for (int e = 0; e < 16; ++e) vals[e] = b[e];
+        uint32_t v[8];
+        const int8_t *rp = plane + (size_t)ch * hw + p0 + seg;
+        if (ch < c && p0 + seg + 32 <= hw && (reinterpret_cast<uintptr_t>(rp) & 15) == 0) {
+            const uint4 a = *reinterpret_cast<const uint4 *>(rp);
+            const uint4 b = *reinterpret_cast<const uint4 *>(rp + 16);
+            v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+            v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
         } else {
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int px = p0 + seg + e;
-                vals[e] = (ch < c && px < hw) ? plane[(size_t)ch * hw + px] : (int8_t)0;
+            for (int e = 0; e < 8; ++e) {
+                uint32_t w = 0;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const int px = p0 + seg + 4 * e + k;
+                    if (ch < c && px < hw) w |= (uint32_t)(uint8_t)rp[4 * e + k] << (8 * k);
+                }
+                v[e] = w;
             }
         }
 #pragma unroll
-        for (int e = 0; e < 16; ++e) tile[row * PK_ROW + seg + e] = (int8_t)sat(vals[e], lo, hi);
+        for (int e = 0; e < 8; ++e) {
+            uint32_t w = v[e];
+            if constexpr (BITS == 4) {
+                uint32_t o = 0;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const int x = (int)(int8_t)byte_of(w, k);
+                    o |= ((uint32_t)(x < LO ? LO : (x > HI ? HI : x)) & 0xFFu) << (8 * k);
+                }
+                w = o;
+            }
+            *reinterpret_cast<uint32_t *>(tile + row * PK_PITCH + seg + 4 * e) = w;
+        }
     }
     __syncthreads();
 
-    // ---- store: one pixel's channel run per group of 4 lanes
-    const int px = tid >> 2;                 // pixel within tile
-    const int part = tid & 3;                // quarter of the 64 channels: 16 channels
-    const int pix = p0 + px;
-    if (pix >= hw) return;
-    const int cq = c0 + part * 16;
-    if (cq >= c) return;
-    if constexpr (BITS == 4) {
-        // 16 channels -> two 32-bit words; channel 8j+i in bits [4i, 4i+3] of word j
-        uint32_t wv[2] = {0u, 0u};
+    // ---- phase 2: a lane takes 8 channels (group g) x 4 pixels (quad q):
+    // 8 dword reads, an in-register transpose, and one output word (4-bit) or
+    // two (8-bit) per pixel
+    const int g = tid & 7;
+    const int q = tid >> 3;
+    const int cg = c0 + 8 * g;
+    if (cg >= c) return;
+    uint32_t d[8];
 #pragma unroll
-        for (int e = 0; e < 16; ++e)
-            wv[e >> 3] |= ((uint32_t)(uint8_t)tile[(part * 16 + e) * PK_ROW + px] & 0xFu) << (4 * (e & 7));
-        uint32_t *out = reinterpret_cast<uint32_t *>(dst) + ((size_t)img * hw + pix) * (c / 8) + cq / 8;
-        if (cq + 16 <= c) {
-            out[0] = wv[0];
-            out[1] = wv[1];
-        } else {
-            out[0] = wv[0];  // c % 8 == 0: the run holds exactly one more word
+    for (int i = 0; i < 8; ++i) d[i] = *reinterpret_cast<const uint32_t *>(tile + (8 * g + i) * PK_PITCH + 4 * q);
+    if constexpr (BITS == 4) {
+        // byte j of t[k]: channel 8g+2k in the low nibble, 8g+2k+1 in the high one, of pixel j
+        uint32_t t[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) t[k] = (d[2 * k] & 0x0F0F0F0Fu) | ((d[2 * k + 1] << 4) & 0xF0F0F0F0u);
+        uint32_t *out = reinterpret_cast<uint32_t *>(dst);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int pix = p0 + 4 * q + j;
+            if (pix < hw) out[((size_t)img * hw + pix) * (c / 8) + cg / 8] = gather_byte(t, j);
         }
     } else {
-        uint8_t bv[16];
+        const uint32_t lo4[4] = {d[0], d[1], d[2], d[3]};
+        const uint32_t hi4[4] = {d[4], d[5], d[6], d[7]};
 #pragma unroll
-        for (int e = 0; e < 16; ++e) bv[e] = (uint8_t)tile[(part * 16 + e) * PK_ROW + px];
-        uint8_t *out = dst + ((size_t)img * hw + pix) * c + cq;
-        const int cnt = min(16, c - cq);
-        if (cnt == 16 && (((size_t)img * hw + pix) * c + cq) % 16 == 0) {
-            *reinterpret_cast<uint4 *>(out) = *reinterpret_cast<const uint4 *>(bv);
-        } else {
-            for (int e = 0; e < cnt; ++e) out[e] = bv[e];
+        for (int j = 0; j < 4; ++j) {
+            const int pix = p0 + 4 * q + j;
+            if (pix >= hw) continue;
+            uint32_t *out = reinterpret_cast<uint32_t *>(dst + ((size_t)img * hw + pix) * c + cg);   // c % 4 == 0
+            out[0] = gather_byte(lo4, j);
+            if (cg + 4 < c) out[1] = gather_byte(hi4, j);
         }
     }
 }
@@ -103,14 +137,14 @@ hipError_t launch_pack(const int8_t *src, void *dst, int32_t n, int32_t c, int32
     const int ptiles = (hw + PK_P - 1) / PK_P;
     const int ctiles = (c + PK_C - 1) / PK_C;
     const long long blocks = (long long)n * ptiles * ctiles;
-    const int lo = is_signed ? -(1 << (bits - 1)) : 0;
-    const int hi = is_signed ? (1 << (bits - 1)) - 1 : (1 << bits) - 1;
-    if (bits == 4)
-        hipLaunchKernelGGL(pack_nchw<4>, dim3((unsigned)blocks), dim3(PK_THREADS), 0, stream, src,
-                           static_cast<uint8_t *>(dst), c, hw, ptiles, ctiles, lo, hi);
+    uint8_t *d = static_cast<uint8_t *>(dst);
+    const dim3 grid((unsigned)blocks), block(PK_THREADS);
+    if (bits == 4 && is_signed)
+        hipLaunchKernelGGL((pack_nchw<4, true>), grid, block, 0, stream, src, d, c, hw, ptiles, ctiles);
+    else if (bits == 4)
+        hipLaunchKernelGGL((pack_nchw<4, false>), grid, block, 0, stream, src, d, c, hw, ptiles, ctiles);
     else
-        hipLaunchKernelGGL(pack_nchw<8>, dim3((unsigned)blocks), dim3(PK_THREADS), 0, stream, src,
-                           static_cast<uint8_t *>(dst), c, hw, ptiles, ctiles, lo, hi);
+        hipLaunchKernelGGL((pack_nchw<8, true>), grid, block, 0, stream, src, d, c, hw, ptiles, ctiles);
     return hipGetLastError();
 }
 

@@ -11,7 +11,7 @@ from dataclasses import dataclass
 
 import torch
 
-from . import qconv
+from . import qconv, sweep
 
 
 @dataclass
@@ -39,7 +39,8 @@ class Chain:
         outs = []
         for L in layers:
             inp = self.x if L.src < 0 else outs[L.src]
-            tile = qconv.default_tile(L.desc) if L.tile == -1 else L.tile
+            tile = sweep.tuned_tile(L.desc) if L.tile == -1 else L.tile
+            tile = qconv.default_tile(L.desc) if tile == -1 else tile
             wprep = qconv.prepare_filters(L.desc, L.w_packed, tile)
             self.filters.append(wprep)
             call = qconv.Conv2dCall(L.desc, inp, wprep, requant=True, mult=L.mult, shift=L.shift,

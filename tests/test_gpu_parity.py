@@ -252,3 +252,36 @@ def test_chained_layers_need_no_relayout():
     announce("chain layer 2")
     g2 = gpu_layer(L2, t2, requant=True, shift=s2, x_packed_dev=g1["y_dev"])
     assert_same(g2["y"], r2["y_packed"], "layer 2")
+
+
+def test_graph_replays_match_eager():
+    """A captured chain replayed several times, with eager work and
+    synchronisation between replays, reproduces the eager outputs every time."""
+    torch, q = _torch(), _qconv()
+    from paper_2202_06819_amd import nets
+    L1 = qi.Layer("g1", 2, 14, 14, 64, 64, 3, 3, 1, 1, w_range=(-7, 7))
+    L2 = qi.Layer("g2", 2, 14, 14, 64, 128, 1, 1, 2, 0, w_range=(-7, 7))
+    t1, t2 = qi.layer_tensors(600, 1, L1), qi.layer_tensors(600, 2, L2)
+    s1, s2 = stress_shift(L1, L1.x_range, L1.w_range), stress_shift(L2, L2.x_range, L2.w_range)
+    xp = q.pack(torch.from_numpy(t1["x"]).cuda(), 4, False)
+    specs = []
+    for L, t, sh, src in ((L1, t1, s1, -1), (L2, t2, s2, 0)):
+        wp = q.pack(torch.from_numpy(t["w"]).cuda(), 4, True)
+        specs.append(nets.LayerSpec(L.desc(), wp, torch.from_numpy(t["mult"]).cuda(), sh, True, (0, 15), src=src))
+    chain = nets.Chain(specs, xp)
+    announce("graph: eager pass")
+    eager = [o.clone() for o in chain.forward()]
+    torch.cuda.synchronize()
+    r1 = ref_layer(L1, t1, requant=True, shift=s1)
+    assert_same(eager[0].cpu().numpy(), r1["y_packed"], "eager layer 1")
+    chain.capture()
+    for i in range(4):
+        for o in chain.outputs:
+            o.zero_()
+        announce(f"graph: replay {i}")
+        outs = chain.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(outs, eager):
+            assert torch.equal(a, b), f"replay {i} differs from the eager pass"
+        chain.forward()   # eager work between replays
+        torch.cuda.synchronize()
