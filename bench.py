@@ -163,14 +163,15 @@ def per_layer_table(cfg: int, layers, dev, reps: int) -> list[dict]:
         from paper_2202_06819_amd import sweep
         x, xp, wp, mult = layer_setup(cfg, lid, L, dev)
         e = L.epilogue
-        tile = sweep.tuned_tile(L.desc(), e is not None)
-        tile = qconv.default_tile(L.desc()) if tile == -1 else tile
+        tile, splits = sweep.tuned_config(L.desc(), e is not None)
         wprep = qconv.prepare_filters(L.desc(), wp, tile)
+        ws = qconv.make_workspace(L.desc(), tile, splits, dev)
 
         def make(stream=None):
             return qconv.Conv2dCall(L.desc(), xp, wprep, requant=e is not None, mult=mult,
                                     shift=e.shift if e else 20, relu=e.relu if e else False,
-                                    clamp=(e.lo, e.hi) if e else (0, 15), tile=tile, prepared=True, stream=stream)
+                                    clamp=(e.lo, e.hi) if e else (0, 15), tile=tile, prepared=True, stream=stream,
+                                    splits=splits, workspace=ws)
 
         call = make()
         for _ in range(5):
@@ -179,11 +180,12 @@ def per_layer_table(cfg: int, layers, dev, reps: int) -> list[dict]:
         g, _ = captured(lambda s: [make(s)], reps)
         us = time_graph(g, 3) * 1000.0 / (3 * reps)
         tops = L.ops / (us * 1e-6) / 1e12
-        rows.append({"layer": L.name, "tile": qconv.tiles()[call.tile]["name"], "us": round(us, 3),
+        rows.append({"layer": L.name, "tile": qconv.tiles()[call.tile]["name"], "splits": splits, "us": round(us, 3),
                      "eager_us": round(eager_us, 3),
                      "tops": round(tops, 2), "pct_int8_peak": round(100 * tops / INT8_PEAK_TOPS, 2),
                      "gops": round(L.ops / 1e9, 4)})
-        log(f"  {L.name:28s} {us:9.2f} us {tops:8.1f} TOP/s {100 * tops / INT8_PEAK_TOPS:5.1f}%  tile {rows[-1]['tile']}")
+        log(f"  {L.name:28s} {us:9.2f} us {tops:8.1f} TOP/s {100 * tops / INT8_PEAK_TOPS:5.1f}%  tile {rows[-1]['tile']}"
+            f" splits {splits}")
     return rows
 
 
@@ -275,7 +277,6 @@ def main() -> int:
     e = L.epilogue
     x, xp, wp, mult = layer_setup(1, 0, L, dev)
     tile = sweep.tuned_tile(L.desc()) if args.tile == -1 else args.tile
-    tile = qconv.default_tile(L.desc()) if tile == -1 else tile
     wprep = qconv.prepare_filters(L.desc(), wp, tile)     # offline, like packing the filters
     y = torch.empty(qconv.packed_shape(L.n, L.p, L.q, L.k, L.bits), dtype=qconv.packed_dtype(L.bits), device=dev)
 

@@ -201,13 +201,38 @@ int qconv2d(const qconv_desc *d, const void *x, const void *w, const qconv_epilo
  *   QCONV_EUNSUPPORTED, QCONV_EHIP.
  * qconv2d_prepared -- qconv2d with prepared filters; `tile_id` must be the
  *   one they were prepared for (-1 resolves the same way for the same
- *   descriptor).  Results are identical to qconv2d.
+ *   descriptor).  `splits` (1 = none) selects split-K, below; `workspace`
+ *   may be NULL when splits == 1.  Results are identical to qconv2d.
  */
 int qconv_prepared_filter_bytes(const qconv_desc *d, int32_t tile_id, size_t *bytes);
 int qconv_prepare_filters(const qconv_desc *d, const void *w_packed, int32_t tile_id, void *w_prepared,
                           size_t bytes, void *stream);
 int qconv2d_prepared(const qconv_desc *d, const void *x, const void *w_prepared, size_t w_prepared_bytes,
-                     const qconv_epilogue *epi, void *y, int32_t tile_id, void *stream);
+                     const qconv_epilogue *epi, void *y, int32_t tile_id, int32_t splits, void *workspace,
+                     size_t workspace_bytes, void *stream);
+
+/*
+ * Split-K over channel chunks (prepared filters, wide tiles).  The depth
+ * C*R*S of the implicit GEMM (Sec. 2.1) is a sum over channel chunks of
+ * `chunk_c` channels; with `splits` > 1 each output tile is computed by
+ * `splits` workgroups, each summing its range of chunks into exact int32
+ * partial sums.  The last workgroup of a tile to finish adds the others'
+ * partial sums and applies the epilogue, so results are identical to
+ * splits == 1 (integer addition is exact and associative).
+ *
+ * qconv_max_splits -- host only: number of channel chunks of `tile_id` for
+ *   this shape (the largest useful `splits`; 1 for staged tiles), or an error.
+ * qconv_workspace_bytes -- host only: workspace `qconv2d_prepared` needs for
+ *   (tile_id, splits): 0 when splits == 1.  Requests past the chunk count are
+ *   QCONV_EUNSUPPORTED; a request that would leave a split empty is reduced.
+ * Workspace contract: caller-owned device memory, 16-byte aligned, not
+ *   overlapping x, w or y, and ZERO-FILLED before its first use; every call
+ *   leaves it ready for the next (its arrival counters return to zero).  Calls
+ *   that use one workspace must not run concurrently.  QCONV_EWORKSPACE when it
+ *   is missing or too small.
+ */
+int qconv_max_splits(const qconv_desc *d, int32_t tile_id);
+int qconv_workspace_bytes(const qconv_desc *d, int32_t tile_id, int32_t splits, size_t *bytes);
 
 /* Number of compiled tile configurations; ids are 0 .. count-1. */
 int qconv_tile_count(void);

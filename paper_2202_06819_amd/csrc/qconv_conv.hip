@@ -345,12 +345,20 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     const int l16 = lane & 15;
     const int gq = lane >> 4;
 
+    // Work assignment.  Without a split, a workgroup walks output tiles j0,
+    // j0 + gpk, ... of one channel tile over all channel chunks.  With a split
+    // (a.splits > 1) it owns one output tile and the chunk range of its split;
+    // the splits of a tile have consecutive logical numbers (one XCD).
     const int lb = xcd_block(blockIdx.x, gridDim.x);
-    const int kt = lb % a.ktiles;
-    const int j0 = lb / a.ktiles;
-    const int gpk = gridDim.x / a.ktiles;                    // workgroups sharing this channel tile
-    const int my_tiles = (a.mtiles - j0 + gpk - 1) / gpk;    // tiles j0, j0 + gpk, ...
-    const int nst = my_tiles * a.nchunks;
+    const int sp = a.splits > 1 ? lb % a.splits : 0;
+    const int lt = a.splits > 1 ? lb / a.splits : lb;
+    const int kt = lt % a.ktiles;
+    const int j0 = lt / a.ktiles;
+    const int gpk = a.splits > 1 ? a.mtiles : gridDim.x / a.ktiles;   // workgroups sharing this channel tile
+    const int my_tiles = (a.mtiles - j0 + gpk - 1) / gpk;              // tiles j0, j0 + gpk, ...
+    const int c_begin = sp * a.cps;                                     // chunks [c_begin, c_end)
+    const int c_end = min(a.nchunks, c_begin + a.cps);
+    const int nst = my_tiles * (c_end - c_begin);
     const int k0 = kt * TK;
     const int R = FIXED ? RC : a.r;
     const int S = FIXED ? SC : a.s;
@@ -515,11 +523,11 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
 
     // ---- prologue: stage 0 (every load in flight before the first wait)
     if (nst > 0) {
-        if (w_image) w_dma(0, 0);
+        if (w_image) w_dma(c_begin, 0);
         set_band(0);
         Fetch fb;
-        band_fetch(0, fb);
-        if (!w_image) w_load_all(0, 0);
+        band_fetch(c_begin, fb);
+        if (!w_image) w_load_all(c_begin, 0);
         __builtin_amdgcn_s_waitcnt(0);
         band_store(fb, 0);
     }
@@ -528,11 +536,11 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
 
     const int nit = rs * KSTEPS;
 
-    int ti = 0, c = 0;
+    int ti = 0, c = c_begin;
     for (int st = 0; st < nst; ++st) {
         int nti = ti, nc = c + 1;
-        if (nc == a.nchunks) {
-            nc = 0;
+        if (nc == c_end) {
+            nc = c_begin;
             ++nti;
         }
         const int cur = st & 1;
@@ -543,7 +551,7 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         if (more) {
             if (nti != ti) set_band(nti);
             band_fetch(nc, fb);
-            if (a.nchunks > 1) {
+            if (c_end - c_begin > 1) {
                 if (w_image)
                     w_dma(nc, cur ^ 1);
                 else if constexpr (!FIXED)
@@ -553,7 +561,7 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
 
         // ---- MFMA loop: int8 fragments straight from LDS, one step of lookahead
         const uint8_t *bb = smem + (cur ? a.off_b1 : a.off_b0);
-        const uint8_t *wb = smem + ((a.nchunks > 1 && cur) ? a.off_w1 : a.off_w0) + lane_a;
+        const uint8_t *wb = smem + ((c_end - c_begin > 1 && cur) ? a.off_w1 : a.off_w0) + lane_a;
         auto offs = [&](int it, int &ao, int &bo) {
             const int tap = it / KSTEPS;
             const int ks = it % KSTEPS;
@@ -647,7 +655,46 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
             if (it + 1 < nit) mm(A1, B1);
         }
 
-        if (c == a.nchunks - 1) {
+        if (c == c_end - 1) {
+            if (a.splits > 1) {
+                // split-K: publish this split's partial sums; the last split of the
+                // tile to arrive adds the others and runs the epilogue
+                const int tile = lt;
+                int4 *mine = reinterpret_cast<int4 *>(a.ws_part) +
+                             ((size_t)(tile * a.splits + sp) * NW + wave) * (FP * FK * 64) + lane;
+#pragma unroll
+                for (int tn = 0; tn < FP; ++tn)
+#pragma unroll
+                    for (int tm = 0; tm < FK; ++tm) {
+                        const v4i v = acc[tn][tm];
+                        mine[(tn * FK + tm) * 64] = int4{v[0], v[1], v[2], v[3]};
+                    }
+                // every wave's partial stores are complete before the one
+                // agent-scope release (an L2 write-back) that publishes them;
+                // the same atomic's acquire side invalidates the caches the
+                // workgroup then reads the other partial sums through
+                __builtin_amdgcn_s_waitcnt(0);
+                __syncthreads();
+                uint32_t *flag = reinterpret_cast<uint32_t *>(smem + a.off_m) + TK;   // past the multipliers
+                if (tid == 0)
+                    *flag = __hip_atomic_fetch_add(a.ws_cnt + tile, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+                __syncthreads();
+                const bool last = *flag == (uint32_t)(a.splits - 1);
+                if (!last) return;   // uniform over the workgroup
+                for (int o = 0; o < a.splits; ++o) {
+                    if (o == sp) continue;
+                    const int4 *other = reinterpret_cast<const int4 *>(a.ws_part) +
+                                        ((size_t)(tile * a.splits + o) * NW + wave) * (FP * FK * 64) + lane;
+#pragma unroll
+                    for (int tn = 0; tn < FP; ++tn)
+#pragma unroll
+                        for (int tm = 0; tm < FK; ++tm) {
+                            const int4 q = other[(tn * FK + tm) * 64];
+                            acc[tn][tm] += v4i{q.x, q.y, q.z, q.w};
+                        }
+                }
+                if (tid == 0) a.ws_cnt[tile] = 0u;   // ready for the next call
+            }
             EpiParams<FK> ep;
             if (a.mode == QCONV_OUT_REQUANT) {
                 int32_t mraw[4 * FK];
@@ -669,7 +716,7 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         if (more) {
             __builtin_amdgcn_s_waitcnt(0);   // prefetched band (and filter DMA) have landed
             band_store(fb, cur ^ 1);
-            if constexpr (!FIXED) if (a.nchunks > 1 && !w_image) {
+            if constexpr (!FIXED) if (c_end - c_begin > 1 && !w_image) {
                 w_gather_store(fw, 0, cur ^ 1);
                 for (int base = NT * MAXV; base < TK * rs * VPP; base += NT * MAXV) {
                     WFetch f2;

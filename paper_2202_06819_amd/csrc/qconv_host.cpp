@@ -155,6 +155,7 @@ struct Plan {
     int64_t rows = 0, pstride_b = 0, pstride_w = 0, lds = 0;
     int64_t off_b0 = 0, off_b1 = 0, off_w0 = 0, off_w1 = 0, off_m = 0;
     int64_t mtiles = 0, ktiles = 0, grid = 0;
+    int64_t splits = 1, cps = 0;   // split-K: splits of the chunk range, chunks per split
 };
 
 constexpr int kWideMaxV = 4;   // packed vectors a thread prefetches per stage in conv_wide
@@ -169,8 +170,9 @@ int64_t per_cu_estimate(const qconv_tile_info &t, int64_t lds) {
 }
 
 // per_cu: workgroups per CU to plan the persistent grid for (0 = estimate).
+// splits: requested split-K factor (wide tiles); normalised so no split is empty.
 int plan_tile(const qconv_desc *d, const qconv_layout_info &li, const qconv_tile_info &t, Plan *out,
-              int64_t per_cu = 0) {
+              int64_t per_cu = 0, int64_t splits = 1) {
     if (t.bits != d->bits)
         return fail(QCONV_EUNSUPPORTED, "tile %s is built for %d-bit operands", t.name, t.bits);
     if ((t.x_signed >= 0 && t.x_signed != d->x_signed) || (t.w_signed >= 0 && t.w_signed != d->w_signed))
@@ -182,6 +184,7 @@ int plan_tile(const qconv_desc *d, const qconv_layout_info &li, const qconv_tile
     pl.mtiles = (li.m + t.tile_p - 1) / t.tile_p;
     pl.ktiles = (d->k + t.tile_k - 1) / t.tile_k;
     if (t.variant == QCONV_VARIANT_STAGED) {
+        if (splits != 1) return fail(QCONV_EUNSUPPORTED, "tile %s has no split-K", t.name);
         const int64_t gran = 2 * d->bits;
         pl.pstride_b = pad_plane(pl.rows * ncols * gran);
         pl.pstride_w = pad_plane((int64_t)d->r * d->s * t.tile_k * gran);
@@ -203,10 +206,31 @@ int plan_tile(const qconv_desc *d, const qconv_layout_info &li, const qconv_tile
         // buffer loads take 32-bit offsets, and offset 2^31 marks padding
         if (li.x_bytes >= (1ll << 31) || pl.ktiles * nchunks * wbuf >= (1ll << 31))
             return fail(QCONV_EUNSUPPORTED, "tile %s addresses operands with 31-bit buffer offsets", t.name);
-        const int64_t mbytes = round_up((int64_t)t.tile_k * 4, 16);
+        const int64_t mbytes = round_up((int64_t)t.tile_k * 4 + 4, 16);   // multipliers + split-K flag
         const int64_t single = bbuf + wbuf + mbytes;
         const int64_t tiles = pl.mtiles * pl.ktiles;
-        if (nchunks == 1 && tiles <= kNumCUs * per_cu_estimate(t, single)) {
+        if (splits < 1 || splits > nchunks)
+            return fail(QCONV_EUNSUPPORTED, "split-K factor %lld outside 1..%lld (channel chunks of tile %s)",
+                        (long long)splits, (long long)nchunks, t.name);
+        pl.cps = (nchunks + splits - 1) / splits;
+        pl.splits = (nchunks + pl.cps - 1) / pl.cps;
+        if (pl.splits > 1) {
+            // one output tile per workgroup, cps chunks each
+            if (pl.cps == 1) {
+                pl.off_b0 = pl.off_b1 = 0;
+                pl.off_w0 = pl.off_w1 = bbuf;
+                pl.off_m = bbuf + wbuf;
+                pl.lds = single;
+            } else {
+                pl.off_b0 = 0;
+                pl.off_b1 = bbuf;
+                pl.off_w0 = 2 * bbuf;
+                pl.off_w1 = pl.off_w0 + wbuf;
+                pl.off_m = pl.off_w1 + wbuf;
+                pl.lds = pl.off_m + mbytes;
+            }
+            pl.grid = tiles * pl.splits;
+        } else if (nchunks == 1 && tiles <= kNumCUs * per_cu_estimate(t, single)) {
             // every workgroup gets exactly one stage: one band buffer suffices
             pl.off_b0 = pl.off_b1 = 0;
             pl.off_w0 = pl.off_w1 = bbuf;
@@ -360,6 +384,15 @@ int64_t prepared_bytes(const qconv_desc *d, const qconv_layout_info &li, const q
     return pl.ktiles * nchunks * (t.chunk_c / 16) * pl.pstride_w;
 }
 
+// Split-K workspace: int32 partial sums of every (tile, split) block in the
+// kernel's register order, then one arrival counter per output tile.
+int64_t split_part_bytes(const qconv_tile_info &t, const Plan &pl) {
+    return pl.splits > 1 ? round_up(pl.mtiles * pl.ktiles * pl.splits * (int64_t)t.tile_p * t.tile_k * 4, 256) : 0;
+}
+int64_t split_workspace_bytes(const qconv_tile_info &t, const Plan &pl) {
+    return pl.splits > 1 ? split_part_bytes(t, pl) + round_up(pl.mtiles * pl.ktiles * 4, 256) : 0;
+}
+
 void fill_args(ConvArgs &a, const qconv_desc *d, const qconv_layout_info &li, const TileEntry &te, const Plan &pl) {
     memset(&a, 0, sizeof(a));
     a.n = d->n; a.h = d->h; a.w = d->w; a.c = d->c; a.k = d->k; a.r = d->r; a.s = d->s;
@@ -383,6 +416,8 @@ void fill_args(ConvArgs &a, const qconv_desc *d, const qconv_layout_info &li, co
     a.pstride_w = (int32_t)pl.pstride_w;
     a.ktiles = (int32_t)pl.ktiles;
     a.mtiles = (int32_t)pl.mtiles;
+    a.splits = (int32_t)pl.splits;
+    a.cps = (int32_t)(pl.cps > 0 ? pl.cps : (d->c + te.info.chunk_c - 1) / te.info.chunk_c);
     a.div_pq = make_fastdiv((uint32_t)(li.p * li.q));
     a.div_q = make_fastdiv((uint32_t)li.q);
     a.div_vh = make_fastdiv((uint32_t)a.vh);
@@ -418,10 +453,11 @@ int ensure_lds_attribute(const void *kernel, int tile_id, int inst, int64_t lds)
 
 // The convolution; w is packed KRSC filters (prepared == false) or the
 // prepared filters of tile_id (prepared == true, w_bytes_given bytes).
+// splits > 1 (prepared filters only): split-K over channel chunks with its
+// workspace in `workspace`.
 int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, size_t w_bytes_given,
              const qconv_epilogue *epi, void *y, void *workspace, size_t workspace_bytes, int32_t tile_id,
-             void *stream) {
-    (void)workspace;
+             int32_t splits, void *stream) {
     qconv_layout_info li;
     int rc = check_desc(d, &li);
     if (rc) return rc;
@@ -437,8 +473,15 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
     tile_id = rc;
     const TileEntry &te = tile_table()[tile_id];
     Plan pl;
-    rc = plan_tile(d, li, te.info, &pl);
+    rc = plan_tile(d, li, te.info, &pl, 0, splits);
     if (rc) return rc;
+    const int64_t wsb = split_workspace_bytes(te.info, pl);
+    if (wsb > 0) {
+        if (!workspace || (int64_t)workspace_bytes < wsb)
+            return fail(QCONV_EWORKSPACE, "split-K workspace of %zu bytes, need %lld", workspace ? workspace_bytes : 0,
+                        (long long)wsb);
+        if (!aligned16(workspace)) return fail(QCONV_EINVAL, "workspace must be 16-byte aligned");
+    }
     const int64_t wb = prepared ? prepared_bytes(d, li, te.info, pl) : li.w_bytes;
     if (prepared && (int64_t)w_bytes_given < wb)
         return fail(QCONV_EINVAL, "prepared filters of %zu bytes, tile %s needs %lld", w_bytes_given, te.info.name,
@@ -449,6 +492,12 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
     const uintptr_t y0 = (uintptr_t)y, y1 = y0 + ybytes;
     if (((uintptr_t)x < y1 && y0 < (uintptr_t)x + li.x_bytes) || ((uintptr_t)w < y1 && y0 < (uintptr_t)w + wb))
         return fail(QCONV_EINVAL, "y overlaps x or w");
+    if (wsb > 0) {
+        const uintptr_t w0 = (uintptr_t)workspace, w1 = w0 + wsb;
+        if ((w0 < y1 && y0 < w1) || ((uintptr_t)x < w1 && w0 < (uintptr_t)x + li.x_bytes) ||
+            ((uintptr_t)w < w1 && w0 < (uintptr_t)w + wb))
+            return fail(QCONV_EINVAL, "workspace overlaps x, w or y");
+    }
     // prepared filters of a 3x3 or 1x1 layer run the tile's fixed-size instance
     ConvLauncher launch = te.launch;
     const void *kernel = te.kernel;
@@ -460,7 +509,7 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
                 kernel = te.fixed[i].kernel;
                 inst = 1 + i;
             }
-    if (te.info.variant == QCONV_VARIANT_WIDE && pl.off_b1 != pl.off_b0) {
+    if (te.info.variant == QCONV_VARIANT_WIDE && pl.splits == 1 && pl.off_b1 != pl.off_b0) {
         // persistent grid: size it by the occupancy the runtime reports for this kernel
         rc = ensure_lds_attribute(kernel, tile_id, inst, pl.lds);
         if (rc) return rc;
@@ -478,6 +527,10 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
     a.yptr = static_cast<uint8_t *>(y);
     a.mult = requant ? epi->mult : nullptr;
     a.w_image = (prepared && te.info.variant == QCONV_VARIANT_WIDE) ? 1 : 0;
+    if (wsb > 0) {
+        a.ws_part = static_cast<int32_t *>(workspace);
+        a.ws_cnt = reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(workspace) + split_part_bytes(te.info, pl));
+    }
     if (a.w_image) a.wbytes = (int32_t)wb;
     a.mode = requant ? QCONV_OUT_REQUANT : QCONV_OUT_RAW_I32;
     if (requant) {
@@ -500,7 +553,35 @@ extern "C" {
 int qconv2d(const qconv_desc *d, const void *x, const void *w, const qconv_epilogue *epi, void *y, void *workspace,
             size_t workspace_bytes, int32_t tile_id, void *stream) {
     g_err[0] = 0;
-    return run_conv(d, x, w, false, 0, epi, y, workspace, workspace_bytes, tile_id, stream);
+    return run_conv(d, x, w, false, 0, epi, y, workspace, workspace_bytes, tile_id, 1, stream);
+}
+
+int qconv_workspace_bytes(const qconv_desc *d, int32_t tile_id, int32_t splits, size_t *bytes) {
+    g_err[0] = 0;
+    qconv_layout_info li;
+    int rc = check_desc(d, &li);
+    if (rc) return rc;
+    if (!bytes) return fail(QCONV_EINVAL, "bytes must be non-NULL");
+    rc = resolve_tile(d, li, tile_id);
+    if (rc < 0) return rc;
+    Plan pl;
+    const TileEntry &te = tile_table()[rc];
+    int prc = plan_tile(d, li, te.info, &pl, 0, splits);
+    if (prc) return prc;
+    *bytes = (size_t)split_workspace_bytes(te.info, pl);
+    return QCONV_OK;
+}
+
+int qconv_max_splits(const qconv_desc *d, int32_t tile_id) {
+    g_err[0] = 0;
+    qconv_layout_info li;
+    int rc = check_desc(d, &li);
+    if (rc) return rc;
+    rc = resolve_tile(d, li, tile_id);
+    if (rc < 0) return rc;
+    const qconv_tile_info &t = tile_table()[rc].info;
+    if (t.variant != QCONV_VARIANT_WIDE) return 1;
+    return (d->c + t.chunk_c - 1) / t.chunk_c;
 }
 
 int qconv_prepared_filter_bytes(const qconv_desc *d, int32_t tile_id, size_t *bytes) {
@@ -553,9 +634,11 @@ int qconv_prepare_filters(const qconv_desc *d, const void *w_packed, int32_t til
 }
 
 int qconv2d_prepared(const qconv_desc *d, const void *x, const void *w_prepared, size_t w_prepared_bytes,
-                     const qconv_epilogue *epi, void *y, int32_t tile_id, void *stream) {
+                     const qconv_epilogue *epi, void *y, int32_t tile_id, int32_t splits, void *workspace,
+                     size_t workspace_bytes, void *stream) {
     g_err[0] = 0;
-    return run_conv(d, x, w_prepared, true, w_prepared_bytes, epi, y, nullptr, 0, tile_id, stream);
+    return run_conv(d, x, w_prepared, true, w_prepared_bytes, epi, y, workspace, workspace_bytes, tile_id, splits,
+                    stream);
 }
 
 // Host-only consistency checks of the helpers the kernels rely on; returns 0

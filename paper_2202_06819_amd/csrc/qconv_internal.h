@@ -60,6 +60,10 @@ struct ConvArgs {
     int32_t pstride_w;      // bytes per granule plane of the filter buffer
     int32_t ktiles;         // workgroup tiles along output channels
     int32_t mtiles;         // workgroup tiles along output pixels
+    int32_t splits;         // split-K factor over channel chunks (1: none)
+    int32_t cps;            // channel chunks per split
+    int32_t *ws_part;       // split-K partial sums (splits > 1)
+    uint32_t *ws_cnt;       // split-K arrival counters, one per output tile, zero between calls
     FastDiv div_pq, div_q, div_vh, div_ncols, div_rs, div_s;
     int32_t x_signed, w_signed;
     // operand widening of 4-bit nibbles to int8 lanes (see widen4)

@@ -26,6 +26,7 @@ class LayerSpec:
     clamp: tuple
     src: int = -1
     tile: int = -1
+    splits: int = 0        # split-K factor; 0: the tuned choice (else 1)
 
 
 class Chain:
@@ -39,12 +40,16 @@ class Chain:
         outs = []
         for L in layers:
             inp = self.x if L.src < 0 else outs[L.src]
-            tile = sweep.tuned_tile(L.desc) if L.tile == -1 else L.tile
-            tile = qconv.default_tile(L.desc) if tile == -1 else tile
+            tile, splits = L.tile, L.splits
+            if tile == -1:
+                tile, tuned_splits = sweep.tuned_config(L.desc)
+                splits = splits or tuned_splits
+            splits = splits or 1
             wprep = qconv.prepare_filters(L.desc, L.w_packed, tile)
             self.filters.append(wprep)
             call = qconv.Conv2dCall(L.desc, inp, wprep, requant=True, mult=L.mult, shift=L.shift,
-                                    relu=L.relu, clamp=L.clamp, tile=tile, stream=stream, prepared=True)
+                                    relu=L.relu, clamp=L.clamp, tile=tile, stream=stream, prepared=True,
+                                    splits=splits)
             outs.append(call.out)
             self.calls.append(call)
         self.outputs = outs
@@ -63,7 +68,8 @@ class Chain:
             # calls marshal the stream at construction: rebuild them for the capture stream
             calls = [qconv.Conv2dCall(c.desc, c.x, c.w, requant=True, mult=c.mult, shift=c.epi.shift,
                                       relu=bool(c.epi.relu), clamp=(c.epi.clamp_lo, c.epi.clamp_hi), out=c.out,
-                                      tile=c.tile, stream=s, prepared=c.prepared) for c in self.calls]
+                                      tile=c.tile, stream=s, prepared=c.prepared, splits=c.splits,
+                                      workspace=getattr(c, "workspace", None)) for c in self.calls]
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g, stream=s):
                 for c in calls:

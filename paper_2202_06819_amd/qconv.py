@@ -83,10 +83,13 @@ def lib() -> ctypes.CDLL:
         L.qconv_selftest.argtypes = []
         L.qconv_prepared_filter_bytes.argtypes = [P(QConvDesc), _i32, P(ctypes.c_size_t)]
         L.qconv_prepare_filters.argtypes = [P(QConvDesc), _vp, _i32, _vp, ctypes.c_size_t, _vp]
-        L.qconv2d_prepared.argtypes = [P(QConvDesc), _vp, _vp, ctypes.c_size_t, P(QConvEpilogue), _vp, _i32, _vp]
+        L.qconv2d_prepared.argtypes = [P(QConvDesc), _vp, _vp, ctypes.c_size_t, P(QConvEpilogue), _vp, _i32, _i32,
+                                       _vp, ctypes.c_size_t, _vp]
+        L.qconv_workspace_bytes.argtypes = [P(QConvDesc), _i32, _i32, P(ctypes.c_size_t)]
+        L.qconv_max_splits.argtypes = [P(QConvDesc), _i32]
         for f in ("qconv_layout", "qconv_pack", "qconv2d", "qconv_tile_count", "qconv_tile_get", "qconv_tile_check",
                   "qconv_default_tile", "qconv_selftest", "qconv_prepared_filter_bytes", "qconv_prepare_filters",
-                  "qconv2d_prepared"):
+                  "qconv2d_prepared", "qconv_workspace_bytes", "qconv_max_splits"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
         return L
@@ -142,6 +145,28 @@ def prepared_filter_bytes(d: dict, tile: int = -1) -> int:
     _check(lib().qconv_prepared_filter_bytes(ctypes.byref(make_desc(d)), int(tile), ctypes.byref(n)),
            "qconv_prepared_filter_bytes")
     return int(n.value)
+
+
+def max_splits(d: dict, tile: int = -1) -> int:
+    """Largest split-K factor of `tile` for this shape (its channel chunks)."""
+    rc = lib().qconv_max_splits(ctypes.byref(make_desc(d)), int(tile))
+    if rc < 0:
+        _check(rc, "qconv_max_splits")
+    return int(rc)
+
+
+def workspace_bytes(d: dict, tile: int = -1, splits: int = 1) -> int:
+    """Split-K workspace bytes for (tile, splits); 0 without a split."""
+    n = ctypes.c_size_t(0)
+    _check(lib().qconv_workspace_bytes(ctypes.byref(make_desc(d)), int(tile), int(splits), ctypes.byref(n)),
+           "qconv_workspace_bytes")
+    return int(n.value)
+
+
+def make_workspace(d: dict, tile: int, splits: int, device) -> torch.Tensor | None:
+    """A zero-filled split-K workspace (None when none is needed)."""
+    n = workspace_bytes(d, tile, splits)
+    return torch.zeros(n, dtype=torch.uint8, device=device) if n else None
 
 
 def prepare_filters(d: dict, w_packed: torch.Tensor, tile: int = -1, out: torch.Tensor | None = None,
@@ -200,7 +225,7 @@ def pack(src: torch.Tensor, bits: int, is_signed: bool, out: torch.Tensor | None
 def conv2d(d: dict, x: torch.Tensor, w: torch.Tensor, *, requant: bool = False, mult: torch.Tensor | None = None,
            shift: int = 20, relu: bool = True, clamp: tuple = (0, 15), out: torch.Tensor | None = None,
            tile: int = -1, workspace: torch.Tensor | None = None, stream=None,
-           prepared: bool = False) -> torch.Tensor:
+           prepared: bool = False, splits: int = 1) -> torch.Tensor:
     """The convolution with its fused epilogue; returns the output tensor.
 
     Raw mode: int32 N x P x Q x K accumulators.  Requant mode: the packed
@@ -231,7 +256,7 @@ def conv2d(d: dict, x: torch.Tensor, w: torch.Tensor, *, requant: bool = False, 
         wb = prepared_filter_bytes(d, tile)
         rc = lib().qconv2d_prepared(ctypes.byref(desc), _dev_ptr(x, "x", info["x_bytes"]), _dev_ptr(w, "w", wb),
                                     w.numel() * w.element_size(), ctypes.byref(epi), _dev_ptr(out, "y", y_bytes),
-                                    int(tile), _vp(_stream(stream)))
+                                    int(tile), int(splits), ws_ptr, ws_bytes, _vp(_stream(stream)))
         _check(rc, "qconv2d_prepared")
         return out
     rc = lib().qconv2d(ctypes.byref(desc), _dev_ptr(x, "x", info["x_bytes"]), _dev_ptr(w, "w", info["w_bytes"]),
@@ -268,7 +293,8 @@ class Conv2dCall:
 
     def __init__(self, d: dict, x: torch.Tensor, w: torch.Tensor, *, requant: bool = False,
                  mult: torch.Tensor | None = None, shift: int = 20, relu: bool = True, clamp: tuple = (0, 15),
-                 out: torch.Tensor | None = None, tile: int = -1, stream=None, prepared: bool = False):
+                 out: torch.Tensor | None = None, tile: int = -1, stream=None, prepared: bool = False,
+                 splits: int = 1, workspace: torch.Tensor | None = None):
         self.desc = make_desc(d)
         info = layout(d)
         bits = self.desc.bits
@@ -289,11 +315,17 @@ class Conv2dCall:
         self.x, self.w, self.mult, self.out, self.info = x, w, mult, out, info
         self.tile = default_tile(d) if tile == -1 else int(tile)
         self.prepared = prepared
+        self.splits = int(splits)
         if prepared:
             wb = prepared_filter_bytes(d, self.tile)
+            if workspace is None and self.splits > 1:
+                workspace = make_workspace(d, self.tile, self.splits, x.device)
+            self.workspace = workspace
+            ws_ptr, ws_bytes = (None, 0) if workspace is None else (_dev_ptr(workspace, "workspace"),
+                                                                   workspace.numel() * workspace.element_size())
             self._args = (ctypes.byref(self.desc), _dev_ptr(x, "x", info["x_bytes"]), _dev_ptr(w, "w", wb),
                           w.numel() * w.element_size(), ctypes.byref(self.epi), _dev_ptr(out, "y", y_bytes),
-                          self.tile, _vp(_stream(stream)))
+                          self.tile, self.splits, ws_ptr, ws_bytes, _vp(_stream(stream)))
             self._fn = lib().qconv2d_prepared
         else:
             self._args = (ctypes.byref(self.desc), _dev_ptr(x, "x", info["x_bytes"]), _dev_ptr(w, "w", info["w_bytes"]),

@@ -44,24 +44,57 @@ def tuned_table() -> dict:
     return _tuned_cache
 
 
-def tuned_tile(d: dict, requant: bool = True) -> int:
-    """The swept best tile id for this shape, else the library's built-in choice (-1)."""
-    name = tuned_table().get(shape_key(d, requant))
-    if name:
+def tuned_config(d: dict, requant: bool = True) -> tuple[int, int]:
+    """(tile id, split-K factor) the sweep found fastest for this shape, else the
+    library's built-in tile without a split."""
+    entry = tuned_table().get(shape_key(d, requant))
+    if isinstance(entry, str):
+        entry = {"tile": entry, "splits": 1}
+    if entry:
         for t in qconv.tiles():
-            if t["name"] == name and qconv.tile_status(d, t["id"]) == 0:
-                return t["id"]
-    return -1
+            if t["name"] == entry["tile"] and qconv.tile_status(d, t["id"]) == 0:
+                splits = int(entry.get("splits", 1))
+                if splits <= max(1, qconv.max_splits(d, t["id"])):
+                    return t["id"], splits
+    return qconv.default_tile(d), 1
 
 
-def _time(call, reps: int, rounds: int) -> float:
+def tuned_tile(d: dict, requant: bool = True) -> int:
+    """The swept best tile id for this shape (the built-in choice when unswept)."""
+    return tuned_config(d, requant)[0]
+
+
+def split_choices(d: dict, tile: int) -> list[int]:
+    """Split-K factors worth timing: 1 and the powers of two up to the chunk count."""
+    top = max(1, qconv.max_splits(d, tile))
+    out, s = [1], 2
+    while s <= top:
+        out.append(s)
+        s *= 2
+    return out
+
+
+def _time(make_call, reps: int, rounds: int) -> float:
+    """Median microseconds per launch: a graph of `reps` back-to-back launches
+    (calls built by make_call(stream) for the capture stream) replayed `rounds`
+    times, timed with HIP events on the replaying stream."""
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        call = make_call(s)
+        call()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            for _ in range(reps):
+                call()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     res = []
     for _ in range(rounds):
         torch.cuda.synchronize()
         e0.record()
-        for _ in range(reps):
-            call()
+        g.replay()
         e1.record()
         torch.cuda.synchronize()
         res.append(e0.elapsed_time(e1) * 1000.0 / reps)
@@ -81,23 +114,31 @@ def sweep_layer(d: dict, x: torch.Tensor, w: torch.Tensor, mult: torch.Tensor | 
     ref = ref_call().clone()   # packed filters, default tile
     rows = []
     for t in qconv.tiles():
-        if qconv.tile_status(d, t["id"]) != 0 or (key, t["name"]) in done:
+        if qconv.tile_status(d, t["id"]) != 0:
             continue
         wprep = qconv.prepare_filters(d, w, t["id"])   # offline filter layout for this tile
-        call = qconv.Conv2dCall(d, x, wprep, requant=requant, mult=mult, shift=shift, relu=relu, clamp=clamp,
-                                tile=t["id"], prepared=True)
-        out = call()
-        torch.cuda.synchronize()
-        same = bool(torch.equal(out, ref))
-        us = _time(call, reps, rounds)
-        tops = ops / (us * 1e-6) / 1e12
-        row = {"shape": key, "tile": t["name"], "tile_id": t["id"], "default": t["id"] == default,
-               "us": round(us, 3), "tops": round(tops, 2), "pct_int8_peak": round(100 * tops / INT8_PEAK_TOPS, 3),
-               "identical": same}
-        rows.append(row)
-        log(json.dumps(row))
-        if not same:
-            raise RuntimeError(f"tile {t['name']} output differs from tile {default} on {key}")
+        for splits in split_choices(d, t["id"]):
+            if (key, t["name"], splits) in done:
+                continue
+            ws = qconv.make_workspace(d, t["id"], splits, x.device)
+
+            def make(stream=None, tid=t["id"], splits=splits, ws=ws):
+                return qconv.Conv2dCall(d, x, wprep, requant=requant, mult=mult, shift=shift, relu=relu,
+                                        clamp=clamp, tile=tid, prepared=True, splits=splits, workspace=ws,
+                                        stream=stream)
+
+            out = make()()
+            torch.cuda.synchronize()
+            same = bool(torch.equal(out, ref))
+            us = _time(make, reps, rounds)
+            tops = ops / (us * 1e-6) / 1e12
+            row = {"shape": key, "tile": t["name"], "tile_id": t["id"], "splits": splits,
+                   "default": t["id"] == default and splits == 1, "us": round(us, 3), "tops": round(tops, 2),
+                   "pct_int8_peak": round(100 * tops / INT8_PEAK_TOPS, 3), "identical": same}
+            rows.append(row)
+            log(json.dumps(row))
+            if not same:
+                raise RuntimeError(f"tile {t['name']} splits {splits} output differs from tile {default} on {key}")
     return rows
 
 
@@ -128,7 +169,7 @@ def main(argv=None) -> int:
             if line.strip():
                 r = json.loads(line)
                 rows.append(r)
-                done.add((r["shape"], r["tile"]))
+                done.add((r["shape"], r["tile"], r.get("splits", 1)))
     dev = torch.device("cuda:0")
     with open(args.out, "a") as fh:
         def log(s):
@@ -153,10 +194,10 @@ def main(argv=None) -> int:
     for key, r in sorted(best.items()):
         dflt = [x for x in rows if x["shape"] == key and x["default"]]
         speed = f" ({dflt[0]['us'] / r['us']:.2f}x vs default {dflt[0]['tile']})" if dflt else ""
-        print(f"best {key}: {r['tile']} {r['us']} us {r['tops']} TOP/s{speed}", flush=True)
+        print(f"best {key}: {r['tile']} splits {r.get('splits', 1)} {r['us']} us {r['tops']} TOP/s{speed}", flush=True)
     if args.write_tuned:
         table = json.load(open(TUNED_PATH)) if os.path.exists(TUNED_PATH) else {}
-        table.update({k: r["tile"] for k, r in best.items()})
+        table.update({k: {"tile": r["tile"], "splits": r.get("splits", 1)} for k, r in best.items()})
         with open(TUNED_PATH, "w") as fh:
             json.dump(table, fh, indent=1, sort_keys=True)
     return 0

@@ -227,8 +227,54 @@ def test_conv_prepared_errors(q):
     need = q.prepared_filter_bytes(d, tid)
     ref = ctypes.byref(desc)
     ok_epi = _epi(q)
+    epi = ctypes.byref(ok_epi)
     # prepared buffer smaller than the tile's layout
-    assert L.qconv2d_prepared(ref, 1 << 32, 1 << 33, need - 16, ctypes.byref(ok_epi), 1 << 34, tid, None) == -1
-    assert L.qconv2d_prepared(ref, 0, 1 << 33, need, ctypes.byref(ok_epi), 1 << 34, tid, None) == -1
-    assert L.qconv2d_prepared(ref, 1 << 32, 1 << 33, need, ctypes.byref(_epi(q, shift=0)), 1 << 34, tid, None) == -1
-    assert L.qconv2d_prepared(None, 1 << 32, 1 << 33, need, None, 1 << 34, tid, None) == -1
+    assert L.qconv2d_prepared(ref, 1 << 32, 1 << 33, need - 16, epi, 1 << 34, tid, 1, None, 0, None) == -1
+    assert L.qconv2d_prepared(ref, 0, 1 << 33, need, epi, 1 << 34, tid, 1, None, 0, None) == -1
+    assert L.qconv2d_prepared(ref, 1 << 32, 1 << 33, need, ctypes.byref(_epi(q, shift=0)), 1 << 34, tid, 1, None, 0,
+                              None) == -1
+    assert L.qconv2d_prepared(None, 1 << 32, 1 << 33, need, None, 1 << 34, tid, 1, None, 0, None) == -1
+
+
+def _wide_tile(q, d):
+    return [t["id"] for t in q.tiles() if t["variant"] == 2 and q.tile_status(d, t["id"]) == 0][0]
+
+
+def test_split_k_workspace(q):
+    d = D(h=7, w=7, c=512, k=512, n=2)
+    tid = _wide_tile(q, d)
+    chunks = q.max_splits(d, tid)
+    assert chunks == 512 // [t for t in q.tiles() if t["id"] == tid][0]["chunk_c"]
+    assert q.workspace_bytes(d, tid, 1) == 0
+    info = q.layout(d)
+    t = q.tiles()[tid]
+    mt = -(-info["m"] // t["tile_p"])
+    kt = -(-d["k"] // t["tile_k"])
+    for s in (2, chunks):
+        n = q.workspace_bytes(d, tid, s)
+        assert n >= mt * kt * s * t["tile_p"] * t["tile_k"] * 4 + mt * kt * 4
+    with pytest.raises(q.QConvError):
+        q.workspace_bytes(d, tid, chunks + 1)
+    staged = [x["id"] for x in q.tiles() if x["variant"] == 0 and q.tile_status(d, x["id"]) == 0]
+    if staged:
+        assert q.max_splits(d, staged[0]) == 1
+        with pytest.raises(q.QConvError):
+            q.workspace_bytes(d, staged[0], 2)
+
+
+def test_split_k_errors(q):
+    L = q.lib()
+    d = D(h=7, w=7, c=512, k=512, n=2)
+    tid = _wide_tile(q, d)
+    desc = q.make_desc(d)
+    need = q.prepared_filter_bytes(d, tid)
+    wsb = q.workspace_bytes(d, tid, 2)
+    epi = ctypes.byref(_epi(q))
+    ref = ctypes.byref(desc)
+    args = (ref, 1 << 32, 1 << 33, need, epi, 1 << 34, tid)
+    assert L.qconv2d_prepared(*args, 2, None, 0, None) == -3                 # no workspace
+    assert L.qconv2d_prepared(*args, 2, 1 << 35, wsb - 16, None) == -3       # too small
+    assert L.qconv2d_prepared(*args, 2, (1 << 35) + 8, wsb, None) == -1      # misaligned
+    assert L.qconv2d_prepared(*args, 2, (1 << 32) + 64, wsb, None) == -1     # overlaps x
+    assert L.qconv2d_prepared(*args, 10 ** 6, 1 << 35, wsb, None) == -2      # more splits than chunks
+    assert L.qconv2d_prepared(*args, 0, None, 0, None) == -2

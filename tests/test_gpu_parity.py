@@ -285,3 +285,55 @@ def test_graph_replays_match_eager():
             assert torch.equal(a, b), f"replay {i} differs from the eager pass"
         chain.forward()   # eager work between replays
         torch.cuda.synchronize()
+
+
+# ----------------------------------------------------------------- split-K
+
+SPLIT_SHAPES = [
+    # name, n, h, c, k, r, stride, pad
+    ("s7_512to512", 2, 7, 512, 512, 3, 1, 1),
+    ("s14_256to256", 2, 14, 256, 256, 3, 1, 1),
+    ("s14_256to512_s2", 2, 14, 256, 512, 3, 2, 1),
+    ("s7_1x1_1024to256", 2, 7, 1024, 256, 1, 1, 0),
+    ("s9_ragged_192to72", 3, 9, 192, 72, 3, 1, 1),
+]
+
+
+@pytest.mark.parametrize("shape", SPLIT_SHAPES, ids=lambda v: v[0])
+def test_split_k_matches_oracle(shape):
+    """Every wide tile and split factor; each configuration runs twice on one
+    workspace (the arrival counters must return to zero between calls)."""
+    torch, q = _torch(), _qconv()
+    name, n, h, c, k, r, stride, pad = shape
+    L = qi.Layer(name, n, h, h, c, k, r, r, stride, pad, w_range=(-7, 7))
+    t = qi.layer_tensors(700, c + k, L)
+    sh = stress_shift(L, L.x_range, L.w_range)
+    ref = ref_layer(L, t, requant=True, shift=sh)
+    ref_raw = ref_layer(L, t, requant=False)
+    dev = torch.device("cuda:0")
+    xp = q.pack(torch.from_numpy(t["x"]).to(dev), 4, False)
+    wp = q.pack(torch.from_numpy(t["w"]).to(dev), 4, True)
+    mult = torch.from_numpy(t["mult"]).to(dev)
+    wide = [tt["id"] for tt in q.tiles() if tt["variant"] == 2 and q.tile_status(L.desc(), tt["id"]) == 0]
+    assert wide
+    for tid in wide:
+        wprep = q.prepare_filters(L.desc(), wp, tid)
+        chunks = q.max_splits(L.desc(), tid)
+        for splits in sorted({2, 3, chunks} & set(range(2, chunks + 1))):
+            ws = q.make_workspace(L.desc(), tid, splits, dev)
+            for rep in range(2):
+                announce(f"split-K {name} tile {tid} splits {splits} rep {rep}")
+                y = q.conv2d(L.desc(), xp, wprep, tile=tid, prepared=True, splits=splits, workspace=ws,
+                             requant=True, mult=mult, shift=sh)
+                torch.cuda.synchronize()
+                assert_same(y.cpu().numpy(), ref["y_packed"], f"{name} tile {tid} splits {splits} rep {rep}")
+            announce(f"split-K {name} tile {tid} splits {splits} raw")
+            y = q.conv2d(L.desc(), xp, wprep, tile=tid, prepared=True, splits=splits, workspace=ws)
+            torch.cuda.synchronize()
+            assert_same(y.cpu().numpy(), ref_raw["acc"], f"{name} tile {tid} splits {splits} raw")
+            info = q.layout(L.desc())
+            tinfo = q.tiles()[tid]
+            ntiles = -(-info["m"] // tinfo["tile_p"]) * -(-L.k // tinfo["tile_k"])
+            part = -(-(ntiles * (-(-chunks // -(-chunks // splits))) * tinfo["tile_p"] * tinfo["tile_k"] * 4) // 256) * 256
+            counters = ws[part:part + 4 * ntiles]
+            assert int(counters.count_nonzero()) == 0, "arrival counters not reset"
