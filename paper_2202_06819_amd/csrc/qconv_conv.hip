@@ -252,7 +252,7 @@ __device__ __forceinline__ void widen_vec(uint4 v, uint4 &g0, uint4 &g1) {
     }
 }
 
-constexpr int kWideMaxV = 4;   // packed 16-byte band vectors a thread prefetches per stage
+constexpr int kWideMaxV = 4;   // packed 16-byte filter vectors a thread gathers per batch
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
@@ -330,10 +330,10 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     constexpr int VPP = CK * BITS / 128;    // packed 16-byte vectors per pixel (or filter tap) and chunk
     constexpr int GPV = 16 / (2 * BITS);    // 16-channel int8 granules per packed vector
     constexpr int CPV = 128 / BITS;         // channels per packed vector
-    constexpr int PJ = kWideMaxV / VPP;     // band pixels a thread stages per chunk
+    constexpr int PJ = wide_band_pixels_per_thread(TP, NT, VPP);   // band pixels a thread stages per chunk
     constexpr int MAXV = kWideMaxV;
     static_assert(BITS == 8 || FK % 2 == 0, "4-bit output packs 8 channels per word: FK must be even");
-    static_assert(VPP >= 1 && kWideMaxV % VPP == 0, "a pixel's vectors must divide the per-thread budget");
+    static_assert(VPP >= 1 && 4 % VPP == 0, "a pixel's vectors must divide the per-thread budget");
 
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
@@ -534,6 +534,21 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     set_tile(0);
     __syncthreads();
 
+    // the workgroup keeps one channel tile: its epilogue multipliers are read
+    // from LDS and prepared once
+    EpiParams<FK> ep;
+    if (a.mode == QCONV_OUT_REQUANT) {
+        int32_t mraw[4 * FK];
+#pragma unroll
+        for (int e = 0; e < 4 * FK; e += 4) {
+            const int4 q = *reinterpret_cast<const int4 *>(mlds + cb - k0 + e);
+            mraw[e] = q.x; mraw[e + 1] = q.y; mraw[e + 2] = q.z; mraw[e + 3] = q.w;
+        }
+        make_epilogue_params<FK>(a, mraw, ep);
+    } else {
+        ep.fast = false;
+    }
+
     const int nit = rs * KSTEPS;
 
     int ti = 0, c = c_begin;
@@ -655,6 +670,21 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
             if (it + 1 < nit) mm(A1, B1);
         }
 
+        // The next stage's operands (in flight during the MFMAs) are waited for
+        // and staged before this stage's epilogue issues its stores: the wait
+        // covers loads only, never the store acknowledgements.
+        if (more) {
+            __builtin_amdgcn_s_waitcnt(0);   // prefetched band (and filter DMA) have landed
+            band_store(fb, cur ^ 1);
+            if constexpr (!FIXED) if (c_end - c_begin > 1 && !w_image) {
+                w_gather_store(fw, 0, cur ^ 1);
+                for (int base = NT * MAXV; base < TK * rs * VPP; base += NT * MAXV) {
+                    WFetch f2;
+                    w_gather(nc, base, f2);
+                    w_gather_store(f2, base, cur ^ 1);
+                }
+            }
+        }
         if (c == c_end - 1) {
             if (a.splits > 1) {
                 // split-K: publish this split's partial sums; the last split of the
@@ -695,18 +725,6 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                 }
                 if (tid == 0) a.ws_cnt[tile] = 0u;   // ready for the next call
             }
-            EpiParams<FK> ep;
-            if (a.mode == QCONV_OUT_REQUANT) {
-                int32_t mraw[4 * FK];
-#pragma unroll
-                for (int e = 0; e < 4 * FK; e += 4) {
-                    const int4 q = *reinterpret_cast<const int4 *>(mlds + cb - k0 + e);
-                    mraw[e] = q.x; mraw[e + 1] = q.y; mraw[e + 2] = q.z; mraw[e + 3] = q.w;
-                }
-                make_epilogue_params<FK>(a, mraw, ep);
-            } else {
-                ep.fast = false;
-            }
             epilogue<BITS, FP, FK>(a, acc, (j0 + ti * gpk) * TP + wp * FP * 16, cb, l16, ep);
 #pragma unroll
             for (int tn = 0; tn < FP; ++tn)
@@ -714,16 +732,6 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                 for (int tm = 0; tm < FK; ++tm) acc[tn][tm] = v4i{0, 0, 0, 0};
         }
         if (more) {
-            __builtin_amdgcn_s_waitcnt(0);   // prefetched band (and filter DMA) have landed
-            band_store(fb, cur ^ 1);
-            if constexpr (!FIXED) if (c_end - c_begin > 1 && !w_image) {
-                w_gather_store(fw, 0, cur ^ 1);
-                for (int base = NT * MAXV; base < TK * rs * VPP; base += NT * MAXV) {
-                    WFetch f2;
-                    w_gather(nc, base, f2);
-                    w_gather_store(f2, base, cur ^ 1);
-                }
-            }
             __syncthreads();
             if (nti != ti) set_tile(nti);
         }

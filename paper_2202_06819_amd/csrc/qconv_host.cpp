@@ -158,8 +158,6 @@ struct Plan {
     int64_t splits = 1, cps = 0;   // split-K: splits of the chunk range, chunks per split
 };
 
-constexpr int kWideMaxV = 4;   // packed vectors a thread prefetches per stage in conv_wide
-
 int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 
 // Workgroups of this tile that fit one CU, from LDS and wave slots only.
@@ -194,7 +192,8 @@ int plan_tile(const qconv_desc *d, const qconv_layout_info &li, const qconv_tile
         if ((d->c * d->bits) % 128 != 0)
             return fail(QCONV_EUNSUPPORTED, "tile %s needs c*bits %% 128 == 0 (whole 16-byte vectors)", t.name);
         const int64_t vpp = (int64_t)t.chunk_c * d->bits / 128;
-        if (pl.rows * ncols * vpp > (int64_t)t.threads * kWideMaxV)
+        const int64_t pj = wide_band_pixels_per_thread(t.tile_p, t.threads, (int)vpp);
+        if (pl.rows * ncols > (int64_t)t.threads * pj)
             return fail(QCONV_EUNSUPPORTED, "tile %s: the input band of this shape exceeds one prefetch batch", t.name);
         const int64_t planes = t.chunk_c / 16;
         // plane strides: multiples of 256 bytes keep the four 16-lane groups of a

@@ -76,6 +76,16 @@ struct ConvArgs {
     int32_t lo, hi;         // clamp bounds, ReLU already folded into lo
 };
 
+// Band pixels one thread of a wide tile stages per channel chunk: the 4
+// packed 16-byte vectors every thread prefetches, or more for tiles whose
+// pixel count reaches the thread count (their band of zero-padded rows can
+// hold about three times as many pixels as the tile).
+constexpr int wide_band_pixels_per_thread(int tile_p, int threads, int vecs_per_pixel) {
+    const int base = 4 / vecs_per_pixel;
+    const int need = (3 * tile_p + threads - 1) / threads;
+    return base > need ? base : need;
+}
+
 using ConvLauncher = hipError_t (*)(const ConvArgs &, dim3 grid, size_t lds_bytes, hipStream_t);
 using PrepLauncher = hipError_t (*)(const ConvArgs &, uint8_t *image, int64_t elems, hipStream_t);
 
