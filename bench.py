@@ -141,6 +141,64 @@ def time_graph(g, replays: int) -> float:
     return e0.elapsed_time(e1)
 
 
+def mfma_probe(dev, blocks: int = 2048, iters: int = 2048, launches: int = 5) -> dict:
+    """The int8 rate of a kernel that issues nothing but MFMAs (all CUs, eight
+    waves per SIMD, eight independent accumulator chains per wave), timed with
+    HIP events; the shader clock it ran at from its own counters."""
+    import statistics
+    import torch
+    from paper_2202_06819_amd import qconv
+    sink = torch.empty(blocks * 256, dtype=torch.int32, device=dev)
+    stamps = torch.zeros(blocks * 4, dtype=torch.int64, device=dev)
+    qconv.probe_mfma_i8(blocks, 16, sink, stamps)
+    torch.cuda.synchronize()
+    best, ops = None, 0
+    for _ in range(launches):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        ops = qconv.probe_mfma_i8(blocks, iters, sink, stamps)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        best = ms if best is None else min(best, ms)
+    st = stamps.view(blocks, 4).cpu().double()
+    ghz = statistics.median(((st[:, 1] - st[:, 0]) / ((st[:, 3] - st[:, 2]) * 10.0)).tolist())
+    tops = ops / (best * 1e-3) / 1e12
+    nominal = 256 * 4 * 2048 * ghz * 1e9 / 1e12   # 256 CUs x 4 SIMDs x 2048 int8 ops per clock
+    return {"tops": round(tops, 1), "clock_ghz": round(ghz, 3), "nominal_tops_at_clock": round(nominal, 1),
+            "frac_of_nominal_peak": round(tops / INT8_PEAK_TOPS, 4), "ms": round(best, 4), "ops": ops,
+            "blocks": blocks, "iters": iters}
+
+
+def layer_bytes(L) -> int:
+    """Algorithmic HBM bytes of one layer: the packed input pixels the
+    convolution touches once (every pixel for a window wider than the stride,
+    only the sampled ones for a 1x1 strided filter), the packed filters once,
+    the packed output once and 4 bytes of multiplier per output channel."""
+    p = (L.h + 2 * L.pad - L.r) // L.stride + 1
+    q = (L.w + 2 * L.pad - L.s) // L.stride + 1
+    touched = L.n * p * q if (L.r == 1 and L.s == 1) else L.n * L.h * L.w
+    out_bits = L.bits if L.epilogue else 32
+    return (touched * L.c * L.bits // 8 + L.k * L.r * L.s * L.c * L.bits // 8 + L.n * p * q * L.k * out_bits // 8
+            + (4 * L.k if L.epilogue else 0))
+
+
+def cold_copies(per_copy_bytes: int, min_bytes: int = 640 << 20) -> int:
+    """How many distinct operand copies exceed the L2 caches plus the 256 MB
+    Infinity Cache, so a launch that rotates through them reads from HBM."""
+    return max(2, -(-min_bytes // max(1, per_copy_bytes)))
+
+
+def cold_time(calls, rounds: int = 3) -> float:
+    """Average microseconds per call when each call of the list works on its
+    own copy of the operands (see cold_copies); best of `rounds` passes."""
+    def run_all():
+        for c in calls:
+            c()
+    run_all()
+    return min(time_loop(run_all, 1) for _ in range(rounds)) / len(calls)
+
+
 def layer_setup(cfg: int, lid: int, L, dev):
     import torch
     import qconv_inputs as qi
@@ -156,6 +214,7 @@ def layer_setup(cfg: int, lid: int, L, dev):
 
 
 def per_layer_table(cfg: int, layers, dev, reps: int) -> list[dict]:
+    import torch
     from paper_2202_06819_amd import qconv
     import qconv_inputs as qi
     rows = []
@@ -167,11 +226,11 @@ def per_layer_table(cfg: int, layers, dev, reps: int) -> list[dict]:
         wprep = qconv.prepare_filters(L.desc(), wp, tile)
         ws = qconv.make_workspace(L.desc(), tile, splits, dev)
 
-        def make(stream=None):
-            return qconv.Conv2dCall(L.desc(), xp, wprep, requant=e is not None, mult=mult,
+        def make(stream=None, x_in=xp, out=None):
+            return qconv.Conv2dCall(L.desc(), x_in, wprep, requant=e is not None, mult=mult,
                                     shift=e.shift if e else 20, relu=e.relu if e else False,
                                     clamp=(e.lo, e.hi) if e else (0, 15), tile=tile, prepared=True, stream=stream,
-                                    splits=splits, workspace=ws)
+                                    splits=splits, workspace=ws, out=out)
 
         call = make()
         for _ in range(5):
@@ -180,12 +239,27 @@ def per_layer_table(cfg: int, layers, dev, reps: int) -> list[dict]:
         g, _ = captured(lambda s: [make(s)], reps)
         us = time_graph(g, 3) * 1000.0 / (3 * reps)
         tops = L.ops / (us * 1e-6) / 1e12
-        rows.append({"layer": L.name, "tile": qconv.tiles()[call.tile]["name"], "splits": splits, "us": round(us, 3),
-                     "eager_us": round(eager_us, 3),
-                     "tops": round(tops, 2), "pct_int8_peak": round(100 * tops / INT8_PEAK_TOPS, 2),
-                     "gops": round(L.ops / 1e9, 4)})
-        log(f"  {L.name:28s} {us:9.2f} us {tops:8.1f} TOP/s {100 * tops / INT8_PEAK_TOPS:5.1f}%  tile {rows[-1]['tile']}"
-            f" splits {splits}")
+        nbytes = layer_bytes(L)
+        row = {"layer": L.name, "tile": qconv.tiles()[call.tile]["name"], "splits": splits, "us": round(us, 3),
+               "eager_us": round(eager_us, 3),
+               "tops": round(tops, 2), "pct_int8_peak": round(100 * tops / INT8_PEAK_TOPS, 2),
+               "gops": round(L.ops / 1e9, 4), "alg_bytes": nbytes,
+               "gbs": round(nbytes / (us * 1e-6) / 1e9, 1)}
+        if L.r == 1 and L.s == 1:
+            # HBM-bound layer: also timed cold, each launch on its own copy of x and y
+            xb, yb = xp.numel() * xp.element_size(), call.out.numel() * call.out.element_size()
+            n_cp = cold_copies(xb + yb)
+            big_x = torch.empty((n_cp,) + tuple(xp.shape), dtype=xp.dtype, device=dev)
+            big_x.copy_(xp.unsqueeze(0).expand_as(big_x))
+            big_y = torch.empty((n_cp,) + tuple(call.out.shape), dtype=call.out.dtype, device=dev)
+            cold_us = cold_time([make(x_in=big_x[i], out=big_y[i]) for i in range(n_cp)])
+            del big_x, big_y
+            row.update({"cold_us": round(cold_us, 3), "cold_gbs": round(nbytes / (cold_us * 1e-6) / 1e9, 1),
+                        "cold_copies": n_cp})
+        rows.append(row)
+        log(f"  {L.name:28s} {us:9.2f} us {tops:8.1f} TOP/s {100 * tops / INT8_PEAK_TOPS:5.1f}%  "
+            f"{row['gbs']:7.1f} GB/s  tile {row['tile']} splits {splits}"
+            + (f"  cold {row['cold_us']:.2f} us {row['cold_gbs']:.0f} GB/s" if "cold_us" in row else ""))
     return rows
 
 
@@ -221,13 +295,13 @@ def chain_time(cfg: int, layers, dev, reps: int) -> dict:
     return out
 
 
-def cpu_baseline(L, seconds: float) -> dict:
+def cpu_baseline(L, seconds: float, threads: int | None = None) -> dict:
     """The oracle, as it stands, on the host cores: pack + conv + requant + repack
-    of the same layer, repeated for about `seconds`."""
+    of the same layer, repeated for about `seconds` (all cores by default)."""
     import oracle
     import qconv_inputs as qi
     t = qi.layer_tensors(1, 0, L)
-    threads = oracle.max_threads()
+    threads = threads or oracle.max_threads()
     e = L.epilogue
     reps, t0 = 0, time.perf_counter()
     while True:
@@ -240,7 +314,7 @@ def cpu_baseline(L, seconds: float) -> dict:
             break
     return {"value": round(L.ops * reps / el / 1e12, 6), "unit": "TOP/s", "cores": threads, "kind": "oracle",
             "sample": f"{reps} full passes of the benchmark layer ({L.name}: relayout+pack, direct conv, "
-                      f"requant, repack) in {el:.1f} s on {threads} OpenMP threads"}
+                      f"requant, repack) in {el:.1f} s on {threads} OpenMP thread{'s' if threads > 1 else ''}"}
 
 
 def main() -> int:
@@ -329,13 +403,20 @@ def main() -> int:
     pack_us = time_graph(g_pack, 5) * 1000.0 / (5 * reps)
     conv_tops = L.ops / (conv_us * 1e-6) / 1e12
     pack_bytes = L.n * L.c * L.h * L.w + L.n * L.h * L.w * L.c // 2
-    p_out = (L.h + 2 * L.pad - L.r) // L.stride + 1
-    q_out = (L.w + 2 * L.pad - L.s) // L.stride + 1
-    conv_bytes = (L.n * L.h * L.w * L.c * L.bits // 8 + L.k * L.r * L.s * L.c * L.bits // 8
-                  + L.n * p_out * q_out * L.k * L.bits // 8 + 4 * L.k)
+    conv_bytes = layer_bytes(L)
     pack_gbs = pack_bytes / (pack_us * 1e-6) / 1e9
     log(f"conv kernel {conv_us:.2f} us = {conv_tops:.1f} TOP/s ({100 * conv_tops / INT8_PEAK_TOPS:.1f}% of int8 peak); "
         f"pack kernel {pack_us:.2f} us = {pack_gbs:.0f} GB/s")
+    # the pack kernel cold: every launch on its own copy, so its bytes come from HBM
+    n_cp = cold_copies(x.numel() + xp.numel() * xp.element_size())
+    big_x = torch.empty((n_cp,) + tuple(x.shape), dtype=x.dtype, device=dev)
+    big_x.copy_(x.unsqueeze(0).expand_as(big_x))
+    big_p = torch.empty((n_cp,) + tuple(xp.shape), dtype=xp.dtype, device=dev)
+    pack_cold_us = cold_time([qconv.PackCall(big_x[i], L.bits, L.x_signed, out=big_p[i]) for i in range(n_cp)])
+    del big_x, big_p
+    probe = mfma_probe(dev)
+    log(f"pack kernel cold ({n_cp} copies): {pack_cold_us:.2f} us = {pack_bytes / (pack_cold_us * 1e-6) / 1e9:.0f} GB/s; "
+        f"MFMA-only probe {probe['tops']:.0f} TOP/s at {probe['clock_ghz']:.2f} GHz")
 
     workload = (f"conv2d n{L.n} {L.h}x{L.w} {L.c}->{L.k} {L.r}x{L.s} stride {L.stride} pad {L.pad}, "
                 f"{L.bits}-bit, fused requant+repack")
@@ -361,10 +442,13 @@ def main() -> int:
                      "frac": round(conv_tops / INT8_PEAK_TOPS, 5), "traffic": traffic,
                      "kernel": "conv_wide" if tile_name.startswith("wide") else "conv_staged",
                      "avg_us": round(conv_us, 3), "algorithmic_ops_per_launch": L.ops,
-                     "algorithmic_bytes_per_launch": conv_bytes, "kernel_digest": kernel_digest(tile_name)},
+                     "algorithmic_bytes_per_launch": conv_bytes, "kernel_digest": kernel_digest(tile_name),
+                     "frac_of_mfma_probe": round(conv_tops / probe["tops"], 5)},
         "kernels": {"conv_us": round(conv_us, 3), "pack_us": round(pack_us, 3),
                     "pack_gbs": round(pack_gbs, 1), "pack_frac_hbm": round(pack_gbs / HBM_PEAK_GBS, 4),
-                    "pack_algorithmic_bytes": pack_bytes},
+                    "pack_algorithmic_bytes": pack_bytes, "pack_cold_us": round(pack_cold_us, 3),
+                    "pack_cold_gbs": round(pack_bytes / (pack_cold_us * 1e-6) / 1e9, 1), "pack_cold_copies": n_cp},
+        "mfma_probe": probe,
     }
 
     tables = [] if args.tables == "none" else [int(v) for v in args.tables.split(",") if v]
@@ -381,6 +465,8 @@ def main() -> int:
     if not args.no_cpu:
         log(f"cpu baseline: oracle for ~{args.cpu_seconds:.0f} s ...")
         result["cpu_baseline"] = cpu_baseline(L, args.cpu_seconds)
+        one = cpu_baseline(L, max(1.0, args.cpu_seconds / 3), threads=1)
+        result["cpu_baseline"]["single_core"] = {"value": one["value"], "unit": one["unit"], "sample": one["sample"]}
         log(f"  {result['cpu_baseline']}")
     print(json.dumps(result), flush=True)
     return 0

@@ -257,6 +257,27 @@ const char *qconv_strerror(int status);
 const char *qconv_last_error(void);
 
 /*
+ * qconv_probe_mfma_i8 -- measurement aid, not part of the convolution: a
+ * kernel that issues nothing but v_mfma_i32_16x16x64_i8 (four waves per
+ * workgroup, eight independent accumulator chains per wave), so a caller can
+ * time the int8 rate the matrix cores sustain on this device and report a
+ * convolution kernel against it as well as against the nominal peak (the
+ * evaluation of Sec. 4 rates kernels by their throughput).
+ *   blocks  workgroups, 1 .. 2^20;  iters  rounds of eight MFMAs per wave, 1 .. 2^24
+ *   sink    device int32[blocks * 256], 4-byte aligned: one sum per lane, written
+ *           so the work stays live (its values mean nothing)
+ *   stamps  device uint64[blocks * 4], 8-byte aligned: per workgroup, wave 0's
+ *           shader-clock counter before and after its loop, then the 100 MHz
+ *           constant counter before and after; their ratio is the shader clock
+ *   ops     host, may be NULL: int8 operations one launch performs
+ *           (blocks * 4 * iters * 8 * 32768)
+ * QCONV_EINVAL for out-of-range sizes or NULL/misaligned buffers; QCONV_EHIP
+ * if the launch is rejected.  Asynchronous on `stream`.
+ */
+int qconv_probe_mfma_i8(int32_t blocks, int32_t iters, int32_t *sink, uint64_t *stamps, int64_t *ops,
+                        void *stream);
+
+/*
  * Host-only self-check of the index arithmetic the kernels use (run-time
  * constant division); touches no device.  Returns 0 when it holds.
  */

@@ -640,6 +640,19 @@ int qconv2d_prepared(const qconv_desc *d, const void *x, const void *w_prepared,
                     stream);
 }
 
+int qconv_probe_mfma_i8(int32_t blocks, int32_t iters, int32_t *sink, uint64_t *stamps, int64_t *ops, void *stream) {
+    g_err[0] = 0;
+    if (blocks < 1 || blocks > (1 << 20) || iters < 1 || iters > (1 << 24))
+        return fail(QCONV_EINVAL, "blocks must be in [1, 2^20] and iters in [1, 2^24] (got %d, %d)", blocks, iters);
+    if (!sink || !stamps) return fail(QCONV_EINVAL, "sink and stamps must be device pointers");
+    if (((uintptr_t)stamps & 7u) != 0 || ((uintptr_t)sink & 3u) != 0)
+        return fail(QCONV_EINVAL, "stamps must be 8-byte and sink 4-byte aligned");
+    if (ops) *ops = mfma_probe_ops(blocks, iters);
+    hipError_t e = launch_mfma_probe(blocks, iters, sink, stamps, (hipStream_t)stream);
+    if (e != hipSuccess) return fail(QCONV_EHIP, "probe launch: %s", hipGetErrorString(e));
+    return QCONV_OK;
+}
+
 // Host-only consistency checks of the helpers the kernels rely on; returns 0
 // when they hold.  Exposed so CPU tests can run them without a device.
 int qconv_selftest(void) {

@@ -87,9 +87,10 @@ def lib() -> ctypes.CDLL:
                                        _vp, ctypes.c_size_t, _vp]
         L.qconv_workspace_bytes.argtypes = [P(QConvDesc), _i32, _i32, P(ctypes.c_size_t)]
         L.qconv_max_splits.argtypes = [P(QConvDesc), _i32]
+        L.qconv_probe_mfma_i8.argtypes = [_i32, _i32, _vp, _vp, P(_i64), _vp]
         for f in ("qconv_layout", "qconv_pack", "qconv2d", "qconv_tile_count", "qconv_tile_get", "qconv_tile_check",
                   "qconv_default_tile", "qconv_selftest", "qconv_prepared_filter_bytes", "qconv_prepare_filters",
-                  "qconv2d_prepared", "qconv_workspace_bytes", "qconv_max_splits"):
+                  "qconv2d_prepared", "qconv_workspace_bytes", "qconv_max_splits", "qconv_probe_mfma_i8"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
         return L
@@ -182,6 +183,21 @@ def prepare_filters(d: dict, w_packed: torch.Tensor, tile: int = -1, out: torch.
                                      _vp(_stream(stream)))
     _check(rc, "qconv_prepare_filters")
     return out
+
+
+def probe_mfma_i8(blocks: int, iters: int, sink: torch.Tensor, stamps: torch.Tensor, stream=None) -> int:
+    """Launch the MFMA-only rate probe (a measurement aid); returns the int8
+    operations the launch performs.  `sink` is int32 [blocks*256] and `stamps`
+    int64 [blocks*4] on the device (shader-clock start/end, 100 MHz start/end
+    per workgroup)."""
+    if sink.dtype != torch.int32 or stamps.dtype != torch.int64:
+        raise QConvError(EINVAL, "sink must be int32 and stamps int64")
+    ops = _i64(0)
+    rc = lib().qconv_probe_mfma_i8(int(blocks), int(iters), _dev_ptr(sink, "sink", 4 * 256 * int(blocks)),
+                                   _dev_ptr(stamps, "stamps", 8 * 4 * int(blocks)), ctypes.byref(ops),
+                                   _vp(_stream(stream)))
+    _check(rc, "qconv_probe_mfma_i8")
+    return int(ops.value)
 
 
 def _stream(stream) -> int:

@@ -278,3 +278,14 @@ def test_split_k_errors(q):
     assert L.qconv2d_prepared(*args, 2, (1 << 32) + 64, wsb, None) == -1     # overlaps x
     assert L.qconv2d_prepared(*args, 10 ** 6, 1 << 35, wsb, None) == -2      # more splits than chunks
     assert L.qconv2d_prepared(*args, 0, None, 0, None) == -2
+
+
+def test_mfma_probe_argument_errors(q):
+    L = q.lib()
+    ops = ctypes.c_int64(0)
+    assert L.qconv_probe_mfma_i8(0, 1, 1 << 32, 1 << 33, ctypes.byref(ops), None) == -1
+    assert L.qconv_probe_mfma_i8(1, 0, 1 << 32, 1 << 33, ctypes.byref(ops), None) == -1
+    assert L.qconv_probe_mfma_i8((1 << 20) + 1, 1, 1 << 32, 1 << 33, ctypes.byref(ops), None) == -1
+    assert L.qconv_probe_mfma_i8(1, 1, None, 1 << 33, ctypes.byref(ops), None) == -1
+    assert L.qconv_probe_mfma_i8(1, 1, 1 << 32, (1 << 33) + 4, ctypes.byref(ops), None) == -1
+    assert ops.value == 0
