@@ -674,6 +674,8 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         // and staged before this stage's epilogue issues its stores: the wait
         // covers loads only, never the store acknowledgements.
         if (more) {
+            // with a single band buffer every wave must be done reading it
+            if (a.off_b1 == a.off_b0) __syncthreads();
             __builtin_amdgcn_s_waitcnt(0);   // prefetched band (and filter DMA) have landed
             band_store(fb, cur ^ 1);
             if constexpr (!FIXED) if (c_end - c_begin > 1 && !w_image) {

@@ -169,8 +169,11 @@ int64_t per_cu_estimate(const qconv_tile_info &t, int64_t lds) {
 
 // per_cu: workgroups per CU to plan the persistent grid for (0 = estimate).
 // splits: requested split-K factor (wide tiles); normalised so no split is empty.
+// one_band: a persistent single-chunk plan keeps one LDS band buffer (the
+// kernel then adds a barrier before restaging it), so that more workgroups fit
+// a CU and their phases overlap.
 int plan_tile(const qconv_desc *d, const qconv_layout_info &li, const qconv_tile_info &t, Plan *out,
-              int64_t per_cu = 0, int64_t splits = 1) {
+              int64_t per_cu = 0, int64_t splits = 1, bool one_band = false) {
     if (t.bits != d->bits)
         return fail(QCONV_EUNSUPPORTED, "tile %s is built for %d-bit operands", t.name, t.bits);
     if ((t.x_signed >= 0 && t.x_signed != d->x_signed) || (t.w_signed >= 0 && t.w_signed != d->w_signed))
@@ -237,12 +240,19 @@ int plan_tile(const qconv_desc *d, const qconv_layout_info &li, const qconv_tile
             pl.lds = single;
             pl.grid = tiles;
         } else {
-            pl.off_b0 = 0;
-            pl.off_b1 = bbuf;
-            pl.off_w0 = 2 * bbuf;
-            pl.off_w1 = pl.off_w0 + (nchunks > 1 ? wbuf : 0);
-            pl.off_m = pl.off_w1 + wbuf;
-            pl.lds = pl.off_m + mbytes;
+            if (one_band && nchunks == 1) {
+                pl.off_b0 = pl.off_b1 = 0;
+                pl.off_w0 = pl.off_w1 = bbuf;
+                pl.off_m = bbuf + wbuf;
+                pl.lds = single;
+            } else {
+                pl.off_b0 = 0;
+                pl.off_b1 = bbuf;
+                pl.off_w0 = 2 * bbuf;
+                pl.off_w1 = pl.off_w0 + (nchunks > 1 ? wbuf : 0);
+                pl.off_m = pl.off_w1 + wbuf;
+                pl.lds = pl.off_m + mbytes;
+            }
             const int64_t pc = per_cu > 0 ? per_cu : per_cu_estimate(t, pl.lds);
             const int64_t gpk = std::min<int64_t>(pl.mtiles, std::max<int64_t>(1, (kNumCUs * pc + pl.ktiles - 1) / pl.ktiles));
             pl.grid = gpk * pl.ktiles;
@@ -516,6 +526,16 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, te.info.threads, (size_t)pl.lds) == hipSuccess &&
             occ > 0) {
             rc = plan_tile(d, li, te.info, &pl, occ);
+            if (rc) return rc;
+        }
+        // a single-chunk layer whose second band buffer is what keeps another
+        // workgroup off the CU runs with one band buffer instead
+        Plan one;
+        int occ1 = 0;
+        if (occ > 0 && plan_tile(d, li, te.info, &one, 0, 1, true) == QCONV_OK && one.lds < pl.lds &&
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ1, kernel, te.info.threads, (size_t)one.lds) == hipSuccess &&
+            occ1 > occ) {
+            rc = plan_tile(d, li, te.info, &pl, occ1, 1, true);
             if (rc) return rc;
         }
     }

@@ -119,6 +119,33 @@ def test_resnet_shapes_every_tile_prepared(shape):
                     f"{name} tile {tid} prepared raw")
 
 
+@pytest.mark.parametrize("shape", [
+    # name, n, h, c, k, r, stride, pad -- enough output tiles that workgroups walk several
+    # of them (persistent plans, with one or two LDS band buffers)
+    ("n32_56_64to64_3x3", 32, 56, 64, 64, 3, 1, 1),
+    ("n64_56_64to256_1x1", 64, 56, 64, 256, 1, 1, 0),
+    ("n64_28_128to128_3x3", 64, 28, 128, 128, 3, 1, 1),
+], ids=lambda v: v[0])
+def test_persistent_plans_every_wide_tile(shape):
+    """Large batches, where each workgroup stages several output tiles in turn."""
+    q = _qconv()
+    name, n, h, c, k, r, stride, pad = shape
+    L = qi.Layer(name, n, h, h, c, k, r, r, stride, pad, w_range=(-7, 7))
+    t = qi.layer_tensors(600, c + k + r, L)
+    sh = stress_shift(L, L.x_range, L.w_range)
+    ref = ref_layer(L, t, requant=True, shift=sh)
+    ref_raw = ref_layer(L, t, requant=False)
+    wide = [tt["id"] for tt in q.tiles() if tt["variant"] == 2 and q.tile_status(L.desc(), tt["id"]) == 0]
+    assert wide
+    for tid in wide:
+        announce(f"{name} tile {tid} prepared requant shift={sh}")
+        assert_same(gpu_layer(L, t, requant=True, tile=tid, shift=sh, prepared=True)["y"], ref["y_packed"],
+                    f"{name} tile {tid} prepared")
+    announce(f"{name} tile {wide[0]} prepared raw")
+    assert_same(gpu_layer(L, t, requant=False, tile=wide[0], prepared=True)["y"], ref_raw["acc"],
+                f"{name} tile {wide[0]} prepared raw")
+
+
 def test_config1_raw_default_tile():
     L = qi.config1()[0]
     t = qi.layer_tensors(1, 0, L)
