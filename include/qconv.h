@@ -234,6 +234,47 @@ int qconv2d_prepared(const qconv_desc *d, const void *x, const void *w_prepared,
 int qconv_max_splits(const qconv_desc *d, int32_t tile_id);
 int qconv_workspace_bytes(const qconv_desc *d, int32_t tile_id, int32_t splits, size_t *bytes);
 
+/*
+ * Schedules.  The knobs of the schedule search space (Sec. 4.1: warps per
+ * block along M and N, MMA tiles per warp along M and N, the input-channel
+ * chunk -- here fixed per compiled tile -- and the loop order), as they exist
+ * in this implementation, plus the launch knobs it adds.  Every valid
+ * schedule computes the same bytes; only the time differs, which is what a
+ * schedule search measures.
+ *   tile_id       compiled tile (qconv_tile_get: waves and fragments per
+ *                 workgroup along pixels and channels, chunk); -1 = the
+ *                 built-in choice
+ *   splits        split-K factor over channel chunks, 1 .. qconv_max_splits
+ *                 (1 for staged tiles)
+ *   wg_per_cu     workgroups per CU a persistent grid is sized for (1..16);
+ *                 0 = the runtime's occupancy figure.  Ignored when every
+ *                 workgroup gets a single stage or with a split.
+ *   band_buffers  LDS band buffers of a persistent single-chunk plan: 1 (one
+ *                 more barrier per stage, less LDS), 2, or 0 = whichever lets
+ *                 more workgroups share a CU.  Ignored where it does not apply.
+ *   xcd_order     1 = consecutive workgroup tiles are placed on one XCD so
+ *                 neighbouring tiles share its L2 (the default elsewhere);
+ *                 0 = the hardware's round-robin order
+ * qconv_schedule_check -- host only: QCONV_OK if the schedule can run `d`
+ *   (QCONV_EINVAL for a knob out of range, else what the call would return).
+ * qconv2d_scheduled -- qconv2d_prepared with every knob given; the prepared
+ *   filters must be those of s->tile_id; `workspace` as for split-K above.
+ *   qconv2d_prepared(..., tile_id, splits, ...) is the schedule
+ *   {tile_id, splits, 0, 0, 1}.
+ */
+typedef struct {
+    int32_t tile_id;
+    int32_t splits;
+    int32_t wg_per_cu;
+    int32_t band_buffers;
+    int32_t xcd_order;
+} qconv_schedule;
+
+int qconv_schedule_check(const qconv_desc *d, const qconv_schedule *s);
+int qconv2d_scheduled(const qconv_desc *d, const void *x, const void *w_prepared, size_t w_prepared_bytes,
+                      const qconv_epilogue *epi, void *y, const qconv_schedule *s, void *workspace,
+                      size_t workspace_bytes, void *stream);
+
 /* Number of compiled tile configurations; ids are 0 .. count-1. */
 int qconv_tile_count(void);
 

@@ -349,7 +349,7 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     // j0 + gpk, ... of one channel tile over all channel chunks.  With a split
     // (a.splits > 1) it owns one output tile and the chunk range of its split;
     // the splits of a tile have consecutive logical numbers (one XCD).
-    const int lb = xcd_block(blockIdx.x, gridDim.x);
+    const int lb = a.xcd_order ? xcd_block(blockIdx.x, gridDim.x) : (int)blockIdx.x;
     const int sp = a.splits > 1 ? lb % a.splits : 0;
     const int lt = a.splits > 1 ? lb / a.splits : lb;
     const int kt = lt % a.ktiles;

@@ -464,9 +464,11 @@ int ensure_lds_attribute(const void *kernel, int tile_id, int inst, int64_t lds)
 // prepared filters of tile_id (prepared == true, w_bytes_given bytes).
 // splits > 1 (prepared filters only): split-K over channel chunks with its
 // workspace in `workspace`.
+// wg_per_cu, band_buffers, xcd_order: the launch knobs of a qconv_schedule.
 int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, size_t w_bytes_given,
              const qconv_epilogue *epi, void *y, void *workspace, size_t workspace_bytes, int32_t tile_id,
-             int32_t splits, void *stream) {
+             int32_t splits, void *stream, int32_t wg_per_cu = 0, int32_t band_buffers = 0,
+             int32_t xcd_order = 1) {
     qconv_layout_info li;
     int rc = check_desc(d, &li);
     if (rc) return rc;
@@ -523,19 +525,21 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
         rc = ensure_lds_attribute(kernel, tile_id, inst, pl.lds);
         if (rc) return rc;
         int occ = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, te.info.threads, (size_t)pl.lds) == hipSuccess &&
-            occ > 0) {
-            rc = plan_tile(d, li, te.info, &pl, occ);
-            if (rc) return rc;
-        }
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, te.info.threads, (size_t)pl.lds) != hipSuccess)
+            occ = 0;
         // a single-chunk layer whose second band buffer is what keeps another
-        // workgroup off the CU runs with one band buffer instead
+        // workgroup off the CU runs with one band buffer instead (automatic
+        // choice; band_buffers forces either)
         Plan one;
         int occ1 = 0;
-        if (occ > 0 && plan_tile(d, li, te.info, &one, 0, 1, true) == QCONV_OK && one.lds < pl.lds &&
-            hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ1, kernel, te.info.threads, (size_t)one.lds) == hipSuccess &&
-            occ1 > occ) {
-            rc = plan_tile(d, li, te.info, &pl, occ1, 1, true);
+        const bool one_ok = plan_tile(d, li, te.info, &one, 0, 1, true) == QCONV_OK && one.lds < pl.lds;
+        if (one_ok &&
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ1, kernel, te.info.threads, (size_t)one.lds) != hipSuccess)
+            occ1 = 0;
+        const bool use_one = band_buffers == 1 ? one_ok : (band_buffers == 2 ? false : one_ok && occ > 0 && occ1 > occ);
+        const int pc = wg_per_cu > 0 ? wg_per_cu : (use_one ? occ1 : occ);
+        if (pc > 0 || use_one) {
+            rc = plan_tile(d, li, te.info, &pl, pc > 0 ? pc : 0, 1, use_one);
             if (rc) return rc;
         }
     }
@@ -546,6 +550,7 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
     a.yptr = static_cast<uint8_t *>(y);
     a.mult = requant ? epi->mult : nullptr;
     a.w_image = (prepared && te.info.variant == QCONV_VARIANT_WIDE) ? 1 : 0;
+    a.xcd_order = xcd_order;
     if (wsb > 0) {
         a.ws_part = static_cast<int32_t *>(workspace);
         a.ws_cnt = reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(workspace) + split_part_bytes(te.info, pl));
@@ -573,6 +578,37 @@ int qconv2d(const qconv_desc *d, const void *x, const void *w, const qconv_epilo
             size_t workspace_bytes, int32_t tile_id, void *stream) {
     g_err[0] = 0;
     return run_conv(d, x, w, false, 0, epi, y, workspace, workspace_bytes, tile_id, 1, stream);
+}
+
+static int check_schedule_knobs(const qconv_schedule *s) {
+    if (!s) return fail(QCONV_EINVAL, "schedule must be non-NULL");
+    if (s->wg_per_cu < 0 || s->wg_per_cu > 16) return fail(QCONV_EINVAL, "wg_per_cu must be in [0, 16]");
+    if (s->band_buffers < 0 || s->band_buffers > 2) return fail(QCONV_EINVAL, "band_buffers must be 0, 1 or 2");
+    if (s->xcd_order != 0 && s->xcd_order != 1) return fail(QCONV_EINVAL, "xcd_order must be 0 or 1");
+    if (s->splits < 1) return fail(QCONV_EUNSUPPORTED, "splits must be >= 1");
+    return QCONV_OK;
+}
+
+int qconv_schedule_check(const qconv_desc *d, const qconv_schedule *s) {
+    g_err[0] = 0;
+    int rc = check_schedule_knobs(s);
+    if (rc) return rc;
+    qconv_layout_info li;
+    rc = check_desc(d, &li);
+    if (rc) return rc;
+    rc = resolve_tile(d, li, s->tile_id);
+    if (rc < 0) return rc;
+    return plan_tile(d, li, tile_table()[rc].info, nullptr, 0, s->splits);
+}
+
+int qconv2d_scheduled(const qconv_desc *d, const void *x, const void *w_prepared, size_t w_prepared_bytes,
+                      const qconv_epilogue *epi, void *y, const qconv_schedule *s, void *workspace,
+                      size_t workspace_bytes, void *stream) {
+    g_err[0] = 0;
+    int rc = check_schedule_knobs(s);
+    if (rc) return rc;
+    return run_conv(d, x, w_prepared, true, w_prepared_bytes, epi, y, workspace, workspace_bytes, s->tile_id,
+                    s->splits, stream, s->wg_per_cu, s->band_buffers, s->xcd_order);
 }
 
 int qconv_workspace_bytes(const qconv_desc *d, int32_t tile_id, int32_t splits, size_t *bytes) {

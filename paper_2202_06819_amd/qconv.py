@@ -49,6 +49,22 @@ class QConvTileInfo(ctypes.Structure):
                                     "tile_k", "threads", "variant", "x_signed", "w_signed")] + [("name", ctypes.c_char * 64)]
 
 
+class QConvSchedule(ctypes.Structure):
+    _fields_ = [(f, _i32) for f in ("tile_id", "splits", "wg_per_cu", "band_buffers", "xcd_order")]
+
+
+SCHEDULE_KNOBS = ("tile_id", "splits", "wg_per_cu", "band_buffers", "xcd_order")
+
+
+def make_schedule(sch: dict | QConvSchedule) -> QConvSchedule:
+    """A qconv_schedule from a dict (missing launch knobs take their defaults)."""
+    if isinstance(sch, QConvSchedule):
+        return sch
+    full = {"tile_id": -1, "splits": 1, "wg_per_cu": 0, "band_buffers": 0, "xcd_order": 1}
+    full.update({k: int(v) for k, v in sch.items() if k in SCHEDULE_KNOBS})
+    return QConvSchedule(**full)
+
+
 class QConvError(RuntimeError):
     def __init__(self, status: int, what: str):
         self.status = status
@@ -88,9 +104,12 @@ def lib() -> ctypes.CDLL:
         L.qconv_workspace_bytes.argtypes = [P(QConvDesc), _i32, _i32, P(ctypes.c_size_t)]
         L.qconv_max_splits.argtypes = [P(QConvDesc), _i32]
         L.qconv_probe_mfma_i8.argtypes = [_i32, _i32, _vp, _vp, P(_i64), _vp]
+        L.qconv_schedule_check.argtypes = [P(QConvDesc), P(QConvSchedule)]
+        L.qconv2d_scheduled.argtypes = [P(QConvDesc), _vp, _vp, ctypes.c_size_t, P(QConvEpilogue), _vp,
+                                        P(QConvSchedule), _vp, ctypes.c_size_t, _vp]
         for f in ("qconv_layout", "qconv_pack", "qconv2d", "qconv_tile_count", "qconv_tile_get", "qconv_tile_check",
                   "qconv_default_tile", "qconv_selftest", "qconv_prepared_filter_bytes", "qconv_prepare_filters",
-                  "qconv2d_prepared", "qconv_workspace_bytes", "qconv_max_splits", "qconv_probe_mfma_i8"):
+                  "qconv2d_prepared", "qconv_workspace_bytes", "qconv_max_splits", "qconv_probe_mfma_i8", "qconv_schedule_check", "qconv2d_scheduled"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
         return L
@@ -146,6 +165,11 @@ def prepared_filter_bytes(d: dict, tile: int = -1) -> int:
     _check(lib().qconv_prepared_filter_bytes(ctypes.byref(make_desc(d)), int(tile), ctypes.byref(n)),
            "qconv_prepared_filter_bytes")
     return int(n.value)
+
+
+def schedule_status(d: dict, sch: dict) -> int:
+    """QCONV_OK if the schedule can run the shape, else the status the call would return."""
+    return lib().qconv_schedule_check(ctypes.byref(make_desc(d)), ctypes.byref(make_schedule(sch)))
 
 
 def max_splits(d: dict, tile: int = -1) -> int:
@@ -310,7 +334,13 @@ class Conv2dCall:
     def __init__(self, d: dict, x: torch.Tensor, w: torch.Tensor, *, requant: bool = False,
                  mult: torch.Tensor | None = None, shift: int = 20, relu: bool = True, clamp: tuple = (0, 15),
                  out: torch.Tensor | None = None, tile: int = -1, stream=None, prepared: bool = False,
-                 splits: int = 1, workspace: torch.Tensor | None = None):
+                 splits: int = 1, workspace: torch.Tensor | None = None, schedule: dict | None = None):
+        """With `schedule` (a dict of qconv_schedule knobs; `w` prepared for its
+        tile) the call goes through qconv2d_scheduled."""
+        if schedule is not None:
+            prepared = True
+            tile = int(schedule.get("tile_id", tile))
+            splits = int(schedule.get("splits", 1))
         self.desc = make_desc(d)
         info = layout(d)
         bits = self.desc.bits
@@ -339,10 +369,17 @@ class Conv2dCall:
             self.workspace = workspace
             ws_ptr, ws_bytes = (None, 0) if workspace is None else (_dev_ptr(workspace, "workspace"),
                                                                    workspace.numel() * workspace.element_size())
-            self._args = (ctypes.byref(self.desc), _dev_ptr(x, "x", info["x_bytes"]), _dev_ptr(w, "w", wb),
-                          w.numel() * w.element_size(), ctypes.byref(self.epi), _dev_ptr(out, "y", y_bytes),
-                          self.tile, self.splits, ws_ptr, ws_bytes, _vp(_stream(stream)))
-            self._fn = lib().qconv2d_prepared
+            if schedule is not None:
+                self.schedule = make_schedule(dict(schedule, tile_id=self.tile, splits=self.splits))
+                self._args = (ctypes.byref(self.desc), _dev_ptr(x, "x", info["x_bytes"]), _dev_ptr(w, "w", wb),
+                              w.numel() * w.element_size(), ctypes.byref(self.epi), _dev_ptr(out, "y", y_bytes),
+                              ctypes.byref(self.schedule), ws_ptr, ws_bytes, _vp(_stream(stream)))
+                self._fn = lib().qconv2d_scheduled
+            else:
+                self._args = (ctypes.byref(self.desc), _dev_ptr(x, "x", info["x_bytes"]), _dev_ptr(w, "w", wb),
+                              w.numel() * w.element_size(), ctypes.byref(self.epi), _dev_ptr(out, "y", y_bytes),
+                              self.tile, self.splits, ws_ptr, ws_bytes, _vp(_stream(stream)))
+                self._fn = lib().qconv2d_prepared
         else:
             self._args = (ctypes.byref(self.desc), _dev_ptr(x, "x", info["x_bytes"]), _dev_ptr(w, "w", info["w_bytes"]),
                           ctypes.byref(self.epi), _dev_ptr(out, "y", y_bytes), None, 0, self.tile,

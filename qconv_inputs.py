@@ -114,6 +114,14 @@ def config1() -> list[Layer]:
     return [Layer("c1_56x56_64to64_3x3_n8", 8, 56, 56, 64, 64, 3, 3, 1, 1)]
 
 
+def table1_stages() -> list[Layer]:
+    """The four 3x3 convolutions of Table 1 (ResNet-50 stages 2-5: 56x56 64->64,
+    28x28 128->128, 14x14 256->256, 7x7 512->512, stride 1, pad 1), at batch 8,
+    where each has exactly the table's 1,849,688,064 ops."""
+    return [Layer(f"t1_stage{i + 2}_{h}x{h}_{c}to{c}_3x3_n8", 8, h, h, c, c, 3, 3, 1, 1)
+            for i, (h, c) in enumerate(((56, 64), (28, 128), (14, 256), (7, 512)))]
+
+
 def _resnet18(n: int, bits: int) -> list[Layer]:
     """The 19 convolutions of ResNet-18 after the 7x7 stem, in forward order.
 

@@ -289,3 +289,31 @@ def test_mfma_probe_argument_errors(q):
     assert L.qconv_probe_mfma_i8(1, 1, None, 1 << 33, ctypes.byref(ops), None) == -1
     assert L.qconv_probe_mfma_i8(1, 1, 1 << 32, (1 << 33) + 4, ctypes.byref(ops), None) == -1
     assert ops.value == 0
+
+
+def test_schedule_check_and_errors(q):
+    L = q.lib()
+    d = D(h=14, w=14, c=256, k=256, n=4)
+    tid = _wide_tile(q, d)
+    staged = [t["id"] for t in q.tiles() if t["variant"] == 0 and q.tile_status(d, t["id"]) == 0][0]
+    base = {"tile_id": tid}
+    assert q.schedule_status(d, base) == 0
+    assert q.schedule_status(d, dict(base, splits=q.max_splits(d, tid), wg_per_cu=3, band_buffers=1,
+                                     xcd_order=0)) == 0
+    assert q.schedule_status(d, dict(base, wg_per_cu=17)) == -1
+    assert q.schedule_status(d, dict(base, wg_per_cu=-1)) == -1
+    assert q.schedule_status(d, dict(base, band_buffers=3)) == -1
+    assert q.schedule_status(d, dict(base, xcd_order=2)) == -1
+    assert q.schedule_status(d, dict(base, splits=0)) == -2
+    assert q.schedule_status(d, dict(base, splits=q.max_splits(d, tid) + 1)) == -2
+    assert q.schedule_status(d, {"tile_id": staged, "splits": 2}) == -2
+    assert q.schedule_status(d, {"tile_id": 10 ** 6}) < 0
+    assert q.schedule_status(D(bits=8, x_signed=1), base) == -2     # tile built for 4-bit
+    desc = q.make_desc(d)
+    need = q.prepared_filter_bytes(d, tid)
+    args = (ctypes.byref(desc), 1 << 32, 1 << 33, need, ctypes.byref(_epi(q)), 1 << 34)
+    assert L.qconv2d_scheduled(*args, None, None, 0, None) == -1          # no schedule
+    bad = q.make_schedule(dict(base, band_buffers=5))
+    assert L.qconv2d_scheduled(*args, ctypes.byref(bad), None, 0, None) == -1
+    two = q.make_schedule(dict(base, splits=2))
+    assert L.qconv2d_scheduled(*args, ctypes.byref(two), None, 0, None) == -3   # split-K without workspace
