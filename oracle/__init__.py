@@ -70,6 +70,8 @@ def _load():
         lib.oracle_conv2d.restype = i32
         lib.oracle_requant.argtypes = [vp, i64, i64, vp, i32, i32, i64, i64, vp]
         lib.oracle_requant.restype = i32
+        lib.oracle_requant_ext.argtypes = [vp, i64, i64, vp, vp, i32, vp, i32, i64, i64, vp]
+        lib.oracle_requant_ext.restype = i32
         lib.oracle_max_threads.argtypes = []
         lib.oracle_max_threads.restype = i32
         _lib = lib
@@ -190,16 +192,31 @@ def conv2d(x_nhwc: np.ndarray, w_krsc: np.ndarray, stride=(1, 1), pad=(0, 0),
     return acc
 
 
-def requant(acc: np.ndarray, mult: np.ndarray, shift: int, relu: bool, lo: int, hi: int) -> np.ndarray:
-    """Per-channel scale, round half up, ReLU, clamp (Sec. 3.2.2 order); channels last."""
+def requant(acc: np.ndarray, mult: np.ndarray, shift: int, relu: bool, lo: int, hi: int,
+            bias: np.ndarray | None = None, residual: np.ndarray | None = None) -> np.ndarray:
+    """Per-channel scale, round half up, ReLU, clamp (Sec. 3.2.2 order); channels last.
+    With ``bias`` (int32 per channel, accumulator units, added before scaling)
+    and/or ``residual`` (int values shaped like acc, output units, added after
+    rounding and before ReLU and clipping)."""
     acc = np.ascontiguousarray(acc, dtype=np.int32)
     mult = np.ascontiguousarray(mult, dtype=np.int32).reshape(-1)
     k = acc.shape[-1]
     if mult.size != k:
         raise OracleError("one multiplier per output channel")
     out = np.empty_like(acc)
-    rc = _load().oracle_requant(_ptr(acc), acc.size // k, k, _ptr(mult), int(shift), int(bool(relu)),
-                                int(lo), int(hi), _ptr(out))
+    if bias is None and residual is None:
+        rc = _load().oracle_requant(_ptr(acc), acc.size // k, k, _ptr(mult), int(shift), int(bool(relu)),
+                                    int(lo), int(hi), _ptr(out))
+    else:
+        b = None if bias is None else np.ascontiguousarray(bias, dtype=np.int32).reshape(-1)
+        if b is not None and b.size != k:
+            raise OracleError("one bias per output channel")
+        r = None if residual is None else np.ascontiguousarray(residual, dtype=np.int32)
+        if r is not None and r.shape != acc.shape:
+            raise OracleError("residual must be shaped like the accumulators")
+        rc = _load().oracle_requant_ext(_ptr(acc), acc.size // k, k, _ptr(mult), None if b is None else _ptr(b),
+                                        int(shift), None if r is None else _ptr(r), int(bool(relu)), int(lo), int(hi),
+                                        _ptr(out))
     if rc != OK:
         raise OracleError("requant: shift must be in [1, 62] and lo <= hi")
     return out
@@ -222,12 +239,14 @@ def pack_output(vals: np.ndarray, bits: int, is_signed: bool) -> np.ndarray:
 
 def qconv_layer(x_nchw: np.ndarray, w_kcrs: np.ndarray, *, bits: int, x_signed: bool, w_signed: bool,
                 stride=(1, 1), pad=(0, 0), mult=None, shift=None, relu=False, lo=None, hi=None,
-                threads: int = 1, packed_x: np.ndarray | None = None) -> dict:
+                threads: int = 1, packed_x: np.ndarray | None = None, bias: np.ndarray | None = None,
+                residual: np.ndarray | None = None) -> dict:
     """The whole path for one layer, step by step.
 
     Returns a dict with ``x_packed``, ``w_packed``, ``acc`` (int32 N x P x Q x K)
     and, when ``mult`` is given, ``y`` (requantised values) and ``y_packed``.
-    ``packed_x`` may be given instead of ``x_nchw`` (a chained layer's input).
+    ``packed_x`` may be given instead of ``x_nchw`` (a chained layer's input);
+    ``bias`` and ``residual`` extend the epilogue as in :func:`requant`.
     """
     if packed_x is None:
         x_packed = relayout_pack(x_nchw, bits, x_signed)
@@ -240,7 +259,7 @@ def qconv_layer(x_nchw: np.ndarray, w_kcrs: np.ndarray, *, bits: int, x_signed: 
     acc = conv2d(xv, wv, stride, pad, threads=threads)
     out = {"x_packed": x_packed, "w_packed": w_packed, "acc": acc}
     if mult is not None:
-        y = requant(acc, mult, shift, relu, lo, hi)
+        y = requant(acc, mult, shift, relu, lo, hi, bias=bias, residual=residual)
         out["y"] = y
         out["y_packed"] = pack_output(y, bits, lo < 0)
     return out

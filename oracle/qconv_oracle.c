@@ -268,6 +268,42 @@ int oracle_requant(const int32_t *acc, int64_t npix, int64_t k, const int32_t *m
     return ORACLE_OK;
 }
 
+/*
+ * The epilogue with the two additions Sec. 3.2.2 and a residual network
+ * need, element by element:
+ *
+ *   t = (acc + bias[ch]) * mult[ch]          (exact, int64; bias may be NULL = 0)
+ *   t = floor((t + 2^(shift-1)) / 2^shift)   (round half up)
+ *   t = t + res[i]                           (res may be NULL = 0)
+ *   t = max(t, 0)                            if relu
+ *   t = min(max(t, lo), hi)
+ *
+ * The bias is an offset in accumulator units (a folded batch norm's shift);
+ * the residual is a tensor already in the output's quantised units (the
+ * shortcut of a residual block), added before ReLU and clipping.  Returns
+ * ORACLE_EINVAL for shift outside [1, 62] or lo > hi.
+ */
+int oracle_requant_ext(const int32_t *acc, int64_t npix, int64_t k, const int32_t *mult, const int32_t *bias,
+                       int shift, const int32_t *res, int relu, int64_t lo, int64_t hi, int32_t *out)
+{
+    if (shift < 1 || shift > 62 || lo > hi)
+        return ORACLE_EINVAL;
+    for (int64_t t = 0; t < npix; ++t)
+        for (int64_t ko = 0; ko < k; ++ko) {
+            int64_t a = (int64_t)acc[t * k + ko] + (bias ? (int64_t)bias[ko] : 0);
+            int64_t v = a * (int64_t)mult[ko];
+            v = floor_div_pow2(v + ((int64_t)1 << (shift - 1)), shift);
+            if (res)
+                v += res[t * k + ko];
+            if (relu && v < 0)
+                v = 0;
+            if (v < lo) v = lo;
+            if (v > hi) v = hi;
+            out[t * k + ko] = (int32_t)v;
+        }
+    return ORACLE_OK;
+}
+
 /* Threads OpenMP would use by default (1 without OpenMP). */
 int oracle_max_threads(void)
 {

@@ -278,6 +278,47 @@ def test_requant_matches_exact_rationals():
             assert np.array_equal(got, ref)
 
 
+def test_requant_bias_and_residual_closed_forms():
+    """Bias is an accumulator offset added before scaling; the residual is added
+    in output units after rounding and before ReLU and clipping."""
+    m = np.full(1, 1 << 14, dtype=np.int32)      # scale 1/64 at shift 20
+
+    def rq(a, bias=0, res=0, relu=False, lo=-1000, hi=1000):
+        return int(oracle.requant(np.array([[a]], dtype=np.int32), m, 20, relu, lo, hi,
+                                  bias=np.array([bias], dtype=np.int32),
+                                  residual=np.array([[res]], dtype=np.int32))[0, 0])
+
+    assert rq(0, bias=32) == 1                # the bias alone rounds: 32/64 = 0.5 -> 1
+    assert rq(32, bias=-32) == 0              # cancels before scaling (after it would give 1 + 0 = 1)
+    assert rq(64, bias=64 * 3) == 4           # (64 + 192) / 64
+    assert rq(64, res=3) == 4                 # 1 + 3
+    assert rq(-128, res=1, relu=True) == 0    # -2 + 1 = -1, then ReLU (ReLU first would give 1)
+    assert rq(-128, res=3, relu=True) == 1    # -2 + 3
+    assert rq(960, res=3, relu=True, lo=0, hi=15) == 15   # 15 + 3 saturates
+    assert rq(31, res=0) == 0 and rq(31, bias=1) == 1     # the bias enters before the rounding
+    assert rq(-33, bias=1, res=-1) == -1      # -32/64 -> 0, then -1
+
+
+def test_requant_extensions_reduce_to_the_plain_epilogue():
+    g = np.random.default_rng(22)
+    acc = g.integers(-(2 ** 20), 2 ** 20, size=(32, 16)).astype(np.int32)
+    mult = g.integers(1 << 14, 1 << 15, size=16).astype(np.int32)
+    plain = oracle.requant(acc, mult, 20, True, 0, 15)
+    zero_b = oracle.requant(acc, mult, 20, True, 0, 15, bias=np.zeros(16, np.int32))
+    zero_r = oracle.requant(acc, mult, 20, True, 0, 15, residual=np.zeros_like(acc))
+    assert np.array_equal(plain, zero_b) and np.array_equal(plain, zero_r)
+    # a bias is the same as adding it to every accumulator of its channel
+    bias = g.integers(-(2 ** 18), 2 ** 18, size=16).astype(np.int32)
+    for relu, lo, hi in ((True, 0, 15), (False, -128, 127)):
+        assert np.array_equal(oracle.requant(acc, mult, 20, relu, lo, hi, bias=bias),
+                              oracle.requant(acc + bias, mult, 20, relu, lo, hi))
+    # without clipping, a residual shifts the rounded result exactly
+    res = g.integers(-8, 8, size=acc.shape).astype(np.int32)
+    wide = (-(2 ** 31), 2 ** 31 - 1)
+    assert np.array_equal(oracle.requant(acc, mult, 20, False, *wide, residual=res),
+                          oracle.requant(acc, mult, 20, False, *wide) + res)
+
+
 def test_requant_rejects_bad_shift():
     a = np.zeros((1, 1), dtype=np.int32)
     m = np.ones(1, dtype=np.int32)
