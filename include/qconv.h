@@ -89,16 +89,32 @@ typedef struct qconv_layout_info {
 } qconv_layout_info;
 
 /*
- * Epilogue (Sec. 3.2.2: the wide accumulator is processed first, then clipped
- * and packed):
- *   t = acc * mult[k]                         (exact, 64-bit)
+ * Epilogue (Sec. 3.2.2: the wide accumulator is processed first -- the bias
+ * addition and batch-norm scaling the section names -- then clipped and
+ * packed):
+ *   t = (acc + bias[k]) * mult[k]             (exact, 64-bit; no bias = 0)
  *   t = floor((t + 2^(shift-1)) / 2^shift)    (round half up)
+ *   t = t + residual[n, p, q, k]              (no residual = 0)
  *   t = max(t, 0) if relu
  *   t = min(max(t, clamp_lo), clamp_hi)
  * The clamp range must fit the output type: 4-bit [0,15] (unsigned output)
  * or [-8,7] (signed), 8-bit [-128,127].  The output is signed iff
- * clamp_lo < 0.  mult: DEVICE pointer to k int32 values.
- * In QCONV_OUT_RAW_I32 mode only `mode` is read.
+ * clamp_lo < 0.
+ *   mult      DEVICE pointer to k int32 values.
+ *   bias      DEVICE pointer to k int32 values, or NULL: an offset in
+ *             accumulator units (a folded batch norm's shift).  The sum
+ *             accumulator + bias is formed in int32 (scaled by 2^acc_shift,
+ *             acc_shift = 4 per signed 4-bit operand, else 0), so every value
+ *             must keep |bias| <= (2^31 - 1) / 2^acc_shift - max_abs_acc
+ *             (qconv_layout); outside that bound results wrap.
+ *   residual  DEVICE pointer, or NULL: a tensor in y's packed layout and bit
+ *             width (n x p x q x k; the shortcut of a residual block, e.g. an
+ *             earlier layer's output), 16-byte aligned; its values are read
+ *             as signed when residual_signed is 1, else unsigned.  It may be y
+ *             itself (updated in place) but must not otherwise overlap y, and
+ *             must not overlap x, w or the workspace.
+ * In QCONV_OUT_RAW_I32 mode only `mode` is read, and bias and residual must
+ * be NULL.
  */
 typedef struct qconv_epilogue {
     int32_t mode;
@@ -106,6 +122,9 @@ typedef struct qconv_epilogue {
     int32_t shift;             /* 1 .. 62 */
     int32_t relu;              /* 0 or 1 */
     int32_t clamp_lo, clamp_hi;
+    const int32_t *bias;       /* NULL = none */
+    const void *residual;      /* NULL = none */
+    int32_t residual_signed;   /* 0 or 1 */
 } qconv_epilogue;
 
 /*

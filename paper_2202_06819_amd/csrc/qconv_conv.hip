@@ -49,7 +49,7 @@ namespace qconv {
 
 // ============================================================== conv_staged
 
-template <int BITS, int WP, int WK, int FP, int FK, int CK>
+template <int BITS, int WP, int WK, int FP, int FK, int CK, bool EXT>
 __global__ void __launch_bounds__(WP * WK * 64) conv_staged(ConvArgs a) {
     constexpr int NT = WP * WK * 64;
     constexpr int TP = WP * FP * 16;
@@ -96,12 +96,16 @@ __global__ void __launch_bounds__(WP * WK * 64) conv_staged(ConvArgs a) {
         pixoff[tn] = ((vr - vlo) * a.ncols + cl) * GRAN;
     }
 
-    v4i acc[FP][FK];
-#pragma unroll
-    for (int tn = 0; tn < FP; ++tn)
-#pragma unroll
-        for (int tm = 0; tm < FK; ++tm) acc[tn][tm] = v4i{0, 0, 0, 0};
     const int cb = k0 + wk * FK * 16 + gq * 4 * FK;
+    v4i acc[FP][FK];
+    if constexpr (EXT) {
+        init_acc<FP, FK>(a, acc, a.bias ? a.bias + cb : nullptr, true, cb);
+    } else {
+#pragma unroll
+        for (int tn = 0; tn < FP; ++tn)
+#pragma unroll
+            for (int tm = 0; tm < FK; ++tm) acc[tn][tm] = v4i{0, 0, 0, 0};
+    }
     EpiParams<FK> ep;
     load_epilogue_params<FK>(a, cb, ep);
 
@@ -229,7 +233,7 @@ __global__ void __launch_bounds__(WP * WK * 64) conv_staged(ConvArgs a) {
                 }
             }
     }
-    epilogue<BITS, FP, FK>(a, acc, m0 + wp * FP * 16, cb, l16, ep);
+    epilogue<BITS, FP, FK, EXT>(a, acc, m0 + wp * FP * 16, cb, l16, ep);
 }
 
 // ============================================================== conv_wide
@@ -319,7 +323,7 @@ __device__ __forceinline__ int xcd_block(int b, int g) {
 // RC, SC: filter height and width fixed at compile time (0: taken from the
 // descriptor).  A fixed-size instance always reads prepared filters and runs a
 // fully unrolled MFMA loop with immediate LDS offsets.
-template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC>
+template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC, bool EXT>
 __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     constexpr bool FIXED = RC > 0 && SC > 0;
     constexpr int NW = WP * WK;
@@ -512,13 +516,21 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         for (int tm = 0; tm < FK; ++tm) acc[tn][tm] = v4i{0, 0, 0, 0};
 
     const int cb = k0 + wk * FK * 16 + gq * 4 * FK;
-    // the workgroup's TK multipliers go to LDS by DMA (read back in the epilogue)
+    // the workgroup's TK multipliers (and biases) go to LDS by DMA, read back
+    // for the epilogue; channels past k repeat the last one and are never stored
     int32_t *mlds = reinterpret_cast<int32_t *>(smem + a.off_m);
+    int32_t *blds = mlds + TK;
     if (a.mode == QCONV_OUT_REQUANT && wave == 0) {
         const u32x4 rm = make_rsrc(a.mult, 4 * a.k);
         for (int e = 0; e < TK; e += 64)
             if (e + lane < TK)   // TK may be 32: only the lanes of the buffer write
                 dma4(reinterpret_cast<const uint8_t *>(mlds + e), (uint32_t)min(k0 + e + lane, a.k - 1) * 4u, rm);
+    }
+    if (EXT && a.mode == QCONV_OUT_REQUANT && a.bias && wave == (NW > 1 ? 1 : 0)) {
+        const u32x4 rb = make_rsrc(a.bias, 4 * a.k);
+        for (int e = 0; e < TK; e += 64)
+            if (e + lane < TK)
+                dma4(reinterpret_cast<const uint8_t *>(blds + e), (uint32_t)min(k0 + e + lane, a.k - 1) * 4u, rb);
     }
 
     // ---- prologue: stage 0 (every load in flight before the first wait)
@@ -548,6 +560,9 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     } else {
         ep.fast = false;
     }
+    // accumulators start from the bias (in the first split of a tile only)
+    const bool bias_here = EXT && a.mode == QCONV_OUT_REQUANT && a.bias && sp == 0;
+    if (bias_here) init_acc<FP, FK>(a, acc, blds + cb - k0, false, cb);
 
     const int nit = rs * KSTEPS;
 
@@ -707,7 +722,7 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                 // workgroup then reads the other partial sums through
                 __builtin_amdgcn_s_waitcnt(0);
                 __syncthreads();
-                uint32_t *flag = reinterpret_cast<uint32_t *>(smem + a.off_m) + TK;   // past the multipliers
+                uint32_t *flag = reinterpret_cast<uint32_t *>(smem + a.off_m) + 2 * TK;   // past multipliers and biases
                 if (tid == 0)
                     *flag = __hip_atomic_fetch_add(a.ws_cnt + tile, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
                 __syncthreads();
@@ -727,11 +742,15 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                 }
                 if (tid == 0) a.ws_cnt[tile] = 0u;   // ready for the next call
             }
-            epilogue<BITS, FP, FK>(a, acc, (j0 + ti * gpk) * TP + wp * FP * 16, cb, l16, ep);
+            epilogue<BITS, FP, FK, EXT>(a, acc, (j0 + ti * gpk) * TP + wp * FP * 16, cb, l16, ep);
+            if (bias_here) {
+                init_acc<FP, FK>(a, acc, blds + cb - k0, false, cb);
+            } else {
 #pragma unroll
-            for (int tn = 0; tn < FP; ++tn)
+                for (int tn = 0; tn < FP; ++tn)
 #pragma unroll
-                for (int tm = 0; tm < FK; ++tm) acc[tn][tm] = v4i{0, 0, 0, 0};
+                    for (int tm = 0; tm < FK; ++tm) acc[tn][tm] = v4i{0, 0, 0, 0};
+            }
         }
         if (more) {
             __syncthreads();
@@ -783,22 +802,23 @@ __global__ void __launch_bounds__(256) build_filter_image(ConvArgs a, int TK, in
 
 // One operand signedness per kernel (the widening is compiled for it); 8-bit
 // operands are always signed.
-template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC>
+template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC, bool EXT>
 __global__ void __launch_bounds__(WP * WK * 64) __attribute__((amdgpu_waves_per_eu(2))) conv_wide(ConvArgs a) {
-    wide_body<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC>(a);
+    wide_body<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC, EXT>(a);
 }
 
 // ============================================================== tile registry
 
-template <int BITS, int WP, int WK, int FP, int FK, int CK>
+template <int BITS, int WP, int WK, int FP, int FK, int CK, bool EXT>
 static hipError_t launch_staged(const ConvArgs &a, dim3 grid, size_t lds, hipStream_t stream) {
-    hipLaunchKernelGGL((conv_staged<BITS, WP, WK, FP, FK, CK>), grid, dim3(WP * WK * 64), lds, stream, a);
+    hipLaunchKernelGGL((conv_staged<BITS, WP, WK, FP, FK, CK, EXT>), grid, dim3(WP * WK * 64), lds, stream, a);
     return hipGetLastError();
 }
 
-template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC>
+template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC, bool EXT>
 static hipError_t launch_wide(const ConvArgs &a, dim3 grid, size_t lds, hipStream_t stream) {
-    hipLaunchKernelGGL((conv_wide<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC>), grid, dim3(WP * WK * 64), lds, stream, a);
+    hipLaunchKernelGGL((conv_wide<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC, EXT>), grid, dim3(WP * WK * 64), lds,
+                       stream, a);
     return hipGetLastError();
 }
 
@@ -850,22 +870,25 @@ static hipError_t launch_prep(const ConvArgs &a, uint8_t *img, int64_t elems, hi
 #define QCONV_TILE_INFO(V, PREFIX, B, WP, WK, FP, FK, CK, XS, WS)                                                 \
     {0, B, WP, WK, FP, FK, CK, WP * FP * 16, WK * FK * 16, WP * WK * 64, V, XS, WS,                              \
      PREFIX #B "_w" #WP "x" #WK "_f" #FP "x" #FK "_c" #CK}
+#define QCONV_STAGED_SET(B, WP, WK, FP, FK, CK, EXT)                                                              \
+    {&launch_staged<B, WP, WK, FP, FK, CK, EXT>,                                                                  \
+     reinterpret_cast<const void *>(&conv_staged<B, WP, WK, FP, FK, CK, EXT>), {}}
 #define QCONV_STAGED_ENTRY(B, WP, WK, FP, FK, CK)                                                                 \
     {QCONV_TILE_INFO(QCONV_VARIANT_STAGED, "staged_b", B, WP, WK, FP, FK, CK, -1, -1),                           \
-     &launch_staged<B, WP, WK, FP, FK, CK>,                                                                       \
-     reinterpret_cast<const void *>(&conv_staged<B, WP, WK, FP, FK, CK>), nullptr, {}},
+     QCONV_STAGED_SET(B, WP, WK, FP, FK, CK, false), QCONV_STAGED_SET(B, WP, WK, FP, FK, CK, true), nullptr},
 // 4-bit: unsigned activations x signed filters; 8-bit: signed x signed.
 // Each wide tile also has fixed-size instances for 3x3 and 1x1 filters, used
 // with prepared filters.
+#define QCONV_WIDE_INST(B, WP, WK, FP, FK, CK, R, S, EXT)                                                         \
+    &launch_wide<B, WP, WK, FP, FK, CK, (B == 8), true, R, S, EXT>,                                               \
+        reinterpret_cast<const void *>(&conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true, R, S, EXT>)
+#define QCONV_WIDE_SET(B, WP, WK, FP, FK, CK, EXT)                                                                \
+    {QCONV_WIDE_INST(B, WP, WK, FP, FK, CK, 0, 0, EXT),                                                           \
+     {{3, 3, QCONV_WIDE_INST(B, WP, WK, FP, FK, CK, 3, 3, EXT)}, {1, 1, QCONV_WIDE_INST(B, WP, WK, FP, FK, CK, 1, 1, EXT)}}}
 #define QCONV_WIDE_ENTRY(B, WP, WK, FP, FK, CK)                                                                   \
     {QCONV_TILE_INFO(QCONV_VARIANT_WIDE, "wide_b", B, WP, WK, FP, FK, CK, (B == 8), 1),                         \
-     &launch_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 0, 0>,                                                   \
-     reinterpret_cast<const void *>(&conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 0, 0>),                    \
-     &launch_prep<B, WK, FK, CK, true>,                                                                           \
-     {{3, 3, &launch_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3>,                                           \
-       reinterpret_cast<const void *>(&conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3>)},                 \
-      {1, 1, &launch_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 1, 1>,                                           \
-       reinterpret_cast<const void *>(&conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 1, 1>)}}},
+     QCONV_WIDE_SET(B, WP, WK, FP, FK, CK, false), QCONV_WIDE_SET(B, WP, WK, FP, FK, CK, true),                 \
+     &launch_prep<B, WK, FK, CK, true>},
 
 static TileEntry g_tiles[] = {QCONV_STAGED_TILES(QCONV_STAGED_ENTRY) QCONV_WIDE_TILES(QCONV_WIDE_ENTRY)};
 

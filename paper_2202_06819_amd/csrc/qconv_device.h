@@ -123,6 +123,71 @@ __device__ __forceinline__ void load_epilogue_params(const ConvArgs &a, int cb, 
     finish_epilogue_params<FK>(a, ep);
 }
 
+// Accumulator start values: bias * 2^acc_shift of this lane's channels, or 0.
+// The bias contract keeps accumulator plus bias inside int32, so both
+// epilogue forms read the biased sum exactly.  `bsrc` holds 4*FK readable
+// entries, or, when `guarded`, is read from channel cb on with channels past
+// k as 0.
+template <int FP, int FK>
+__device__ __forceinline__ void init_acc(const ConvArgs &a, v4i (&acc)[FP][FK], const int32_t *bsrc, bool guarded,
+                                         int cb) {
+#pragma unroll
+    for (int tm = 0; tm < FK; ++tm) {
+        v4i b = v4i{0, 0, 0, 0};
+        if (a.bias) {
+            if (guarded) {
+#pragma unroll
+                for (int v = 0; v < 4; ++v) b[v] = cb + 4 * tm + v < a.k ? bsrc[4 * tm + v] : 0;
+            } else {
+                const int4 q = *reinterpret_cast<const int4 *>(bsrc + 4 * tm);
+                b = v4i{q.x, q.y, q.z, q.w};
+            }
+            b = (v4i)((__attribute__((ext_vector_type(4))) unsigned)b << (unsigned)a.acc_shift);
+        }
+#pragma unroll
+        for (int tn = 0; tn < FP; ++tn) acc[tn][tm] = b;
+    }
+}
+
+// The residual words of one pixel's channel run (the same words store_run
+// writes); zeros for a pixel past the output.
+template <int BITS, int FK>
+__device__ __forceinline__ void load_run(const ConvArgs &a, int m, int cb, uint32_t *words) {
+    constexpr int CPW = 32 / BITS;
+    constexpr int NWD = 4 * FK / CPW;
+#pragma unroll
+    for (int wd = 0; wd < NWD; ++wd) words[wd] = 0u;
+    if (m >= a.m) return;
+    const uint32_t *rw = reinterpret_cast<const uint32_t *>(a.res + (size_t)m * (a.k * BITS / 8) + cb * BITS / 8);
+    const bool vec_ok = ((a.k * BITS / 8) % (NWD * 4)) == 0;
+    if constexpr (NWD == 2) {
+        if (vec_ok && cb + 2 * CPW <= a.k) {
+            const uint2 v = *reinterpret_cast<const uint2 *>(rw);
+            words[0] = v.x;
+            words[1] = v.y;
+            return;
+        }
+    } else if constexpr (NWD == 4) {
+        if (vec_ok && cb + 4 * CPW <= a.k) {
+            const uint4 v = *reinterpret_cast<const uint4 *>(rw);
+            words[0] = v.x; words[1] = v.y; words[2] = v.z; words[3] = v.w;
+            return;
+        }
+    }
+#pragma unroll
+    for (int wd = 0; wd < NWD; ++wd)
+        if (cb + wd * CPW < a.k) words[wd] = rw[wd];
+}
+
+// Value of field `e` of a packed run (BITS bits per value).
+template <int BITS>
+__device__ __forceinline__ int32_t run_value(const uint32_t *words, int e, bool is_signed) {
+    constexpr int CPW = 32 / BITS;
+    const uint32_t w = words[e / CPW];
+    const int off = BITS * (e % CPW);
+    return is_signed ? (int32_t)__builtin_amdgcn_sbfe((int)w, off, BITS) : (int32_t)__builtin_amdgcn_ubfe(w, off, BITS);
+}
+
 // Clamp to [lo, hi] in one instruction (lo <= hi is checked on the host).
 __device__ __forceinline__ int32_t clamp_med3(int32_t x, int32_t lo, int32_t hi) {
     int32_t r;
@@ -156,13 +221,19 @@ __device__ __forceinline__ void store_run(const ConvArgs &a, int m, int cb, cons
 // Fast requantisation (see EpiParams): one v_mad_i64_i32, one v_med3_i32 and
 // one shift-or per value.  A non-negative clamp range needs no mask: the
 // clamped value already fits its field.
-template <int BITS, int FP, int FK, bool UNSIGNED_OUT>
+template <int BITS, int FP, int FK, bool UNSIGNED_OUT, bool RES>
 __device__ __forceinline__ void epilogue_fast(const ConvArgs &a, v4i (&acc)[FP][FK], int mbase, int cb, int l16,
                                               const EpiParams<FK> &ep) {
     constexpr int CPW = 32 / BITS;
     constexpr int NWD = 4 * FK / CPW;
     constexpr uint32_t VMASK = (1u << BITS) - 1u;
     const int lo = a.lo, hi = a.hi;
+    // residual words of every pixel first: their loads overlap the arithmetic
+    uint32_t rw[FP][RES ? NWD : 1];
+    if constexpr (RES) {
+#pragma unroll
+        for (int tn = 0; tn < FP; ++tn) load_run<BITS, FK>(a, mbase + tn * 16 + l16, cb, rw[tn]);
+    }
 #pragma unroll
     for (int tn = 0; tn < FP; ++tn) {
         uint32_t words[NWD];
@@ -174,7 +245,9 @@ __device__ __forceinline__ void epilogue_fast(const ConvArgs &a, v4i (&acc)[FP][
             for (int v = 0; v < 4; ++v) {
                 const int e = 4 * tm + v;
                 const int64_t s64 = (int64_t)acc[tn][tm][v] * ep.mul[e] + ((int64_t)1 << 31);
-                const uint32_t t = (uint32_t)clamp_med3((int32_t)(s64 >> 32), lo, hi);
+                int32_t r = (int32_t)(s64 >> 32);
+                if constexpr (RES) r += run_value<BITS>(rw[tn], e, a.res_signed != 0);
+                const uint32_t t = (uint32_t)clamp_med3(r, lo, hi);
                 words[e / CPW] |= (UNSIGNED_OUT ? t : (t & VMASK)) << (BITS * (e % CPW));
             }
         const int m = mbase + tn * 16 + l16;
@@ -185,7 +258,9 @@ __device__ __forceinline__ void epilogue_fast(const ConvArgs &a, v4i (&acc)[FP][
 // The epilogue for one wave (Sec. 3.2.2: work on the wide accumulator, then
 // clip and pack before the store).  acc[tn][tm][v] is output channel
 // cb + 4*tm + v of pixel mbase + 16*tn + l16.
-template <int BITS, int FP, int FK>
+// EXT: the kernel supports a bias (already in the accumulators, see init_acc)
+// and a residual; without it neither is looked at.
+template <int BITS, int FP, int FK, bool EXT>
 __device__ __forceinline__ void epilogue(const ConvArgs &a, v4i (&acc)[FP][FK], int mbase, int cb, int l16,
                                          const EpiParams<FK> &ep) {
     constexpr int CPW = 32 / BITS;   // channels per 32-bit word
@@ -210,10 +285,17 @@ __device__ __forceinline__ void epilogue(const ConvArgs &a, v4i (&acc)[FP][FK], 
     }
     const int lo = a.lo, hi = a.hi;
     if (ep.fast) {
-        if (lo >= 0)
-            epilogue_fast<BITS, FP, FK, true>(a, acc, mbase, cb, l16, ep);
-        else
-            epilogue_fast<BITS, FP, FK, false>(a, acc, mbase, cb, l16, ep);
+        if (EXT && a.res) {
+            if (lo >= 0)
+                epilogue_fast<BITS, FP, FK, true, true>(a, acc, mbase, cb, l16, ep);
+            else
+                epilogue_fast<BITS, FP, FK, false, true>(a, acc, mbase, cb, l16, ep);
+        } else {
+            if (lo >= 0)
+                epilogue_fast<BITS, FP, FK, true, false>(a, acc, mbase, cb, l16, ep);
+            else
+                epilogue_fast<BITS, FP, FK, false, false>(a, acc, mbase, cb, l16, ep);
+        }
         return;
     }
     const int64_t rnd = (int64_t)1 << (a.shift - 1);
@@ -222,6 +304,8 @@ __device__ __forceinline__ void epilogue(const ConvArgs &a, v4i (&acc)[FP][FK], 
         uint32_t words[NWD];
 #pragma unroll
         for (int wd = 0; wd < NWD; ++wd) words[wd] = 0u;
+        uint32_t rw[NWD];
+        if (EXT && a.res) load_run<BITS, FK>(a, mbase + tn * 16 + l16, cb, rw);
 #pragma unroll
         for (int tm = 0; tm < FK; ++tm)
 #pragma unroll
@@ -229,6 +313,7 @@ __device__ __forceinline__ void epilogue(const ConvArgs &a, v4i (&acc)[FP][FK], 
                 const int e = 4 * tm + v;
                 int64_t t64 = (int64_t)(acc[tn][tm][v] >> a.acc_shift) * ep.mul[e] + rnd;
                 t64 >>= a.shift;   // arithmetic: floor
+                if (EXT && a.res) t64 += run_value<BITS>(rw, e, a.res_signed != 0);
                 t64 = t64 < lo ? lo : (t64 > hi ? hi : t64);
                 words[e / CPW] |= ((uint32_t)(int32_t)t64 & VMASK) << (BITS * (e % CPW));
             }

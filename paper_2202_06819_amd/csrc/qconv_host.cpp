@@ -101,7 +101,11 @@ int check_desc(const qconv_desc *d, qconv_layout_info *info) {
 }
 
 int check_epilogue(const qconv_desc *d, const qconv_epilogue *e) {
+    if (e && e->mode == QCONV_OUT_RAW_I32 && (e->bias || e->residual))
+        return fail(QCONV_EINVAL, "bias and residual apply to the requant epilogue only");
     if (!e || e->mode == QCONV_OUT_RAW_I32) return QCONV_OK;
+    if (e->residual_signed != 0 && e->residual_signed != 1) return fail(QCONV_EINVAL, "residual_signed must be 0 or 1");
+    if (e->residual && !aligned16(e->residual)) return fail(QCONV_EINVAL, "residual must be 16-byte aligned");
     if (e->mode != QCONV_OUT_REQUANT) return fail(QCONV_EINVAL, "unknown epilogue mode %d", e->mode);
     if (!e->mult) return fail(QCONV_EINVAL, "requant epilogue needs a multiplier array");
     if (e->shift < 1 || e->shift > 62) return fail(QCONV_EINVAL, "shift must be in [1, 62] (got %d)", e->shift);
@@ -208,7 +212,7 @@ int plan_tile(const qconv_desc *d, const qconv_layout_info &li, const qconv_tile
         // buffer loads take 32-bit offsets, and offset 2^31 marks padding
         if (li.x_bytes >= (1ll << 31) || pl.ktiles * nchunks * wbuf >= (1ll << 31))
             return fail(QCONV_EUNSUPPORTED, "tile %s addresses operands with 31-bit buffer offsets", t.name);
-        const int64_t mbytes = round_up((int64_t)t.tile_k * 4 + 4, 16);   // multipliers + split-K flag
+        const int64_t mbytes = round_up((int64_t)t.tile_k * 8 + 4, 16);   // multipliers, biases, split-K flag
         const int64_t single = bbuf + wbuf + mbytes;
         const int64_t tiles = pl.mtiles * pl.ktiles;
         if (splits < 1 || splits > nchunks)
@@ -445,12 +449,13 @@ void fill_args(ConvArgs &a, const qconv_desc *d, const qconv_layout_info &li, co
     a.acc_shift = d->bits == 4 ? 4 * (d->x_signed + d->w_signed) : 0;
 }
 
-// inst: 0 = the tile's generic kernel, 1 + i = its fixed-size instance i.
+// inst: 0 = the tile's generic kernel, 1 + i = its fixed-size instance i; 3 + the same for
+// the kernels with the bias and residual epilogue.
 int ensure_lds_attribute(const void *kernel, int tile_id, int inst, int64_t lds) {
     if (lds <= 64 * 1024) return QCONV_OK;
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return fail(QCONV_EHIP, "hipGetDevice failed");
-    const long long key = ((long long)dev * 4096 + tile_id) * 4 + inst;
+    const long long key = ((long long)dev * 4096 + tile_id) * 8 + inst;
     std::lock_guard<std::mutex> g(g_attr.mu);
     if (!g_attr.done[key]) {
         hipError_t e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
@@ -509,16 +514,29 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
             ((uintptr_t)w < w1 && w0 < (uintptr_t)w + wb))
             return fail(QCONV_EINVAL, "workspace overlaps x, w or y");
     }
+    if (requant && epi->residual) {
+        // each lane reads its own output words of the residual before storing
+        // them, so y itself may be the residual; any other overlap may not
+        const uintptr_t r0 = (uintptr_t)epi->residual, r1 = r0 + ybytes;
+        if (r0 != y0 && r0 < y1 && y0 < r1) return fail(QCONV_EINVAL, "residual overlaps y without being y");
+        if (((uintptr_t)x < r1 && r0 < (uintptr_t)x + li.x_bytes) || ((uintptr_t)w < r1 && r0 < (uintptr_t)w + wb))
+            return fail(QCONV_EINVAL, "residual overlaps x or w");
+        if (wsb > 0 && (uintptr_t)workspace < r1 && r0 < (uintptr_t)workspace + wsb)
+            return fail(QCONV_EINVAL, "residual overlaps the workspace");
+    }
+    // the epilogue flavour: bias and residual are compiled into separate kernels;
     // prepared filters of a 3x3 or 1x1 layer run the tile's fixed-size instance
-    ConvLauncher launch = te.launch;
-    const void *kernel = te.kernel;
-    int inst = 0;
+    const bool ext = requant && (epi->bias || epi->residual);
+    const KernelSet &ks = ext ? te.ext : te.plain;
+    ConvLauncher launch = ks.launch;
+    const void *kernel = ks.kernel;
+    int inst = ext ? 3 : 0;
     if (prepared && te.info.variant == QCONV_VARIANT_WIDE)
         for (int i = 0; i < 2; ++i)
-            if (te.fixed[i].launch && te.fixed[i].r == d->r && te.fixed[i].s == d->s) {
-                launch = te.fixed[i].launch;
-                kernel = te.fixed[i].kernel;
-                inst = 1 + i;
+            if (ks.fixed[i].launch && ks.fixed[i].r == d->r && ks.fixed[i].s == d->s) {
+                launch = ks.fixed[i].launch;
+                kernel = ks.fixed[i].kernel;
+                inst = (ext ? 3 : 0) + 1 + i;
             }
     if (te.info.variant == QCONV_VARIANT_WIDE && pl.splits == 1 && pl.off_b1 != pl.off_b0) {
         // persistent grid: size it by the occupancy the runtime reports for this kernel
@@ -558,6 +576,9 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
     if (a.w_image) a.wbytes = (int32_t)wb;
     a.mode = requant ? QCONV_OUT_REQUANT : QCONV_OUT_RAW_I32;
     if (requant) {
+        a.bias = epi->bias;
+        a.res = static_cast<const uint8_t *>(epi->residual);
+        a.res_signed = epi->residual_signed;
         a.shift = epi->shift;
         a.lo = epi->relu ? std::max(epi->clamp_lo, 0) : epi->clamp_lo;
         a.hi = epi->clamp_hi;

@@ -75,6 +75,9 @@ struct ConvArgs {
     int32_t mode;           // QCONV_OUT_RAW_I32 / QCONV_OUT_REQUANT
     int32_t shift;
     int32_t lo, hi;         // clamp bounds, ReLU already folded into lo
+    const int32_t *bias;    // per-channel accumulator offsets, or null
+    const uint8_t *res;     // residual in y's packed layout, or null
+    int32_t res_signed;     // residual values are signed
 };
 
 // Band pixels one thread of a wide tile stages per channel chunk: the 4
@@ -97,12 +100,18 @@ struct FixedInstance {
     const void *kernel;
 };
 
-struct TileEntry {
-    qconv_tile_info info;
+// The kernels of one tile for one epilogue flavour.
+struct KernelSet {
     ConvLauncher launch;
     const void *kernel;     // for hipFuncSetAttribute
-    PrepLauncher prep;      // builds the filter image (wide tiles), else null
     FixedInstance fixed[2]; // wide tiles: 3x3 and 1x1 instances; empty (r == 0) otherwise
+};
+
+struct TileEntry {
+    qconv_tile_info info;
+    KernelSet plain;        // epilogue without bias and residual
+    KernelSet ext;          // epilogue with bias and/or residual
+    PrepLauncher prep;      // builds the filter image (wide tiles), else null
 };
 
 // Defined in qconv_conv.hip.

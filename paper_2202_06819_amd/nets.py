@@ -27,6 +27,9 @@ class LayerSpec:
     src: int = -1
     tile: int = -1
     splits: int = 0        # split-K factor; 0: the tuned choice (else 1)
+    bias: torch.Tensor | None = None   # int32 per output channel (accumulator units)
+    residual_src: int | None = None    # layer whose output is added before ReLU (-1: the input); None: none
+    residual_signed: bool = False
 
 
 class Chain:
@@ -47,9 +50,12 @@ class Chain:
             splits = splits or 1
             wprep = qconv.prepare_filters(L.desc, L.w_packed, tile)
             self.filters.append(wprep)
+            res = None
+            if L.residual_src is not None:
+                res = self.x if L.residual_src < 0 else outs[L.residual_src]
             call = qconv.Conv2dCall(L.desc, inp, wprep, requant=True, mult=L.mult, shift=L.shift,
                                     relu=L.relu, clamp=L.clamp, tile=tile, stream=stream, prepared=True,
-                                    splits=splits)
+                                    splits=splits, bias=L.bias, residual=res, residual_signed=L.residual_signed)
             outs.append(call.out)
             self.calls.append(call)
         self.outputs = outs
@@ -69,7 +75,9 @@ class Chain:
             calls = [qconv.Conv2dCall(c.desc, c.x, c.w, requant=True, mult=c.mult, shift=c.epi.shift,
                                       relu=bool(c.epi.relu), clamp=(c.epi.clamp_lo, c.epi.clamp_hi), out=c.out,
                                       tile=c.tile, stream=s, prepared=c.prepared, splits=c.splits,
-                                      workspace=getattr(c, "workspace", None)) for c in self.calls]
+                                      workspace=getattr(c, "workspace", None), bias=c.bias,
+                                      residual=c.residual, residual_signed=bool(c.epi.residual_signed))
+                     for c in self.calls]
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g, stream=s):
                 for c in calls:

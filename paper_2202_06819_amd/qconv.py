@@ -41,7 +41,7 @@ class QConvLayoutInfo(ctypes.Structure):
 
 class QConvEpilogue(ctypes.Structure):
     _fields_ = [("mode", _i32), ("mult", _vp), ("shift", _i32), ("relu", _i32), ("clamp_lo", _i32),
-                ("clamp_hi", _i32)]
+                ("clamp_hi", _i32), ("bias", _vp), ("residual", _vp), ("residual_signed", _i32)]
 
 
 class QConvTileInfo(ctypes.Structure):
@@ -262,10 +262,22 @@ def pack(src: torch.Tensor, bits: int, is_signed: bool, out: torch.Tensor | None
     return out
 
 
+def _epilogue_extras(epi: QConvEpilogue, desc: QConvDesc, y_bytes: int, bias, residual, residual_signed) -> None:
+    """Fill the optional bias and residual of a requant epilogue."""
+    if bias is not None:
+        if bias.dtype != torch.int32 or bias.numel() != desc.k:
+            raise QConvError(EINVAL, "bias needs one int32 per output channel")
+        epi.bias = _dev_ptr(bias, "bias", 4 * desc.k)
+    if residual is not None:
+        epi.residual = _dev_ptr(residual, "residual", y_bytes)
+        epi.residual_signed = int(bool(residual_signed))
+
+
 def conv2d(d: dict, x: torch.Tensor, w: torch.Tensor, *, requant: bool = False, mult: torch.Tensor | None = None,
            shift: int = 20, relu: bool = True, clamp: tuple = (0, 15), out: torch.Tensor | None = None,
            tile: int = -1, workspace: torch.Tensor | None = None, stream=None,
-           prepared: bool = False, splits: int = 1) -> torch.Tensor:
+           prepared: bool = False, splits: int = 1, bias: torch.Tensor | None = None,
+           residual: torch.Tensor | None = None, residual_signed: bool = False) -> torch.Tensor:
     """The convolution with its fused epilogue; returns the output tensor.
 
     Raw mode: int32 N x P x Q x K accumulators.  Requant mode: the packed
@@ -287,6 +299,7 @@ def conv2d(d: dict, x: torch.Tensor, w: torch.Tensor, *, requant: bool = False, 
             raise QConvError(EINVAL, "requant needs an int32 multiplier per output channel")
         epi.mode, epi.mult = OUT_REQUANT, _dev_ptr(mult, "mult", 4 * desc.k)
         epi.shift, epi.relu, epi.clamp_lo, epi.clamp_hi = int(shift), int(bool(relu)), int(clamp[0]), int(clamp[1])
+        _epilogue_extras(epi, desc, info["y_packed_bytes"], bias, residual, residual_signed)
     else:
         epi.mode = OUT_RAW_I32
     ws_ptr, ws_bytes = (None, 0) if workspace is None else (_dev_ptr(workspace, "workspace"),
@@ -334,7 +347,9 @@ class Conv2dCall:
     def __init__(self, d: dict, x: torch.Tensor, w: torch.Tensor, *, requant: bool = False,
                  mult: torch.Tensor | None = None, shift: int = 20, relu: bool = True, clamp: tuple = (0, 15),
                  out: torch.Tensor | None = None, tile: int = -1, stream=None, prepared: bool = False,
-                 splits: int = 1, workspace: torch.Tensor | None = None, schedule: dict | None = None):
+                 splits: int = 1, workspace: torch.Tensor | None = None, schedule: dict | None = None,
+                 bias: torch.Tensor | None = None, residual: torch.Tensor | None = None,
+                 residual_signed: bool = False):
         """With `schedule` (a dict of qconv_schedule knobs; `w` prepared for its
         tile) the call goes through qconv2d_scheduled."""
         if schedule is not None:
@@ -355,10 +370,12 @@ class Conv2dCall:
             self.epi.mode, self.epi.mult = OUT_REQUANT, _dev_ptr(mult, "mult", 4 * self.desc.k)
             self.epi.shift, self.epi.relu = int(shift), int(bool(relu))
             self.epi.clamp_lo, self.epi.clamp_hi = int(clamp[0]), int(clamp[1])
+            _epilogue_extras(self.epi, self.desc, info["y_packed_bytes"], bias, residual, residual_signed)
         else:
             self.epi.mode = OUT_RAW_I32
         y_bytes = info["y_packed_bytes"] if requant else info["y_raw_bytes"]
         self.x, self.w, self.mult, self.out, self.info = x, w, mult, out, info
+        self.bias, self.residual = bias, residual
         self.tile = default_tile(d) if tile == -1 else int(tile)
         self.prepared = prepared
         self.splits = int(splits)

@@ -317,3 +317,21 @@ def test_schedule_check_and_errors(q):
     assert L.qconv2d_scheduled(*args, ctypes.byref(bad), None, 0, None) == -1
     two = q.make_schedule(dict(base, splits=2))
     assert L.qconv2d_scheduled(*args, ctypes.byref(two), None, 0, None) == -3   # split-K without workspace
+
+
+def test_bias_and_residual_argument_errors(q):
+    L = q.lib()
+    d = D()
+    desc = q.make_desc(d)
+    info = q.layout(d)
+    ref = ctypes.byref(desc)
+    x, w, y = 1 << 32, 1 << 33, 1 << 34
+    raw = _epi(q, mode=0, bias=1 << 36)
+    assert L.qconv2d(ref, x, w, ctypes.byref(raw), y, None, 0, -1, None) == -1           # raw mode takes no bias
+    assert L.qconv2d(ref, x, w, ctypes.byref(_epi(q, residual=(1 << 36) + 8)), y, None, 0, -1, None) == -1
+    assert L.qconv2d(ref, x, w, ctypes.byref(_epi(q, residual=1 << 36, residual_signed=2)), y, None, 0, -1,
+                     None) == -1
+    part = _epi(q, residual=y + 16 * (info["y_packed_bytes"] // 32))                   # overlaps y, is not y
+    assert L.qconv2d(ref, x, w, ctypes.byref(part), y, None, 0, -1, None) == -1
+    over_x = _epi(q, residual=x + 64)
+    assert L.qconv2d(ref, x, w, ctypes.byref(over_x), y, None, 0, -1, None) == -1

@@ -10,7 +10,7 @@ import pytest
 
 import oracle
 import qconv_inputs as qi
-from _util import announce, assert_same, gpu_layer, ref_layer, stress_shift
+from _util import announce, assert_same, gpu_layer, oracle_threads, ref_layer, stress_shift
 
 pytestmark = pytest.mark.gpu
 
@@ -364,3 +364,93 @@ def test_split_k_matches_oracle(shape):
             part = -(-(ntiles * (-(-chunks // -(-chunks // splits))) * tinfo["tile_p"] * tinfo["tile_k"] * 4) // 256) * 256
             counters = ws[part:part + 4 * ntiles]
             assert int(counters.count_nonzero()) == 0, "arrival counters not reset"
+
+
+# ----------------------------------------------------------------- bias and residual epilogue
+
+BIAS_SHAPES = [
+    # name, n, h, c, k, r, stride, pad, bits
+    ("e_2x14_64to64_3x3", 2, 14, 64, 64, 3, 1, 1, 4),
+    ("e_2x28_128to256_1x1_s2", 2, 28, 128, 256, 1, 2, 0, 4),
+    ("e_2x7_512to512_3x3", 2, 7, 512, 512, 3, 1, 1, 4),
+    ("e8_2x14_64to64_3x3", 2, 14, 64, 64, 3, 1, 1, 8),
+]
+
+
+@pytest.mark.parametrize("shape", BIAS_SHAPES, ids=lambda v: v[0])
+def test_bias_and_residual_every_tile(shape):
+    """Bias (fast and 64-bit paths), residual (unsigned and signed, in place),
+    on every tile from packed and from prepared filters, and with split-K."""
+    torch, q = _torch(), _qconv()
+    name, n, h, c, k, r, stride, pad, bits = shape
+    if bits == 4:
+        L = qi.Layer(name, n, h, h, c, k, r, r, stride, pad, w_range=(-7, 7))
+    else:
+        L = qi.Layer(name, n, h, h, c, k, r, r, stride, pad, bits=8, x_signed=True, w_signed=True,
+                     x_range=qi.S8, w_range=qi.S8, epilogue=qi.Epilogue(relu=False, lo=-128, hi=127))
+    t = qi.layer_tensors(910, c + k + bits, L)
+    g = np.random.default_rng([910, c, k, bits])
+    sh = stress_shift(L, L.x_range, L.w_range)
+    p = (h + 2 * pad - r) // stride + 1
+    dev = torch.device("cuda:0")
+    xp = q.pack(torch.from_numpy(t["x"]).to(dev), bits, L.x_signed)
+    wp = q.pack(torch.from_numpy(t["w"]).to(dev), bits, L.w_signed)
+    acc_mag = int(np.sqrt(c * r * r) * 8 * (8 if bits == 4 else 80))
+    small_bias = g.integers(-acc_mag, acc_mag, size=k).astype(np.int32)
+    # the largest bias the contract allows for this shape (accumulator + bias in int32)
+    acc_shift = 4 * (int(L.x_signed) + int(L.w_signed)) if bits == 4 else 0
+    bmax = (2 ** 31 - 1) // 2 ** acc_shift - _qconv().layout(L.desc())["max_abs_acc"]
+    big_bias = g.integers(-bmax, bmax + 1, size=k).astype(np.int32)
+    if bits == 4:
+        ranges = [(True, 0, 15, False), (False, -8, 7, True)]   # relu, lo, hi, signed residual
+    else:
+        ranges = [(False, -128, 127, True), (True, -128, 127, True)]
+    # multipliers too large for the one-instruction requantiser take the 64-bit form
+    big_mult = g.integers(2 ** 29, 2 ** 30, size=k).astype(np.int32)
+    cases = []
+    for relu, lo, hi, rsig in ranges:
+        rlo, rhi = (-(2 ** (bits - 1)), 2 ** (bits - 1) - 1) if rsig else (0, 2 ** bits - 1)
+        res_vals = g.integers(rlo, rhi + 1, size=(n, p, p, k)).astype(np.int32)
+        res_packed = oracle.pack_output(res_vals, bits, rsig)
+        for bias, mlt, shift in ((small_bias, t["mult"], sh), (big_bias, t["mult"], sh), (None, t["mult"], sh),
+                                 (small_bias, big_mult, sh + 15)):
+            for use_res in (True, False):
+                if bias is None and not use_res:
+                    continue
+                ref = oracle.qconv_layer(t["x"], t["w"], bits=bits, x_signed=L.x_signed, w_signed=L.w_signed,
+                                         stride=(stride, stride), pad=(pad, pad), mult=mlt, shift=shift, relu=relu,
+                                         lo=lo, hi=hi, bias=bias, residual=res_vals if use_res else None,
+                                         threads=oracle_threads())
+                cases.append((relu, lo, hi, rsig, bias, mlt, shift, res_packed if use_res else None, ref["y_packed"]))
+    tiles = _valid_tiles(L)
+    for tid in tiles:
+        wide = q.tiles()[tid]["variant"] == 2
+        wprep = q.prepare_filters(L.desc(), wp, tid) if wide else None
+        for ci, (relu, lo, hi, rsig, bias, mlt, shift, res_packed, want) in enumerate(cases):
+            b = None if bias is None else torch.from_numpy(bias).to(dev)
+            res = None if res_packed is None else torch.from_numpy(np.ascontiguousarray(res_packed)).to(dev)
+            kw = dict(requant=True, mult=torch.from_numpy(mlt).to(dev), shift=shift, relu=relu, clamp=(lo, hi),
+                      bias=b, residual=res, residual_signed=rsig)
+            announce(f"{name} tile {tid} case {ci} packed filters")
+            y = q.conv2d(L.desc(), xp, wp, tile=tid, **kw)
+            torch.cuda.synchronize()
+            assert_same(y.cpu().numpy(), want, f"{name} tile {tid} case {ci}")
+            if wide:
+                announce(f"{name} tile {tid} case {ci} prepared")
+                y = q.conv2d(L.desc(), xp, wprep, tile=tid, prepared=True, **kw)
+                torch.cuda.synchronize()
+                assert_same(y.cpu().numpy(), want, f"{name} tile {tid} case {ci} prepared")
+                if res is not None:
+                    announce(f"{name} tile {tid} case {ci} in place")
+                    yy = res.clone()
+                    kw_in = dict(kw, residual=yy)
+                    q.conv2d(L.desc(), xp, wprep, tile=tid, prepared=True, out=yy, **kw_in)
+                    torch.cuda.synchronize()
+                    assert_same(yy.cpu().numpy(), want, f"{name} tile {tid} case {ci} in place")
+                chunks = q.max_splits(L.desc(), tid)
+                if chunks > 1:
+                    ws = q.make_workspace(L.desc(), tid, 2, dev)
+                    announce(f"{name} tile {tid} case {ci} split 2")
+                    y = q.conv2d(L.desc(), xp, wprep, tile=tid, prepared=True, splits=2, workspace=ws, **kw)
+                    torch.cuda.synchronize()
+                    assert_same(y.cpu().numpy(), want, f"{name} tile {tid} case {ci} split 2")
