@@ -263,8 +263,42 @@ def per_layer_table(cfg: int, layers, dev, reps: int) -> list[dict]:
     return rows
 
 
-def chain_time(cfg: int, layers, dev, reps: int) -> dict:
-    """End-to-end time of a chained network (each output feeds the next layer)."""
+def residual_order(layers):
+    """The ResNet-18 stack as residual blocks: each block's second 3x3 adds its
+    shortcut (the block input, or the stage's 1x1 projection, which is moved
+    ahead of it) before ReLU.  Returns (layers in run order, source index,
+    shortcut index or None) per layer."""
+    order = []
+    names = [L.name for L in layers]
+    for i, L in enumerate(layers):
+        if L.name.endswith("downsample"):
+            continue
+        order.append(i)
+        if L.name.endswith(".0.conv1"):
+            ds = L.name.replace("conv1", "downsample")
+            if ds in names:
+                order.append(names.index(ds))
+    pos = {old: new for new, old in enumerate(order)}
+    out = []
+    for old in order:
+        L = layers[old]
+        src = -1 if L.src < 0 else pos[L.src]
+        short = None
+        if L.name.endswith("conv2"):
+            ds = L.name.replace("conv2", "downsample")
+            if ds in names:
+                short = pos[names.index(ds)]
+            else:
+                block_in = layers[L.src].src     # conv1's input is the block input
+                short = -1 if block_in < 0 else pos[block_in]
+        out.append((L, src, short, old))
+    return out
+
+
+def chain_time(cfg: int, layers, dev, reps: int, residual: bool = False) -> dict:
+    """End-to-end time of a chained network (each output feeds the next layer);
+    with `residual`, as residual blocks with a per-channel bias in every layer."""
+    import numpy as np
     import torch
     import qconv_inputs as qi
     from paper_2202_06819_amd import nets, qconv
@@ -272,12 +306,18 @@ def chain_time(cfg: int, layers, dev, reps: int) -> dict:
     x = torch.from_numpy(t0["x"]).to(dev)
     xp = qconv.pack(x, layers[0].bits, layers[0].x_signed)
     specs = []
-    for lid, L in enumerate(layers):
+    plan = residual_order(layers) if residual else [(L, L.src, None, i) for i, L in enumerate(layers)]
+    for L, src, short, lid in plan:
         t = qi.layer_tensors(cfg, lid, L)
         wp = qconv.pack(torch.from_numpy(t["w"]).to(dev), L.bits, L.w_signed)
         e = L.epilogue
+        bias = None
+        if residual:
+            bias = torch.from_numpy(np.random.default_rng([cfg, lid, 3]).integers(-256, 256, size=L.k)
+                                    .astype(np.int32)).to(dev)
         specs.append(nets.LayerSpec(L.desc(), wp, torch.from_numpy(t["mult"]).to(dev), e.shift, e.relu,
-                                    (e.lo, e.hi), src=L.src))
+                                    (e.lo, e.hi), src=src, bias=bias, residual_src=short,
+                                    residual_signed=e.lo < 0))
     chain = nets.Chain(specs, xp)
     for _ in range(3):
         chain.forward()
@@ -460,6 +500,8 @@ def main() -> int:
         if cfg in (2, 3):
             entry["chain"] = chain_time(cfg, layers, dev, max(20, args.layer_reps // 4))
             log(f"  chained network: {entry['chain']}")
+            entry["chain_residual"] = chain_time(cfg, layers, dev, max(20, args.layer_reps // 4), residual=True)
+            log(f"  as residual blocks with biases: {entry['chain_residual']}")
         result[f"workload{cfg}"] = entry
 
     if not args.no_cpu:

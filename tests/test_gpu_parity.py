@@ -454,3 +454,57 @@ def test_bias_and_residual_every_tile(shape):
                     y = q.conv2d(L.desc(), xp, wprep, tile=tid, prepared=True, splits=2, workspace=ws, **kw)
                     torch.cuda.synchronize()
                     assert_same(y.cpu().numpy(), want, f"{name} tile {tid} case {ci} split 2")
+
+
+def test_residual_blocks_chain_eager_and_graph():
+    """Two basic residual blocks (conv-bias-ReLU, conv-bias-+shortcut-ReLU; the
+    second block with a strided 1x1 projection shortcut), chained on the GPU
+    with no relayout, eager and as replays of a captured graph, against the
+    oracle layer by layer."""
+    torch, q = _torch(), _qconv()
+    from paper_2202_06819_amd import nets
+    dev = torch.device("cuda:0")
+    n, h = 2, 16
+    # name, c, k, r, stride, pad, src, residual_src
+    spec = [("b1c1", 64, 64, 3, 1, 1, -1, None), ("b1c2", 64, 64, 3, 1, 1, 0, -1),
+            ("b2c1", 64, 128, 3, 2, 1, 1, None), ("b2ds", 64, 128, 1, 2, 0, 1, None),
+            ("b2c2", 128, 128, 3, 1, 1, 2, 3)]
+    g = np.random.default_rng(77)
+    x = g.integers(0, 16, size=(n, 64, h, h)).astype(np.int8)
+    layers, refs, specs = [], [], []
+    xp_ref = oracle.relayout_pack(x, 4, False)
+    outs_vals = []
+    in_vals = oracle.unpack_tensor(xp_ref, 64, 4, False)
+    for i, (name, c, k, r, stride, pad, src, rsrc) in enumerate(spec):
+        hin = h if src < 0 else refs[src]["y"].shape[1]
+        L = qi.Layer(name, n, hin, hin, c, k, r, r, stride, pad, w_range=(-7, 7))
+        t = qi.layer_tensors(950, i, L)
+        sh = stress_shift(L, L.x_range, L.w_range)
+        bias = g.integers(-400, 400, size=k).astype(np.int32)
+        packed_in = xp_ref if src < 0 else refs[src]["y_packed"]
+        res = None if rsrc is None else (in_vals if rsrc < 0 else refs[rsrc]["y"])
+        ref = oracle.qconv_layer(None, t["w"], bits=4, x_signed=False, w_signed=True, stride=(stride, stride),
+                                 pad=(pad, pad), mult=t["mult"], shift=sh, relu=True, lo=0, hi=15, bias=bias,
+                                 residual=res, packed_x=packed_in, threads=oracle_threads())
+        refs.append(ref)
+        wp = q.pack(torch.from_numpy(t["w"]).to(dev), 4, True)
+        specs.append(nets.LayerSpec(L.desc(), wp, torch.from_numpy(t["mult"]).to(dev), sh, True, (0, 15), src=src,
+                                    bias=torch.from_numpy(bias).to(dev), residual_src=rsrc))
+    xp = q.pack(torch.from_numpy(x).to(dev), 4, False)
+    chain = nets.Chain(specs, xp)
+    announce("residual chain eager")
+    outs = [o.clone() for o in chain.forward()]
+    torch.cuda.synchronize()
+    for (name, *_), o, ref in zip(spec, outs, refs):
+        assert_same(o.cpu().numpy(), ref["y_packed"], f"eager {name}")
+    chain.capture()
+    for i in range(3):
+        for o in chain.outputs:
+            o.zero_()
+        announce(f"residual chain replay {i}")
+        got = chain.replay()
+        torch.cuda.synchronize()
+        for (name, *_), o, ref in zip(spec, got, refs):
+            assert_same(o.cpu().numpy(), ref["y_packed"], f"replay {i} {name}")
+        chain.forward()
+        torch.cuda.synchronize()
