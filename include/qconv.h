@@ -274,12 +274,22 @@ int qconv_workspace_bytes(const qconv_desc *d, int32_t tile_id, int32_t splits, 
  *   xcd_order     1 = consecutive workgroup tiles are placed on one XCD so
  *                 neighbouring tiles share its L2 (the default elsewhere);
  *                 0 = the hardware's round-robin order
+ *   ablation      0 for normal use.  For measuring the techniques (the
+ *                 ablation of Sec. 4.4), a bit mask of techniques switched
+ *                 off: 1 = duplicate-aware loading (Sec. 3.1) -- every tile
+ *                 pixel is staged once per filter tap, as the lowered matrix;
+ *                 2 = register-level packing (Sec. 3.2) -- the int32
+ *                 accumulators pass through LDS to a separate requantise and
+ *                 pack step.  Compiled for 4-bit 3x3 layers on the tiles
+ *                 wide_b4_w4x1_f1x4_c64, wide_b4_w8x1_f1x4_c64 and
+ *                 wide_b4_w4x1_f2x4_c64, without split, bias or residual;
+ *                 QCONV_EUNSUPPORTED otherwise.  Results are identical.
  * qconv_schedule_check -- host only: QCONV_OK if the schedule can run `d`
  *   (QCONV_EINVAL for a knob out of range, else what the call would return).
  * qconv2d_scheduled -- qconv2d_prepared with every knob given; the prepared
  *   filters must be those of s->tile_id; `workspace` as for split-K above.
  *   qconv2d_prepared(..., tile_id, splits, ...) is the schedule
- *   {tile_id, splits, 0, 0, 1}.
+ *   {tile_id, splits, 0, 0, 1, 0}.
  */
 typedef struct {
     int32_t tile_id;
@@ -287,6 +297,7 @@ typedef struct {
     int32_t wg_per_cu;
     int32_t band_buffers;
     int32_t xcd_order;
+    int32_t ablation;
 } qconv_schedule;
 
 int qconv_schedule_check(const qconv_desc *d, const qconv_schedule *s);

@@ -41,6 +41,7 @@
 //                (C*bits % 128 == 0).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+#include <string.h>
 
 #include "qconv_device.h"
 #include "qconv_internal.h"
@@ -323,9 +324,17 @@ __device__ __forceinline__ int xcd_block(int b, int g) {
 // RC, SC: filter height and width fixed at compile time (0: taken from the
 // descriptor).  A fixed-size instance always reads prepared filters and runs a
 // fully unrolled MFMA loop with immediate LDS offsets.
-template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC, bool EXT>
+// ABL (ablation of the techniques, for measurement): bit 0 stages the lowered
+// (im2col) operand instead of the band -- one copy of every pixel per filter
+// tap, as without duplicate awareness; bit 1 sends the int32 accumulators
+// through LDS to a separate requantise-and-pack pass instead of packing them
+// in registers before the store.
+template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC, bool EXT, int ABL = 0>
 __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     constexpr bool FIXED = RC > 0 && SC > 0;
+    constexpr bool LOWERED = (ABL & 1) != 0;
+    constexpr bool LDSEPI = (ABL & 2) != 0;
+    static_assert(ABL == 0 || (FIXED && !EXT), "ablation instances are fixed-size, without bias or residual");
     constexpr int NW = WP * WK;
     constexpr int NT = NW * 64;
     constexpr int TP = WP * FP * 16;
@@ -334,7 +343,8 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     constexpr int VPP = CK * BITS / 128;    // packed 16-byte vectors per pixel (or filter tap) and chunk
     constexpr int GPV = 16 / (2 * BITS);    // 16-channel int8 granules per packed vector
     constexpr int CPV = 128 / BITS;         // channels per packed vector
-    constexpr int PJ = wide_band_pixels_per_thread(TP, NT, VPP);   // band pixels a thread stages per chunk
+    // band pixels (lowered entries) a thread stages per chunk
+    constexpr int PJ = LOWERED ? (RC * SC * TP + NT - 1) / NT : wide_band_pixels_per_thread(TP, NT, VPP);
     constexpr int MAXV = kWideMaxV;
     static_assert(BITS == 8 || FK % 2 == 0, "4-bit output packs 8 channels per word: FK must be even");
     static_assert(VPP >= 1 && 4 % VPP == 0, "a pixel's vectors must divide the per-thread budget");
@@ -382,6 +392,26 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     int npix = 0;
     auto set_band = [&](int ti) {
         const int m0 = (j0 + ti * gpk) * TP;
+        if constexpr (LOWERED) {
+            // entry e = tap * TP + p: tile pixel p shifted by filter tap `tap`
+            npix = RC * SC * TP;
+#pragma unroll
+            for (int j = 0; j < PJ; ++j) {
+                const int e = j * NT + tid;
+                const int tap = e / TP;
+                const int p = e - tap * TP;
+                int vr, cl;
+                pixel_origin(a, min(m0 + p, a.m - 1), vr, cl);
+                const int vrow = vr + tap / SC;
+                const int col = cl + tap % SC;
+                const int img = (int)fdiv((uint32_t)vrow, a.div_vh);
+                const int hh = vrow - img * a.vh - a.ph;
+                const int ww = col - a.pw;
+                const bool in = e < npix && img < a.n && hh >= 0 && hh < a.h && ww >= 0 && ww < a.w;
+                poff[j] = in ? (uint32_t)(((img * a.h + hh) * a.w + ww) * a.xpix) : kOutOfRange;
+            }
+            return;
+        }
         int vlo, vlast, cu;
         pixel_origin(a, m0, vlo, cu);
         pixel_origin(a, min(m0 + TP, a.m) - 1, vlast, cu);
@@ -498,6 +528,11 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     int pixoff[FP];
     auto set_tile = [&](int ti) {
         const int m0 = (j0 + ti * gpk) * TP;
+        if constexpr (LOWERED) {
+#pragma unroll
+            for (int tn = 0; tn < FP; ++tn) pixoff[tn] = (wp * FP * 16 + tn * 16 + l16) * 16 + lane_b;
+            return;
+        }
         int vlo, cu;
         pixel_origin(a, m0, vlo, cu);
 #pragma unroll
@@ -566,6 +601,58 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
 
     const int nit = rs * KSTEPS;
 
+    // Ablation: the tile's int32 accumulators go to LDS; then every thread takes
+    // whole output words (pixel, CPW channels), requantises, packs and stores
+    // them.  Two barriers per tile.
+    auto lds_epilogue = [&](int ti) {
+        int32_t *elds = reinterpret_cast<int32_t *>(smem + a.off_e);
+        const int pl0 = wp * FP * 16 + l16;
+#pragma unroll
+        for (int tn = 0; tn < FP; ++tn)
+#pragma unroll
+            for (int tm = 0; tm < FK; ++tm) {
+                const v4i v = acc[tn][tm];
+                *reinterpret_cast<int4 *>(elds + (pl0 + tn * 16) * TK + (cb - k0) + 4 * tm) = int4{v[0], v[1], v[2], v[3]};
+            }
+        __syncthreads();
+        const int m0 = (j0 + ti * gpk) * TP;
+        if (a.mode == QCONV_OUT_RAW_I32) {
+            for (int i = tid; i < TP * TK / 4; i += NT) {
+                const int pl = i / (TK / 4), c4 = (i - pl * (TK / 4)) * 4;
+                const int m = m0 + pl;
+                if (m >= a.m || k0 + c4 >= a.k) continue;
+                const int4 q = *reinterpret_cast<const int4 *>(elds + pl * TK + c4);
+                *reinterpret_cast<int4 *>(reinterpret_cast<int32_t *>(a.yptr) + (size_t)m * a.k + k0 + c4) =
+                    int4{q.x >> a.acc_shift, q.y >> a.acc_shift, q.z >> a.acc_shift, q.w >> a.acc_shift};
+            }
+        } else {
+            constexpr int CPW = 32 / BITS;
+            constexpr uint32_t VMASK = (1u << BITS) - 1u;
+            const int e = 32 - a.shift - a.acc_shift;
+            const int64_t rnd = (int64_t)1 << (a.shift - 1);
+            for (int i = tid; i < TP * TK / CPW; i += NT) {
+                const int pl = i / (TK / CPW), c0 = (i - pl * (TK / CPW)) * CPW;
+                const int m = m0 + pl;
+                if (m >= a.m || k0 + c0 >= a.k) continue;
+                uint32_t word = 0u;
+#pragma unroll
+                for (int qv = 0; qv < CPW; ++qv) {
+                    const int32_t v = elds[pl * TK + c0 + qv];
+                    const int32_t mu = mlds[c0 + qv];
+                    int64_t t;
+                    if (e >= 0 && (e == 0 || (uint32_t)mu + (1u << (31 - e)) < (2u << (31 - e))))
+                        t = ((int64_t)v * (int32_t)((uint32_t)mu << e) + ((int64_t)1 << 31)) >> 32;
+                    else
+                        t = ((int64_t)(v >> a.acc_shift) * mu + rnd) >> a.shift;
+                    t = t < a.lo ? a.lo : (t > a.hi ? a.hi : t);
+                    word |= ((uint32_t)(int32_t)t & VMASK) << (BITS * qv);
+                }
+                *reinterpret_cast<uint32_t *>(a.yptr + (size_t)m * (a.k * BITS / 8) + (k0 + c0) * BITS / 8) = word;
+            }
+        }
+        __syncthreads();
+    };
+
     int ti = 0, c = c_begin;
     for (int st = 0; st < nst; ++st) {
         int nti = ti, nc = c + 1;
@@ -614,7 +701,8 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                 for (int rr = 0; rr < RC; ++rr)
 #pragma unroll
                     for (int ks = 0; ks < KSTEPS; ++ks)
-                        brow[tn][rr][ks] = bb + pixoff[tn] + rr * a.ncols * 16 + ks * 4 * a.pstride_b;
+                        brow[tn][rr][ks] = bb + pixoff[tn] + (LOWERED ? rr * SC * TP : rr * a.ncols) * 16 +
+                                           ks * 4 * a.pstride_b;
             v4i A[2][FK], B[2][FP];
             auto ld = [&](int it, int set) {
                 const int tap = it / KSTEPS, ks = it % KSTEPS, rr = tap / SC, ss = tap % SC;
@@ -623,7 +711,7 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                     A[set][tm] = *reinterpret_cast<const v4i *>(wa + ks * 4 * PSW + tap * TK * 16 + tm * 256);
 #pragma unroll
                 for (int tn = 0; tn < FP; ++tn)
-                    B[set][tn] = *reinterpret_cast<const v4i *>(brow[tn][rr][ks] + ss * 16);
+                    B[set][tn] = *reinterpret_cast<const v4i *>(brow[tn][rr][ks] + ss * (LOWERED ? TP * 16 : 16));
             };
             ld(0, 0);
 #pragma unroll
@@ -742,7 +830,10 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                 }
                 if (tid == 0) a.ws_cnt[tile] = 0u;   // ready for the next call
             }
-            epilogue<BITS, FP, FK, EXT>(a, acc, (j0 + ti * gpk) * TP + wp * FP * 16, cb, l16, ep);
+            if constexpr (LDSEPI)
+                lds_epilogue(ti);
+            else
+                epilogue<BITS, FP, FK, EXT>(a, acc, (j0 + ti * gpk) * TP + wp * FP * 16, cb, l16, ep);
             if (bias_here) {
                 init_acc<FP, FK>(a, acc, blds + cb - k0, false, cb);
             } else {
@@ -802,9 +893,9 @@ __global__ void __launch_bounds__(256) build_filter_image(ConvArgs a, int TK, in
 
 // One operand signedness per kernel (the widening is compiled for it); 8-bit
 // operands are always signed.
-template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC, bool EXT>
+template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC, bool EXT, int ABL = 0>
 __global__ void __launch_bounds__(WP * WK * 64) __attribute__((amdgpu_waves_per_eu(2))) conv_wide(ConvArgs a) {
-    wide_body<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC, EXT>(a);
+    wide_body<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC, EXT, ABL>(a);
 }
 
 // ============================================================== tile registry
@@ -815,9 +906,9 @@ static hipError_t launch_staged(const ConvArgs &a, dim3 grid, size_t lds, hipStr
     return hipGetLastError();
 }
 
-template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC, bool EXT>
+template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC, bool EXT, int ABL = 0>
 static hipError_t launch_wide(const ConvArgs &a, dim3 grid, size_t lds, hipStream_t stream) {
-    hipLaunchKernelGGL((conv_wide<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC, EXT>), grid, dim3(WP * WK * 64), lds,
+    hipLaunchKernelGGL((conv_wide<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC, EXT, ABL>), grid, dim3(WP * WK * 64), lds,
                        stream, a);
     return hipGetLastError();
 }
@@ -902,5 +993,20 @@ const TileEntry *tile_table() {
 }
 
 int tile_table_size() { return (int)(sizeof(g_tiles) / sizeof(g_tiles[0])); }
+
+// Ablation instances (4-bit, 3x3, prepared filters): each technique switched
+// off alone and both together, for three tiles.
+#define QCONV_ABL(WP, WK, FP, FK, MASK)                                                                           \
+    {"wide_b4_w" #WP "x" #WK "_f" #FP "x" #FK "_c64", MASK,                                                        \
+     &launch_wide<4, WP, WK, FP, FK, 64, false, true, 3, 3, false, MASK>,                                         \
+     reinterpret_cast<const void *>(&conv_wide<4, WP, WK, FP, FK, 64, false, true, 3, 3, false, MASK>)}
+#define QCONV_ABL3(WP, WK, FP, FK) QCONV_ABL(WP, WK, FP, FK, 1), QCONV_ABL(WP, WK, FP, FK, 2), QCONV_ABL(WP, WK, FP, FK, 3)
+static const AblationInstance g_ablation[] = {QCONV_ABL3(4, 1, 1, 4), QCONV_ABL3(8, 1, 1, 4), QCONV_ABL3(4, 1, 2, 4)};
+
+const AblationInstance *ablation_instance(const char *tile_name, int mask) {
+    for (const AblationInstance &e : g_ablation)
+        if (e.mask == mask && strcmp(e.tile, tile_name) == 0) return &e;
+    return nullptr;
+}
 
 }  // namespace qconv

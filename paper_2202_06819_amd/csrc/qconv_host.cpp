@@ -157,7 +157,7 @@ constexpr int kNumCUs = 256;   // MI355X compute units
 
 struct Plan {
     int64_t rows = 0, pstride_b = 0, pstride_w = 0, lds = 0;
-    int64_t off_b0 = 0, off_b1 = 0, off_w0 = 0, off_w1 = 0, off_m = 0;
+    int64_t off_b0 = 0, off_b1 = 0, off_w0 = 0, off_w1 = 0, off_m = 0, off_e = 0;
     int64_t mtiles = 0, ktiles = 0, grid = 0;
     int64_t splits = 1, cps = 0;   // split-K: splits of the chunk range, chunks per split
 };
@@ -176,8 +176,10 @@ int64_t per_cu_estimate(const qconv_tile_info &t, int64_t lds) {
 // one_band: a persistent single-chunk plan keeps one LDS band buffer (the
 // kernel then adds a barrier before restaging it), so that more workgroups fit
 // a CU and their phases overlap.
+// ablation: the techniques switched off (bit 0 lowered staging, bit 1 LDS
+// epilogue), for the measurement instances of 3x3 layers.
 int plan_tile(const qconv_desc *d, const qconv_layout_info &li, const qconv_tile_info &t, Plan *out,
-              int64_t per_cu = 0, int64_t splits = 1, bool one_band = false) {
+              int64_t per_cu = 0, int64_t splits = 1, bool one_band = false, int ablation = 0) {
     if (t.bits != d->bits)
         return fail(QCONV_EUNSUPPORTED, "tile %s is built for %d-bit operands", t.name, t.bits);
     if ((t.x_signed >= 0 && t.x_signed != d->x_signed) || (t.w_signed >= 0 && t.w_signed != d->w_signed))
@@ -200,19 +202,24 @@ int plan_tile(const qconv_desc *d, const qconv_layout_info &li, const qconv_tile
             return fail(QCONV_EUNSUPPORTED, "tile %s needs c*bits %% 128 == 0 (whole 16-byte vectors)", t.name);
         const int64_t vpp = (int64_t)t.chunk_c * d->bits / 128;
         const int64_t pj = wide_band_pixels_per_thread(t.tile_p, t.threads, (int)vpp);
-        if (pl.rows * ncols > (int64_t)t.threads * pj)
+        const bool lowered = (ablation & 1) != 0, ldsepi = (ablation & 2) != 0;
+        if (ablation && (d->r != 3 || d->s != 3 || splits != 1))
+            return fail(QCONV_EUNSUPPORTED, "ablation instances run 3x3 filters without a split");
+        if (!lowered && pl.rows * ncols > (int64_t)t.threads * pj)
             return fail(QCONV_EUNSUPPORTED, "tile %s: the input band of this shape exceeds one prefetch batch", t.name);
         const int64_t planes = t.chunk_c / 16;
         // plane strides: multiples of 256 bytes keep the four 16-lane groups of a
         // 16-byte LDS read in distinct banks; filter planes are whole KiB so a
         // prepared filter block is copied with 1 KiB LDS-DMA instructions
-        pl.pstride_b = round_up(pl.rows * ncols * 16, 256);
+        // (the lowered operand holds every tile pixel once per tap instead)
+        pl.pstride_b = lowered ? round_up((int64_t)d->r * d->s * t.tile_p * 16, 256) : round_up(pl.rows * ncols * 16, 256);
         pl.pstride_w = round_up((int64_t)d->r * d->s * t.tile_k * 16, 1024);
         const int64_t bbuf = planes * pl.pstride_b, wbuf = planes * pl.pstride_w;
         // buffer loads take 32-bit offsets, and offset 2^31 marks padding
         if (li.x_bytes >= (1ll << 31) || pl.ktiles * nchunks * wbuf >= (1ll << 31))
             return fail(QCONV_EUNSUPPORTED, "tile %s addresses operands with 31-bit buffer offsets", t.name);
-        const int64_t mbytes = round_up((int64_t)t.tile_k * 8 + 4, 16);   // multipliers, biases, split-K flag
+        const int64_t mbytes0 = round_up((int64_t)t.tile_k * 8 + 4, 16);   // multipliers, biases, split-K flag
+        const int64_t mbytes = mbytes0 + (ldsepi ? (int64_t)t.tile_p * t.tile_k * 4 : 0);   // + int32 tile
         const int64_t single = bbuf + wbuf + mbytes;
         const int64_t tiles = pl.mtiles * pl.ktiles;
         if (splits < 1 || splits > nchunks)
@@ -262,6 +269,7 @@ int plan_tile(const qconv_desc *d, const qconv_layout_info &li, const qconv_tile
             pl.grid = gpk * pl.ktiles;
         }
     }
+    if (t.variant == QCONV_VARIANT_WIDE && (ablation & 2)) pl.off_e = pl.off_m + round_up((int64_t)t.tile_k * 8 + 4, 16);
     if (pl.lds > kLdsBytes)
         return fail(QCONV_EUNSUPPORTED, "tile %s needs %lld bytes of LDS for this shape (limit %lld)", t.name,
                     (long long)pl.lds, (long long)kLdsBytes);
@@ -425,6 +433,7 @@ void fill_args(ConvArgs &a, const qconv_desc *d, const qconv_layout_info &li, co
     a.off_w0 = (int32_t)pl.off_w0;
     a.off_w1 = (int32_t)pl.off_w1;
     a.off_m = (int32_t)pl.off_m;
+    a.off_e = (int32_t)pl.off_e;
     a.pstride_b = (int32_t)pl.pstride_b;
     a.pstride_w = (int32_t)pl.pstride_w;
     a.ktiles = (int32_t)pl.ktiles;
@@ -450,12 +459,12 @@ void fill_args(ConvArgs &a, const qconv_desc *d, const qconv_layout_info &li, co
 }
 
 // inst: 0 = the tile's generic kernel, 1 + i = its fixed-size instance i; 3 + the same for
-// the kernels with the bias and residual epilogue.
+// the kernels with the bias and residual epilogue; 8 + mask for an ablation instance.
 int ensure_lds_attribute(const void *kernel, int tile_id, int inst, int64_t lds) {
     if (lds <= 64 * 1024) return QCONV_OK;
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return fail(QCONV_EHIP, "hipGetDevice failed");
-    const long long key = ((long long)dev * 4096 + tile_id) * 8 + inst;
+    const long long key = ((long long)dev * 4096 + tile_id) * 16 + inst;
     std::lock_guard<std::mutex> g(g_attr.mu);
     if (!g_attr.done[key]) {
         hipError_t e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
@@ -473,7 +482,7 @@ int ensure_lds_attribute(const void *kernel, int tile_id, int inst, int64_t lds)
 int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, size_t w_bytes_given,
              const qconv_epilogue *epi, void *y, void *workspace, size_t workspace_bytes, int32_t tile_id,
              int32_t splits, void *stream, int32_t wg_per_cu = 0, int32_t band_buffers = 0,
-             int32_t xcd_order = 1) {
+             int32_t xcd_order = 1, int32_t ablation = 0) {
     qconv_layout_info li;
     int rc = check_desc(d, &li);
     if (rc) return rc;
@@ -489,7 +498,9 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
     tile_id = rc;
     const TileEntry &te = tile_table()[tile_id];
     Plan pl;
-    rc = plan_tile(d, li, te.info, &pl, 0, splits);
+    if (ablation && (!prepared || te.info.variant != QCONV_VARIANT_WIDE || !ablation_instance(te.info.name, ablation)))
+        return fail(QCONV_EUNSUPPORTED, "no ablation instance %d of tile %s", ablation, te.info.name);
+    rc = plan_tile(d, li, te.info, &pl, 0, splits, false, ablation);
     if (rc) return rc;
     const int64_t wsb = split_workspace_bytes(te.info, pl);
     if (wsb > 0) {
@@ -527,6 +538,7 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
     // the epilogue flavour: bias and residual are compiled into separate kernels;
     // prepared filters of a 3x3 or 1x1 layer run the tile's fixed-size instance
     const bool ext = requant && (epi->bias || epi->residual);
+    if (ablation && ext) return fail(QCONV_EUNSUPPORTED, "ablation instances have no bias or residual epilogue");
     const KernelSet &ks = ext ? te.ext : te.plain;
     ConvLauncher launch = ks.launch;
     const void *kernel = ks.kernel;
@@ -538,6 +550,12 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
                 kernel = ks.fixed[i].kernel;
                 inst = (ext ? 3 : 0) + 1 + i;
             }
+    if (ablation) {
+        const AblationInstance *ai = ablation_instance(te.info.name, ablation);
+        launch = ai->launch;
+        kernel = ai->kernel;
+        inst = 8 + ablation;
+    }
     if (te.info.variant == QCONV_VARIANT_WIDE && pl.splits == 1 && pl.off_b1 != pl.off_b0) {
         // persistent grid: size it by the occupancy the runtime reports for this kernel
         rc = ensure_lds_attribute(kernel, tile_id, inst, pl.lds);
@@ -550,14 +568,14 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
         // choice; band_buffers forces either)
         Plan one;
         int occ1 = 0;
-        const bool one_ok = plan_tile(d, li, te.info, &one, 0, 1, true) == QCONV_OK && one.lds < pl.lds;
+        const bool one_ok = plan_tile(d, li, te.info, &one, 0, 1, true, ablation) == QCONV_OK && one.lds < pl.lds;
         if (one_ok &&
             hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ1, kernel, te.info.threads, (size_t)one.lds) != hipSuccess)
             occ1 = 0;
         const bool use_one = band_buffers == 1 ? one_ok : (band_buffers == 2 ? false : one_ok && occ > 0 && occ1 > occ);
         const int pc = wg_per_cu > 0 ? wg_per_cu : (use_one ? occ1 : occ);
         if (pc > 0 || use_one) {
-            rc = plan_tile(d, li, te.info, &pl, pc > 0 ? pc : 0, 1, use_one);
+            rc = plan_tile(d, li, te.info, &pl, pc > 0 ? pc : 0, 1, use_one, ablation);
             if (rc) return rc;
         }
     }
@@ -606,6 +624,7 @@ static int check_schedule_knobs(const qconv_schedule *s) {
     if (s->wg_per_cu < 0 || s->wg_per_cu > 16) return fail(QCONV_EINVAL, "wg_per_cu must be in [0, 16]");
     if (s->band_buffers < 0 || s->band_buffers > 2) return fail(QCONV_EINVAL, "band_buffers must be 0, 1 or 2");
     if (s->xcd_order != 0 && s->xcd_order != 1) return fail(QCONV_EINVAL, "xcd_order must be 0 or 1");
+    if (s->ablation < 0 || s->ablation > 3) return fail(QCONV_EINVAL, "ablation must be in [0, 3]");
     if (s->splits < 1) return fail(QCONV_EUNSUPPORTED, "splits must be >= 1");
     return QCONV_OK;
 }
@@ -619,7 +638,10 @@ int qconv_schedule_check(const qconv_desc *d, const qconv_schedule *s) {
     if (rc) return rc;
     rc = resolve_tile(d, li, s->tile_id);
     if (rc < 0) return rc;
-    return plan_tile(d, li, tile_table()[rc].info, nullptr, 0, s->splits);
+    const qconv_tile_info &t = tile_table()[rc].info;
+    if (s->ablation && (t.variant != QCONV_VARIANT_WIDE || !ablation_instance(t.name, s->ablation)))
+        return fail(QCONV_EUNSUPPORTED, "no ablation instance %d of tile %s", s->ablation, t.name);
+    return plan_tile(d, li, t, nullptr, 0, s->splits, false, s->ablation);
 }
 
 int qconv2d_scheduled(const qconv_desc *d, const void *x, const void *w_prepared, size_t w_prepared_bytes,
@@ -629,7 +651,7 @@ int qconv2d_scheduled(const qconv_desc *d, const void *x, const void *w_prepared
     int rc = check_schedule_knobs(s);
     if (rc) return rc;
     return run_conv(d, x, w_prepared, true, w_prepared_bytes, epi, y, workspace, workspace_bytes, s->tile_id,
-                    s->splits, stream, s->wg_per_cu, s->band_buffers, s->xcd_order);
+                    s->splits, stream, s->wg_per_cu, s->band_buffers, s->xcd_order, s->ablation);
 }
 
 int qconv_workspace_bytes(const qconv_desc *d, int32_t tile_id, int32_t splits, size_t *bytes) {

@@ -55,6 +55,7 @@ struct ConvArgs {
     int32_t off_b0, off_b1; // LDS byte offsets of the two band buffers (pipelined kernel)
     int32_t off_w0, off_w1; // LDS byte offsets of the two filter buffers (equal when one chunk)
     int32_t off_m;          // LDS byte offset of the workgroup's multipliers (wide kernel)
+    int32_t off_e;          // LDS byte offset of the int32 accumulator tile (ablation: LDS epilogue)
     int32_t w_image;        // 1: wptr is a prepared filter image (wide kernel), 0: packed KRSC filters
     int32_t pstride_b;      // bytes per granule plane of the band buffer
     int32_t pstride_w;      // bytes per granule plane of the filter buffer
@@ -114,9 +115,18 @@ struct TileEntry {
     PrepLauncher prep;      // builds the filter image (wide tiles), else null
 };
 
+// A kernel with some of the techniques switched off (for measurement).
+struct AblationInstance {
+    const char *tile;       // the tile it is a variant of
+    int mask;               // 1: lowered staging, 2: LDS epilogue, 3: both
+    ConvLauncher launch;
+    const void *kernel;
+};
+
 // Defined in qconv_conv.hip.
 const TileEntry *tile_table();
 int tile_table_size();
+const AblationInstance *ablation_instance(const char *tile_name, int mask);
 
 // Defined in qconv_pack.hip.
 hipError_t launch_pack(const int8_t *src, void *dst, int32_t n, int32_t c, int32_t h, int32_t w, int32_t bits,

@@ -49,18 +49,18 @@ class QConvTileInfo(ctypes.Structure):
                                     "tile_k", "threads", "variant", "x_signed", "w_signed")] + [("name", ctypes.c_char * 64)]
 
 
+SCHEDULE_KNOBS = ("tile_id", "splits", "wg_per_cu", "band_buffers", "xcd_order", "ablation")
+
+
 class QConvSchedule(ctypes.Structure):
-    _fields_ = [(f, _i32) for f in ("tile_id", "splits", "wg_per_cu", "band_buffers", "xcd_order")]
-
-
-SCHEDULE_KNOBS = ("tile_id", "splits", "wg_per_cu", "band_buffers", "xcd_order")
+    _fields_ = [(f, _i32) for f in SCHEDULE_KNOBS]
 
 
 def make_schedule(sch: dict | QConvSchedule) -> QConvSchedule:
     """A qconv_schedule from a dict (missing launch knobs take their defaults)."""
     if isinstance(sch, QConvSchedule):
         return sch
-    full = {"tile_id": -1, "splits": 1, "wg_per_cu": 0, "band_buffers": 0, "xcd_order": 1}
+    full = {"tile_id": -1, "splits": 1, "wg_per_cu": 0, "band_buffers": 0, "xcd_order": 1, "ablation": 0}
     full.update({k: int(v) for k, v in sch.items() if k in SCHEDULE_KNOBS})
     return QConvSchedule(**full)
 

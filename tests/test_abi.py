@@ -335,3 +335,15 @@ def test_bias_and_residual_argument_errors(q):
     assert L.qconv2d(ref, x, w, ctypes.byref(part), y, None, 0, -1, None) == -1
     over_x = _epi(q, residual=x + 64)
     assert L.qconv2d(ref, x, w, ctypes.byref(over_x), y, None, 0, -1, None) == -1
+
+
+def test_ablation_schedules(q):
+    d = D(n=2)
+    names = {t["name"]: t["id"] for t in q.tiles()}
+    for name in ("wide_b4_w4x1_f1x4_c64", "wide_b4_w8x1_f1x4_c64", "wide_b4_w4x1_f2x4_c64"):
+        for mask in (1, 2, 3):
+            assert q.schedule_status(d, {"tile_id": names[name], "ablation": mask}) == 0, (name, mask)
+    assert q.schedule_status(d, {"tile_id": names["wide_b4_w4x1_f4x4_c64"], "ablation": 1}) == -2   # not compiled
+    assert q.schedule_status(d, {"tile_id": names["wide_b4_w4x1_f1x4_c64"], "ablation": 4}) == -1
+    assert q.schedule_status(D(r=1, s=1, pad_h=0, pad_w=0), {"tile_id": names["wide_b4_w4x1_f1x4_c64"],
+                                                           "ablation": 1}) == -2              # 3x3 only

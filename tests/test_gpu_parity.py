@@ -508,3 +508,42 @@ def test_residual_blocks_chain_eager_and_graph():
             assert_same(o.cpu().numpy(), ref["y_packed"], f"replay {i} {name}")
         chain.forward()
         torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("shape", [
+    ("a_2x56_64to64", 2, 56, 64, 64),
+    ("a_2x28_128to128", 2, 28, 128, 128),
+    ("a_8x7_512to512", 8, 7, 512, 512),
+], ids=lambda v: v[0])
+def test_ablation_instances_match_oracle(shape):
+    """The kernels with duplicate-aware loading and/or register-level packing
+    switched off (measurement instances) compute the same bytes."""
+    torch, q = _torch(), _qconv()
+    name, n, h, c, k = shape
+    L = qi.Layer(name, n, h, h, c, k, 3, 3, 1, 1, w_range=(-7, 7))
+    t = qi.layer_tensors(960, c, L)
+    sh = stress_shift(L, L.x_range, L.w_range)
+    ref = ref_layer(L, t, requant=True, shift=sh)
+    ref_raw = ref_layer(L, t, requant=False)
+    dev = torch.device("cuda:0")
+    xp = q.pack(torch.from_numpy(t["x"]).to(dev), 4, False)
+    wp = q.pack(torch.from_numpy(t["w"]).to(dev), 4, True)
+    mult = torch.from_numpy(t["mult"]).to(dev)
+    names = {tt["name"]: tt["id"] for tt in q.tiles()}
+    ran = 0
+    for tname in ("wide_b4_w4x1_f1x4_c64", "wide_b4_w8x1_f1x4_c64", "wide_b4_w4x1_f2x4_c64"):
+        tid = names[tname]
+        wprep = q.prepare_filters(L.desc(), wp, tid)
+        for mask in (1, 2, 3):
+            sch = {"tile_id": tid, "ablation": mask}
+            if q.schedule_status(L.desc(), sch) != 0:
+                continue
+            ran += 1
+            announce(f"{name} {tname} ablation {mask}")
+            y = q.Conv2dCall(L.desc(), xp, wprep, schedule=sch, requant=True, mult=mult, shift=sh)()
+            torch.cuda.synchronize()
+            assert_same(y.cpu().numpy(), ref["y_packed"], f"{name} {tname} ablation {mask}")
+            y = q.Conv2dCall(L.desc(), xp, wprep, schedule=sch)()
+            torch.cuda.synchronize()
+            assert_same(y.cpu().numpy(), ref_raw["acc"], f"{name} {tname} ablation {mask} raw")
+    assert ran >= 3
