@@ -186,6 +186,28 @@ int qconv_pack(const int8_t *src, void *dst, int32_t n, int32_t c, int32_t h, in
                int32_t bits, int32_t is_signed, void *stream);
 
 /*
+ * qconv_unroll -- width unrolling for layers with very few input channels
+ * (e.g. the 3-channel 7x7 stem of a ResNet): folds the `taps` filter columns
+ * into the channel axis so the layer runs as a (taps_h x 1) convolution over
+ * c_out channels on the same kernels (the MMA depth then holds taps*c real
+ * values instead of c).
+ *   src   DEVICE int8, n x c x h x w (NCHW)
+ *   dst   DEVICE int8, n x h x wout x c_out, 16-byte aligned, not overlapping
+ *         src; wout = (w + 2*pad - taps) / stride + 1
+ *   dst[n][y][q][s*c + ci] = src[n][ci][y][q*stride + s - pad] for s < taps,
+ *   ci < c (0 where the column is outside the input), and 0 for channels
+ *   from taps*c to c_out.
+ * The convolution of x with filters k x c x R x S, stride (sh, sw) and
+ * padding (ph, pw) equals the convolution of unroll(x; S, sw, pw) with
+ * unroll(filters; S, 1, 0) -- a k x R x 1 x c_out bank -- with stride (sh, 1),
+ * padding (ph, 0).  8-bit operands (signed).  Needs taps*c <= c_out and
+ * c_out % 16 == 0.  Errors: QCONV_EINVAL (NULL, sizes, overlap, alignment),
+ * QCONV_EHIP.  Zero-sized tensors are a no-op.
+ */
+int qconv_unroll(const int8_t *src, int8_t *dst, int32_t n, int32_t c, int32_t h, int32_t w, int32_t taps,
+                 int32_t stride, int32_t pad, int32_t c_out, void *stream);
+
+/*
  * qconv2d -- the convolution (Sec. 2.1) as an implicit GEMM with the
  * epilogue of Sec. 3.2.2 fused into it.
  *   x          DEVICE, packed activations, 16-byte aligned

@@ -739,6 +739,27 @@ int qconv2d_prepared(const qconv_desc *d, const void *x, const void *w_prepared,
                     stream);
 }
 
+int qconv_unroll(const int8_t *src, int8_t *dst, int32_t n, int32_t c, int32_t h, int32_t w, int32_t taps,
+                 int32_t stride, int32_t pad, int32_t c_out, void *stream) {
+    g_err[0] = 0;
+    if (n < 0 || c < 0 || h < 0 || w < 0) return fail(QCONV_EINVAL, "sizes must be >= 0");
+    if (taps < 1 || stride < 1 || pad < 0) return fail(QCONV_EINVAL, "taps and stride must be >= 1, pad >= 0");
+    if (c_out < 16 || c_out % 16 != 0) return fail(QCONV_EINVAL, "c_out must be a positive multiple of 16");
+    if ((int64_t)taps * c > c_out) return fail(QCONV_EINVAL, "taps * c (%lld) exceeds c_out (%d)", (long long)taps * c, c_out);
+    const int64_t span = (int64_t)w + 2 * pad - taps;
+    if (span < 0) return fail(QCONV_EINVAL, "filter width larger than the padded input");
+    const int64_t wout = span / stride + 1;
+    const int64_t in_bytes = (int64_t)n * c * h * w, out_bytes = (int64_t)n * h * wout * c_out;
+    if (in_bytes == 0 || out_bytes == 0) return QCONV_OK;
+    if (!src || !dst) return fail(QCONV_EINVAL, "src and dst must be non-NULL");
+    if (!aligned16(dst)) return fail(QCONV_EINVAL, "dst must be 16-byte aligned");
+    if ((uintptr_t)src < (uintptr_t)dst + out_bytes && (uintptr_t)dst < (uintptr_t)src + in_bytes)
+        return fail(QCONV_EINVAL, "src and dst overlap");
+    hipError_t e = launch_unroll(src, dst, n, c, h, w, taps, stride, pad, (int32_t)wout, c_out, (hipStream_t)stream);
+    if (e != hipSuccess) return fail(QCONV_EHIP, "unroll launch: %s", hipGetErrorString(e));
+    return QCONV_OK;
+}
+
 int qconv_probe_mfma_i8(int32_t blocks, int32_t iters, int32_t *sink, uint64_t *stamps, int64_t *ops, void *stream) {
     g_err[0] = 0;
     if (blocks < 1 || blocks > (1 << 20) || iters < 1 || iters > (1 << 24))

@@ -132,6 +132,10 @@ const AblationInstance *ablation_instance(const char *tile_name, int mask);
 hipError_t launch_pack(const int8_t *src, void *dst, int32_t n, int32_t c, int32_t h, int32_t w, int32_t bits,
                        int32_t is_signed, hipStream_t stream);
 
+// Defined in qconv_unroll.hip.
+hipError_t launch_unroll(const int8_t *src, int8_t *dst, int32_t n, int32_t c, int32_t h, int32_t w, int32_t taps,
+                         int32_t stride, int32_t pad, int32_t wout, int32_t c_out, hipStream_t stream);
+
 // Defined in qconv_probe.hip (measurement aid).
 int64_t mfma_probe_ops(int blocks, int iters);
 hipError_t launch_mfma_probe(int blocks, int iters, int32_t *sink, uint64_t *stamps, hipStream_t stream);

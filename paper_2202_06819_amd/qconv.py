@@ -105,11 +105,12 @@ def lib() -> ctypes.CDLL:
         L.qconv_max_splits.argtypes = [P(QConvDesc), _i32]
         L.qconv_probe_mfma_i8.argtypes = [_i32, _i32, _vp, _vp, P(_i64), _vp]
         L.qconv_schedule_check.argtypes = [P(QConvDesc), P(QConvSchedule)]
+        L.qconv_unroll.argtypes = [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _vp]
         L.qconv2d_scheduled.argtypes = [P(QConvDesc), _vp, _vp, ctypes.c_size_t, P(QConvEpilogue), _vp,
                                         P(QConvSchedule), _vp, ctypes.c_size_t, _vp]
         for f in ("qconv_layout", "qconv_pack", "qconv2d", "qconv_tile_count", "qconv_tile_get", "qconv_tile_check",
                   "qconv_default_tile", "qconv_selftest", "qconv_prepared_filter_bytes", "qconv_prepare_filters",
-                  "qconv2d_prepared", "qconv_workspace_bytes", "qconv_max_splits", "qconv_probe_mfma_i8", "qconv_schedule_check", "qconv2d_scheduled"):
+                  "qconv2d_prepared", "qconv_workspace_bytes", "qconv_max_splits", "qconv_probe_mfma_i8", "qconv_schedule_check", "qconv2d_scheduled", "qconv_unroll"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
         return L
@@ -271,6 +272,22 @@ def _epilogue_extras(epi: QConvEpilogue, desc: QConvDesc, y_bytes: int, bias, re
     if residual is not None:
         epi.residual = _dev_ptr(residual, "residual", y_bytes)
         epi.residual_signed = int(bool(residual_signed))
+
+
+def unroll(src: torch.Tensor, taps: int, stride: int, pad: int, c_out: int, out: torch.Tensor | None = None,
+           stream=None) -> torch.Tensor:
+    """int8 N x C x H x W -> N x H x Wout x c_out with the `taps` filter columns
+    folded into channels (see qconv_unroll); for filters use stride 1, pad 0."""
+    if src.dtype != torch.int8 or src.dim() != 4:
+        raise QConvError(EINVAL, "unroll expects a 4-d int8 tensor")
+    n, c, h, w = src.shape
+    wout = (w + 2 * pad - taps) // stride + 1
+    if out is None:
+        out = torch.empty((n, h, max(wout, 0), c_out), dtype=torch.int8, device=src.device)
+    rc = lib().qconv_unroll(_dev_ptr(src, "src"), _dev_ptr(out, "dst", n * h * max(wout, 0) * c_out), n, c, h, w,
+                            int(taps), int(stride), int(pad), int(c_out), _vp(_stream(stream)))
+    _check(rc, "qconv_unroll")
+    return out
 
 
 def conv2d(d: dict, x: torch.Tensor, w: torch.Tensor, *, requant: bool = False, mult: torch.Tensor | None = None,

@@ -347,3 +347,15 @@ def test_ablation_schedules(q):
     assert q.schedule_status(d, {"tile_id": names["wide_b4_w4x1_f1x4_c64"], "ablation": 4}) == -1
     assert q.schedule_status(D(r=1, s=1, pad_h=0, pad_w=0), {"tile_id": names["wide_b4_w4x1_f1x4_c64"],
                                                            "ablation": 1}) == -2              # 3x3 only
+
+
+def test_unroll_argument_errors(q):
+    L = q.lib()
+    src, dst = 1 << 32, 1 << 34
+    assert L.qconv_unroll(src, dst, 1, 3, 8, 8, 7, 2, 3, 20, None) == -1        # c_out not a multiple of 16
+    assert L.qconv_unroll(src, dst, 1, 3, 8, 8, 7, 2, 3, 16, None) == -1        # 7 * 3 > 16
+    assert L.qconv_unroll(src, dst, 1, 3, 8, 8, 0, 2, 3, 32, None) == -1        # no taps
+    assert L.qconv_unroll(src, dst, 1, 3, 8, 2, 7, 1, 0, 32, None) == -1        # window wider than the input
+    assert L.qconv_unroll(src, dst + 8, 1, 3, 8, 8, 7, 2, 3, 32, None) == -1    # misaligned
+    assert L.qconv_unroll(src, src + 64, 1, 3, 8, 8, 7, 2, 3, 32, None) == -1   # overlap
+    assert L.qconv_unroll(None, None, 0, 3, 8, 8, 7, 2, 3, 32, None) == 0       # empty: no-op

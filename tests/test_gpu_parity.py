@@ -547,3 +547,52 @@ def test_ablation_instances_match_oracle(shape):
             torch.cuda.synchronize()
             assert_same(y.cpu().numpy(), ref_raw["acc"], f"{name} {tname} ablation {mask} raw")
     assert ran >= 3
+
+
+def test_stem_7x7_by_width_unrolling():
+    """The 3-channel 7x7 stride-2 stem (8-bit): the input and the filters are
+    width-unrolled on the GPU and the 7x1 convolution runs on every tile that
+    takes it; the result equals the oracle's direct 7x7 convolution of the
+    original tensors."""
+    torch, q = _torch(), _qconv()
+    n, h, c, k = 2, 224, 3, 64
+    L = qi.Layer("stem", n, h, h, c, k, 7, 7, 2, 3, bits=8, x_signed=True, w_signed=True, x_range=qi.S8,
+                 w_range=qi.S8, epilogue=qi.Epilogue(relu=True, lo=-128, hi=127))
+    t = qi.layer_tensors(990, 0, L)
+    sh = stress_shift(L, L.x_range, L.w_range)
+    ref = oracle.qconv_layer(t["x"], t["w"], bits=8, x_signed=True, w_signed=True, stride=(2, 2), pad=(3, 3),
+                             mult=t["mult"], shift=sh, relu=True, lo=-128, hi=127, threads=oracle_threads())
+    dev = torch.device("cuda:0")
+    announce("stem unroll")
+    xu = q.unroll(torch.from_numpy(t["x"]).to(dev), 7, 2, 3, 32)
+    wu = q.unroll(torch.from_numpy(t["w"]).to(dev), 7, 1, 0, 32)
+    torch.cuda.synchronize()
+    # the unrolled layouts, spot-checked against their definition
+    xn, wn = xu.cpu().numpy(), wu.cpu().numpy()
+    assert xu.shape == (n, h, 112, 32) and wu.shape == (k, 7, 1, 32)
+    for (img, row, qq) in [(0, 0, 0), (1, 100, 57), (0, 223, 111), (1, 5, 1)]:
+        for ch in range(32):
+            s, ci = divmod(ch, 3)
+            col = qq * 2 + s - 3
+            want = t["x"][img, ci, row, col] if ch < 21 and 0 <= col < h else 0
+            assert xn[img, row, qq, ch] == want
+    assert np.array_equal(wn[:, :, 0, :21].reshape(k, 7, 7, 3), t["w"].transpose(0, 2, 3, 1))
+    assert not wn[:, :, 0, 21:].any()
+    d = dict(n=n, h=h, w=112, c=32, k=k, r=7, s=1, stride_h=2, stride_w=1, pad_h=3, pad_w=0, bits=8, x_signed=1,
+             w_signed=1)
+    mult = torch.from_numpy(t["mult"]).to(dev)
+    ran = 0
+    for tt in q.tiles():
+        if q.tile_status(d, tt["id"]) != 0:
+            continue
+        ran += 1
+        announce(f"stem 7x1 conv tile {tt['name']}")
+        y = q.conv2d(d, xu, wu, tile=tt["id"], requant=True, mult=mult, shift=sh, relu=True, clamp=(-128, 127))
+        torch.cuda.synchronize()
+        assert_same(y.cpu().numpy(), ref["y_packed"], f"stem {tt['name']}")
+        if tt["variant"] == 2:
+            wprep = q.prepare_filters(d, wu, tt["id"])
+            y = q.conv2d(d, xu, wprep, tile=tt["id"], prepared=True)
+            torch.cuda.synchronize()
+            assert_same(y.cpu().numpy(), ref["acc"], f"stem {tt['name']} prepared raw")
+    assert ran >= 2
