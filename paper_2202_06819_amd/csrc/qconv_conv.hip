@@ -935,6 +935,8 @@ static hipError_t launch_prep(const ConvArgs &a, uint8_t *img, int64_t elems, hi
 
 #define QCONV_WIDE_TILES(X) \
     X(4, 4, 1, 1, 4, 64)    \
+    X(4, 4, 2, 2, 2, 64)    \
+    X(4, 2, 2, 2, 2, 64)    \
     X(4, 4, 1, 2, 4, 64)    \
     X(4, 4, 1, 4, 4, 64)    \
     X(4, 8, 1, 1, 4, 64)    \
@@ -951,6 +953,7 @@ static hipError_t launch_prep(const ConvArgs &a, uint8_t *img, int64_t elems, hi
     X(4, 2, 4, 2, 4, 128)   \
     X(4, 1, 4, 4, 4, 128)   \
     X(8, 4, 1, 2, 4, 64)    \
+    X(8, 4, 2, 2, 2, 64)    \
     X(8, 4, 1, 4, 4, 64)    \
     X(8, 8, 1, 2, 4, 64)    \
     X(8, 4, 2, 4, 4, 64)    \
