@@ -35,6 +35,12 @@
  *          bits [4i, 4i+3] of word j; signed values are two's-complement
  *          nibbles.
  *   b = 8: each pixel is C int8 values.
+ *   batch-interleaved (qconv_desc.nb > 1; the NHWCnc layout of Sec. 3.3.2
+ *   with n = nb images and c = the whole channel run): N/nb x H x W x nb x C,
+ *   i.e. image i's pixel (y, x) is pixel ((i/nb)*H + y)*W*nb + x*nb + i%nb
+ *   of the plain layout; each pixel's channels are packed as above.  Nb
+ *   consecutive pixels -- one MMA tile's rows -- then hold the same (y, x)
+ *   of nb images, and a row of the tensor is contiguous for all of them.
  */
 #ifndef QCONV_H
 #define QCONV_H
@@ -63,7 +69,10 @@ extern "C" {
  * k: output channels; r, s: filter height and width; stride and zero padding
  * per axis; bits: 4 or 8; x_signed / w_signed: 0 or 1 (8-bit needs both 1).
  * Output extent P = (h + 2*pad_h - r)/stride_h + 1, Q likewise (Sec. 2.1; no
- * dilation, no groups; cross-correlation, no filter flip).
+ * dilation, no groups; cross-correlation, no filter flip).  nb: activation
+ * layout, 0 or 1 for N x H x W x C, nb > 1 for the batch-interleaved layout
+ * (input, output and residual alike); it needs n % nb == 0, and stride_w == 1
+ * (else QCONV_EUNSUPPORTED).  The filters' layout does not change.
  */
 typedef struct qconv_desc {
     int32_t n, h, w, c;
@@ -72,6 +81,7 @@ typedef struct qconv_desc {
     int32_t pad_h, pad_w;
     int32_t bits;
     int32_t x_signed, w_signed;
+    int32_t nb;
 } qconv_desc;
 
 /* Sizes derived from a qconv_desc (bytes unless stated). */
@@ -186,26 +196,43 @@ int qconv_pack(const int8_t *src, void *dst, int32_t n, int32_t c, int32_t h, in
                int32_t bits, int32_t is_signed, void *stream);
 
 /*
- * qconv_unroll -- width unrolling for layers with very few input channels
- * (e.g. the 3-channel 7x7 stem of a ResNet): folds the `taps` filter columns
- * into the channel axis so the layer runs as a (taps_h x 1) convolution over
- * c_out channels on the same kernels (the MMA depth then holds taps*c real
- * values instead of c).
- *   src   DEVICE int8, n x c x h x w (NCHW)
- *   dst   DEVICE int8, n x h x wout x c_out, 16-byte aligned, not overlapping
- *         src; wout = (w + 2*pad - taps) / stride + 1
- *   dst[n][y][q][s*c + ci] = src[n][ci][y][q*stride + s - pad] for s < taps,
- *   ci < c (0 where the column is outside the input), and 0 for channels
- *   from taps*c to c_out.
- * The convolution of x with filters k x c x R x S, stride (sh, sw) and
- * padding (ph, pw) equals the convolution of unroll(x; S, sw, pw) with
- * unroll(filters; S, 1, 0) -- a k x R x 1 x c_out bank -- with stride (sh, 1),
- * padding (ph, 0).  8-bit operands (signed).  Needs taps*c <= c_out and
- * c_out % 16 == 0.  Errors: QCONV_EINVAL (NULL, sizes, overlap, alignment),
- * QCONV_EHIP.  Zero-sized tensors are a no-op.
+ * qconv_pack_interleaved -- qconv_pack of activations into the
+ * batch-interleaved layout (Sec. 3.3.2's NHWCnc, nb images per pixel): the
+ * same values and packing, image i's pixel (y, x) stored at pixel
+ * ((i/nb)*h + y)*w*nb + x*nb + i%nb.  nb = 1 is qconv_pack.  Needs
+ * n % nb == 0 (QCONV_EINVAL otherwise); other rules and errors as qconv_pack.
  */
-int qconv_unroll(const int8_t *src, int8_t *dst, int32_t n, int32_t c, int32_t h, int32_t w, int32_t taps,
-                 int32_t stride, int32_t pad, int32_t c_out, void *stream);
+int qconv_pack_interleaved(const int8_t *src, void *dst, int32_t n, int32_t c, int32_t h, int32_t w,
+                           int32_t bits, int32_t is_signed, int32_t nb, void *stream);
+
+/*
+ * qconv_unroll -- patch unrolling for layers with very few input channels
+ * (e.g. the 3-channel 7x7 stride-2 stem of a ResNet): folds filter taps into
+ * the channel axis so the layer runs on the channel-packed kernels with
+ * taps_h*taps_w*c real values per MMA depth instead of c.
+ *   src   DEVICE int8, n x c x h x w (NCHW); may be NULL when it is empty
+ *   dst   DEVICE int8, n x out_h x wout x c_out, 16-byte aligned, not
+ *         overlapping src; wout = (w + 2*pad_w - taps_w) / stride_w + 1
+ *   dst[n][u][q][(b*taps_w + s)*c + ci] =
+ *       src[n][ci][u*stride_h + b - pad_h][q*stride_w + s - pad_w]
+ *   for b < taps_h, s < taps_w, ci < c (0 where the row or column is outside
+ *   the input), and 0 for channels from taps_h*taps_w*c to c_out.
+ * For a layer x (*) f with filters k x c x R x S, stride (sh, sw), padding
+ * (ph, pw) and output P x Q, two foldings give the same result:
+ *   - all rows:  unroll(x; R, sh, ph, P; S, sw, pw) (*) unroll(f; R, 1, 0, 1;
+ *     S, 1, 0), a 1x1 convolution at stride 1;
+ *   - row groups of sh:  unroll(x; sh, sh, ph, P + R' - 1; S, sw, pw) (*)
+ *     unroll(f; sh, sh, 0, R'; S, 1, 0) with R' = ceil(R / sh), an R' x 1
+ *     convolution at stride 1 without padding (filter rows beyond R are 0).
+ * The unrolled operands are 8-bit (signed).  Needs taps_h*taps_w*c <= c_out,
+ * c_out % 16 == 0, and 4*c_out + c*taps_h*(w + 2*pad_w) <= 65536 (bytes
+ * staged per output row).  Errors: QCONV_EINVAL (NULL, sizes, overlap,
+ * alignment), QCONV_EUNSUPPORTED (staging limit), QCONV_EHIP.  An empty
+ * destination is a no-op.
+ */
+int qconv_unroll(const int8_t *src, int8_t *dst, int32_t n, int32_t c, int32_t h, int32_t w, int32_t taps_h,
+                 int32_t stride_h, int32_t pad_h, int32_t out_h, int32_t taps_w, int32_t stride_w, int32_t pad_w,
+                 int32_t c_out, void *stream);
 
 /*
  * qconv2d -- the convolution (Sec. 2.1) as an implicit GEMM with the

@@ -685,7 +685,7 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
             const int rr = (int)fdiv((uint32_t)tap, a.div_s);
             const int ss = tap - rr * a.s;
             ao = ks * 4 * a.pstride_w + tap * TK * 16;
-            bo = ks * 4 * a.pstride_b + (rr * a.ncols + ss) * 16;
+            bo = ks * 4 * a.pstride_b + (rr * a.ncols + ss * a.tap_w) * 16;
         };
         if constexpr (FIXED) {
             // every step's LDS offsets are known: filter reads use immediate

@@ -31,6 +31,7 @@ int fail(int code, const char *fmt, ...) {
 }
 
 constexpr int64_t kLdsBytes = 160 * 1024;   // LDS per workgroup on gfx950
+constexpr int64_t kUnrollLdsBytes = 64 * 1024;   // LDS the unroll kernel may stage per row
 constexpr int64_t kMaxBytes = (int64_t)1 << 31;
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
@@ -56,6 +57,10 @@ int check_desc(const qconv_desc *d, qconv_layout_info *info) {
     if (d->pad_h < 0 || d->pad_w < 0) return fail(QCONV_EINVAL, "padding must be >= 0");
     if ((d->x_signed != 0 && d->x_signed != 1) || (d->w_signed != 0 && d->w_signed != 1))
         return fail(QCONV_EINVAL, "x_signed and w_signed must be 0 or 1");
+    if (d->nb < 0 || (d->nb > 1 && d->n % d->nb != 0))
+        return fail(QCONV_EINVAL, "nb must be 0, 1 or a divisor of n (n=%d nb=%d)", d->n, d->nb);
+    if (d->nb > 1 && d->stride_w != 1)
+        return fail(QCONV_EUNSUPPORTED, "the batch-interleaved layout needs stride_w == 1 (got %d)", d->stride_w);
     int64_t p = out_dim(d->h, d->r, d->stride_h, d->pad_h);
     int64_t q = out_dim(d->w, d->s, d->stride_w, d->pad_w);
     if (p < 1 || q < 1) return fail(QCONV_EINVAL, "filter window larger than the padded input");
@@ -96,6 +101,27 @@ int check_desc(const qconv_desc *d, qconv_layout_info *info) {
         info->y_packed_bytes = y_packed;
         info->workspace_bytes = 0;
         info->max_abs_acc = worst;
+    }
+    return QCONV_OK;
+}
+
+// Validates d and gives the geometry the kernels run.  The batch-interleaved
+// layout (nb > 1) is plain NHWC of n/nb images nb times as wide, in which a
+// filter's columns lie nb pixels apart: padding nb*pad_w, output width q*nb
+// (stride_w is 1), and kd->nb is that tap spacing.  Otherwise kd = *d, nb 1.
+int kernel_desc(const qconv_desc *d, qconv_desc *kd, qconv_layout_info *kli) {
+    int rc = check_desc(d, kli);
+    if (rc != QCONV_OK) return rc;
+    *kd = *d;
+    kd->nb = d->nb > 1 ? d->nb : 1;
+    if (kd->nb > 1) {
+        const int64_t w = (int64_t)d->w * kd->nb, pw = (int64_t)d->pad_w * kd->nb, q = (int64_t)kli->q * kd->nb;
+        if (w + 2 * pw >= (1ll << 30) || q >= (1ll << 30))
+            return fail(QCONV_EUNSUPPORTED, "interleaved rows of %lld padded pixels are too wide", (long long)(w + 2 * pw));
+        kd->n = d->n / kd->nb;
+        kd->w = (int32_t)w;
+        kd->pad_w = (int32_t)pw;
+        kli->q = (int32_t)q;
     }
     return QCONV_OK;
 }
@@ -192,6 +218,7 @@ int plan_tile(const qconv_desc *d, const qconv_layout_info &li, const qconv_tile
     pl.ktiles = (d->k + t.tile_k - 1) / t.tile_k;
     if (t.variant == QCONV_VARIANT_STAGED) {
         if (splits != 1) return fail(QCONV_EUNSUPPORTED, "tile %s has no split-K", t.name);
+        if (d->nb > 1) return fail(QCONV_EUNSUPPORTED, "tile %s does not read the batch-interleaved layout", t.name);
         const int64_t gran = 2 * d->bits;
         pl.pstride_b = pad_plane(pl.rows * ncols * gran);
         pl.pstride_w = pad_plane((int64_t)d->r * d->s * t.tile_k * gran);
@@ -203,8 +230,8 @@ int plan_tile(const qconv_desc *d, const qconv_layout_info &li, const qconv_tile
         const int64_t vpp = (int64_t)t.chunk_c * d->bits / 128;
         const int64_t pj = wide_band_pixels_per_thread(t.tile_p, t.threads, (int)vpp);
         const bool lowered = (ablation & 1) != 0, ldsepi = (ablation & 2) != 0;
-        if (ablation && (d->r != 3 || d->s != 3 || splits != 1))
-            return fail(QCONV_EUNSUPPORTED, "ablation instances run 3x3 filters without a split");
+        if (ablation && (d->r != 3 || d->s != 3 || splits != 1 || d->nb > 1))
+            return fail(QCONV_EUNSUPPORTED, "ablation instances run 3x3 filters without a split, plain layout");
         if (!lowered && pl.rows * ncols > (int64_t)t.threads * pj)
             return fail(QCONV_EUNSUPPORTED, "tile %s: the input band of this shape exceeds one prefetch batch", t.name);
         const int64_t planes = t.chunk_c / 16;
@@ -346,8 +373,10 @@ int qconv_tile_get(int32_t tile_id, qconv_tile_info *out) {
 int qconv_tile_check(const qconv_desc *d, int32_t tile_id) {
     g_err[0] = 0;
     qconv_layout_info li;
-    int rc = check_desc(d, &li);
+    qconv_desc kd;
+    int rc = kernel_desc(d, &kd, &li);
     if (rc) return rc;
+    d = &kd;
     if (tile_id < 0 || tile_id >= tile_table_size()) return fail(QCONV_EINVAL, "unknown tile %d", tile_id);
     return plan_tile(d, li, tile_table()[tile_id].info, nullptr);
 }
@@ -355,17 +384,20 @@ int qconv_tile_check(const qconv_desc *d, int32_t tile_id) {
 int qconv_default_tile(const qconv_desc *d) {
     g_err[0] = 0;
     qconv_layout_info li;
-    int rc = check_desc(d, &li);
+    qconv_desc kd;
+    int rc = kernel_desc(d, &kd, &li);
     if (rc) return rc;
+    d = &kd;
     int t = pick_default(d, li);
     if (t < 0) return fail(QCONV_EUNSUPPORTED, "no compiled tile fits this shape");
     return t;
 }
 
-int qconv_pack(const int8_t *src, void *dst, int32_t n, int32_t c, int32_t h, int32_t w, int32_t bits,
-               int32_t is_signed, void *stream) {
+int qconv_pack_interleaved(const int8_t *src, void *dst, int32_t n, int32_t c, int32_t h, int32_t w, int32_t bits,
+                           int32_t is_signed, int32_t nb, void *stream) {
     g_err[0] = 0;
     if (n < 0 || c < 0 || h < 0 || w < 0) return fail(QCONV_EINVAL, "sizes must be non-negative");
+    if (nb < 1 || n % nb != 0) return fail(QCONV_EINVAL, "nb must be >= 1 and divide n (n=%d nb=%d)", n, nb);
     if (is_signed != 0 && is_signed != 1) return fail(QCONV_EINVAL, "is_signed must be 0 or 1");
     if (bits != 4 && bits != 8) return fail(QCONV_EUNSUPPORTED, "bits must be 4 or 8 (got %d)", bits);
     if (bits == 4 && c % 8) return fail(QCONV_EUNSUPPORTED, "4-bit packing needs c %% 8 == 0 (c=%d)", c);
@@ -378,9 +410,14 @@ int qconv_pack(const int8_t *src, void *dst, int32_t n, int32_t c, int32_t h, in
     const uintptr_t s0 = (uintptr_t)src, s1 = s0 + count;
     const uintptr_t d0 = (uintptr_t)dst, d1 = d0 + count * bits / 8;
     if (s0 < d1 && d0 < s1) return fail(QCONV_EINVAL, "src and dst overlap");
-    hipError_t e = launch_pack(src, dst, n, c, h, w, bits, is_signed, (hipStream_t)stream);
+    hipError_t e = launch_pack(src, dst, n, c, h, w, bits, is_signed, nb, (hipStream_t)stream);
     if (e != hipSuccess) return fail(QCONV_EHIP, "pack launch: %s", hipGetErrorString(e));
     return QCONV_OK;
+}
+
+int qconv_pack(const int8_t *src, void *dst, int32_t n, int32_t c, int32_t h, int32_t w, int32_t bits,
+               int32_t is_signed, void *stream) {
+    return qconv_pack_interleaved(src, dst, n, c, h, w, bits, is_signed, 1, stream);
 }
 
 }  // extern "C"
@@ -422,6 +459,7 @@ void fill_args(ConvArgs &a, const qconv_desc *d, const qconv_layout_info &li, co
     a.m = (int32_t)li.m;
     a.vh = d->h + 2 * d->pad_h;
     a.ncols = d->w + 2 * d->pad_w;
+    a.tap_w = d->nb > 1 ? d->nb : 1;
     a.xpix = d->c * d->bits / 8;
     a.nchunks = (d->c + te.info.chunk_c - 1) / te.info.chunk_c;
     a.vec16 = (d->c * d->bits) % 128 == 0;
@@ -484,8 +522,10 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
              int32_t splits, void *stream, int32_t wg_per_cu = 0, int32_t band_buffers = 0,
              int32_t xcd_order = 1, int32_t ablation = 0) {
     qconv_layout_info li;
-    int rc = check_desc(d, &li);
+    qconv_desc kd;
+    int rc = kernel_desc(d, &kd, &li);
     if (rc) return rc;
+    d = &kd;
     rc = check_epilogue(d, epi);
     if (rc) return rc;
     if (!x || !w || !y) return fail(QCONV_EINVAL, "x, w and y must be non-NULL");
@@ -537,6 +577,7 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
     }
     // the epilogue flavour: bias and residual are compiled into separate kernels;
     // prepared filters of a 3x3 or 1x1 layer run the tile's fixed-size instance
+    // (whose taps are one column apart: not for 3x3 in the interleaved layout)
     const bool ext = requant && (epi->bias || epi->residual);
     if (ablation && ext) return fail(QCONV_EUNSUPPORTED, "ablation instances have no bias or residual epilogue");
     const KernelSet &ks = ext ? te.ext : te.plain;
@@ -545,7 +586,7 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
     int inst = ext ? 3 : 0;
     if (prepared && te.info.variant == QCONV_VARIANT_WIDE)
         for (int i = 0; i < 2; ++i)
-            if (ks.fixed[i].launch && ks.fixed[i].r == d->r && ks.fixed[i].s == d->s) {
+            if (ks.fixed[i].launch && ks.fixed[i].r == d->r && ks.fixed[i].s == d->s && (d->nb == 1 || d->s == 1)) {
                 launch = ks.fixed[i].launch;
                 kernel = ks.fixed[i].kernel;
                 inst = (ext ? 3 : 0) + 1 + i;
@@ -634,8 +675,10 @@ int qconv_schedule_check(const qconv_desc *d, const qconv_schedule *s) {
     int rc = check_schedule_knobs(s);
     if (rc) return rc;
     qconv_layout_info li;
-    rc = check_desc(d, &li);
+    qconv_desc kd;
+    rc = kernel_desc(d, &kd, &li);
     if (rc) return rc;
+    d = &kd;
     rc = resolve_tile(d, li, s->tile_id);
     if (rc < 0) return rc;
     const qconv_tile_info &t = tile_table()[rc].info;
@@ -657,8 +700,10 @@ int qconv2d_scheduled(const qconv_desc *d, const void *x, const void *w_prepared
 int qconv_workspace_bytes(const qconv_desc *d, int32_t tile_id, int32_t splits, size_t *bytes) {
     g_err[0] = 0;
     qconv_layout_info li;
-    int rc = check_desc(d, &li);
+    qconv_desc kd;
+    int rc = kernel_desc(d, &kd, &li);
     if (rc) return rc;
+    d = &kd;
     if (!bytes) return fail(QCONV_EINVAL, "bytes must be non-NULL");
     rc = resolve_tile(d, li, tile_id);
     if (rc < 0) return rc;
@@ -673,8 +718,10 @@ int qconv_workspace_bytes(const qconv_desc *d, int32_t tile_id, int32_t splits, 
 int qconv_max_splits(const qconv_desc *d, int32_t tile_id) {
     g_err[0] = 0;
     qconv_layout_info li;
-    int rc = check_desc(d, &li);
+    qconv_desc kd;
+    int rc = kernel_desc(d, &kd, &li);
     if (rc) return rc;
+    d = &kd;
     rc = resolve_tile(d, li, tile_id);
     if (rc < 0) return rc;
     const qconv_tile_info &t = tile_table()[rc].info;
@@ -685,8 +732,10 @@ int qconv_max_splits(const qconv_desc *d, int32_t tile_id) {
 int qconv_prepared_filter_bytes(const qconv_desc *d, int32_t tile_id, size_t *bytes) {
     g_err[0] = 0;
     qconv_layout_info li;
-    int rc = check_desc(d, &li);
+    qconv_desc kd;
+    int rc = kernel_desc(d, &kd, &li);
     if (rc) return rc;
+    d = &kd;
     if (!bytes) return fail(QCONV_EINVAL, "bytes must be non-NULL");
     rc = resolve_tile(d, li, tile_id);
     if (rc < 0) return rc;
@@ -702,8 +751,10 @@ int qconv_prepare_filters(const qconv_desc *d, const void *w_packed, int32_t til
                           size_t bytes, void *stream) {
     g_err[0] = 0;
     qconv_layout_info li;
-    int rc = check_desc(d, &li);
+    qconv_desc kd;
+    int rc = kernel_desc(d, &kd, &li);
     if (rc) return rc;
+    d = &kd;
     if (!w_packed || !w_prepared) return fail(QCONV_EINVAL, "filter pointers must be non-NULL");
     if (!aligned16(w_packed) || !aligned16(w_prepared)) return fail(QCONV_EINVAL, "filters must be 16-byte aligned");
     rc = resolve_tile(d, li, tile_id);
@@ -739,23 +790,34 @@ int qconv2d_prepared(const qconv_desc *d, const void *x, const void *w_prepared,
                     stream);
 }
 
-int qconv_unroll(const int8_t *src, int8_t *dst, int32_t n, int32_t c, int32_t h, int32_t w, int32_t taps,
-                 int32_t stride, int32_t pad, int32_t c_out, void *stream) {
+int qconv_unroll(const int8_t *src, int8_t *dst, int32_t n, int32_t c, int32_t h, int32_t w, int32_t taps_h,
+                 int32_t stride_h, int32_t pad_h, int32_t out_h, int32_t taps_w, int32_t stride_w, int32_t pad_w,
+                 int32_t c_out, void *stream) {
     g_err[0] = 0;
-    if (n < 0 || c < 0 || h < 0 || w < 0) return fail(QCONV_EINVAL, "sizes must be >= 0");
-    if (taps < 1 || stride < 1 || pad < 0) return fail(QCONV_EINVAL, "taps and stride must be >= 1, pad >= 0");
+    if (n < 0 || c < 0 || h < 0 || w < 0 || out_h < 0) return fail(QCONV_EINVAL, "sizes must be >= 0");
+    if (taps_h < 1 || taps_w < 1 || stride_h < 1 || stride_w < 1 || pad_h < 0 || pad_w < 0)
+        return fail(QCONV_EINVAL, "taps and strides must be >= 1, pads >= 0");
     if (c_out < 16 || c_out % 16 != 0) return fail(QCONV_EINVAL, "c_out must be a positive multiple of 16");
-    if ((int64_t)taps * c > c_out) return fail(QCONV_EINVAL, "taps * c (%lld) exceeds c_out (%d)", (long long)taps * c, c_out);
-    const int64_t span = (int64_t)w + 2 * pad - taps;
+    const int64_t real = (int64_t)taps_h * taps_w * c;
+    if (real > c_out) return fail(QCONV_EINVAL, "taps_h * taps_w * c (%lld) exceeds c_out (%d)", (long long)real, c_out);
+    const int64_t span = (int64_t)w + 2 * pad_w - taps_w;
     if (span < 0) return fail(QCONV_EINVAL, "filter width larger than the padded input");
-    const int64_t wout = span / stride + 1;
-    const int64_t in_bytes = (int64_t)n * c * h * w, out_bytes = (int64_t)n * h * wout * c_out;
-    if (in_bytes == 0 || out_bytes == 0) return QCONV_OK;
-    if (!src || !dst) return fail(QCONV_EINVAL, "src and dst must be non-NULL");
+    const int64_t wout = span / stride_w + 1;
+    const int64_t in_bytes = (int64_t)n * c * h * w, out_bytes = (int64_t)n * out_h * wout * c_out;
+    if (out_bytes == 0) return QCONV_OK;
+    if (!dst || (in_bytes > 0 && !src)) return fail(QCONV_EINVAL, "src and dst must be non-NULL");
     if (!aligned16(dst)) return fail(QCONV_EINVAL, "dst must be 16-byte aligned");
-    if ((uintptr_t)src < (uintptr_t)dst + out_bytes && (uintptr_t)dst < (uintptr_t)src + in_bytes)
+    if (in_bytes > 0 && (uintptr_t)src < (uintptr_t)dst + out_bytes && (uintptr_t)dst < (uintptr_t)src + in_bytes)
         return fail(QCONV_EINVAL, "src and dst overlap");
-    hipError_t e = launch_unroll(src, dst, n, c, h, w, taps, stride, pad, (int32_t)wout, c_out, (hipStream_t)stream);
+    const int64_t lw = (int64_t)w + 2 * pad_w, staged = 4ll * c_out + lw * c * taps_h;
+    if (staged > kUnrollLdsBytes)
+        return fail(QCONV_EUNSUPPORTED, "unroll stages %lld bytes per output row (limit %lld): meant for few channels",
+                    (long long)staged, (long long)kUnrollLdsBytes);
+    UnrollArgs a{n, c, h, w, taps_h, stride_h, pad_h, out_h, taps_w, stride_w, pad_w, (int32_t)wout, c_out,
+                 (int32_t)lw};
+    if ((int64_t)n * out_h >= (1ll << 31) || wout * (c_out / 16) >= (1ll << 31))
+        return fail(QCONV_EUNSUPPORTED, "unroll grid out of range");
+    hipError_t e = launch_unroll(src, dst, a, (hipStream_t)stream);
     if (e != hipSuccess) return fail(QCONV_EHIP, "unroll launch: %s", hipGetErrorString(e));
     return QCONV_OK;
 }

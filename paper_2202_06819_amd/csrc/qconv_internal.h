@@ -46,6 +46,7 @@ struct ConvArgs {
     int32_t m;              // n * p * q
     int32_t vh;             // h + 2*ph: rows of one zero-padded image
     int32_t ncols;          // w + 2*pw: columns of one zero-padded row
+    int32_t tap_w;          // band columns between horizontal filter taps: 1, or nb (batch-interleaved)
     int32_t xpix;           // bytes per input pixel (and per filter tap)
     int32_t nchunks;        // channel chunks of the main loop
     int32_t vec16;          // 1: every 16-byte vector of a pixel is whole (C*bits % 128 == 0)
@@ -130,11 +131,20 @@ const AblationInstance *ablation_instance(const char *tile_name, int mask);
 
 // Defined in qconv_pack.hip.
 hipError_t launch_pack(const int8_t *src, void *dst, int32_t n, int32_t c, int32_t h, int32_t w, int32_t bits,
-                       int32_t is_signed, hipStream_t stream);
+                       int32_t is_signed, int32_t nb, hipStream_t stream);
+
+// Patch unrolling (qconv_unroll): source n x c x h x w, destination
+// n x out_h x wout x c_out; lw = w + 2 * pad_w is the staged row length.
+struct UnrollArgs {
+    int32_t n, c, h, w;
+    int32_t taps_h, stride_h, pad_h, out_h;
+    int32_t taps_w, stride_w, pad_w, wout;
+    int32_t c_out, lw;
+};
 
 // Defined in qconv_unroll.hip.
-hipError_t launch_unroll(const int8_t *src, int8_t *dst, int32_t n, int32_t c, int32_t h, int32_t w, int32_t taps,
-                         int32_t stride, int32_t pad, int32_t wout, int32_t c_out, hipStream_t stream);
+int64_t unroll_lds_bytes(const UnrollArgs &a);
+hipError_t launch_unroll(const int8_t *src, int8_t *dst, const UnrollArgs &a, hipStream_t stream);
 
 // Defined in qconv_probe.hip (measurement aid).
 int64_t mfma_probe_ops(int blocks, int iters);

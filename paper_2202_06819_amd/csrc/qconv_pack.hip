@@ -40,7 +40,8 @@ __device__ __forceinline__ uint32_t gather_byte(const uint32_t (&t)[4], int j) {
 
 template <int BITS, bool SIGNED>
 __global__ void __launch_bounds__(PK_THREADS)
-    pack_nchw(const int8_t *__restrict__ src, uint8_t *__restrict__ dst, int c, int hw, int ptiles, int ctiles) {
+    pack_nchw(const int8_t *__restrict__ src, uint8_t *__restrict__ dst, int c, int hw, int ptiles, int ctiles,
+              int nb) {
     constexpr int LO = SIGNED ? -(1 << (BITS - 1)) : 0;
     constexpr int HI = SIGNED ? (1 << (BITS - 1)) - 1 : (1 << BITS) - 1;
     __shared__ __attribute__((aligned(16))) uint8_t tile[PK_C * PK_PITCH];
@@ -53,6 +54,10 @@ __global__ void __launch_bounds__(PK_THREADS)
     const int c0 = ct * PK_C;
     const int p0 = pt * PK_P;
     const int8_t *plane = src + (size_t)img * c * hw;
+    // destination pixel of (img, pix): nb images interleaved per pixel
+    // (nb = 1: plain N x H x W x C)
+    const size_t obase = (size_t)(img / nb) * hw * nb + img % nb;
+    auto out_pixel = [&](int px) { return obase + (size_t)px * nb; };
 
     // ---- phase 1: 64 channel rows x 128 pixels; a lane reads 32 consecutive
     // pixels of one row, saturates them and parks them in LDS
@@ -115,7 +120,7 @@ __global__ void __launch_bounds__(PK_THREADS)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int pix = p0 + 4 * q + j;
-            if (pix < hw) out[((size_t)img * hw + pix) * (c / 8) + cg / 8] = gather_byte(t, j);
+            if (pix < hw) out[out_pixel(pix) * (c / 8) + cg / 8] = gather_byte(t, j);
         }
     } else {
         const uint32_t lo4[4] = {d[0], d[1], d[2], d[3]};
@@ -124,7 +129,7 @@ __global__ void __launch_bounds__(PK_THREADS)
         for (int j = 0; j < 4; ++j) {
             const int pix = p0 + 4 * q + j;
             if (pix >= hw) continue;
-            uint32_t *out = reinterpret_cast<uint32_t *>(dst + ((size_t)img * hw + pix) * c + cg);   // c % 4 == 0
+            uint32_t *out = reinterpret_cast<uint32_t *>(dst + out_pixel(pix) * c + cg);   // c % 4 == 0
             out[0] = gather_byte(lo4, j);
             if (cg + 4 < c) out[1] = gather_byte(hi4, j);
         }
@@ -132,7 +137,7 @@ __global__ void __launch_bounds__(PK_THREADS)
 }
 
 hipError_t launch_pack(const int8_t *src, void *dst, int32_t n, int32_t c, int32_t h, int32_t w, int32_t bits,
-                       int32_t is_signed, hipStream_t stream) {
+                       int32_t is_signed, int32_t nb, hipStream_t stream) {
     const int hw = h * w;
     const int ptiles = (hw + PK_P - 1) / PK_P;
     const int ctiles = (c + PK_C - 1) / PK_C;
@@ -140,11 +145,11 @@ hipError_t launch_pack(const int8_t *src, void *dst, int32_t n, int32_t c, int32
     uint8_t *d = static_cast<uint8_t *>(dst);
     const dim3 grid((unsigned)blocks), block(PK_THREADS);
     if (bits == 4 && is_signed)
-        hipLaunchKernelGGL((pack_nchw<4, true>), grid, block, 0, stream, src, d, c, hw, ptiles, ctiles);
+        hipLaunchKernelGGL((pack_nchw<4, true>), grid, block, 0, stream, src, d, c, hw, ptiles, ctiles, nb);
     else if (bits == 4)
-        hipLaunchKernelGGL((pack_nchw<4, false>), grid, block, 0, stream, src, d, c, hw, ptiles, ctiles);
+        hipLaunchKernelGGL((pack_nchw<4, false>), grid, block, 0, stream, src, d, c, hw, ptiles, ctiles, nb);
     else
-        hipLaunchKernelGGL((pack_nchw<8, true>), grid, block, 0, stream, src, d, c, hw, ptiles, ctiles);
+        hipLaunchKernelGGL((pack_nchw<8, true>), grid, block, 0, stream, src, d, c, hw, ptiles, ctiles, nb);
     return hipGetLastError();
 }
 

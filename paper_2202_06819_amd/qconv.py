@@ -30,7 +30,7 @@ _i32, _i64, _vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p
 
 class QConvDesc(ctypes.Structure):
     _fields_ = [(f, _i32) for f in ("n", "h", "w", "c", "k", "r", "s", "stride_h", "stride_w", "pad_h", "pad_w",
-                                    "bits", "x_signed", "w_signed")]
+                                    "bits", "x_signed", "w_signed", "nb")]
 
 
 class QConvLayoutInfo(ctypes.Structure):
@@ -105,12 +105,13 @@ def lib() -> ctypes.CDLL:
         L.qconv_max_splits.argtypes = [P(QConvDesc), _i32]
         L.qconv_probe_mfma_i8.argtypes = [_i32, _i32, _vp, _vp, P(_i64), _vp]
         L.qconv_schedule_check.argtypes = [P(QConvDesc), P(QConvSchedule)]
-        L.qconv_unroll.argtypes = [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _vp]
+        L.qconv_unroll.argtypes = [_vp, _vp] + [_i32] * 12 + [_vp]
+        L.qconv_pack_interleaved.argtypes = [_vp, _vp] + [_i32] * 7 + [_vp]
         L.qconv2d_scheduled.argtypes = [P(QConvDesc), _vp, _vp, ctypes.c_size_t, P(QConvEpilogue), _vp,
                                         P(QConvSchedule), _vp, ctypes.c_size_t, _vp]
         for f in ("qconv_layout", "qconv_pack", "qconv2d", "qconv_tile_count", "qconv_tile_get", "qconv_tile_check",
                   "qconv_default_tile", "qconv_selftest", "qconv_prepared_filter_bytes", "qconv_prepare_filters",
-                  "qconv2d_prepared", "qconv_workspace_bytes", "qconv_max_splits", "qconv_probe_mfma_i8", "qconv_schedule_check", "qconv2d_scheduled", "qconv_unroll"):
+                  "qconv2d_prepared", "qconv_workspace_bytes", "qconv_max_splits", "qconv_probe_mfma_i8", "qconv_schedule_check", "qconv2d_scheduled", "qconv_unroll", "qconv_pack_interleaved"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
         return L
@@ -126,7 +127,7 @@ def _check(rc: int, what: str) -> int:
 def make_desc(d: dict | QConvDesc) -> QConvDesc:
     if isinstance(d, QConvDesc):
         return d
-    return QConvDesc(**{f: int(d[f]) for f, _ in QConvDesc._fields_})
+    return QConvDesc(**{f: int(d.get(f, 0) if f == "nb" else d[f]) for f, _ in QConvDesc._fields_})
 
 
 def layout(d: dict) -> dict:
@@ -241,24 +242,42 @@ def _dev_ptr(t: torch.Tensor, name: str, min_bytes: int = 0) -> int:
     return t.data_ptr()
 
 
-def packed_shape(n: int, h: int, w: int, c: int, bits: int) -> tuple:
-    return (n, h, w, c // 8) if bits == 4 else (n, h, w, c)
+def packed_shape(n: int, h: int, w: int, c: int, bits: int, nb: int = 1) -> tuple:
+    """N x H x W x C' packed; with nb > 1 the batch-interleaved N/nb x H x W x nb x C'."""
+    cw = c // 8 if bits == 4 else c
+    return (n // nb, h, w, nb, cw) if nb > 1 else (n, h, w, cw)
+
+
+def raw_shape(desc: QConvDesc, info: dict) -> tuple:
+    """int32 output: N x P x Q x K, or N/nb x P x Q x nb x K in the batch-interleaved layout."""
+    if desc.nb > 1:
+        return (desc.n // desc.nb, info["p"], info["q"], desc.nb, desc.k)
+    return (desc.n, info["p"], info["q"], desc.k)
 
 
 def packed_dtype(bits: int) -> torch.dtype:
     return torch.int32 if bits == 4 else torch.int8
 
 
-def pack(src: torch.Tensor, bits: int, is_signed: bool, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
-    """int8 N x C x H x W (or K x C x R x S) -> saturated channel-packed N x H x W x ... ."""
+def pack(src: torch.Tensor, bits: int, is_signed: bool, out: torch.Tensor | None = None, stream=None,
+         nb: int = 1) -> torch.Tensor:
+    """int8 N x C x H x W (or K x C x R x S) -> saturated channel-packed N x H x W x ... ;
+    nb > 1: the batch-interleaved layout (qconv_pack_interleaved)."""
     if src.dtype != torch.int8 or src.dim() != 4:
         raise QConvError(EINVAL, "pack expects a 4-d int8 tensor")
     n, c, h, w = src.shape
+    nb = max(int(nb), 1)
     if out is None:
-        out = torch.empty(packed_shape(n, h, w, c, bits), dtype=packed_dtype(bits), device=src.device)
-    rc = lib().qconv_pack(_dev_ptr(src, "src"), _dev_ptr(out, "dst", n * c * h * w * bits // 8), n, c, h, w,
-                          int(bits), int(bool(is_signed)),
-                          _vp(_stream(stream)))
+        if n % nb:
+            raise QConvError(EINVAL, f"nb={nb} does not divide n={n}")
+        out = torch.empty(packed_shape(n, h, w, c, bits, nb), dtype=packed_dtype(bits), device=src.device)
+    dst = _dev_ptr(out, "dst", n * c * h * w * bits // 8)
+    if nb == 1:
+        rc = lib().qconv_pack(_dev_ptr(src, "src"), dst, n, c, h, w, int(bits), int(bool(is_signed)),
+                              _vp(_stream(stream)))
+    else:
+        rc = lib().qconv_pack_interleaved(_dev_ptr(src, "src"), dst, n, c, h, w, int(bits), int(bool(is_signed)),
+                                          nb, _vp(_stream(stream)))
     _check(rc, "qconv_pack")
     return out
 
@@ -274,20 +293,58 @@ def _epilogue_extras(epi: QConvEpilogue, desc: QConvDesc, y_bytes: int, bias, re
         epi.residual_signed = int(bool(residual_signed))
 
 
-def unroll(src: torch.Tensor, taps: int, stride: int, pad: int, c_out: int, out: torch.Tensor | None = None,
+def unroll(src: torch.Tensor, c_out: int, *, taps_w: int, stride_w: int = 1, pad_w: int = 0, taps_h: int = 1,
+           stride_h: int = 1, pad_h: int = 0, out_h: int | None = None, out: torch.Tensor | None = None,
            stream=None) -> torch.Tensor:
-    """int8 N x C x H x W -> N x H x Wout x c_out with the `taps` filter columns
-    folded into channels (see qconv_unroll); for filters use stride 1, pad 0."""
+    """int8 N x C x H x W -> N x out_h x Wout x c_out with filter taps folded
+    into channels (see qconv_unroll).  ``out_h`` defaults to the rows a
+    stride_h window of taps_h rows covers."""
     if src.dtype != torch.int8 or src.dim() != 4:
         raise QConvError(EINVAL, "unroll expects a 4-d int8 tensor")
     n, c, h, w = src.shape
-    wout = (w + 2 * pad - taps) // stride + 1
+    wout = max((w + 2 * pad_w - taps_w) // stride_w + 1, 0)
+    if out_h is None:
+        out_h = max((h + 2 * pad_h - taps_h) // stride_h + 1, 0)
     if out is None:
-        out = torch.empty((n, h, max(wout, 0), c_out), dtype=torch.int8, device=src.device)
-    rc = lib().qconv_unroll(_dev_ptr(src, "src"), _dev_ptr(out, "dst", n * h * max(wout, 0) * c_out), n, c, h, w,
-                            int(taps), int(stride), int(pad), int(c_out), _vp(_stream(stream)))
+        out = torch.empty((n, out_h, wout, c_out), dtype=torch.int8, device=src.device)
+    rc = lib().qconv_unroll(_dev_ptr(src, "src"), _dev_ptr(out, "dst", n * out_h * wout * c_out), n, c, h, w,
+                            int(taps_h), int(stride_h), int(pad_h), int(out_h), int(taps_w), int(stride_w),
+                            int(pad_w), int(c_out), _vp(_stream(stream)))
     _check(rc, "qconv_unroll")
     return out
+
+
+def few_channel_plan(d: dict, c_out: int, fold: str = "rows") -> dict:
+    """How a few-channel layer ``d`` (8-bit) runs as an unrolled one.
+
+    fold="all": every filter tap goes into the channels, leaving a 1x1
+    convolution over c_out >= R*S*C channels; fold="rows": the filter columns
+    and groups of stride_h rows go into the channels, leaving a
+    ceil(R/stride_h) x 1 convolution at stride 1 over c_out >= stride_h*S*C
+    channels.  Returns the unroll arguments of the input (``x``) and of the
+    filters (``w``, given as K x C x R x S) and the descriptor (``desc``) of the
+    equivalent convolution; its output is the layer's output.
+    """
+    r, s_, sh = d["r"], d["s"], d["stride_h"]
+    p = (d["h"] + 2 * d["pad_h"] - r) // sh + 1
+    q = (d["w"] + 2 * d["pad_w"] - s_) // d["stride_w"] + 1
+    if p < 1 or q < 1:
+        raise QConvError(EINVAL, "the filter is larger than the padded input")
+    if fold == "all":
+        x = dict(taps_h=r, stride_h=sh, pad_h=d["pad_h"], out_h=p)
+        w = dict(taps_h=r, stride_h=1, pad_h=0, out_h=1)
+        rr, hh = 1, p
+    elif fold == "rows":
+        rr = -(-r // sh)
+        x = dict(taps_h=sh, stride_h=sh, pad_h=d["pad_h"], out_h=p + rr - 1)
+        w = dict(taps_h=sh, stride_h=sh, pad_h=0, out_h=rr)
+        hh = p + rr - 1
+    else:
+        raise QConvError(EINVAL, f"fold must be 'rows' or 'all', not {fold!r}")
+    x.update(taps_w=s_, stride_w=d["stride_w"], pad_w=d["pad_w"])
+    w.update(taps_w=s_, stride_w=1, pad_w=0)
+    desc = dict(d, h=hh, w=q, c=c_out, r=rr, s=1, stride_h=1, stride_w=1, pad_h=0, pad_w=0)
+    return {"x": x, "w": w, "desc": desc}
 
 
 def conv2d(d: dict, x: torch.Tensor, w: torch.Tensor, *, requant: bool = False, mult: torch.Tensor | None = None,
@@ -306,10 +363,10 @@ def conv2d(d: dict, x: torch.Tensor, w: torch.Tensor, *, requant: bool = False, 
     bits = desc.bits
     if out is None:
         if requant:
-            out = torch.empty(packed_shape(desc.n, info["p"], info["q"], desc.k, bits), dtype=packed_dtype(bits),
-                              device=x.device)
+            out = torch.empty(packed_shape(desc.n, info["p"], info["q"], desc.k, bits, desc.nb),
+                              dtype=packed_dtype(bits), device=x.device)
         else:
-            out = torch.empty((desc.n, info["p"], info["q"], desc.k), dtype=torch.int32, device=x.device)
+            out = torch.empty(raw_shape(desc, info), dtype=torch.int32, device=x.device)
     epi = QConvEpilogue()
     if requant:
         if mult is None or mult.dtype != torch.int32 or mult.numel() != desc.k:
@@ -377,8 +434,8 @@ class Conv2dCall:
         info = layout(d)
         bits = self.desc.bits
         if out is None:
-            shape = (packed_shape(self.desc.n, info["p"], info["q"], self.desc.k, bits) if requant
-                     else (self.desc.n, info["p"], info["q"], self.desc.k))
+            shape = (packed_shape(self.desc.n, info["p"], info["q"], self.desc.k, bits, self.desc.nb) if requant
+                     else raw_shape(self.desc, info))
             out = torch.empty(shape, dtype=packed_dtype(bits) if requant else torch.int32, device=x.device)
         self.epi = QConvEpilogue()
         if requant:

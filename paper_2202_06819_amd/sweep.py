@@ -30,8 +30,9 @@ INT8_PEAK_TOPS = 5000.0
 
 
 def shape_key(d: dict, requant: bool = True) -> str:
+    nb = int(d.get("nb", 0))
     return ("n{n}_h{h}_w{w}_c{c}_k{k}_r{r}_s{s}_st{stride_h}x{stride_w}_p{pad_h}x{pad_w}_b{bits}_xs{x_signed}"
-            "_ws{w_signed}".format(**d) + ("_rq" if requant else "_raw"))
+            "_ws{w_signed}".format(**d) + (f"_nb{nb}" if nb > 1 else "") + ("_rq" if requant else "_raw"))
 
 
 _tuned_cache = None

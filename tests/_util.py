@@ -87,3 +87,24 @@ def assert_same(got: np.ndarray, ref: np.ndarray, what: str) -> None:
         bad = np.argwhere(g != r)
         raise AssertionError(f"{what}: {len(bad)} of {g.size} elements differ; first at {bad[0].tolist()}: "
                              f"got {g[tuple(bad[0])]} want {r[tuple(bad[0])]}")
+
+
+def unroll_def(src, c_out, taps_h, stride_h, pad_h, out_h, taps_w, stride_w, pad_w):
+    """The patch unroll of include/qconv.h written out with numpy:
+    dst[n][u][q][(b*taps_w + s)*c + ci] = src[n][ci][u*stride_h + b - pad_h][q*stride_w + s - pad_w],
+    0 outside the input and for channels from taps_h*taps_w*c on."""
+    n, c, h, w = src.shape
+    wout = (w + 2 * pad_w - taps_w) // stride_w + 1
+    dst = np.zeros((n, out_h, wout, c_out), dtype=np.int8)
+    u, q = np.arange(out_h), np.arange(wout)
+    for b in range(taps_h):
+        y = u * stride_h + b - pad_h
+        uu = np.nonzero((y >= 0) & (y < h))[0]
+        for s in range(taps_w):
+            col = q * stride_w + s - pad_w
+            qq = np.nonzero((col >= 0) & (col < w))[0]
+            base = (b * taps_w + s) * c
+            # src[:, :, y, col] -> n x c x |uu| x |qq|, moved to n x |uu| x |qq| x c
+            block = src[:, :, y[uu]][:, :, :, col[qq]]
+            dst[:, uu[:, None], qq[None, :], base:base + c] = block.transpose(0, 2, 3, 1)
+    return dst

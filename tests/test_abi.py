@@ -352,10 +352,83 @@ def test_ablation_schedules(q):
 def test_unroll_argument_errors(q):
     L = q.lib()
     src, dst = 1 << 32, 1 << 34
-    assert L.qconv_unroll(src, dst, 1, 3, 8, 8, 7, 2, 3, 20, None) == -1        # c_out not a multiple of 16
-    assert L.qconv_unroll(src, dst, 1, 3, 8, 8, 7, 2, 3, 16, None) == -1        # 7 * 3 > 16
-    assert L.qconv_unroll(src, dst, 1, 3, 8, 8, 0, 2, 3, 32, None) == -1        # no taps
-    assert L.qconv_unroll(src, dst, 1, 3, 8, 2, 7, 1, 0, 32, None) == -1        # window wider than the input
-    assert L.qconv_unroll(src, dst + 8, 1, 3, 8, 8, 7, 2, 3, 32, None) == -1    # misaligned
-    assert L.qconv_unroll(src, src + 64, 1, 3, 8, 8, 7, 2, 3, 32, None) == -1   # overlap
-    assert L.qconv_unroll(None, None, 0, 3, 8, 8, 7, 2, 3, 32, None) == 0       # empty: no-op
+    rows = (1, 1, 0, 8)   # taps_h, stride_h, pad_h, out_h: width unrolling only
+
+    def call(s, d, n, c, h, w, rows, cols, c_out):
+        return L.qconv_unroll(s, d, n, c, h, w, *rows, *cols, c_out, None)
+
+    assert call(src, dst, 1, 3, 8, 8, rows, (7, 2, 3), 20) == -1          # c_out not a multiple of 16
+    assert call(src, dst, 1, 3, 8, 8, rows, (7, 2, 3), 16) == -1          # 7 * 3 > 16
+    assert call(src, dst, 1, 3, 8, 8, (7, 2, 3, 4), (7, 2, 3), 144) == -1  # 7 * 7 * 3 > 144
+    assert call(src, dst, 1, 3, 8, 8, rows, (0, 2, 3), 32) == -1          # no taps
+    assert call(src, dst, 1, 3, 8, 8, (1, 0, 0, 8), (7, 2, 3), 32) == -1  # row stride 0
+    assert call(src, dst, 1, 3, 8, 8, (1, 1, -1, 8), (7, 2, 3), 32) == -1 # negative row padding
+    assert call(src, dst, 1, 3, 8, 8, (1, 1, 0, -1), (7, 2, 3), 32) == -1 # negative row count
+    assert call(src, dst, 1, 3, 8, 2, rows, (7, 1, 0), 32) == -1          # window wider than the input
+    assert call(src, dst + 8, 1, 3, 8, 8, rows, (7, 2, 3), 32) == -1      # misaligned
+    assert call(src, src + 64, 1, 3, 8, 8, rows, (7, 2, 3), 32) == -1     # overlap
+    assert call(None, dst, 1, 3, 8, 8, rows, (7, 2, 3), 32) == -1         # NULL source of a non-empty input
+    assert call(src, dst, 1, 64, 8, 4000, (8, 1, 0, 8), (1, 1, 0), 512) == -2   # stages more than 64 KiB per row
+    assert call(None, None, 0, 3, 8, 8, rows, (7, 2, 3), 32) == 0         # empty: no-op
+    assert call(src, None, 1, 3, 8, 8, (1, 1, 0, 0), (7, 2, 3), 32) == 0  # no output rows: no-op
+
+
+def test_few_channel_plan_shapes(q):
+    """The folding plans of the 7x7 stride-2 stem: the unrolled shapes and the
+    equivalent convolution (the arithmetic is checked in test_oracle and on
+    the GPU)."""
+    d = dict(n=2, h=224, w=224, c=3, k=64, r=7, s=7, stride_h=2, stride_w=2, pad_h=3, pad_w=3, bits=8, x_signed=1,
+             w_signed=1)
+    rows = q.few_channel_plan(d, 64, "rows")
+    assert rows["x"] == dict(taps_h=2, stride_h=2, pad_h=3, out_h=115, taps_w=7, stride_w=2, pad_w=3)
+    assert rows["w"] == dict(taps_h=2, stride_h=2, pad_h=0, out_h=4, taps_w=7, stride_w=1, pad_w=0)
+    assert (rows["desc"]["h"], rows["desc"]["w"], rows["desc"]["c"], rows["desc"]["r"], rows["desc"]["s"]) == \
+        (115, 112, 64, 4, 1)
+    assert q.layout(rows["desc"])["p"] == 112 and q.layout(rows["desc"])["q"] == 112
+    full = q.few_channel_plan(d, 192, "all")
+    assert full["x"] == dict(taps_h=7, stride_h=2, pad_h=3, out_h=112, taps_w=7, stride_w=2, pad_w=3)
+    assert full["w"] == dict(taps_h=7, stride_h=1, pad_h=0, out_h=1, taps_w=7, stride_w=1, pad_w=0)
+    assert (full["desc"]["h"], full["desc"]["r"], full["desc"]["stride_h"], full["desc"]["pad_h"]) == (112, 1, 1, 0)
+    with pytest.raises(q.QConvError):
+        q.few_channel_plan(d, 64, "cols")
+
+
+def test_interleaved_layout_rules(q):
+    """The batch-interleaved layout: sizes equal the plain layout's, n must
+    divide by nb, stride_w must be 1, and only the wide tiles' generic
+    kernels read it (no staged tile, no ablation instance)."""
+    plain = q.layout(D())
+    for nb in (2, 4, 8):
+        assert q.layout(D(nb=nb)) == plain
+    assert q.layout(D(nb=0)) == plain and q.layout(D(nb=1)) == plain
+    with pytest.raises(q.QConvError) as e:
+        q.layout(D(nb=3))
+    assert e.value.status == -1
+    with pytest.raises(q.QConvError) as e:
+        q.layout(D(nb=-1))
+    assert e.value.status == -1
+    with pytest.raises(q.QConvError) as e:
+        q.layout(D(nb=2, stride_h=2, stride_w=2))
+    assert e.value.status == -2
+    assert q.layout(D(nb=2, stride_h=2, stride_w=1))["p"] == 28        # row stride alone is fine
+    usable = 0
+    for t in q.tiles():
+        st = q.tile_status(D(nb=4), t["id"])
+        if t["variant"] != 2:
+            assert st == -2, t["name"]
+        usable += st == 0
+    assert usable >= 4
+    names = {t["name"]: t["id"] for t in q.tiles()}
+    assert q.schedule_status(D(nb=4), {"tile_id": names["wide_b4_w4x1_f1x4_c64"], "ablation": 1}) == -2
+    from paper_2202_06819_amd import sweep
+    assert sweep.shape_key(D(nb=4)) != sweep.shape_key(D()) and sweep.shape_key(D(nb=1)) == sweep.shape_key(D())
+
+
+def test_pack_interleaved_argument_errors(q):
+    L = q.lib()
+    src, dst = 1 << 32, 1 << 34
+    assert L.qconv_pack_interleaved(src, dst, 6, 64, 8, 8, 4, 0, 4, None) == -1   # 4 does not divide 6
+    assert L.qconv_pack_interleaved(src, dst, 6, 64, 8, 8, 4, 0, 0, None) == -1   # nb 0
+    assert L.qconv_pack_interleaved(src, dst, 4, 60, 8, 8, 4, 0, 2, None) == -2   # c % 8 for 4-bit
+    assert L.qconv_pack_interleaved(src, dst + 2, 4, 64, 8, 8, 4, 0, 2, None) == -1   # misaligned
+    assert L.qconv_pack_interleaved(None, None, 0, 64, 8, 8, 4, 0, 2, None) == 0  # empty: no-op

@@ -10,7 +10,7 @@ import pytest
 
 import oracle
 import qconv_inputs as qi
-from _util import announce, assert_same, gpu_layer, oracle_threads, ref_layer, stress_shift
+from _util import announce, assert_same, gpu_layer, oracle_threads, ref_layer, stress_shift, unroll_def
 
 pytestmark = pytest.mark.gpu
 
@@ -549,9 +549,11 @@ def test_ablation_instances_match_oracle(shape):
     assert ran >= 3
 
 
-def test_stem_7x7_by_width_unrolling():
+@pytest.mark.parametrize("fold", ["rows", "all"])
+def test_stem_7x7_by_patch_unrolling(fold):
     """The 3-channel 7x7 stride-2 stem (8-bit): the input and the filters are
-    width-unrolled on the GPU and the 7x1 convolution runs on every tile that
+    patch-unrolled on the GPU (row pairs and columns into 64 channels, or
+    every tap into 192) and the folded convolution runs on every tile that
     takes it; the result equals the oracle's direct 7x7 convolution of the
     original tensors."""
     torch, q = _torch(), _qconv()
@@ -563,36 +565,123 @@ def test_stem_7x7_by_width_unrolling():
     ref = oracle.qconv_layer(t["x"], t["w"], bits=8, x_signed=True, w_signed=True, stride=(2, 2), pad=(3, 3),
                              mult=t["mult"], shift=sh, relu=True, lo=-128, hi=127, threads=oracle_threads())
     dev = torch.device("cuda:0")
-    announce("stem unroll")
-    xu = q.unroll(torch.from_numpy(t["x"]).to(dev), 7, 2, 3, 32)
-    wu = q.unroll(torch.from_numpy(t["w"]).to(dev), 7, 1, 0, 32)
+    c_out = 64 if fold == "rows" else 192
+    plan = q.few_channel_plan(L.desc(), c_out, fold)
+    announce(f"stem unroll, fold {fold}")
+    xu = q.unroll(torch.from_numpy(t["x"]).to(dev), c_out, **plan["x"])
+    wu = q.unroll(torch.from_numpy(t["w"]).to(dev), c_out, **plan["w"])
     torch.cuda.synchronize()
-    # the unrolled layouts, spot-checked against their definition
-    xn, wn = xu.cpu().numpy(), wu.cpu().numpy()
-    assert xu.shape == (n, h, 112, 32) and wu.shape == (k, 7, 1, 32)
-    for (img, row, qq) in [(0, 0, 0), (1, 100, 57), (0, 223, 111), (1, 5, 1)]:
-        for ch in range(32):
-            s, ci = divmod(ch, 3)
-            col = qq * 2 + s - 3
-            want = t["x"][img, ci, row, col] if ch < 21 and 0 <= col < h else 0
-            assert xn[img, row, qq, ch] == want
-    assert np.array_equal(wn[:, :, 0, :21].reshape(k, 7, 7, 3), t["w"].transpose(0, 2, 3, 1))
-    assert not wn[:, :, 0, 21:].any()
-    d = dict(n=n, h=h, w=112, c=32, k=k, r=7, s=1, stride_h=2, stride_w=1, pad_h=3, pad_w=0, bits=8, x_signed=1,
-             w_signed=1)
+    # the unrolled layouts against their definition, written out on the host
+    assert np.array_equal(xu.cpu().numpy(), unroll_def(t["x"], c_out, **plan["x"]))
+    assert np.array_equal(wu.cpu().numpy(), unroll_def(t["w"], c_out, **plan["w"]))
+    d = plan["desc"]
     mult = torch.from_numpy(t["mult"]).to(dev)
     ran = 0
     for tt in q.tiles():
         if q.tile_status(d, tt["id"]) != 0:
             continue
         ran += 1
-        announce(f"stem 7x1 conv tile {tt['name']}")
+        announce(f"stem folded conv ({fold}) tile {tt['name']}")
         y = q.conv2d(d, xu, wu, tile=tt["id"], requant=True, mult=mult, shift=sh, relu=True, clamp=(-128, 127))
         torch.cuda.synchronize()
-        assert_same(y.cpu().numpy(), ref["y_packed"], f"stem {tt['name']}")
+        assert_same(y.cpu().numpy(), ref["y_packed"], f"stem {fold} {tt['name']}")
         if tt["variant"] == 2:
             wprep = q.prepare_filters(d, wu, tt["id"])
             y = q.conv2d(d, xu, wprep, tile=tt["id"], prepared=True)
             torch.cuda.synchronize()
-            assert_same(y.cpu().numpy(), ref["acc"], f"stem {tt['name']} prepared raw")
+            assert_same(y.cpu().numpy(), ref["acc"], f"stem {fold} {tt['name']} prepared raw")
     assert ran >= 2
+
+
+# ------------------------------------------------- batch-interleaved layout
+
+def interleave(a: np.ndarray, nb: int) -> np.ndarray:
+    """N x H x W x ... -> N/nb x H x W x nb x ... : the batch-interleaved
+    layout's definition (image i's pixel (y, x) at [i // nb, y, x, i % nb])."""
+    n = a.shape[0]
+    b = a.reshape(n // nb, nb, *a.shape[1:])
+    return np.ascontiguousarray(b.transpose(0, 2, 3, 1, *range(4, b.ndim)))
+
+
+INTERLEAVED_CASES = [
+    # name, n, h, w, c, k, r, (stride_h, stride_w), pad, bits, nb
+    ("i4_3x3_ragged_nb2", 4, 13, 11, 64, 64, 3, (1, 1), 1, 4, 2),
+    ("i4_3x3_nb4", 8, 14, 14, 128, 64, 3, (1, 1), 1, 4, 4),
+    ("i4_1x1_nb4", 4, 9, 7, 64, 128, 1, (1, 1), 0, 4, 4),
+    ("i4_5x5_nb2", 2, 12, 12, 64, 64, 5, (1, 1), 2, 4, 2),
+    ("i4_3x3_rows_s2_nb2", 4, 15, 9, 64, 64, 3, (2, 1), 1, 4, 2),
+    ("i8_3x3_nb2", 4, 10, 10, 64, 64, 3, (1, 1), 1, 8, 2),
+    ("i4_7x7_512_nb16", 16, 7, 7, 256, 256, 3, (1, 1), 1, 4, 16),
+]
+
+
+@pytest.mark.parametrize("case", INTERLEAVED_CASES, ids=[c[0] for c in INTERLEAVED_CASES])
+def test_interleaved_layout(case):
+    """Pack into the batch-interleaved layout and convolve in it (input,
+    output and residual interleaved) on every tile that reads it, from packed
+    and prepared filters, raw and requantised, with a bias and a residual, and
+    split over channel chunks where there are several; every result equals
+    the oracle's plain-layout result put in the interleaved order."""
+    torch, q = _torch(), _qconv()
+    name, n, h, w, c, k, r, (sh_, sw_), pad, bits, nb = case
+    signed8 = bits == 8
+    g = np.random.default_rng([977, n, h, w, c, k, r, sh_, bits, nb])
+    xr = qi.S8 if signed8 else (0, 15)
+    wr = qi.S8 if signed8 else (-7, 7)
+    x = g.integers(xr[0], xr[1] + 1, size=(n, c, h, w)).astype(np.int8)
+    f = g.integers(wr[0], wr[1] + 1, size=(k, c, r, r)).astype(np.int8)
+    mult = g.integers(2 ** 14, 2 ** 15, size=k).astype(np.int32)
+    d = dict(n=n, h=h, w=w, c=c, k=k, r=r, s=r, stride_h=sh_, stride_w=sw_, pad_h=pad, pad_w=pad, bits=bits,
+             x_signed=int(signed8), w_signed=1, nb=nb)
+    L = qi.Layer(name, n, h, w, c, k, r, r, 1, pad, bits=bits, x_signed=signed8, w_signed=True, x_range=xr,
+                 w_range=wr)
+    sh = stress_shift(L, xr, wr)
+    lo, hi, relu = (-128, 127, False) if signed8 else (0, 15, True)
+    p, qq = (h + 2 * pad - r) // sh_ + 1, (w + 2 * pad - r) // sw_ + 1
+    bias = g.integers(-4000, 4000, size=k).astype(np.int32)
+    rlo, rhi = (-128, 127) if signed8 else (0, 15)
+    res_vals = g.integers(rlo, rhi + 1, size=(n, p, qq, k)).astype(np.int32)
+    res_packed = oracle.pack_output(res_vals, bits, signed8)
+    kw = dict(bits=bits, x_signed=signed8, w_signed=True, stride=(sh_, sw_), pad=(pad, pad), mult=mult, shift=sh,
+              relu=relu, lo=lo, hi=hi, threads=oracle_threads())
+    ref = oracle.qconv_layer(x, f, **kw)
+    ref_ext = oracle.qconv_layer(x, f, bias=bias, residual=res_vals, **kw)
+    dev = torch.device("cuda:0")
+    announce(f"{name}: interleaved pack")
+    xp = q.pack(torch.from_numpy(x).to(dev), bits, signed8, nb=nb)
+    torch.cuda.synchronize()
+    assert_same(xp.cpu().numpy(), interleave(ref["x_packed"], nb), f"{name} pack")
+    wp = q.pack(torch.from_numpy(f).to(dev), bits, True)
+    m_dev = torch.from_numpy(mult).to(dev)
+    b_dev = torch.from_numpy(bias).to(dev)
+    res_dev = torch.from_numpy(interleave(res_packed, nb)).to(dev)
+    want_y, want_acc, want_ext = (interleave(ref["y_packed"], nb), interleave(ref["acc"], nb),
+                                  interleave(ref_ext["y_packed"], nb))
+    rq = dict(requant=True, mult=m_dev, shift=sh, relu=relu, clamp=(lo, hi))
+    ran = 0
+    for t in q.tiles():
+        if q.tile_status(d, t["id"]) != 0:
+            continue
+        ran += 1
+        tid = t["id"]
+        announce(f"{name} tile {t['name']} packed filters")
+        y = q.conv2d(d, xp, wp, tile=tid, **rq)
+        torch.cuda.synchronize()
+        assert_same(y.cpu().numpy(), want_y, f"{name} {t['name']}")
+        wprep = q.prepare_filters(d, wp, tid)
+        announce(f"{name} tile {t['name']} prepared, raw")
+        y = q.conv2d(d, xp, wprep, tile=tid, prepared=True)
+        torch.cuda.synchronize()
+        assert_same(y.cpu().numpy(), want_acc, f"{name} {t['name']} raw")
+        announce(f"{name} tile {t['name']} prepared, bias and residual")
+        y = q.conv2d(d, xp, wprep, tile=tid, prepared=True, bias=b_dev, residual=res_dev, residual_signed=signed8,
+                     **rq)
+        torch.cuda.synchronize()
+        assert_same(y.cpu().numpy(), want_ext, f"{name} {t['name']} bias+residual")
+        if q.max_splits(d, tid) > 1:
+            announce(f"{name} tile {t['name']} split 2")
+            y = q.conv2d(d, xp, wprep, tile=tid, prepared=True, splits=2,
+                         workspace=q.make_workspace(d, tid, 2, dev), **rq)
+            torch.cuda.synchronize()
+            assert_same(y.cpu().numpy(), want_y, f"{name} {t['name']} split 2")
+    assert ran >= 2, f"{name}: only {ran} tiles read the interleaved layout"
