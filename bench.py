@@ -386,6 +386,76 @@ def stem_time(dev, n: int, reps: int) -> dict:
             "best_fold": pick, "tops": folds[pick]["tops"], "folds": folds}
 
 
+def layout_table(dev, reps: int) -> list[dict]:
+    """The batch-interleaved layout (NHWCnc, nb images per pixel) against the
+    plain one on the stride-1 3x3 layers: per layer the plain layout's tuned
+    schedule, and for each nb the fastest tile of a short sweep; plus the
+    pack kernel of the layer's input in each layout."""
+    import torch
+    import qconv_inputs as qi
+    from paper_2202_06819_amd import qconv, sweep
+    layers = [qi.CONFIGS[1]()[0]] + [L for L in qi.distinct(qi.CONFIGS[2]()) if L.r == 3 and L.stride == 1]
+    rows = []
+    for lid, L in enumerate(layers):
+        e = L.epilogue
+        t = qi.layer_tensors(40, lid, L)
+        x = torch.from_numpy(t["x"]).to(dev)
+        wp = qconv.pack(torch.from_numpy(t["w"]).to(dev), L.bits, L.w_signed)
+        mult = torch.from_numpy(t["mult"]).to(dev)
+        row = {"layer": L.name, "n": L.n, "h": L.h, "c": L.c, "k": L.k, "gops": round(L.ops / 1e9, 4)}
+        ref = None
+        for nb in (1, 2, 4, 8, 16):
+            if L.n % nb:
+                continue
+            d = dict(L.desc(), nb=nb)
+            xp = qconv.pack(x, L.bits, L.x_signed, nb=nb)
+            if nb == 1:
+                cands = [sweep.tuned_config(d)]
+            else:
+                cands = [(tt["id"], sp) for tt in qconv.tiles() if qconv.tile_status(d, tt["id"]) == 0
+                         for sp in sweep.split_choices(d, tt["id"])]
+            if not cands:   # no tile stages the band of rows this wide
+                row[f"nb{nb}"] = None
+                continue
+            best = None
+            for tid, splits in cands:
+                wprep = qconv.prepare_filters(d, wp, tid)
+                ws = qconv.make_workspace(d, tid, splits, dev)
+
+                def make(stream=None, tid=tid, splits=splits, wprep=wprep, ws=ws, d=d, xp=xp):
+                    return qconv.Conv2dCall(d, xp, wprep, requant=True, mult=mult, shift=e.shift, relu=e.relu,
+                                            clamp=(e.lo, e.hi), tile=tid, prepared=True, stream=stream,
+                                            splits=splits, workspace=ws)
+
+                out = make()()
+                torch.cuda.synchronize()
+                flat = out.reshape(-1, *out.shape[-1:]) if nb == 1 else \
+                    out.permute(0, 3, 1, 2, 4).reshape(-1, out.shape[-1])
+                if ref is None:
+                    ref = flat.clone()
+                elif not torch.equal(flat, ref):
+                    raise RuntimeError(f"{L.name} nb={nb} tile {tid}: output differs from the plain layout")
+                g, _ = captured(lambda st: [make(st)], 20 if len(cands) > 1 else reps)
+                us = time_graph(g, 3) * 1000.0 / (60 if len(cands) > 1 else 3 * reps)
+                if best is None or us < best[0]:
+                    best = (us, tid, make, splits)
+            if len(cands) > 1:
+                g, _ = captured(lambda st: [best[2](st)], reps)
+                best = (time_graph(g, 3) * 1000.0 / (3 * reps),) + best[1:]
+
+            def make_pack(stream=None, nb=nb, xp=xp):
+                return lambda: qconv.pack(x, L.bits, L.x_signed, out=xp, stream=stream, nb=nb)
+
+            g, _ = captured(lambda st: [make_pack(st)], reps)
+            pack_us = time_graph(g, 3) * 1000.0 / (3 * reps)
+            row[f"nb{nb}"] = {"tile": qconv.tiles()[best[1]]["name"], "splits": best[3], "us": round(best[0], 3),
+                              "tops": round(L.ops / (best[0] * 1e-6) / 1e12, 1), "pack_us": round(pack_us, 3)}
+        rows.append(row)
+        log(f"  {L.name:24s} " + "  ".join(f"{k}: {v['us']:.2f} us (pack {v['pack_us']:.2f})" if v else f"{k}: n/a"
+                                            for k, v in row.items() if k.startswith("nb")))
+    return rows
+
+
 def cpu_baseline(L, seconds: float, threads: int | None = None) -> dict:
     """The oracle, as it stands, on the host cores: pack + conv + requant + repack
     of the same layer, repeated for about `seconds` (all cores by default)."""
@@ -415,6 +485,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--layer-reps", type=int, default=200, help="repetitions per layer in the per-layer tables")
     ap.add_argument("--tables", default="2", help="comma list of workloads with per-layer tables (2,3,4) or 'none'")
+    ap.add_argument("--layout-table", action="store_true",
+                    help="also time the batch-interleaved layout against the plain one")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--tile", type=int, default=-1)
@@ -557,6 +629,10 @@ def main() -> int:
             entry["stem"] = stem_time(dev, 16, max(20, args.layer_reps // 4))
             log(f"  stem: {entry['stem']}")
         result[f"workload{cfg}"] = entry
+
+    if args.layout_table:
+        log("layouts: plain NHWC vs batch-interleaved (nb images per pixel)")
+        result["layouts"] = layout_table(dev, max(20, args.layer_reps // 4))
 
     if not args.no_cpu:
         log(f"cpu baseline: oracle for ~{args.cpu_seconds:.0f} s ...")
