@@ -43,7 +43,8 @@ def log(msg: str) -> None:
     print(msg, file=sys.stderr, flush=True)
 
 
-KERNEL_SOURCES = ("qconv_conv.hip", "qconv_device.h", "qconv_internal.h", "qconv_host.cpp", "qconv_pack.hip")
+KERNEL_SOURCES = ("qconv_kernels.h", "qconv_conv.hip", "qconv_tiles_b.hip", "qconv_tiles_c.hip", "qconv_tiles_d.hip",
+                  "qconv_device.h", "qconv_internal.h", "qconv_host.cpp", "qconv_pack.hip")
 
 
 def kernel_digest(tile_name: str) -> str:

@@ -497,7 +497,8 @@ void fill_args(ConvArgs &a, const qconv_desc *d, const qconv_layout_info &li, co
 }
 
 // inst: 0 = the tile's generic kernel, 1 + i = its fixed-size instance i; 3 + the same for
-// the kernels with the bias and residual epilogue; 8 + mask for an ablation instance.
+// the kernels with the bias and residual epilogue; 6 / 7 the multi-chunk 3x3 instance
+// (plain / with bias and residual); 8 + mask for an ablation instance.
 int ensure_lds_attribute(const void *kernel, int tile_id, int inst, int64_t lds) {
     if (lds <= 64 * 1024) return QCONV_OK;
     int dev = 0;
@@ -587,9 +588,12 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
     if (prepared && te.info.variant == QCONV_VARIANT_WIDE)
         for (int i = 0; i < 2; ++i)
             if (ks.fixed[i].launch && ks.fixed[i].r == d->r && ks.fixed[i].s == d->s && (d->nb == 1 || d->s == 1)) {
-                launch = ks.fixed[i].launch;
-                kernel = ks.fixed[i].kernel;
-                inst = (ext ? 3 : 0) + 1 + i;
+                // several channel chunks per workgroup: the instance that spreads
+                // the next chunk's filter copies over the MFMA loop
+                const bool mc = pl.cps > 1 && ks.fixed[i].launch_mc;
+                launch = mc ? ks.fixed[i].launch_mc : ks.fixed[i].launch;
+                kernel = mc ? ks.fixed[i].kernel_mc : ks.fixed[i].kernel;
+                inst = mc ? (ext ? 7 : 6) : (ext ? 3 : 0) + 1 + i;
             }
     if (ablation) {
         const AblationInstance *ai = ablation_instance(te.info.name, ablation);

@@ -100,6 +100,8 @@ struct FixedInstance {
     int r, s;
     ConvLauncher launch;
     const void *kernel;
+    ConvLauncher launch_mc; // variant for plans with several channel chunks per workgroup, or null
+    const void *kernel_mc;
 };
 
 // The kernels of one tile for one epilogue flavour.
