@@ -280,6 +280,27 @@ int qconv2d_prepared(const qconv_desc *d, const void *x, const void *w_prepared,
                      size_t workspace_bytes, void *stream);
 
 /*
+ * qconv2d_packing -- qconv_pack of the activations fused into
+ * qconv2d_prepared (Sec. 1 packing, Sec. 3.1 staging): the convolution reads
+ * int8 activations and saturates each value into the b-bit range of
+ * d->x_signed while it stages its input band, so y is exactly
+ * qconv2d_prepared(qconv_pack(x_nchw)).  One launch instead of two, for a
+ * network's first layer.
+ *   x_nchw    DEVICE int8, n x c x h x w, 16-byte aligned
+ *   x_packed  DEVICE, qconv_layout_info.x_bytes, 16-byte aligned, or NULL:
+ *             also receives qconv_pack(x_nchw), each pixel written by the
+ *             workgroup whose band's rows it starts (needs bands that cover
+ *             every input row: stride_h <= r and the last window reaching the
+ *             last row, else QCONV_EUNSUPPORTED)
+ * Runs a wide tile's 3x3 instance (tile_id as for the prepared filters;
+ * d->r == d->s == 3), plain layout, no split, no bias or residual; other
+ * requests return QCONV_EUNSUPPORTED.  No operand may overlap another.
+ * Errors as qconv2d_prepared.
+ */
+int qconv2d_packing(const qconv_desc *d, const int8_t *x_nchw, void *x_packed, const void *w_prepared,
+                    size_t w_prepared_bytes, const qconv_epilogue *epi, void *y, int32_t tile_id, void *stream);
+
+/*
  * Split-K over channel chunks (prepared filters, wide tiles).  The depth
  * C*R*S of the implicit GEMM (Sec. 2.1) is a sum over channel chunks of
  * `chunk_c` channels; with `splits` > 1 each output tile is computed by

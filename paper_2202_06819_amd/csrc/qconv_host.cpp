@@ -484,6 +484,8 @@ void fill_args(ConvArgs &a, const qconv_desc *d, const qconv_layout_info &li, co
     a.div_ncols = make_fastdiv((uint32_t)a.ncols);
     a.div_rs = make_fastdiv((uint32_t)(d->r * d->s));
     a.div_s = make_fastdiv((uint32_t)d->s);
+    a.div_w = make_fastdiv((uint32_t)d->w);
+    a.div_wq = make_fastdiv((uint32_t)((d->w + 3) / 4));
     a.x_signed = d->x_signed;
     a.w_signed = d->w_signed;
     // widening: unsigned nibble -> low half of a byte; signed nibble -> high half (value * 16)
@@ -518,10 +520,14 @@ int ensure_lds_attribute(const void *kernel, int tile_id, int inst, int64_t lds)
 // splits > 1 (prepared filters only): split-K over channel chunks with its
 // workspace in `workspace`.
 // wg_per_cu, band_buffers, xcd_order: the launch knobs of a qconv_schedule.
+// x_nchw (then x is unused): int8 N x C x H x W activations, packed on the way
+// by the tile's fused instance, which also writes the packed copy to x_packed
+// when that is not null.
 int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, size_t w_bytes_given,
              const qconv_epilogue *epi, void *y, void *workspace, size_t workspace_bytes, int32_t tile_id,
              int32_t splits, void *stream, int32_t wg_per_cu = 0, int32_t band_buffers = 0,
-             int32_t xcd_order = 1, int32_t ablation = 0) {
+             int32_t xcd_order = 1, int32_t ablation = 0, const int8_t *x_nchw = nullptr,
+             void *x_packed = nullptr) {
     qconv_layout_info li;
     qconv_desc kd;
     int rc = kernel_desc(d, &kd, &li);
@@ -529,6 +535,10 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
     d = &kd;
     rc = check_epilogue(d, epi);
     if (rc) return rc;
+    // the fused pack reads int8 NCHW activations (n*c*h*w bytes) instead of packed ones
+    const bool fused = x_nchw != nullptr;
+    if (fused) x = x_nchw;
+    const int64_t xin_bytes = fused ? (int64_t)d->n * d->nb * d->c * d->h * (d->w / d->nb) : li.x_bytes;
     if (!x || !w || !y) return fail(QCONV_EINVAL, "x, w and y must be non-NULL");
     if (!aligned16(x) || !aligned16(w) || !aligned16(y)) return fail(QCONV_EINVAL, "x, w and y must be 16-byte aligned");
     if ((int64_t)workspace_bytes < li.workspace_bytes)
@@ -558,11 +568,11 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
     const bool requant = epi && epi->mode == QCONV_OUT_REQUANT;
     const int64_t ybytes = requant ? li.y_packed_bytes : li.y_raw_bytes;
     const uintptr_t y0 = (uintptr_t)y, y1 = y0 + ybytes;
-    if (((uintptr_t)x < y1 && y0 < (uintptr_t)x + li.x_bytes) || ((uintptr_t)w < y1 && y0 < (uintptr_t)w + wb))
+    if (((uintptr_t)x < y1 && y0 < (uintptr_t)x + xin_bytes) || ((uintptr_t)w < y1 && y0 < (uintptr_t)w + wb))
         return fail(QCONV_EINVAL, "y overlaps x or w");
     if (wsb > 0) {
         const uintptr_t w0 = (uintptr_t)workspace, w1 = w0 + wsb;
-        if ((w0 < y1 && y0 < w1) || ((uintptr_t)x < w1 && w0 < (uintptr_t)x + li.x_bytes) ||
+        if ((w0 < y1 && y0 < w1) || ((uintptr_t)x < w1 && w0 < (uintptr_t)x + xin_bytes) ||
             ((uintptr_t)w < w1 && w0 < (uintptr_t)w + wb))
             return fail(QCONV_EINVAL, "workspace overlaps x, w or y");
     }
@@ -571,7 +581,7 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
         // them, so y itself may be the residual; any other overlap may not
         const uintptr_t r0 = (uintptr_t)epi->residual, r1 = r0 + ybytes;
         if (r0 != y0 && r0 < y1 && y0 < r1) return fail(QCONV_EINVAL, "residual overlaps y without being y");
-        if (((uintptr_t)x < r1 && r0 < (uintptr_t)x + li.x_bytes) || ((uintptr_t)w < r1 && r0 < (uintptr_t)w + wb))
+        if (((uintptr_t)x < r1 && r0 < (uintptr_t)x + xin_bytes) || ((uintptr_t)w < r1 && r0 < (uintptr_t)w + wb))
             return fail(QCONV_EINVAL, "residual overlaps x or w");
         if (wsb > 0 && (uintptr_t)workspace < r1 && r0 < (uintptr_t)workspace + wsb)
             return fail(QCONV_EINVAL, "residual overlaps the workspace");
@@ -601,6 +611,28 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
         kernel = ai->kernel;
         inst = 8 + ablation;
     }
+    if (fused) {
+        if (!prepared || !te.fused.launch || d->r != te.fused.r || d->s != te.fused.s || ext || ablation || d->nb != 1)
+            return fail(QCONV_EUNSUPPORTED, "the fused pack runs %s's 3x3 instance from prepared filters, plain "
+                        "layout, without bias, residual or ablation", te.info.name);
+        if (xin_bytes >= kMaxBytes) return fail(QCONV_EUNSUPPORTED, "int8 activations must stay below 2 GiB");
+        if (x_packed) {
+            // every input row must lie in some tile's band (windows that touch,
+            // reaching the last row) for the packed copy to be complete
+            if (d->stride_h > d->r || (int64_t)(li.p - 1) * d->stride_h + d->r - d->pad_h < d->h)
+                return fail(QCONV_EUNSUPPORTED, "the bands of this shape skip input rows: no packed copy");
+            if (!aligned16(x_packed)) return fail(QCONV_EINVAL, "x_packed must be 16-byte aligned");
+            const uintptr_t p0 = (uintptr_t)x_packed, p1 = p0 + li.x_bytes;
+            auto hits = [&](const void *q, int64_t bytes) {
+                return q && (uintptr_t)q < p1 && p0 < (uintptr_t)q + bytes;
+            };
+            if (hits(x, xin_bytes) || hits(w, wb) || hits(y, ybytes) || (wsb > 0 && hits(workspace, wsb)))
+                return fail(QCONV_EINVAL, "x_packed overlaps another operand");
+        }
+        launch = te.fused.launch;
+        kernel = te.fused.kernel;
+        inst = 12;
+    }
     if (te.info.variant == QCONV_VARIANT_WIDE && pl.splits == 1 && pl.off_b1 != pl.off_b0) {
         // persistent grid: size it by the occupancy the runtime reports for this kernel
         rc = ensure_lds_attribute(kernel, tile_id, inst, pl.lds);
@@ -627,6 +659,11 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
     ConvArgs a;
     fill_args(a, d, li, te, pl);
     a.xptr = static_cast<const uint8_t *>(x);
+    if (fused) {
+        a.xsrc = x_nchw;
+        a.xsrc_bytes = (int32_t)xin_bytes;
+        a.xpk = static_cast<uint8_t *>(x_packed);
+    }
     a.wptr = static_cast<const uint8_t *>(w);
     a.yptr = static_cast<uint8_t *>(y);
     a.mult = requant ? epi->mult : nullptr;
@@ -792,6 +829,14 @@ int qconv2d_prepared(const qconv_desc *d, const void *x, const void *w_prepared,
     g_err[0] = 0;
     return run_conv(d, x, w_prepared, true, w_prepared_bytes, epi, y, workspace, workspace_bytes, tile_id, splits,
                     stream);
+}
+
+int qconv2d_packing(const qconv_desc *d, const int8_t *x_nchw, void *x_packed, const void *w_prepared,
+                    size_t w_prepared_bytes, const qconv_epilogue *epi, void *y, int32_t tile_id, void *stream) {
+    g_err[0] = 0;
+    if (!x_nchw) return fail(QCONV_EINVAL, "x_nchw must be non-NULL");
+    return run_conv(d, nullptr, w_prepared, true, w_prepared_bytes, epi, y, nullptr, 0, tile_id, 1, stream, 0, 0, 1,
+                    0, x_nchw, x_packed);
 }
 
 int qconv_unroll(const int8_t *src, int8_t *dst, int32_t n, int32_t c, int32_t h, int32_t w, int32_t taps_h,

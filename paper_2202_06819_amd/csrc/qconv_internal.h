@@ -80,6 +80,11 @@ struct ConvArgs {
     const int32_t *bias;    // per-channel accumulator offsets, or null
     const uint8_t *res;     // residual in y's packed layout, or null
     int32_t res_signed;     // residual values are signed
+    // the pack fused into the convolution (NCHW instances)
+    const int8_t *xsrc;     // int8 N x C x H x W activations
+    int32_t xsrc_bytes;
+    uint8_t *xpk;           // packed copy of the input written on the way, or null
+    FastDiv div_w, div_wq;  // by w and by its column quads
 };
 
 // Band pixels one thread of a wide tile stages per channel chunk: the 4
@@ -116,6 +121,7 @@ struct TileEntry {
     KernelSet plain;        // epilogue without bias and residual
     KernelSet ext;          // epilogue with bias and/or residual
     PrepLauncher prep;      // builds the filter image (wide tiles), else null
+    FixedInstance fused;    // 3x3 instance reading int8 NCHW activations (the pack fused in), or empty
 };
 
 // A kernel with some of the techniques switched off (for measurement).

@@ -261,6 +261,45 @@ __device__ __forceinline__ void widen_vec(uint4 v, uint4 &g0, uint4 &g1) {
 
 constexpr int kWideMaxV = 4;   // packed 16-byte filter vectors a thread gathers per batch
 
+// ---- the pack fused into the convolution (int8 N x C x H x W activations).
+// Four int8 values of one channel -> the int8 MFMA operand bytes that
+// widening the packed 4-bit values gives: saturated into [0, 15] (unsigned)
+// or [-8, 7] and moved to the high nibble (signed, value * 16).  8-bit values
+// pass unchanged.
+template <int BITS, bool SIGNED>
+__device__ __forceinline__ uint32_t saturate_operand(uint32_t x) {
+    if constexpr (BITS == 8) {
+        return x;
+    } else if constexpr (!SIGNED) {
+        if ((x & 0xF0F0F0F0u) == 0u) return x;                          // all in range
+        const uint32_t neg = x & 0x80808080u;                           // negative bytes
+        const uint32_t big = (((x & 0x7F7F7F7Fu) + 0x70707070u) & 0x80808080u) & ~neg;   // above 15
+        uint32_t r = (x & 0x0F0F0F0Fu) | ((big >> 7) * 0x0Fu);
+        return r & ~((neg >> 7) * 0xFFu);
+    } else {
+        uint32_t r = 0u;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int v = (int)(int8_t)(x >> (8 * i));
+            const int c = v < -8 ? -8 : (v > 7 ? 7 : v);
+            r |= ((uint32_t)(c << 4) & 0xF0u) << (8 * i);
+        }
+        return r;
+    }
+}
+
+// 4x4 byte transpose: t[e] holds byte e of a0, a1, a2, a3 (in that order).
+__device__ __forceinline__ void transpose4x4(uint32_t a0, uint32_t a1, uint32_t a2, uint32_t a3, uint32_t (&t)[4]) {
+    const uint32_t lo01 = __builtin_amdgcn_perm(a1, a0, 0x05010400u);   // a0.b0 a1.b0 a0.b1 a1.b1
+    const uint32_t hi01 = __builtin_amdgcn_perm(a1, a0, 0x07030602u);   // a0.b2 a1.b2 a0.b3 a1.b3
+    const uint32_t lo23 = __builtin_amdgcn_perm(a3, a2, 0x05010400u);
+    const uint32_t hi23 = __builtin_amdgcn_perm(a3, a2, 0x07030602u);
+    t[0] = __builtin_amdgcn_perm(lo23, lo01, 0x05040100u);
+    t[1] = __builtin_amdgcn_perm(lo23, lo01, 0x07060302u);
+    t[2] = __builtin_amdgcn_perm(hi23, hi01, 0x05040100u);
+    t[3] = __builtin_amdgcn_perm(hi23, hi01, 0x07060302u);
+}
+
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 constexpr uint32_t kRsrcWord3 = 0x00020000u;   // raw buffer, dword data format (gfx9 family)
@@ -352,11 +391,12 @@ __device__ __forceinline__ int xcd_block(int b, int g) {
 // through LDS to a separate requantise-and-pack pass instead of packing them
 // in registers before the store.
 template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC, bool EXT, int ABL = 0,
-          bool MC = false>
+          bool MC = false, bool NCHW = false>
 __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     constexpr bool FIXED = RC > 0 && SC > 0;
     constexpr bool LOWERED = (ABL & 1) != 0;
     constexpr bool LDSEPI = (ABL & 2) != 0;
+    static_assert(!NCHW || (!LOWERED && !MC), "the fused pack stages the band itself");
     static_assert(ABL == 0 || (FIXED && !EXT), "ablation instances are fixed-size, without bias or residual");
     constexpr int NW = WP * WK;
     constexpr int NT = NW * 64;
@@ -483,6 +523,139 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         }
     };
 
+    // ---- band staging from int8 N x C x H x W (NCHW instances: the pack fused
+    // into the convolution).  Item (band row, column quad, channel octet):
+    // eight dwords -- 4 columns of one image row for each of 8 channels --
+    // saturated like qconv_pack, transposed in registers into 4 pixels x 8
+    // channels in the band's granule byte order, and written with one 8-byte
+    // LDS store per pixel.  The granule of channels 16g .. 16g+15 keeps the
+    // order the widening of packed values gives: 4-bit dwords hold channels
+    // {0,2,4,6}, {1,3,5,7}, {8,10,..}, {9,11,..}; 8-bit ones 0..3, 4..7, ...
+    // Padding columns are written as zeros; padding rows load as zeros.
+    const __amdgpu_buffer_rsrc_t rsx = make_brsrc(a.xsrc, a.xsrc_bytes);
+    auto band_rows_of = [&](int ti, int &vlo, int &nrows, int &vend_own) {
+        const int m0 = (j0 + ti * gpk) * TP;
+        int vlast, cu;
+        pixel_origin(a, m0, vlo, cu);
+        pixel_origin(a, min(m0 + TP, a.m) - 1, vlast, cu);
+        nrows = vlast + R - vlo;
+        // rows this tile writes to the packed copy: up to the next tile's first
+        vend_own = vlast + R;
+        if (m0 + TP < a.m) {
+            int vnext;
+            pixel_origin(a, m0 + TP, vnext, cu);
+            vend_own = min(vend_own, vnext);
+        }
+    };
+    auto nchw_stage = [&](int ti, int c, int buf) {
+        uint8_t *bb = smem + (buf ? a.off_b1 : a.off_b0);
+        int vlo, nrows, vend_own;
+        band_rows_of(ti, vlo, nrows, vend_own);
+        constexpr int NG = CK / 16;   // granule planes of a chunk
+        const int npad = nrows * 2 * a.pw;
+        for (int e = tid; e < npad * NG; e += NT) {
+            const int g = e % NG, q = e / NG;
+            const int rowl = q / (2 * a.pw), side = q - rowl * 2 * a.pw;
+            const int col = side < a.pw ? side : a.w + side;
+            *reinterpret_cast<uint4 *>(bb + (size_t)g * a.pstride_b + (rowl * a.ncols + col) * 16) = uint4{0u, 0u, 0u, 0u};
+        }
+        constexpr int NCO = CK / 8;   // channel octets of a chunk
+        constexpr int IB = 2;         // items a thread has in flight at once
+        const int nwq = (a.w + 3) >> 2;
+        const int items = nrows * NCO * nwq;
+        const bool dwords = (a.w & 3) == 0;
+        for (int base = 0; base < items; base += NT * IB) {
+            uint32_t L[IB][8];
+            int pix0[IB], nvalid[IB], plane[IB], half[IB];
+#pragma unroll
+            for (int u = 0; u < IB; ++u) {
+                const int it = base + u * NT + tid;
+                const int t = (int)fdiv((uint32_t)it, a.div_wq);
+                const int wq = it - t * nwq;
+                const int co = t % NCO, rowl = t / NCO;
+                const int vrow = vlo + rowl;
+                const int img = (int)fdiv((uint32_t)vrow, a.div_vh);
+                const int hh = vrow - img * a.vh - a.ph;
+                const bool row_ok = it < items && img < a.n && hh >= 0 && hh < a.h;
+                const int ww0 = wq * 4;
+                const int ch0 = c * CK + co * 8;
+                pix0[u] = it < items ? rowl * a.ncols + a.pw + ww0 : -1;
+                nvalid[u] = min(4, a.w - ww0);
+                plane[u] = co >> 1;
+                half[u] = (co & 1) * 8;
+#pragma unroll
+                for (int k = 0; k < 8; ++k) {
+                    const bool ok = row_ok && ch0 + k < a.c;
+                    const uint32_t off = (uint32_t)((((img * a.c + ch0 + k) * a.h + hh) * a.w) + ww0);
+                    if (dwords) {
+                        L[u][k] = __builtin_amdgcn_raw_buffer_load_b32(rsx, ok ? (int)off : (int)kOutOfRange, 0, 0);
+                    } else {
+                        uint32_t v = 0u;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            v |= (uint32_t)__builtin_amdgcn_raw_buffer_load_b8(
+                                     rsx, ok && e < nvalid[u] ? (int)(off + e) : (int)kOutOfRange, 0, 0)
+                                 << (8 * e);
+                        L[u][k] = v;
+                    }
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < IB; ++u) {
+                if (pix0[u] < 0) continue;
+#pragma unroll
+                for (int k = 0; k < 8; ++k) L[u][k] = saturate_operand<BITS, XS>(L[u][k]);
+                uint32_t d0[4], d1[4];
+                if constexpr (BITS == 4) {
+                    transpose4x4(L[u][0], L[u][2], L[u][4], L[u][6], d0);
+                    transpose4x4(L[u][1], L[u][3], L[u][5], L[u][7], d1);
+                } else {
+                    transpose4x4(L[u][0], L[u][1], L[u][2], L[u][3], d0);
+                    transpose4x4(L[u][4], L[u][5], L[u][6], L[u][7], d1);
+                }
+                uint8_t *dst = bb + (size_t)plane[u] * a.pstride_b + pix0[u] * 16 + half[u];
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (e < nvalid[u]) *reinterpret_cast<uint2 *>(dst + e * 16) = uint2{d0[e], d1[e]};
+            }
+        }
+    };
+    // The packed copy of the input (qconv_pack's output), for the rows this
+    // tile owns -- from its band's first row up to the next tile's -- and this
+    // chunk's channels: each (pixel, granule) read back from the band and
+    // repacked (the inverse of the widening).
+    auto nchw_write_packed = [&](int ti, int c, int buf) {
+        const uint8_t *bb = smem + (buf ? a.off_b1 : a.off_b0);
+        int vlo, nrows, vend_own;
+        band_rows_of(ti, vlo, nrows, vend_own);
+        constexpr int NG = CK / 16;
+        const int units = (vend_own - vlo) * a.w * NG;
+        for (int e = tid; e < units; e += NT) {
+            const int g = e % NG, t = e / NG;
+            const int rowl = (int)fdiv((uint32_t)t, a.div_w), ww = t - rowl * a.w;
+            const int vrow = vlo + rowl;
+            const int img = (int)fdiv((uint32_t)vrow, a.div_vh);
+            const int hh = vrow - img * a.vh - a.ph;
+            const int ch0 = c * CK + g * 16;
+            if (img >= a.n || hh < 0 || hh >= a.h || ch0 >= a.c) continue;
+            const uint4 v = *reinterpret_cast<const uint4 *>(bb + (size_t)g * a.pstride_b + (rowl * a.ncols + a.pw + ww) * 16);
+            const size_t pix = ((size_t)img * a.h + hh) * a.w + ww;
+            if constexpr (BITS == 4) {
+                uint2 w;
+                if constexpr (XS) {
+                    w.x = ((v.x >> 4) & 0x0F0F0F0Fu) | (v.y & 0xF0F0F0F0u);
+                    w.y = ((v.z >> 4) & 0x0F0F0F0Fu) | (v.w & 0xF0F0F0F0u);
+                } else {
+                    w.x = (v.x & 0x0F0F0F0Fu) | ((v.y & 0x0F0F0F0Fu) << 4);
+                    w.y = (v.z & 0x0F0F0F0Fu) | ((v.w & 0x0F0F0F0Fu) << 4);
+                }
+                *reinterpret_cast<uint2 *>(a.xpk + pix * (a.c / 2) + ch0 / 2) = w;
+            } else {
+                *reinterpret_cast<uint4 *>(a.xpk + pix * a.c + ch0) = v;
+            }
+        }
+    };
+
     // ---- filter staging.  Prepared filters (a.w_image): the block of this
     // channel tile and chunk is already the LDS image (int8, MFMA row order,
     // planes of pstride_w bytes), copied with asynchronous LDS-DMA.  Otherwise
@@ -594,12 +767,17 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     // ---- prologue: stage 0 (every load in flight before the first wait)
     if (nst > 0) {
         if (w_image) w_dma(c_begin, 0);
-        set_band(0);
-        Fetch fb;
-        band_fetch(c_begin, fb);
-        if (!w_image) w_load_all(c_begin, 0);
-        __builtin_amdgcn_s_waitcnt(0);
-        band_store(fb, 0);
+        if constexpr (NCHW) {
+            nchw_stage(0, c_begin, 0);
+            __builtin_amdgcn_s_waitcnt(0);
+        } else {
+            set_band(0);
+            Fetch fb;
+            band_fetch(c_begin, fb);
+            if (!w_image) w_load_all(c_begin, 0);
+            __builtin_amdgcn_s_waitcnt(0);
+            band_store(fb, 0);
+        }
     }
     set_tile(0);
     __syncthreads();
@@ -689,8 +867,10 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         Fetch fb;
         WFetch fw;
         if (more) {
-            if (nti != ti) set_band(nti);
-            band_fetch(nc, fb);
+            if constexpr (!NCHW) {
+                if (nti != ti) set_band(nti);
+                band_fetch(nc, fb);
+            }
             if (c_end - c_begin > 1) {
                 // (the multi-chunk instances issue their filter DMA inside the MFMA loop)
                 if (w_image) {
@@ -820,6 +1000,12 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
             if (it + 1 < nit) mm(A1, B1);
         }
 
+        // the packed copy of this stage's band rows: before the next stage is
+        // staged when that reuses the one band buffer, else after it (its
+        // loads are then waited for without these stores)
+        if constexpr (NCHW)
+            if (a.xpk && a.off_b1 == a.off_b0) nchw_write_packed(ti, c, cur);
+
         // The next stage's operands (in flight during the MFMAs) are waited for
         // and staged before this stage's epilogue issues its stores: the wait
         // covers loads only, never the store acknowledgements.
@@ -827,7 +1013,10 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
             // with a single band buffer every wave must be done reading it
             if (a.off_b1 == a.off_b0) __syncthreads();
             __builtin_amdgcn_s_waitcnt(0);   // prefetched band (and filter DMA) have landed
-            band_store(fb, cur ^ 1);
+            if constexpr (NCHW)
+                nchw_stage(nti, nc, cur ^ 1);
+            else
+                band_store(fb, cur ^ 1);
             if constexpr (!FIXED) if (c_end - c_begin > 1 && !w_image) {
                 w_gather_store(fw, 0, cur ^ 1);
                 for (int base = NT * MAXV; base < TK * rs * VPP; base += NT * MAXV) {
@@ -837,6 +1026,8 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                 }
             }
         }
+        if constexpr (NCHW)
+            if (a.xpk && a.off_b1 != a.off_b0) nchw_write_packed(ti, c, cur);
         if (c == c_end - 1) {
             if (a.splits > 1) {
                 // split-K: publish this split's partial sums; the last split of the
@@ -941,9 +1132,9 @@ __global__ void __launch_bounds__(256) build_filter_image(ConvArgs a, int TK, in
 // One operand signedness per kernel (the widening is compiled for it); 8-bit
 // operands are always signed.
 template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC, bool EXT, int ABL = 0,
-          bool MC = false>
+          bool MC = false, bool NCHW = false>
 __global__ void __launch_bounds__(WP * WK * 64) __attribute__((amdgpu_waves_per_eu(2))) conv_wide(ConvArgs a) {
-    wide_body<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC, EXT, ABL, MC>(a);
+    wide_body<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC, EXT, ABL, MC, NCHW>(a);
 }
 
 // ============================================================== tile registry
@@ -955,9 +1146,9 @@ static hipError_t launch_staged(const ConvArgs &a, dim3 grid, size_t lds, hipStr
 }
 
 template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC, bool EXT, int ABL = 0,
-          bool MC = false>
+          bool MC = false, bool NCHW = false>
 static hipError_t launch_wide(const ConvArgs &a, dim3 grid, size_t lds, hipStream_t stream) {
-    hipLaunchKernelGGL((conv_wide<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC, EXT, ABL, MC>), grid, dim3(WP * WK * 64),
+    hipLaunchKernelGGL((conv_wide<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC, EXT, ABL, MC, NCHW>), grid, dim3(WP * WK * 64),
                        lds, stream, a);
     return hipGetLastError();
 }
@@ -1022,7 +1213,7 @@ static hipError_t launch_prep(const ConvArgs &a, uint8_t *img, int64_t elems, hi
      reinterpret_cast<const void *>(&conv_staged<B, WP, WK, FP, FK, CK, EXT>), {}}
 #define QCONV_STAGED_ENTRY(B, WP, WK, FP, FK, CK)                                                                 \
     {QCONV_TILE_INFO(QCONV_VARIANT_STAGED, "staged_b", B, WP, WK, FP, FK, CK, -1, -1),                           \
-     QCONV_STAGED_SET(B, WP, WK, FP, FK, CK, false), QCONV_STAGED_SET(B, WP, WK, FP, FK, CK, true), nullptr},
+     QCONV_STAGED_SET(B, WP, WK, FP, FK, CK, false), QCONV_STAGED_SET(B, WP, WK, FP, FK, CK, true), nullptr, {}},
 // 4-bit: unsigned activations x signed filters; 8-bit: signed x signed.
 // Each wide tile also has fixed-size instances for 3x3 and 1x1 filters, used
 // with prepared filters.
@@ -1036,9 +1227,13 @@ static hipError_t launch_prep(const ConvArgs &a, uint8_t *img, int64_t elems, hi
     {QCONV_WIDE_INST(B, WP, WK, FP, FK, CK, 0, 0, EXT),                                                           \
      {{3, 3, QCONV_WIDE_INST(B, WP, WK, FP, FK, CK, 3, 3, EXT), QCONV_WIDE_MC(B, WP, WK, FP, FK, CK, 3, 3, EXT)}, \
       {1, 1, QCONV_WIDE_INST(B, WP, WK, FP, FK, CK, 1, 1, EXT), nullptr, nullptr}}}
+#define QCONV_WIDE_FUSED(B, WP, WK, FP, FK, CK)                                                                   \
+    {3, 3, &launch_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, false, 0, false, true>,                      \
+     reinterpret_cast<const void *>(&conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, false, 0, false, true>), \
+     nullptr, nullptr}
 #define QCONV_WIDE_ENTRY(B, WP, WK, FP, FK, CK)                                                                   \
     {QCONV_TILE_INFO(QCONV_VARIANT_WIDE, "wide_b", B, WP, WK, FP, FK, CK, (B == 8), 1),                         \
      QCONV_WIDE_SET(B, WP, WK, FP, FK, CK, false), QCONV_WIDE_SET(B, WP, WK, FP, FK, CK, true),                 \
-     &launch_prep<B, WK, FK, CK, true>},
+     &launch_prep<B, WK, FK, CK, true>, QCONV_WIDE_FUSED(B, WP, WK, FP, FK, CK)},
 
 }  // namespace qconv

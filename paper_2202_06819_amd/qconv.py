@@ -107,11 +107,14 @@ def lib() -> ctypes.CDLL:
         L.qconv_schedule_check.argtypes = [P(QConvDesc), P(QConvSchedule)]
         L.qconv_unroll.argtypes = [_vp, _vp] + [_i32] * 12 + [_vp]
         L.qconv_pack_interleaved.argtypes = [_vp, _vp] + [_i32] * 7 + [_vp]
+        L.qconv2d_packing.argtypes = [P(QConvDesc), _vp, _vp, _vp, ctypes.c_size_t, P(QConvEpilogue), _vp, _i32,
+                                      _vp]
         L.qconv2d_scheduled.argtypes = [P(QConvDesc), _vp, _vp, ctypes.c_size_t, P(QConvEpilogue), _vp,
                                         P(QConvSchedule), _vp, ctypes.c_size_t, _vp]
         for f in ("qconv_layout", "qconv_pack", "qconv2d", "qconv_tile_count", "qconv_tile_get", "qconv_tile_check",
                   "qconv_default_tile", "qconv_selftest", "qconv_prepared_filter_bytes", "qconv_prepare_filters",
-                  "qconv2d_prepared", "qconv_workspace_bytes", "qconv_max_splits", "qconv_probe_mfma_i8", "qconv_schedule_check", "qconv2d_scheduled", "qconv_unroll", "qconv_pack_interleaved"):
+                  "qconv2d_prepared", "qconv_workspace_bytes", "qconv_max_splits", "qconv_probe_mfma_i8", "qconv_schedule_check", "qconv2d_scheduled", "qconv_unroll", "qconv_pack_interleaved",
+                  "qconv2d_packing"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
         return L
@@ -479,4 +482,50 @@ class Conv2dCall:
 
     def __call__(self) -> torch.Tensor:
         _check(self._fn(*self._args), "qconv2d")
+        return self.out
+
+
+class PackingConv2dCall:
+    """A qconv2d_packing call (the pack fused into the convolution) with its
+    arguments marshalled once; ``()`` enqueues it and returns y.  `x` is the
+    int8 N x C x H x W activations, `w_prepared` the filters prepared for
+    `tile`; with ``x_packed`` (a tensor, or True to allocate one) the packed
+    input is written too."""
+
+    def __init__(self, d: dict, x: torch.Tensor, w_prepared: torch.Tensor, *, tile: int, requant: bool = True,
+                 mult: torch.Tensor | None = None, shift: int = 20, relu: bool = True, clamp: tuple = (0, 15),
+                 out: torch.Tensor | None = None, x_packed=None, stream=None):
+        if x.dtype != torch.int8 or x.dim() != 4:
+            raise QConvError(EINVAL, "the fused pack reads a 4-d int8 tensor")
+        self.desc = make_desc(d)
+        info = layout(d)
+        bits = self.desc.bits
+        if out is None:
+            shape = (packed_shape(self.desc.n, info["p"], info["q"], self.desc.k, bits) if requant
+                     else raw_shape(self.desc, info))
+            out = torch.empty(shape, dtype=packed_dtype(bits) if requant else torch.int32, device=x.device)
+        if x_packed is True:
+            x_packed = torch.empty(packed_shape(self.desc.n, self.desc.h, self.desc.w, self.desc.c, bits),
+                                   dtype=packed_dtype(bits), device=x.device)
+        self.epi = QConvEpilogue()
+        if requant:
+            if mult is None or mult.dtype != torch.int32 or mult.numel() != self.desc.k:
+                raise QConvError(EINVAL, "requant needs an int32 multiplier per output channel")
+            self.epi.mode, self.epi.mult = OUT_REQUANT, _dev_ptr(mult, "mult", 4 * self.desc.k)
+            self.epi.shift, self.epi.relu = int(shift), int(bool(relu))
+            self.epi.clamp_lo, self.epi.clamp_hi = int(clamp[0]), int(clamp[1])
+        else:
+            self.epi.mode = OUT_RAW_I32
+        y_bytes = info["y_packed_bytes"] if requant else info["y_raw_bytes"]
+        self.x, self.w, self.mult, self.out, self.x_packed = x, w_prepared, mult, out, x_packed
+        self.tile = int(tile)
+        wb = prepared_filter_bytes(d, self.tile)
+        xp_ptr = None if x_packed is None else _dev_ptr(x_packed, "x_packed", info["x_bytes"])
+        self._args = (ctypes.byref(self.desc), _dev_ptr(x, "x", x.numel()), xp_ptr, _dev_ptr(w_prepared, "w", wb),
+                      w_prepared.numel() * w_prepared.element_size(), ctypes.byref(self.epi),
+                      _dev_ptr(out, "y", y_bytes), self.tile, _vp(_stream(stream)))
+        self._fn = lib().qconv2d_packing
+
+    def __call__(self) -> torch.Tensor:
+        _check(self._fn(*self._args), "qconv2d_packing")
         return self.out

@@ -432,3 +432,28 @@ def test_pack_interleaved_argument_errors(q):
     assert L.qconv_pack_interleaved(src, dst, 4, 60, 8, 8, 4, 0, 2, None) == -2   # c % 8 for 4-bit
     assert L.qconv_pack_interleaved(src, dst + 2, 4, 64, 8, 8, 4, 0, 2, None) == -1   # misaligned
     assert L.qconv_pack_interleaved(None, None, 0, 64, 8, 8, 4, 0, 2, None) == 0  # empty: no-op
+
+
+def test_fused_pack_argument_errors(q):
+    """qconv2d_packing rejects what its fused instance does not run, before
+    anything is launched."""
+    import ctypes as C
+    L = q.lib()
+    names = {t["name"]: t["id"] for t in q.tiles()}
+    tid = names["wide_b4_w4x2_f2x2_c64"]
+    x, xp, w, y = 1 << 32, 1 << 33, 1 << 34, 1 << 35
+    epi = q.QConvEpilogue()
+    epi.mode = 0
+
+    def call(d, x_=x, xp_=xp, tile=tid):
+        desc = q.make_desc(d)
+        wb = q.prepared_filter_bytes(d, tile) if q.tile_status(d, tile) == 0 else 1 << 20
+        return L.qconv2d_packing(C.byref(desc), x_, xp_, w, wb, C.byref(epi), y, tile, None)
+
+    assert call(D(n=2), x_=None) == -1                                   # no input
+    assert call(D(n=2, r=1, s=1, pad_h=0, pad_w=0)) == -2                # no 1x1 fused instance
+    assert call(D(n=2), tile=names["staged_b4_w4x1_f1x4_c64"]) == -2     # staged tile
+    assert call(D(n=2, nb=2)) == -2                                      # interleaved layout
+    assert call(D(n=2, stride_h=4, stride_w=4)) == -2                    # bands skip rows: no packed copy
+    assert call(D(n=2), xp_=xp + 8) == -1                                # misaligned packed copy
+    assert call(D(n=2), xp_=x + 64) == -1                                # packed copy overlaps x

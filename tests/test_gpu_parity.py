@@ -685,3 +685,63 @@ def test_interleaved_layout(case):
             torch.cuda.synchronize()
             assert_same(y.cpu().numpy(), want_y, f"{name} {t['name']} split 2")
     assert ran >= 2, f"{name}: only {ran} tiles read the interleaved layout"
+
+
+# ------------------------------------------------ the pack fused into the conv
+
+FUSED_CASES = [
+    # name, n, h, w, c, k, stride, bits, value range of x
+    ("b4_56x56_64_n8", 8, 56, 56, 64, 64, 1, 4, (0, 15)),
+    ("b4_out_of_range", 2, 20, 24, 64, 64, 1, 4, (-128, 127)),   # saturation of every kind
+    ("b4_ragged_w14_c128", 4, 14, 14, 128, 64, 1, 4, (0, 15)),   # byte loads, two channel chunks
+    ("b4_odd_13x11", 3, 13, 11, 64, 128, 1, 4, (-3, 20)),
+    ("b4_stride2", 4, 28, 28, 64, 128, 2, 4, (0, 15)),
+    ("b4_persistent_n32", 32, 56, 56, 64, 64, 1, 4, (0, 15)),    # several tiles per workgroup
+    ("b8_28x28_64", 4, 28, 28, 64, 64, 1, 8, (-128, 127)),
+]
+
+
+@pytest.mark.parametrize("case", FUSED_CASES, ids=[c[0] for c in FUSED_CASES])
+def test_fused_pack_conv(case):
+    """qconv2d_packing on every tile that has the fused instance: y (requant
+    and raw) equals the oracle's layer on the same int8 NCHW input (which the
+    oracle packs with saturation), and the packed copy equals the oracle's
+    packed input."""
+    torch, q = _torch(), _qconv()
+    name, n, h, w, c, k, stride, bits, xr = case
+    signed = bits == 8
+    g = np.random.default_rng([991, n, h, w, c, k, stride, bits])
+    x = g.integers(xr[0], xr[1] + 1, size=(n, c, h, w)).astype(np.int8)
+    wr = (-128, 127) if signed else (-7, 7)
+    f = g.integers(wr[0], wr[1] + 1, size=(k, c, 3, 3)).astype(np.int8)
+    mult = g.integers(2 ** 14, 2 ** 15, size=k).astype(np.int32)
+    L = qi.Layer(name, n, h, w, c, k, 3, 3, stride, 1, bits=bits, x_signed=signed, w_signed=True,
+                 x_range=(0, 15) if not signed else qi.S8, w_range=wr)
+    sh = stress_shift(L, L.x_range, L.w_range)
+    lo, hi, relu = (-128, 127, False) if signed else (0, 15, True)
+    ref = oracle.qconv_layer(x, f, bits=bits, x_signed=signed, w_signed=True, stride=(stride, stride), pad=(1, 1),
+                             mult=mult, shift=sh, relu=relu, lo=lo, hi=hi, threads=oracle_threads())
+    d = L.desc()
+    dev = torch.device("cuda:0")
+    x_dev = torch.from_numpy(x).to(dev)
+    wp = q.pack(torch.from_numpy(f).to(dev), bits, True)
+    m_dev = torch.from_numpy(mult).to(dev)
+    ran = 0
+    for t in q.tiles():
+        if t["variant"] != 2 or q.tile_status(d, t["id"]) != 0:
+            continue
+        ran += 1
+        tid = t["id"]
+        wprep = q.prepare_filters(d, wp, tid)
+        announce(f"fused pack {name} tile {t['name']}")
+        call = q.PackingConv2dCall(d, x_dev, wprep, tile=tid, mult=m_dev, shift=sh, relu=relu, clamp=(lo, hi),
+                                   x_packed=True)
+        y = call()
+        torch.cuda.synchronize()
+        assert_same(y.cpu().numpy(), ref["y_packed"], f"{name} {t['name']} y")
+        assert_same(call.x_packed.cpu().numpy(), ref["x_packed"], f"{name} {t['name']} packed copy")
+        announce(f"fused pack {name} tile {t['name']} raw, no packed copy")
+        y = q.PackingConv2dCall(d, x_dev, wprep, tile=tid, requant=False)()
+        torch.cuda.synchronize()
+        assert_same(y.cpu().numpy(), ref["acc"], f"{name} {t['name']} raw")
+    assert ran >= 4
