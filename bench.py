@@ -457,6 +457,40 @@ def layout_table(dev, reps: int) -> list[dict]:
     return rows
 
 
+def fused_step_time(L, x, xp_ref, wp, mult, y_ref, dev, reps: int) -> dict:
+    """The benchmark step as one launch: qconv2d_packing, the pack fused into
+    the convolution, writing the packed input too.  The fastest tile of a
+    short sweep; its output and packed copy are checked against the
+    two-launch step's."""
+    import torch
+    from paper_2202_06819_amd import qconv
+    e = L.epilogue
+    d = L.desc()
+    best = None
+    for t in qconv.tiles():
+        if t["variant"] != 2 or qconv.tile_status(d, t["id"]) != 0:
+            continue
+        wprep = qconv.prepare_filters(d, wp, t["id"])
+
+        def make(stream=None, tid=t["id"], wprep=wprep):
+            return qconv.PackingConv2dCall(d, x, wprep, tile=tid, mult=mult, shift=e.shift, relu=e.relu,
+                                           clamp=(e.lo, e.hi), x_packed=True, stream=stream)
+
+        call = make()
+        y = call()
+        torch.cuda.synchronize()
+        if not (torch.equal(y, y_ref) and torch.equal(call.x_packed, xp_ref)):
+            raise RuntimeError(f"fused pack + conv on {t['name']} differs from the two-launch step")
+        g, _ = captured(lambda st: [make(st)], 20)
+        us = time_graph(g, 3) * 1000.0 / 60
+        if best is None or us < best[0]:
+            best = (us, t["name"], make)
+    g, _ = captured(lambda st: [best[2](st)], reps)
+    us = time_graph(g, 5) * 1000.0 / (5 * reps)
+    return {"us": round(us, 3), "tops": round(L.ops / (us * 1e-6) / 1e12, 2), "tile": best[1],
+            "entry": "qconv2d_packing", "packed_copy": True}
+
+
 def cpu_baseline(L, seconds: float, threads: int | None = None) -> dict:
     """The oracle, as it stands, on the host cores: pack + conv + requant + repack
     of the same layer, repeated for about `seconds` (all cores by default)."""
@@ -578,6 +612,9 @@ def main() -> int:
     big_p = torch.empty((n_cp,) + tuple(xp.shape), dtype=xp.dtype, device=dev)
     pack_cold_us = cold_time([qconv.PackCall(big_x[i], L.bits, L.x_signed, out=big_p[i]) for i in range(n_cp)])
     del big_x, big_p
+    fused = fused_step_time(L, x, xp, wp, mult, ref_out, dev, reps)
+    log(f"the step as one launch (pack fused into the conv, packed copy written): {fused['us']:.2f} us = "
+        f"{fused['tops']:.1f} TOP/s, tile {fused['tile']}")
     probe = mfma_probe(dev)
     log(f"pack kernel cold ({n_cp} copies): {pack_cold_us:.2f} us = {pack_bytes / (pack_cold_us * 1e-6) / 1e9:.0f} GB/s; "
         f"MFMA-only probe {probe['tops']:.0f} TOP/s at {probe['clock_ghz']:.2f} GHz")
@@ -611,7 +648,8 @@ def main() -> int:
         "kernels": {"conv_us": round(conv_us, 3), "pack_us": round(pack_us, 3),
                     "pack_gbs": round(pack_gbs, 1), "pack_frac_hbm": round(pack_gbs / HBM_PEAK_GBS, 4),
                     "pack_algorithmic_bytes": pack_bytes, "pack_cold_us": round(pack_cold_us, 3),
-                    "pack_cold_gbs": round(pack_bytes / (pack_cold_us * 1e-6) / 1e9, 1), "pack_cold_copies": n_cp},
+                    "pack_cold_gbs": round(pack_bytes / (pack_cold_us * 1e-6) / 1e9, 1), "pack_cold_copies": n_cp,
+                    "fused_step": fused},
         "mfma_probe": probe,
     }
 
