@@ -88,13 +88,19 @@ __global__ void __launch_bounds__(PK_THREADS)
         for (int e = 0; e < 8; ++e) {
             uint32_t w = v[e];
             if constexpr (BITS == 4) {
-                uint32_t o = 0;
+                // byte-parallel range test (for signed values on v + 8, added per
+                // byte without carries); only words with a byte out of range
+                // take the per-byte clamp
+                const uint32_t t = SIGNED ? (((w & 0x7F7F7F7Fu) + 0x08080808u) ^ (w & 0x80808080u)) : w;
+                if ((t & 0xF0F0F0F0u) != 0u) {
+                    uint32_t o = 0;
 #pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const int x = (int)(int8_t)byte_of(w, k);
-                    o |= ((uint32_t)(x < LO ? LO : (x > HI ? HI : x)) & 0xFFu) << (8 * k);
+                    for (int k = 0; k < 4; ++k) {
+                        const int x = (int)(int8_t)byte_of(w, k);
+                        o |= ((uint32_t)(x < LO ? LO : (x > HI ? HI : x)) & 0xFFu) << (8 * k);
+                    }
+                    w = o;
                 }
-                w = o;
             }
             *reinterpret_cast<uint32_t *>(tile + row * PK_PITCH + seg + 4 * e) = w;
         }

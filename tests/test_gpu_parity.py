@@ -39,6 +39,9 @@ PACK_CASES = [
     (2, 72, 3, 11, 4, True, (-128, 127)),
     (3, 136, 9, 9, 4, True, (-9, 9)),
     (64, 64, 3, 3, 4, True, (-8, 7)),           # filters K x C x R x S
+    (4, 64, 28, 28, 4, False, (0, 15)),         # every value in range (no clamping needed)
+    (2, 32, 14, 14, 4, True, (-8, 7)),
+    (2, 32, 14, 14, 4, True, (-9, 8)),          # just outside both ends
     (2, 64, 56, 56, 8, True, (-128, 127)),
     (1, 20, 7, 5, 8, True, (-128, 127)),
     (2, 100, 1, 1, 8, True, (-128, 127)),
