@@ -180,6 +180,9 @@ int64_t band_rows(const qconv_desc *d, int64_t p, int64_t q, int64_t tile_p) {
 int64_t pad_plane(int64_t bytes) { return (bytes + 255) / 256 * 256 + 128; }
 
 constexpr int kNumCUs = 256;   // MI355X compute units
+// staging rounds of an 8-bit wide tile's band: the first is prefetched during
+// the previous stage's MFMAs, the rest are loaded and written in turn
+constexpr int64_t kBandRounds = 4;
 
 struct Plan {
     int64_t rows = 0, pstride_b = 0, pstride_w = 0, lds = 0;
@@ -232,8 +235,10 @@ int plan_tile(const qconv_desc *d, const qconv_layout_info &li, const qconv_tile
         const bool lowered = (ablation & 1) != 0, ldsepi = (ablation & 2) != 0;
         if (ablation && (d->r != 3 || d->s != 3 || splits != 1 || d->nb > 1))
             return fail(QCONV_EUNSUPPORTED, "ablation instances run 3x3 filters without a split, plain layout");
-        if (!lowered && pl.rows * ncols > (int64_t)t.threads * pj)
-            return fail(QCONV_EUNSUPPORTED, "tile %s: the input band of this shape exceeds one prefetch batch", t.name);
+        const int64_t rounds = d->bits == 8 ? kBandRounds : 1;
+        if (!lowered && pl.rows * ncols > rounds * (int64_t)t.threads * pj)
+            return fail(QCONV_EUNSUPPORTED, "tile %s: the input band of this shape exceeds %d staging round(s)", t.name,
+                        (int)rounds);
         const int64_t planes = t.chunk_c / 16;
         // plane strides: multiples of 256 bytes keep the four 16-lane groups of a
         // 16-byte LDS read in distinct banks; filter planes are whole KiB so a
@@ -295,6 +300,16 @@ int plan_tile(const qconv_desc *d, const qconv_layout_info &li, const qconv_tile
             const int64_t gpk = std::min<int64_t>(pl.mtiles, std::max<int64_t>(1, (kNumCUs * pc + pl.ktiles - 1) / pl.ktiles));
             pl.grid = gpk * pl.ktiles;
         }
+    }
+    if (t.variant == QCONV_VARIANT_WIDE && pl.lds > kLdsBytes && pl.off_b1 != pl.off_b0) {
+        // two band buffers do not fit: keep one (the kernel then waits for every
+        // wave to finish reading it before restaging; filters stay double)
+        const int64_t shift_b = pl.off_b1 - pl.off_b0;
+        pl.off_b1 = pl.off_b0;
+        pl.off_w0 -= shift_b;
+        pl.off_w1 -= shift_b;
+        pl.off_m -= shift_b;
+        pl.lds -= shift_b;
     }
     if (t.variant == QCONV_VARIANT_WIDE && (ablation & 2)) pl.off_e = pl.off_m + round_up((int64_t)t.tile_k * 8 + 4, 16);
     if (pl.lds > kLdsBytes)

@@ -452,7 +452,7 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     // chunk) of every band pixel, 16 bytes each: one write instruction fills
     // one plane contiguously.
     uint32_t poff[PJ];
-    int npix = 0;
+    int npix = 0, band_vlo = 0;
     auto set_band = [&](int ti) {
         const int m0 = (j0 + ti * gpk) * TP;
         if constexpr (LOWERED) {
@@ -478,7 +478,8 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         int vlo, vlast, cu;
         pixel_origin(a, m0, vlo, cu);
         pixel_origin(a, min(m0 + TP, a.m) - 1, vlast, cu);
-        npix = (vlast + R - vlo) * a.ncols;   // <= NT * PJ (host-checked)
+        npix = (vlast + R - vlo) * a.ncols;   // beyond NT * PJ: staged by band_rest
+        band_vlo = vlo;
 #pragma unroll
         for (int j = 0; j < PJ; ++j) {
             const int pix = j * NT + tid;
@@ -506,11 +507,11 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                 f.v[j][p] = buffer_load16(rx, ok ? poff[j] + cbyte + p * 16 : kOutOfRange);
             }
     };
-    auto band_store = [&](const Fetch &f, int buf) {
+    auto band_store = [&](const Fetch &f, int buf, int base = 0) {
         uint8_t *bb = smem + (buf ? a.off_b1 : a.off_b0);
 #pragma unroll
         for (int j = 0; j < PJ; ++j) {
-            const int pix = j * NT + tid;
+            const int pix = base + j * NT + tid;
             if (pix >= npix) continue;
 #pragma unroll
             for (int p = 0; p < VPP; ++p) {
@@ -519,6 +520,40 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                 *reinterpret_cast<uint4 *>(bb + (size_t)(p * GPV) * a.pstride_b + pix * 16) = g0;
                 if constexpr (GPV == 2)
                     *reinterpret_cast<uint4 *>(bb + (size_t)(p * GPV + 1) * a.pstride_b + pix * 16) = g1;
+            }
+        }
+    };
+
+    // Band pixels past the first NT * PJ (bands of strided layers can be
+    // several times the tile): staged here in further rounds, each loaded and
+    // written before the next, after the first round is in place.  8-bit
+    // tiles only, whose per-thread budget is one pixel per round; compiled into
+    // the 4-bit kernels the idle rounds cost 2-9 %, and their budget of two
+    // pixels already covers the strided layers.
+    auto band_rest = [&](int c, int buf) {
+        if constexpr (!LOWERED && BITS == 8) {
+            const uint32_t cbyte = (uint32_t)c * (CK * BITS / 8);
+            const int cbase = c * CK;
+            for (int base = NT * PJ; base < npix; base += NT * PJ) {
+                Fetch f;
+#pragma unroll
+                for (int j = 0; j < PJ; ++j) {
+                    const int pix = base + j * NT + tid;
+                    const int rowl = (int)fdiv((uint32_t)pix, a.div_ncols);
+                    const int col = pix - rowl * a.ncols;
+                    const int vrow = band_vlo + rowl;
+                    const int img = (int)fdiv((uint32_t)vrow, a.div_vh);
+                    const int hh = vrow - img * a.vh - a.ph;
+                    const int ww = col - a.pw;
+                    const bool in = pix < npix && img < a.n && hh >= 0 && hh < a.h && ww >= 0 && ww < a.w;
+                    const uint32_t off = in ? (uint32_t)(((img * a.h + hh) * a.w + ww) * a.xpix) : kOutOfRange;
+#pragma unroll
+                    for (int p = 0; p < VPP; ++p) {
+                        const bool ok = off != kOutOfRange && cbase + p * CPV < a.c;
+                        f.v[j][p] = buffer_load16(rx, ok ? off + cbyte + p * 16 : kOutOfRange);
+                    }
+                }
+                band_store(f, buf, base);
             }
         }
     };
@@ -777,6 +812,7 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
             if (!w_image) w_load_all(c_begin, 0);
             __builtin_amdgcn_s_waitcnt(0);
             band_store(fb, 0);
+            band_rest(c_begin, 0);
         }
     }
     set_tile(0);
@@ -1013,10 +1049,12 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
             // with a single band buffer every wave must be done reading it
             if (a.off_b1 == a.off_b0) __syncthreads();
             __builtin_amdgcn_s_waitcnt(0);   // prefetched band (and filter DMA) have landed
-            if constexpr (NCHW)
+            if constexpr (NCHW) {
                 nchw_stage(nti, nc, cur ^ 1);
-            else
+            } else {
                 band_store(fb, cur ^ 1);
+                band_rest(nc, cur ^ 1);
+            }
             if constexpr (!FIXED) if (c_end - c_begin > 1 && !w_image) {
                 w_gather_store(fw, 0, cur ^ 1);
                 for (int base = NT * MAXV; base < TK * rs * VPP; base += NT * MAXV) {

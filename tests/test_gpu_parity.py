@@ -748,3 +748,35 @@ def test_fused_pack_conv(case):
         torch.cuda.synchronize()
         assert_same(y.cpu().numpy(), ref["acc"], f"{name} {t['name']} raw")
     assert ran >= 4
+
+
+@pytest.mark.parametrize("shape", [
+    # name, n, h, c, k, stride, bits -- strided 3x3 layers whose bands take
+    # several staging rounds, and multi-chunk ones with a single band buffer
+    ("b8_s2_28to14_128to256", 4, 28, 128, 256, 2, 8),
+    ("b8_s2_14to7_256to512", 4, 14, 256, 512, 2, 8),
+    ("b8_s2_56to28_64to128", 2, 56, 64, 128, 2, 8),
+    ("b4_s2_28to14_128to256", 4, 28, 128, 256, 2, 4),
+    ("b8_s3_30to10_64to64", 2, 30, 64, 64, 3, 8),
+], ids=lambda v: v[0])
+def test_strided_bands_every_wide_tile(shape):
+    q = _qconv()
+    name, n, h, c, k, stride, bits = shape
+    if bits == 8:
+        L = qi.Layer(name, n, h, h, c, k, 3, 3, stride, 1, bits=8, x_signed=True, w_signed=True, x_range=qi.S8,
+                     w_range=qi.S8, epilogue=qi.Epilogue(relu=False, lo=-128, hi=127))
+    else:
+        L = qi.Layer(name, n, h, h, c, k, 3, 3, stride, 1, w_range=(-7, 7))
+    t = qi.layer_tensors(800, c + k + stride, L)
+    sh = stress_shift(L, L.x_range, L.w_range)
+    ref = ref_layer(L, t, requant=True, shift=sh)
+    ref_raw = ref_layer(L, t, requant=False)
+    wide = [tt["id"] for tt in q.tiles() if tt["variant"] == 2 and q.tile_status(L.desc(), tt["id"]) == 0]
+    assert len(wide) >= 2
+    for tid in wide:
+        announce(f"{name} tile {tid} prepared requant shift={sh}")
+        assert_same(gpu_layer(L, t, requant=True, tile=tid, shift=sh, prepared=True)["y"], ref["y_packed"],
+                    f"{name} tile {tid} prepared")
+        announce(f"{name} tile {tid} prepared raw")
+        assert_same(gpu_layer(L, t, requant=False, tile=tid, prepared=True)["y"], ref_raw["acc"],
+                    f"{name} tile {tid} prepared raw")
