@@ -339,8 +339,10 @@ __device__ __forceinline__ void dma16(const uint8_t *lds_dst, uint32_t voff, u32
                  : "memory", "m0");
 }
 // dma16 with the LDS destination as a byte address, a scalar offset added to
-// voff (one address register serves a run of copies), and only the lanes of
-// `lanes` (all or none) enabled for the copy; exec is restored after it.
+// voff (one address register serves a run of copies), and the wave's lanes
+// set to `lanes` (all or none) for the copy; exec is restored after it.  (A
+// plain move, not an AND: the copy is a whole 1 KiB block either way, and no
+// condition code is written behind the compiler's back.)
 __device__ __forceinline__ void dma16m(uint32_t lds_addr, uint32_t voff, uint32_t soff, u32x4 rsrc,
                                        uint64_t lanes) {
     const uint32_t m0v = __builtin_amdgcn_readfirstlane(lds_addr);
@@ -350,13 +352,13 @@ __device__ __forceinline__ void dma16m(uint32_t lds_addr, uint32_t voff, uint32_
     uint64_t saved;
     asm volatile(
         "s_mov_b64 %0, exec\n\t"
-        "s_and_b64 exec, exec, %1\n\t"
+        "s_mov_b64 exec, %1\n\t"
         "s_mov_b32 m0, %2\n\t"
         "buffer_load_dwordx4 %3, %4, %5 offen lds\n\t"
         "s_mov_b64 exec, %0"
         : "=&s"(saved)
         : "s"(mask), "s"(m0v), "v"(voff), "s"(rsrc), "s"(so)
-        : "memory", "m0", "scc");
+        : "memory", "m0");
 }
 __device__ __forceinline__ void dma4(const uint8_t *lds_dst, uint32_t voff, u32x4 rsrc) {
     const uint32_t m0v = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void *)lds_dst);
