@@ -395,7 +395,7 @@ def layout_table(dev, reps: int) -> list[dict]:
     import torch
     import qconv_inputs as qi
     from paper_2202_06819_amd import qconv, sweep
-    layers = [qi.CONFIGS[1]()[0]] + [L for L in qi.distinct(qi.CONFIGS[2]()) if L.r == 3 and L.stride == 1]
+    layers = [qi.WORKLOADS[1]()[0]] + [L for L in qi.distinct(qi.WORKLOADS[2]()) if L.r == 3 and L.stride == 1]
     rows = []
     for lid, L in enumerate(layers):
         e = L.epilogue
@@ -545,7 +545,7 @@ def main() -> int:
     if not os.path.exists(hip_build.LIB):
         hip_build.build()
     dev = torch.device("cuda:0")
-    L = qi.config1()[0]
+    L = qi.workload1()[0]
     e = L.epilogue
     x, xp, wp, mult = layer_setup(1, 0, L, dev)
     tile = sweep.tuned_tile(L.desc()) if args.tile == -1 else args.tile
@@ -655,7 +655,7 @@ def main() -> int:
 
     tables = [] if args.tables == "none" else [int(v) for v in args.tables.split(",") if v]
     for cfg in tables:
-        layers = qi.CONFIGS[cfg]()
+        layers = qi.WORKLOADS[cfg]()
         log(f"workload {cfg}: per-layer ({len(qi.distinct(layers)) if cfg in (2, 3) else len(layers)} layers)")
         rows = per_layer_table(cfg, qi.distinct(layers) if cfg in (2, 3) else layers, dev, args.layer_reps)
         entry = {"per_layer": rows}

@@ -343,7 +343,7 @@ def _layers(workload: str):
     import qconv_inputs as qi
     if workload == "table1":
         return qi.table1_stages()
-    layers = qi.CONFIGS[int(workload)]()
+    layers = qi.WORKLOADS[int(workload)]()
     if int(workload) in (2, 3):
         layers = qi.distinct(layers)
     return [L for L in layers if L.r == 3 and L.stride == 1]

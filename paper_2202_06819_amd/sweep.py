@@ -178,7 +178,7 @@ def main(argv=None) -> int:
             fh.write(s + "\n")
             fh.flush()
         for cfg in args.workload:
-            layers = qi.CONFIGS[cfg]()
+            layers = qi.WORKLOADS[cfg]()
             if cfg in (2, 3):
                 layers = qi.distinct(layers)
             for lid, L in enumerate(layers):

@@ -4,8 +4,8 @@ This module holds no arithmetic of the method: it only draws integers and
 names shapes.  It is the one module both the GPU path's tests/benchmark and the
 CPU oracle's callers use, so that both sides see the same bytes.
 
-Every tensor of layer ``layer_id`` in workload ``config_id`` is drawn from
-``numpy.random.default_rng([config_id, layer_id, tensor_id])`` with tensor_id
+Every tensor of layer ``layer_id`` in workload ``workload_id`` is drawn from
+``numpy.random.default_rng([workload_id, layer_id, tensor_id])`` with tensor_id
 0 = activations (int8, N x C x H x W), 1 = filters (int8, K x C x R x S),
 2 = per-output-channel multipliers (int32, K).
 
@@ -84,8 +84,8 @@ class Layer:
                     bits=self.bits, x_signed=int(self.x_signed), w_signed=int(self.w_signed))
 
 
-def rng(config_id: int, layer_id: int, tensor_id: int) -> np.random.Generator:
-    return np.random.default_rng([config_id, layer_id, tensor_id])
+def rng(workload_id: int, layer_id: int, tensor_id: int) -> np.random.Generator:
+    return np.random.default_rng([workload_id, layer_id, tensor_id])
 
 
 def draw_int8(g: np.random.Generator, shape, lo: int, hi: int) -> np.ndarray:
@@ -93,24 +93,24 @@ def draw_int8(g: np.random.Generator, shape, lo: int, hi: int) -> np.ndarray:
     return g.integers(lo, hi + 1, size=shape, dtype=np.int64).astype(np.int8)
 
 
-def layer_tensors(config_id: int, layer_id: int, layer: Layer) -> dict:
+def layer_tensors(workload_id: int, layer_id: int, layer: Layer) -> dict:
     """x (N,C,H,W) int8, w (K,C,R,S) int8 and mult (K,) int32 for one layer."""
-    x = draw_int8(rng(config_id, layer_id, 0), (layer.n, layer.c, layer.h, layer.w), *layer.x_range)
-    w = draw_int8(rng(config_id, layer_id, 1), (layer.k, layer.c, layer.r, layer.s), *layer.w_range)
+    x = draw_int8(rng(workload_id, layer_id, 0), (layer.n, layer.c, layer.h, layer.w), *layer.x_range)
+    w = draw_int8(rng(workload_id, layer_id, 1), (layer.k, layer.c, layer.r, layer.s), *layer.w_range)
     out = {"x": x, "w": w, "mult": None}
     if layer.epilogue is not None:
         lo, hi = layer.epilogue.mult_range
-        out["mult"] = rng(config_id, layer_id, 2).integers(lo, hi, size=layer.k, dtype=np.int64).astype(np.int32)
+        out["mult"] = rng(workload_id, layer_id, 2).integers(lo, hi, size=layer.k, dtype=np.int64).astype(np.int32)
     return out
 
 
 # --------------------------------------------------------------------------- workloads
 
-def config0() -> list[Layer]:
+def workload0() -> list[Layer]:
     return [Layer("c0_56x56_64to64_3x3", 1, 56, 56, 64, 64, 3, 3, 1, 1, epilogue=None)]
 
 
-def config1() -> list[Layer]:
+def workload1() -> list[Layer]:
     return [Layer("c1_56x56_64to64_3x3_n8", 8, 56, 56, 64, 64, 3, 3, 1, 1)]
 
 
@@ -157,11 +157,11 @@ def _resnet18(n: int, bits: int) -> list[Layer]:
     return layers
 
 
-def config2() -> list[Layer]:
+def workload2() -> list[Layer]:
     return _resnet18(16, 4)
 
 
-def config3() -> list[Layer]:
+def workload3() -> list[Layer]:
     return _resnet18(16, 8)
 
 
@@ -179,7 +179,7 @@ def distinct(layers: list[Layer]) -> list[Layer]:
 BOTTLENECK_REPEATS = {56: 3, 28: 4, 14: 6, 7: 3}
 
 
-def config4() -> list[Layer]:
+def workload4() -> list[Layer]:
     """ResNet-50 bottleneck layers at N=64 (1x1 reduce, 3x3, 1x1 expand per stage), stride 1."""
     out = []
     for h, c_in, mid in ((56, 256, 64), (28, 512, 128), (14, 1024, 256), (7, 2048, 512)):
@@ -189,7 +189,7 @@ def config4() -> list[Layer]:
     return out
 
 
-CONFIGS = {0: config0, 1: config1, 2: config2, 3: config3, 4: config4}
+WORKLOADS = {0: workload0, 1: workload1, 2: workload2, 3: workload3, 4: workload4}
 
 
 def table1_layers(n: int = 8) -> list[Layer]:

@@ -180,7 +180,7 @@ def test_tile_table_is_consistent(q):
 
 
 def test_every_workload_layer_has_a_tile(q):
-    for cfg, make in qi.CONFIGS.items():
+    for cfg, make in qi.WORKLOADS.items():
         for L in make():
             tid = q.default_tile(L.desc())
             assert q.tile_status(L.desc(), tid) == 0

@@ -71,28 +71,28 @@ def test_pack_zero_size_is_noop():
 # ----------------------------------------------------------------- configs 0 and 1 at full size
 
 def test_config0_raw_every_tile():
-    L = qi.config0()[0]
+    L = qi.workload0()[0]
     t = qi.layer_tensors(0, 0, L)
     ref = ref_layer(L, t, requant=False)
     for tid in _valid_tiles(L):
-        announce(f"config0 raw tile {tid}")
+        announce(f"workload0 raw tile {tid}")
         got = gpu_layer(L, t, requant=False, tile=tid)
         assert_same(got["x_packed"], ref["x_packed"], "x packed")
         assert_same(got["w_packed"], ref["w_packed"], "w packed")
         assert_same(got["y"], ref["acc"], f"raw acc tile {tid}")
-        announce(f"config0 raw tile {tid} prepared filters")
+        announce(f"workload0 raw tile {tid} prepared filters")
         assert_same(gpu_layer(L, t, requant=False, tile=tid, prepared=True)["y"], ref["acc"], f"prepared tile {tid}")
 
 
 def test_config1_requant_every_tile():
-    L = qi.config1()[0]
+    L = qi.workload1()[0]
     t = qi.layer_tensors(1, 0, L)
     ref = ref_layer(L, t, requant=True)
     for tid in _valid_tiles(L):
-        announce(f"config1 requant tile {tid}")
+        announce(f"workload1 requant tile {tid}")
         got = gpu_layer(L, t, requant=True, tile=tid)
         assert_same(got["y"], ref["y_packed"], f"requant tile {tid}")
-        announce(f"config1 requant tile {tid} prepared filters")
+        announce(f"workload1 requant tile {tid} prepared filters")
         got = gpu_layer(L, t, requant=True, tile=tid, prepared=True)
         assert_same(got["y"], ref["y_packed"], f"requant tile {tid} prepared")
 
@@ -150,10 +150,10 @@ def test_persistent_plans_every_wide_tile(shape):
 
 
 def test_config1_raw_default_tile():
-    L = qi.config1()[0]
+    L = qi.workload1()[0]
     t = qi.layer_tensors(1, 0, L)
     ref = ref_layer(L, t, requant=False)
-    announce("config1 raw default tile")
+    announce("workload1 raw default tile")
     assert_same(gpu_layer(L, t, requant=False)["y"], ref["acc"], "raw acc")
 
 
@@ -258,7 +258,7 @@ def test_every_output_written_and_nothing_past_the_end():
 
 
 def test_run_twice_identical():
-    L = qi.config1()[0]
+    L = qi.workload1()[0]
     t = qi.layer_tensors(1, 0, L)
     announce("determinism")
     a = gpu_layer(L, t, requant=True)["y"]

@@ -19,7 +19,7 @@ def _torch():
 
 
 def _layers(cfg):
-    layers = qi.CONFIGS[cfg]()
+    layers = qi.WORKLOADS[cfg]()
     return list(enumerate(qi.distinct(layers) if cfg in (2, 3) else layers))
 
 
@@ -74,7 +74,7 @@ def test_chain_full_size(cfg, residual):
     import bench
     from paper_2202_06819_amd import nets, qconv
     dev = torch.device("cuda:0")
-    layers = qi.CONFIGS[cfg]()
+    layers = qi.WORKLOADS[cfg]()
     t0 = qi.layer_tensors(cfg, 0, layers[0])
     xp = qconv.pack(torch.from_numpy(t0["x"]).to(dev), layers[0].bits, layers[0].x_signed)
     plan = bench.residual_order(layers) if residual else [(L, L.src, None, i) for i, L in enumerate(layers)]

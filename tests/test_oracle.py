@@ -51,7 +51,7 @@ def test_table1_op_count():
         assert [n for n in range(1, 65) if 2 * n * p * q * ch * ch * r * s == gold["ops_per_conv"]] == [8]
     for L in qi.table1_layers(8):
         assert L.ops == gold["ops_per_conv"]
-    assert qi.config1()[0].ops == gold["ops_per_conv"]
+    assert qi.workload1()[0].ops == gold["ops_per_conv"]
 
 
 def test_out_dim_cases():
@@ -226,7 +226,7 @@ def test_accumulator_bound_is_enforced():
 def test_worst_case_accumulators_of_the_workloads_fit():
     """Largest |acc| any workload can reach stays below 2^31 (Sec. 3.2.1)."""
     for cfg in (2, 3, 4):
-        for L in qi.CONFIGS[cfg]():
+        for L in qi.WORKLOADS[cfg]():
             xm = max(abs(v) for v in L.x_range)
             wm = max(abs(v) for v in L.w_range)
             assert L.c * L.r * L.s * xm * wm < 2 ** 31
@@ -389,7 +389,7 @@ def test_saturate():
 # ----------------------------------------------------------------- the composed layer
 
 def test_qconv_layer_composes_the_steps():
-    L = qi.scaled(qi.config1()[0], n=1, h=9, w=11)
+    L = qi.scaled(qi.workload1()[0], n=1, h=9, w=11)
     t = qi.layer_tensors(1, 0, L)
     out = oracle.qconv_layer(t["x"], t["w"], bits=4, x_signed=False, w_signed=True,
                              stride=(1, 1), pad=(1, 1), mult=t["mult"], shift=20, relu=True, lo=0, hi=15)

@@ -99,7 +99,7 @@ def test_real_space_of_the_benchmark_layer():
     import qconv_inputs as qi
     if not os.path.exists(build.LIB):
         build.build()
-    L = qi.config1()[0]
+    L = qi.workload1()[0]
     space = S.ScheduleSpace.for_shape(L.desc())
     assert len(space) > 100
     rng = random.Random(3)
