@@ -319,19 +319,26 @@ def chain_time(cfg: int, layers, dev, reps: int, residual: bool = False) -> dict
         specs.append(nets.LayerSpec(L.desc(), wp, torch.from_numpy(t["mult"]).to(dev), e.shift, e.relu,
                                     (e.lo, e.hi), src=src, bias=bias, residual_src=short,
                                     residual_signed=e.lo < 0))
-    chain = nets.Chain(specs, xp)
-    for _ in range(3):
-        chain.forward()
-    eager = time_loop(chain.forward, reps)
-    out = {"layers": len(layers), "gops": round(sum(L.ops for L in layers) / 1e9, 3), "eager_us": round(eager, 2)}
-    try:
-        chain.capture()
+    out = {"layers": len(layers), "gops": round(sum(L.ops for L in layers) / 1e9, 3)}
+    best = None
+    # one stream, then the projection shortcuts on a second stream beside the strided 3x3s
+    for branches, tag in ((False, ""), (True, "branches_")):
+        chain = nets.Chain(specs, xp, branches=branches)
         for _ in range(3):
-            chain.replay()
-        out["graph_us"] = round(time_loop(chain.replay, reps), 2)
-    except Exception as exc:  # graph capture is an extra, report why it is missing
-        out["graph_error"] = str(exc)[:200]
-    best = min(out.get("graph_us", eager), eager)
+            chain.forward()
+        eager = time_loop(chain.forward, reps)
+        out[tag + "eager_us"] = round(eager, 2)
+        t = eager
+        try:
+            chain.capture()
+            for _ in range(3):
+                chain.replay()
+            out[tag + "graph_us"] = round(time_loop(chain.replay, reps), 2)
+            t = min(t, out[tag + "graph_us"])
+        except Exception as exc:  # graph capture is an extra, report why it is missing
+            out[tag + "graph_error"] = str(exc)[:200]
+        best = t if best is None else min(best, t)
+        del chain
     out["tops"] = round(sum(L.ops for L in layers) / (best * 1e-6) / 1e12, 2)
     return out
 

@@ -459,11 +459,13 @@ def test_bias_and_residual_every_tile(shape):
                     assert_same(y.cpu().numpy(), want, f"{name} tile {tid} case {ci} split 2")
 
 
-def test_residual_blocks_chain_eager_and_graph():
+@pytest.mark.parametrize("branches", [False, True], ids=["one_stream", "two_streams"])
+def test_residual_blocks_chain_eager_and_graph(branches):
     """Two basic residual blocks (conv-bias-ReLU, conv-bias-+shortcut-ReLU; the
     second block with a strided 1x1 projection shortcut), chained on the GPU
     with no relayout, eager and as replays of a captured graph, against the
-    oracle layer by layer."""
+    oracle layer by layer; with `branches` the projection runs on a second
+    stream."""
     torch, q = _torch(), _qconv()
     from paper_2202_06819_amd import nets
     dev = torch.device("cuda:0")
@@ -494,8 +496,9 @@ def test_residual_blocks_chain_eager_and_graph():
         specs.append(nets.LayerSpec(L.desc(), wp, torch.from_numpy(t["mult"]).to(dev), sh, True, (0, 15), src=src,
                                     bias=torch.from_numpy(bias).to(dev), residual_src=rsrc))
     xp = q.pack(torch.from_numpy(x).to(dev), 4, False)
-    chain = nets.Chain(specs, xp)
-    announce("residual chain eager")
+    chain = nets.Chain(specs, xp, branches=branches)
+    assert chain.on_side == [False, False, False, branches, False]
+    announce(f"residual chain eager, branches={branches}")
     outs = [o.clone() for o in chain.forward()]
     torch.cuda.synchronize()
     for (name, *_), o, ref in zip(spec, outs, refs):
@@ -504,7 +507,7 @@ def test_residual_blocks_chain_eager_and_graph():
     for i in range(3):
         for o in chain.outputs:
             o.zero_()
-        announce(f"residual chain replay {i}")
+        announce(f"residual chain replay {i}, branches={branches}")
         got = chain.replay()
         torch.cuda.synchronize()
         for (name, *_), o, ref in zip(spec, got, refs):

@@ -68,8 +68,9 @@ def test_workload_layers_full_size(cfg):
 @pytest.mark.parametrize("cfg,residual", [(2, False), (2, True), (3, False), (3, True)])
 def test_chain_full_size(cfg, residual):
     """The chained stack as bench.py builds it (inputs, biases, shortcut order),
-    every layer's output against the oracle fed with the oracle's own packed
-    outputs."""
+    on one stream and with the projections on a second stream (eager and as a
+    graph replay), every layer's output against the oracle fed with the
+    oracle's own packed outputs."""
     torch = _torch()
     import bench
     from paper_2202_06819_amd import nets, qconv
@@ -94,6 +95,16 @@ def test_chain_full_size(cfg, residual):
     chain = nets.Chain(specs, xp)
     outs = [o.cpu().numpy() for o in chain.forward()]
     torch.cuda.synchronize()
+    announce(f"chain workload {cfg} residual={residual}: projections on a second stream, eager and replayed")
+    chain_b = nets.Chain(specs, xp, branches=True)
+    assert sum(chain_b.on_side) == 3
+    outs_b = [o.cpu().numpy() for o in chain_b.forward()]
+    chain_b.capture()
+    for o in chain_b.outputs:
+        o.zero_()
+    chain_b.replay()
+    torch.cuda.synchronize()
+    outs_g = [o.cpu().numpy() for o in chain_b.outputs]
     x_packed = oracle.relayout_pack(t0["x"], layers[0].bits, layers[0].x_signed)
     ref_out = []
     for i, (L, src, short, t, bias) in enumerate(host):
@@ -109,3 +120,5 @@ def test_chain_full_size(cfg, residual):
                                  residual=res)
         ref_out.append(ref["y_packed"])
         assert_same(outs[i], ref["y_packed"], f"chain {cfg} layer {i} ({L.name})")
+        assert_same(outs_b[i], ref["y_packed"], f"chain {cfg} layer {i} ({L.name}), two streams")
+        assert_same(outs_g[i], ref["y_packed"], f"chain {cfg} layer {i} ({L.name}), two streams replayed")
