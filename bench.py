@@ -464,6 +464,60 @@ def layout_table(dev, reps: int) -> list[dict]:
     return rows
 
 
+def batch_table(dev, reps: int, batches=(16, 32, 64, 128, 256)) -> list[dict]:
+    """The four 4-bit 3x3 stride-1 layers of the ResNet-18 stack (fused
+    epilogue) at growing batch: the fastest (tile, split) of a short sweep per
+    batch, its time and fraction of the int8 MFMA peak.  Shows how much of a
+    launch is fixed cost (launch, prologue, epilogue) at batch 16."""
+    import torch
+    from paper_2202_06819_amd import qconv, sweep
+    import qconv_inputs as qi
+    shapes = [L for L in qi.distinct(qi.WORKLOADS[2]()) if L.r == 3 and L.stride == 1]
+    rows = []
+    for lid, L0 in enumerate(shapes):
+        e = L0.epilogue
+        for n in batches:
+            L = qi.Layer(L0.name, n, L0.h, L0.w, L0.c, L0.k, 3, 3, 1, 1)
+            t = qi.layer_tensors(41, lid, L)
+            d = L.desc()
+            xp = qconv.pack(torch.from_numpy(t["x"]).to(dev), L.bits, L.x_signed)
+            wp = qconv.pack(torch.from_numpy(t["w"]).to(dev), L.bits, L.w_signed)
+            mult = torch.from_numpy(t["mult"]).to(dev)
+            ref, best = None, None
+            for tt in qconv.tiles():
+                if qconv.tile_status(d, tt["id"]) != 0 or not tt["name"].startswith("wide"):
+                    continue
+                wprep = qconv.prepare_filters(d, wp, tt["id"])
+                for splits in sweep.split_choices(d, tt["id"]):
+                    ws = qconv.make_workspace(d, tt["id"], splits, dev)
+
+                    def make(stream=None, tid=tt["id"], splits=splits, wprep=wprep, ws=ws):
+                        return qconv.Conv2dCall(d, xp, wprep, requant=True, mult=mult, shift=e.shift, relu=e.relu,
+                                                clamp=(e.lo, e.hi), tile=tid, prepared=True, stream=stream,
+                                                splits=splits, workspace=ws)
+
+                    out = make()()
+                    torch.cuda.synchronize()
+                    if ref is None:
+                        ref = out.clone()
+                    elif not torch.equal(out, ref):
+                        raise RuntimeError(f"{L.name} n={n} tile {tt['name']} splits {splits}: output differs")
+                    g, _ = captured(lambda st: [make(st)], 20)
+                    us = time_graph(g, 3) * 1000.0 / 60
+                    if best is None or us < best[0]:
+                        best = (us, tt["name"], splits, make)
+            g, _ = captured(lambda st: [best[3](st)], reps)
+            us = time_graph(g, 3) * 1000.0 / (3 * reps)
+            tops = L.ops / (us * 1e-6) / 1e12
+            row = {"layer": L.name, "n": n, "gops": round(L.ops / 1e9, 3), "tile": best[1], "splits": best[2],
+                   "us": round(us, 3), "tops": round(tops, 1), "pct_int8_peak": round(100 * tops / INT8_PEAK_TOPS, 2)}
+            rows.append(row)
+            log(f"  {L.name:24s} N={n:3d} {us:8.2f} us {tops:7.1f} TOP/s {row['pct_int8_peak']:5.1f}%  "
+                f"tile {best[1]} splits {best[2]}")
+            del xp, wp, ref
+    return rows
+
+
 def fused_step_time(L, x, xp_ref, wp, mult, y_ref, dev, reps: int) -> dict:
     """The benchmark step as one launch: qconv2d_packing, the pack fused into
     the convolution, writing the packed input too.  The fastest tile of a
@@ -529,6 +583,8 @@ def main() -> int:
     ap.add_argument("--tables", default="2", help="comma list of workloads with per-layer tables (2,3,4) or 'none'")
     ap.add_argument("--layout-table", action="store_true",
                     help="also time the batch-interleaved layout against the plain one")
+    ap.add_argument("--batch-table", action="store_true",
+                    help="also time the 4-bit 3x3 stride-1 ResNet-18 layers at batch 16..256 (best tile each)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--tile", type=int, default=-1)
@@ -679,6 +735,10 @@ def main() -> int:
     if args.layout_table:
         log("layouts: plain NHWC vs batch-interleaved (nb images per pixel)")
         result["layouts"] = layout_table(dev, max(20, args.layer_reps // 4))
+
+    if args.batch_table:
+        log("batch scaling: 4-bit 3x3 stride-1 ResNet-18 layers, best tile per batch")
+        result["batch_scaling"] = batch_table(dev, max(20, args.layer_reps // 4))
 
     if not args.no_cpu:
         log(f"cpu baseline: oracle for ~{args.cpu_seconds:.0f} s ...")
