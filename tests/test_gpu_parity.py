@@ -783,3 +783,63 @@ def test_strided_bands_every_wide_tile(shape):
         announce(f"{name} tile {tid} prepared raw")
         assert_same(gpu_layer(L, t, requant=False, tile=tid, prepared=True)["y"], ref_raw["acc"],
                     f"{name} tile {tid} prepared raw")
+
+
+# ------------------------------------------------------------ persistent grids
+
+PIPE_CASES = [
+    # name, n, h, bits, relu, lo, hi  (n*h*h is not a multiple of any tile's pixels: a ragged last tile)
+    ("u4_relu_n33_55", 33, 55, 4, True, 0, 15),
+    ("s4_n33_55", 33, 55, 4, False, -8, 7),
+    ("s8_n33_55", 33, 55, 8, False, -128, 127),
+]
+
+
+@pytest.mark.parametrize("case", PIPE_CASES, ids=lambda c: c[0])
+def test_persistent_3x3_requant_every_tile(case):
+    """Persistent grids of single-chunk 3x3 layers with the requantising
+    epilogue: sized for one workgroup per CU, every workgroup walks several
+    tiles through both band buffers.  Every wide tile's output equals the
+    generic instance's byte for byte, and sampled pixels (with the ragged tail)
+    equal the oracle's; unsigned 4-bit, signed 4-bit and signed 8-bit outputs."""
+    torch, q = _torch(), _qconv()
+    name, n, h, bits, relu, lo, hi = case
+    signed = bits == 8
+    L = qi.Layer(name, n, h, h, 64, 64, 3, 3, 1, 1, bits=bits, x_signed=signed, w_signed=True,
+                 x_range=qi.S8 if signed else qi.U4, w_range=qi.S8 if signed else qi.S4)
+    t = qi.layer_tensors(970, bits, L)
+    sh = stress_shift(L, L.x_range, L.w_range)
+    d = L.desc()
+    dev = torch.device("cuda:0")
+    xp = q.pack(torch.from_numpy(t["x"]).to(dev), bits, signed)
+    wp = q.pack(torch.from_numpy(t["w"]).to(dev), bits, True)
+    kw = dict(requant=True, mult=torch.from_numpy(t["mult"]).to(dev), shift=sh, relu=relu, clamp=(lo, hi))
+    announce(f"{name}: generic instance")
+    ref = q.conv2d(d, xp, wp, **kw)
+    torch.cuda.synchronize()
+    ref_np = ref.cpu().numpy()
+    # the oracle at sampled pixels, the last ones included
+    m = n * h * h
+    g = np.random.default_rng(971)
+    pix = np.unique(np.concatenate([g.choice(m, 96, replace=False), np.arange(m - 8, m)])).astype(np.int64)
+    acc = oracle.conv2d(t["x"].transpose(0, 2, 3, 1), t["w"].transpose(0, 2, 3, 1), (1, 1), (1, 1), pixels=pix)
+    want = oracle.requant(acc, t["mult"], sh, relu, lo, hi)
+    got_ref = oracle.unpack_tensor(ref_np, 64, bits, lo < 0).reshape(m, 64)[pix]
+    assert np.array_equal(got_ref, want), f"{name}: generic instance differs from the oracle"
+    ran = 0
+    for tt in q.tiles():
+        if not tt["name"].startswith("wide") or q.tile_status(d, tt["id"]) != 0 or 64 % tt["tile_k"]:
+            continue
+        tiles = -(-m // tt["tile_p"]) * (64 // tt["tile_k"])
+        assert tiles > 256, "the grid of one workgroup per CU must be persistent"
+        wprep = q.prepare_filters(d, wp, tt["id"])
+        announce(f"{name}: tile {tt['name']}, one workgroup per CU, {tiles} tiles")
+        y = q.Conv2dCall(d, xp, wprep, tile=tt["id"], prepared=True,
+                         schedule={"tile_id": tt["id"], "wg_per_cu": 1}, **kw)()
+        torch.cuda.synchronize()
+        y_np = y.cpu().numpy()
+        assert_same(y_np, ref_np, f"{name} tile {tt['name']}")
+        got = oracle.unpack_tensor(y_np, 64, bits, lo < 0).reshape(m, 64)[pix]
+        assert np.array_equal(got, want), f"{name} tile {tt['name']}: sampled pixels differ from the oracle"
+        ran += 1
+    assert ran >= 3
