@@ -238,11 +238,13 @@ def per_layer_table(cfg: int, layers, dev, reps: int) -> list[dict]:
             call()
         eager_us = time_loop(call, reps)
         g, _ = captured(lambda s: [make(s)], reps)
-        us = time_graph(g, 3) * 1000.0 / (3 * reps)
+        # per-launch time of each of 5 replays of the reps-launch graph: median and min
+        per = sorted(time_graph(g, 1) * 1000.0 / reps for _ in range(5))
+        us, us_min = per[2], per[0]
         tops = L.ops / (us * 1e-6) / 1e12
         nbytes = layer_bytes(L)
         row = {"layer": L.name, "tile": qconv.tiles()[call.tile]["name"], "splits": splits, "us": round(us, 3),
-               "eager_us": round(eager_us, 3),
+               "us_min": round(us_min, 3), "eager_us": round(eager_us, 3),
                "tops": round(tops, 2), "pct_int8_peak": round(100 * tops / INT8_PEAK_TOPS, 2),
                "gops": round(L.ops / 1e9, 4), "alg_bytes": nbytes,
                "gbs": round(nbytes / (us * 1e-6) / 1e9, 1)}
@@ -341,6 +343,56 @@ def chain_time(cfg: int, layers, dev, reps: int, residual: bool = False) -> dict
         del chain
     out["tops"] = round(sum(L.ops for L in layers) / (best * 1e-6) / 1e12, 2)
     return out
+
+
+def bottleneck_stack_time(dev, reps: int) -> dict:
+    """The ResNet-50 bottleneck stack of workload 4 with its block counts
+    (3, 4, 6, 3 blocks at 56, 28, 14, 7): per stage, the blocks chained (1x1
+    reduce, 3x3, 1x1 expand, the expand's output feeding the next block's
+    reduce), each stage timed end to end eager and as a graph replay.  The
+    stages' first blocks keep the repeated blocks' shapes (no strided entry
+    block, no projection shortcut, no residual add): a bottleneck stack, not a
+    full ResNet-50."""
+    import torch
+    import qconv_inputs as qi
+    from paper_2202_06819_amd import nets, qconv
+    layers = qi.WORKLOADS[4]()
+    stages, total_eager, total_graph, total_ops = [], 0.0, 0.0, 0
+    for st in range(4):
+        red, mid, exp = layers[3 * st: 3 * st + 3]
+        blocks = qi.BOTTLENECK_REPEATS[red.h]
+        t0 = qi.layer_tensors(4, 3 * st, red)
+        xp = qconv.pack(torch.from_numpy(t0["x"]).to(dev), red.bits, red.x_signed)
+        specs = []
+        for b in range(blocks):
+            for j, L in enumerate((red, mid, exp)):
+                t = t0 if j == 0 else qi.layer_tensors(4, 3 * st + j, L)
+                e = L.epilogue
+                src = len(specs) - 1
+                specs.append(nets.LayerSpec(L.desc(), qconv.pack(torch.from_numpy(t["w"]).to(dev), L.bits, L.w_signed),
+                                            torch.from_numpy(t["mult"]).to(dev), e.shift, e.relu, (e.lo, e.hi),
+                                            src=src))
+        chain = nets.Chain(specs, xp)
+        for _ in range(3):
+            chain.forward()
+        eager = time_loop(chain.forward, reps)
+        chain.capture()
+        for _ in range(3):
+            chain.replay()
+        graph = time_loop(chain.replay, reps)
+        ops = blocks * (red.ops + mid.ops + exp.ops)
+        stages.append({"stage": f"{red.h}x{red.h}", "blocks": blocks, "layers": 3 * blocks,
+                       "gops": round(ops / 1e9, 3), "eager_us": round(eager, 2), "graph_us": round(graph, 2),
+                       "tops": round(ops / (min(eager, graph) * 1e-6) / 1e12, 1)})
+        total_eager += eager
+        total_graph += graph
+        total_ops += ops
+        del chain
+    best = min(total_eager, total_graph)
+    return {"stack": "ResNet-50 bottleneck blocks 3/4/6/3, N=64, 4-bit, stride 1 (not a full ResNet-50)",
+            "layers": sum(s["layers"] for s in stages), "gops": round(total_ops / 1e9, 2),
+            "eager_us": round(total_eager, 1), "graph_us": round(total_graph, 1),
+            "tops": round(total_ops / (best * 1e-6) / 1e12, 1), "stages": stages}
 
 
 def stem_time(dev, n: int, reps: int) -> dict:
@@ -730,6 +782,9 @@ def main() -> int:
         if cfg == 3:
             entry["stem"] = stem_time(dev, 16, max(20, args.layer_reps // 4))
             log(f"  stem: {entry['stem']}")
+        if cfg == 4:
+            entry["bottleneck_stack"] = bottleneck_stack_time(dev, max(10, args.layer_reps // 10))
+            log(f"  bottleneck stack: {entry['bottleneck_stack']}")
         result[f"workload{cfg}"] = entry
 
     if args.layout_table:
