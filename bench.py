@@ -626,6 +626,38 @@ def cpu_baseline(L, seconds: float, threads: int | None = None) -> dict:
                       f"requant, repack) in {el:.1f} s on {threads} OpenMP thread{'s' if threads > 1 else ''}"}
 
 
+def cpu_network_times(cfgs, single_thread_cfgs) -> dict:
+    """The oracle, as it stands, over every layer of whole workloads (each
+    layer once: relayout+pack, direct conv, requant, repack), per layer and
+    per network in seconds, on all host threads and, for `single_thread_cfgs`,
+    on one thread.  A reported baseline for the per-network GPU times."""
+    import oracle
+    import qconv_inputs as qi
+    out = {}
+    for cfg in cfgs:
+        layers = qi.WORKLOADS[cfg]()
+        modes = [oracle.max_threads()] + ([1] if cfg in single_thread_cfgs else [])
+        entry = {"layers": len(layers), "gops": round(sum(L.ops for L in layers) / 1e9, 3)}
+        for th in modes:
+            per, total = [], 0.0
+            for lid, L in enumerate(layers):
+                t = qi.layer_tensors(cfg, lid, L)
+                e = L.epilogue
+                t0 = time.perf_counter()
+                oracle.qconv_layer(t["x"], t["w"], bits=L.bits, x_signed=L.x_signed, w_signed=L.w_signed,
+                                   stride=(L.stride, L.stride), pad=(L.pad, L.pad), mult=t["mult"], shift=e.shift,
+                                   relu=e.relu, lo=e.lo, hi=e.hi, threads=th)
+                el = time.perf_counter() - t0
+                per.append({"layer": L.name, "s": round(el, 4)})
+                total += el
+            key = "all_threads" if th > 1 else "one_thread"
+            entry[key] = {"threads": th, "network_s": round(total, 3),
+                          "tops": round(sum(L.ops for L in layers) / total / 1e12, 5), "per_layer": per}
+            log(f"  oracle, workload {cfg}, {th} thread{'s' if th > 1 else ''}: {total:.2f} s")
+        out[f"workload{cfg}"] = entry
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -638,6 +670,8 @@ def main() -> int:
     ap.add_argument("--batch-table", action="store_true",
                     help="also time the 4-bit 3x3 stride-1 ResNet-18 layers at batch 16..256 (best tile each)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cpu-networks", action="store_true",
+                    help="also time the oracle over every layer of workloads 2 and 4 (per layer and per network)")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--tile", type=int, default=-1)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -801,6 +835,8 @@ def main() -> int:
         one = cpu_baseline(L, max(1.0, args.cpu_seconds / 3), threads=1)
         result["cpu_baseline"]["single_core"] = {"value": one["value"], "unit": one["unit"], "sample": one["sample"]}
         log(f"  {result['cpu_baseline']}")
+        if args.cpu_networks:
+            result["cpu_baseline"]["networks"] = cpu_network_times((2, 4), single_thread_cfgs=(2,))
     print(json.dumps(result), flush=True)
     return 0
 
