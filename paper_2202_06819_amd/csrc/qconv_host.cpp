@@ -8,6 +8,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <initializer_list>
 #include <mutex>
 #include <string>
 #include <unordered_map>
@@ -42,6 +43,18 @@ int64_t out_dim(int64_t in, int64_t win, int64_t stride, int64_t pad) {
     return span / stride + 1;
 }
 
+// Product of non-negative factors, saturated at 2^62 so that a descriptor
+// with huge dimensions cannot wrap its size checks.
+int64_t mul_sat(std::initializer_list<int64_t> fs) {
+    constexpr int64_t kCap = (int64_t)1 << 62;
+    int64_t r = 1;
+    for (int64_t f : fs) {
+        if (f != 0 && r > kCap / f) return kCap;
+        r *= f;
+    }
+    return r;
+}
+
 int64_t max_abs(int bits, int is_signed) {
     if (bits == 4) return is_signed ? 8 : 15;
     return is_signed ? 128 : 255;
@@ -72,13 +85,14 @@ int check_desc(const qconv_desc *d, qconv_layout_info *info) {
     if (d->bits == 8 && (!d->x_signed || !d->w_signed))
         return fail(QCONV_EUNSUPPORTED, "8-bit operands must be signed (the int8 MFMA is signed)");
     const int64_t bits = d->bits;
-    const int64_t m = (int64_t)d->n * p * q;
-    const int64_t x_bytes = (int64_t)d->n * d->h * d->w * d->c * bits / 8;
-    const int64_t w_bytes = (int64_t)d->k * d->r * d->s * d->c * bits / 8;
-    const int64_t y_raw = m * d->k * 4;
-    const int64_t y_packed = m * d->k * bits / 8;
+    const int64_t m = mul_sat({d->n, p, q});
+    const int64_t x_bytes = mul_sat({d->n, d->h, d->w, d->c, bits}) / 8;
+    const int64_t w_bytes = mul_sat({d->k, d->r, d->s, d->c, bits}) / 8;
+    const int64_t y_raw = mul_sat({m, d->k, 4});
     if (x_bytes >= kMaxBytes || w_bytes >= kMaxBytes || y_raw >= kMaxBytes)
         return fail(QCONV_EUNSUPPORTED, "tensors must stay below 2 GiB (32-bit indexing)");
+    // every product below is now far from overflowing
+    const int64_t y_packed = m * d->k * bits / 8;
     const int64_t depth = (int64_t)d->c * d->r * d->s;
     const int64_t worst = depth * max_abs(d->bits, d->x_signed) * max_abs(d->bits, d->w_signed);
     if (worst >= ((int64_t)1 << 31))
@@ -417,7 +431,7 @@ int qconv_pack_interleaved(const int8_t *src, void *dst, int32_t n, int32_t c, i
     if (bits != 4 && bits != 8) return fail(QCONV_EUNSUPPORTED, "bits must be 4 or 8 (got %d)", bits);
     if (bits == 4 && c % 8) return fail(QCONV_EUNSUPPORTED, "4-bit packing needs c %% 8 == 0 (c=%d)", c);
     if (bits == 8 && !is_signed) return fail(QCONV_EUNSUPPORTED, "8-bit values are signed");
-    const int64_t count = (int64_t)n * c * h * w;
+    const int64_t count = mul_sat({n, c, h, w});
     if (count == 0) return QCONV_OK;
     if (count >= kMaxBytes) return fail(QCONV_EUNSUPPORTED, "tensor must stay below 2^31 values");
     if (!src || !dst) return fail(QCONV_EINVAL, "src and dst must be non-NULL");
@@ -867,8 +881,11 @@ int qconv_unroll(const int8_t *src, int8_t *dst, int32_t n, int32_t c, int32_t h
     const int64_t span = (int64_t)w + 2 * pad_w - taps_w;
     if (span < 0) return fail(QCONV_EINVAL, "filter width larger than the padded input");
     const int64_t wout = span / stride_w + 1;
-    const int64_t in_bytes = (int64_t)n * c * h * w, out_bytes = (int64_t)n * out_h * wout * c_out;
+    const int64_t in_bytes = mul_sat({n, c, h, w}), out_bytes = mul_sat({n, out_h, wout, c_out});
     if (out_bytes == 0) return QCONV_OK;
+    if (in_bytes >= ((int64_t)1 << 62) || out_bytes >= ((int64_t)1 << 62) ||
+        (int64_t)out_h * stride_h + taps_h >= (1ll << 31) || (int64_t)w + 2ll * pad_w >= (1ll << 31))
+        return fail(QCONV_EUNSUPPORTED, "unroll sizes out of range");
     if (!dst || (in_bytes > 0 && !src)) return fail(QCONV_EINVAL, "src and dst must be non-NULL");
     if (!aligned16(dst)) return fail(QCONV_EINVAL, "dst must be 16-byte aligned");
     if (in_bytes > 0 && (uintptr_t)src < (uintptr_t)dst + out_bytes && (uintptr_t)dst < (uintptr_t)src + in_bytes)

@@ -85,6 +85,9 @@ def test_layout_sizes(q):
     (dict(bits=8, x_signed=0), -2), (dict(bits=8, x_signed=1, c=6), -2),
     (dict(c=4096, r=7, s=7, x_signed=1), -2),           # accumulator bound with the widening factor
     (dict(bits=8, x_signed=1, c=131072, r=1, s=1), -2), # 128*128*2^17 = 2^31
+    # dimensions whose byte counts wrap 64 bits are rejected as too large
+    (dict(n=1 << 30, h=1 << 30, w=1 << 30, c=64, r=1, s=1, pad_h=0, pad_w=0), -2),
+    (dict(n=1 << 30, h=1 << 20, w=1 << 20, c=8, k=8, r=1, s=1, pad_h=0, pad_w=0), -2),
 ])
 def test_descriptor_errors(q, kw, status):
     with pytest.raises(q.QConvError) as e:
@@ -155,6 +158,8 @@ def test_pack_errors(q):
     assert L.qconv_pack(4096, 4096 + 64, 1, 16, 4, 4, 4, 0, None) == -1   # overlap
     assert L.qconv_pack(4096, 8194, 1, 16, 4, 4, 4, 0, None) == -1        # dst misaligned
     assert L.qconv_pack(0, 0, 0, 16, 4, 4, 4, 0, None) == 0               # empty: no-op
+    # sizes whose product wraps 64 bits (2^30 * 2^30 * 2^8 * 2^28 = 2^96) are too large, not small
+    assert L.qconv_pack(4096, 1 << 40, 1 << 30, 1 << 30, 1 << 8, 1 << 28, 4, 0, None) == -2
 
 
 def test_strerror_and_last_error(q):
@@ -370,6 +375,9 @@ def test_unroll_argument_errors(q):
     assert call(None, dst, 1, 3, 8, 8, rows, (7, 2, 3), 32) == -1         # NULL source of a non-empty input
     assert call(src, dst, 1, 64, 8, 4000, (8, 1, 0, 8), (1, 1, 0), 512) == -2   # stages more than 64 KiB per row
     assert call(None, None, 0, 3, 8, 8, rows, (7, 2, 3), 32) == 0         # empty: no-op
+    # row arithmetic and byte counts that would leave 32 (or wrap 64) bits
+    assert call(src, dst, 1, 3, 8, 8, (1, 1 << 20, 0, 1 << 12), (7, 2, 3), 32) == -2
+    assert call(src, dst, 1 << 30, 16, 1 << 30, 64, (1, 1, 0, 1 << 30), (1, 1, 0), 16) == -2
     assert call(src, None, 1, 3, 8, 8, (1, 1, 0, 0), (7, 2, 3), 32) == 0  # no output rows: no-op
 
 
