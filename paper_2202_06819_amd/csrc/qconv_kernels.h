@@ -1244,7 +1244,8 @@ static hipError_t launch_prep(const ConvArgs &a, uint8_t *img, int64_t elems, hi
     X(8, 2, 2, 4, 4, 64) \
     X(8, 2, 4, 4, 4, 64) \
     X(8, 1, 4, 4, 4, 64) \
-    X(4, 8, 1, 2, 4, 128)
+    X(4, 8, 1, 2, 4, 128) \
+    X(4, 4, 2, 2, 2, 128)
 #define QCONV_WIDE_TILES(X) QCONV_WIDE_TILES_A(X) QCONV_WIDE_TILES_B(X) QCONV_WIDE_TILES_C(X) QCONV_WIDE_TILES_D(X)
 #define QCONV_TILE_INFO(V, PREFIX, B, WP, WK, FP, FK, CK, XS, WS)                                                 \
     {0, B, WP, WK, FP, FK, CK, WP * FP * 16, WK * FK * 16, WP * WK * 64, V, XS, WS,                              \
