@@ -43,18 +43,37 @@ def log(msg: str) -> None:
     print(msg, file=sys.stderr, flush=True)
 
 
-KERNEL_SOURCES = ("qconv_kernels.h", "qconv_conv.hip", "qconv_tiles_b.hip", "qconv_tiles_c.hip", "qconv_tiles_d.hip",
-                  "qconv_device.h", "qconv_internal.h", "qconv_host.cpp", "qconv_pack.hip")
+# measurement aids, not kernels of the path: their sources do not enter the kernel digest
+NOT_KERNEL_SOURCES = ("qconv_probe.hip", "qconv_unroll.hip")
 
 
 def kernel_digest(tile_name: str) -> str:
-    """Digest of the kernel sources and the tile: HBM traffic counters taken
-    for another digest describe another kernel and are not reported."""
+    """Digest of the kernel sources and the tile: profiler summaries taken for
+    another digest describe another kernel and are not reported."""
     h = hashlib.sha256(tile_name.encode())
-    for f in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, "paper_2202_06819_amd", "csrc", f), "rb") as fh:
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2202_06819_amd", "csrc", "*"))):
+        if os.path.basename(f) in NOT_KERNEL_SOURCES:
+            continue
+        with open(f, "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
+
+
+def profile_values(kind: str, workload: str, tile_name: str) -> dict | None:
+    """The machine-readable lines (`- key: value`) of the committed rocprofv3
+    summary profiles/*_<kind>.md of this workload, or None when there is none
+    for the current kernel sources and tile."""
+    digest = kernel_digest(tile_name)
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", f"*_{kind}.md"))):
+        kv = {}
+        for line in open(path):
+            if line.startswith("- ") and ": " in line:
+                k, v = line[2:].split(": ", 1)
+                kv[k.strip()] = v.strip().strip("`")
+        if kv.get("workload") == workload and kv.get("kernel_digest") == digest:
+            kv["file"] = os.path.relpath(path, ROOT)
+            return kv
+    return None
 
 
 def measured_traffic(workload: str, tile_name: str):
@@ -62,19 +81,26 @@ def measured_traffic(workload: str, tile_name: str):
     FETCH_SIZE / WRITE_SIZE summary of this workload (each counter divided by
     what it reads per byte of a plain copy kernel), or None when there is no
     summary for the current kernel sources and tile."""
-    digest = kernel_digest(tile_name)
-    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*_traffic.md"))):
-        kv = {}
-        for line in open(path):
-            if line.startswith("- ") and ": " in line:
-                k, v = line[2:].split(": ", 1)
-                kv[k.strip()] = v.strip().strip("`")
-        if kv.get("workload") == workload and kv.get("kernel_digest") == digest:
-            try:
-                return int(float(kv["hbm_bytes_per_launch"]))
-            except (KeyError, ValueError):
-                return None
-    return None
+    kv = profile_values("traffic", workload, tile_name)
+    try:
+        return int(float(kv["hbm_bytes_per_launch"])) if kv else None
+    except (KeyError, ValueError):
+        return None
+
+
+def launch_floor(dev, grids, reps: int = 200) -> list[dict]:
+    """Per-launch time of an empty kernel (qconv_probe_launch) over each
+    (workgroups, threads, dynamic LDS) grid, back to back in a replayed graph
+    (median and min of five replays)."""
+    from paper_2202_06819_amd import qconv
+    rows = []
+    for blocks, threads, lds in grids:
+        g, calls = captured(lambda s: [qconv.ProbeLaunchCall(blocks, threads, lds, s)], reps)
+        per = sorted(time_graph(g, 1) * 1000.0 / reps for _ in range(5))
+        rows.append({"blocks": blocks, "threads": threads, "lds_bytes": lds, "graph_us": round(per[2], 3),
+                     "graph_us_min": round(per[0], 3)})
+        del g
+    return rows
 
 
 def copy_calibration(mib: int, reps: int) -> int:
@@ -266,6 +292,12 @@ def per_layer_table(cfg: int, layers, dev, reps: int) -> list[dict]:
     return rows
 
 
+def qi_shape(layers, name: str) -> str:
+    """A layer's shape as text: 56x56 64->64 3x3 s1."""
+    L = next(L for L in layers if L.name == name)
+    return f"{L.h}x{L.w} {L.c}->{L.k} {L.r}x{L.s} s{L.stride}"
+
+
 def residual_order(layers):
     """The ResNet-18 stack as residual blocks: each block's second 3x3 adds its
     shortcut (the block input, or the stage's 1x1 projection, which is moved
@@ -323,9 +355,12 @@ def chain_time(cfg: int, layers, dev, reps: int, residual: bool = False) -> dict
                                     residual_signed=e.lo < 0))
     out = {"layers": len(layers), "gops": round(sum(L.ops for L in layers) / 1e9, 3)}
     best = None
-    # one stream, then the projection shortcuts on a second stream beside the strided 3x3s
-    for branches, tag in ((False, ""), (True, "branches_")):
-        chain = nets.Chain(specs, xp, branches=branches)
+    # one stream with each stage's projection fused into its strided 3x3 (the
+    # chain's default), then unfused on one stream, then the projections on a
+    # second stream beside the strided 3x3s
+    for kw, tag in ((dict(), ""), (dict(fuse_projections=False), "unfused_"), (dict(branches=True), "branches_")):
+        chain = nets.Chain(specs, xp, **kw)
+        out[tag + "launches"] = chain.launches
         for _ in range(3):
             chain.forward()
         eager = time_loop(chain.forward, reps)
@@ -339,10 +374,65 @@ def chain_time(cfg: int, layers, dev, reps: int, residual: bool = False) -> dict
             t = min(t, out[tag + "graph_us"])
         except Exception as exc:  # graph capture is an extra, report why it is missing
             out[tag + "graph_error"] = str(exc)[:200]
-        best = t if best is None else min(best, t)
+        if not tag:
+            best = t
         del chain
     out["tops"] = round(sum(L.ops for L in layers) / (best * 1e-6) / 1e12, 2)
     return out
+
+
+def proj_table(cfg: int, layers, dev, reps: int) -> list[dict]:
+    """Each stage entry of a ResNet-18 stack (strided 3x3 and its 1x1
+    projection, which read the same block input) as one fused launch
+    (qconv2d_proj, tuned tile), against the two layers' separate launches."""
+    import torch
+    import qconv_inputs as qi
+    from paper_2202_06819_amd import qconv, sweep
+    names = [L.name for L in layers]
+    rows = []
+    for i, L in enumerate(layers):
+        if not (L.name.endswith(".0.conv1") and L.stride == 2):
+            continue
+        j = names.index(L.name.replace("conv1", "downsample"))
+        P = layers[j]
+        t, tp = qi.layer_tensors(cfg, i, L), qi.layer_tensors(cfg, j, P)
+        xp = qconv.pack(torch.from_numpy(t["x"]).to(dev), L.bits, L.x_signed)
+        w3 = qconv.pack(torch.from_numpy(t["w"]).to(dev), L.bits, L.w_signed)
+        w1 = qconv.pack(torch.from_numpy(tp["w"]).to(dev), P.bits, P.w_signed)
+        m3, m1 = torch.from_numpy(t["mult"]).to(dev), torch.from_numpy(tp["mult"]).to(dev)
+        e, ep = L.epilogue, P.epilogue
+        tile = sweep.tuned_proj_tile(L.desc())
+        wprep = qconv.prepare_filters_proj(L.desc(), w3, w1, tile)
+
+        def make(stream=None):
+            return qconv.ProjConv2dCall(L.desc(), xp, wprep, tile=tile, requant=True, mult=m3, shift=e.shift,
+                                        relu=e.relu, clamp=(e.lo, e.hi),
+                                        proj=dict(mult=m1, shift=ep.shift, relu=ep.relu, clamp=(ep.lo, ep.hi)),
+                                        stream=stream)
+
+        g, _ = captured(lambda s: [make(s)], reps)
+        per = sorted(time_graph(g, 1) * 1000.0 / reps for _ in range(5))
+        sep = []
+        for lay, tt, wpk, mm in ((L, t, w3, m3), (P, tp, w1, m1)):
+            tl, sp = sweep.tuned_config(lay.desc())
+            wpr = qconv.prepare_filters(lay.desc(), wpk, tl)
+            ws = qconv.make_workspace(lay.desc(), tl, sp, dev)
+            ee = lay.epilogue
+
+            def mk(stream=None, lay=lay, wpr=wpr, tl=tl, sp=sp, ws=ws, mm=mm, ee=ee):
+                return qconv.Conv2dCall(lay.desc(), xp, wpr, requant=True, mult=mm, shift=ee.shift, relu=ee.relu,
+                                        clamp=(ee.lo, ee.hi), tile=tl, prepared=True, splits=sp, workspace=ws,
+                                        stream=stream)
+            gs, _ = captured(lambda s, mk=mk: [mk(s)], reps)
+            sep.append(sorted(time_graph(gs, 1) * 1000.0 / reps for _ in range(5))[2])
+        ops = L.ops + P.ops
+        rows.append({"layers": f"{L.name} + {P.name}", "tile": qconv.tiles()[tile]["name"],
+                     "fused_us": round(per[2], 3), "separate_us": round(sum(sep), 3),
+                     "conv3x3_us": round(sep[0], 3), "proj_us": round(sep[1], 3),
+                     "gops": round(ops / 1e9, 4), "tops": round(ops / (per[2] * 1e-6) / 1e12, 2)})
+        log(f"  fused {L.name} + {P.name}: {per[2]:.2f} us vs {sum(sep):.2f} us as two launches "
+            f"(tile {rows[-1]['tile']})")
+    return rows
 
 
 def bottleneck_stack_time(dev, reps: int) -> dict:
@@ -664,7 +754,10 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=2000)
     ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--layer-reps", type=int, default=200, help="repetitions per layer in the per-layer tables")
-    ap.add_argument("--tables", default="2", help="comma list of workloads with per-layer tables (2,3,4) or 'none'")
+    ap.add_argument("--tables", default="2,3,4",
+                    help="comma list of workloads with per-layer tables (2,3,4) or 'none'")
+    ap.add_argument("--launch-floor", action="store_true",
+                    help="also time the empty-kernel launch probe over a range of grid shapes")
     ap.add_argument("--layout-table", action="store_true",
                     help="also time the batch-interleaved layout against the plain one")
     ap.add_argument("--batch-table", action="store_true",
@@ -691,8 +784,7 @@ def main() -> int:
     from paper_2202_06819_amd import build as hip_build
     from paper_2202_06819_amd import qconv, sweep
 
-    if not os.path.exists(hip_build.LIB):
-        hip_build.build()
+    hip_build.ensure_built()   # rebuilds when the library is missing or older than its sources
     dev = torch.device("cuda:0")
     L = qi.workload1()[0]
     e = L.epilogue
@@ -771,6 +863,11 @@ def main() -> int:
     workload = (f"conv2d n{L.n} {L.h}x{L.w} {L.c}->{L.k} {L.r}x{L.s} stride {L.stride} pad {L.pad}, "
                 f"{L.bits}-bit, fused requant+repack")
     traffic = measured_traffic(workload, tile_name)
+    stats = profile_values("kernel_stats", workload, tile_name)
+    conv()
+    geo = qconv.last_launch()
+    torch.cuda.synchronize()
+    floor = launch_floor(dev, [(geo["grid"], geo["threads"], 0)])[0]
     result = {
         "metric": METRIC,
         "value": round(value, 3),
@@ -800,7 +897,19 @@ def main() -> int:
                     "pack_cold_gbs": round(pack_bytes / (pack_cold_us * 1e-6) / 1e9, 1), "pack_cold_copies": n_cp,
                     "fused_step": fused},
         "mfma_probe": probe,
+        "launch_floor": {"grid": floor, "note": "empty kernel over the conv kernel's grid (qconv_probe_launch)"},
+        "build": {"source_digest": hip_build.source_digest(), "library_digest": qconv.build_digest()},
     }
+    if stats:
+        # the committed kernel-trace summary of this kernel (same sources and tile): its
+        # average over the dispatches that started back to back (< 1 us after the
+        # previous one ended, as in the timed graph), and over all of them (the
+        # tracer's own gaps between dispatches slow the kernel that follows)
+        pavg = float(stats["conv_avg_ns_back_to_back"]) / 1000.0
+        result["roofline"].update({"profile_avg_us": round(pavg, 3),
+                                   "profile_frac": round(L.ops / (pavg * 1e-6) / 1e12 / INT8_PEAK_TOPS, 5),
+                                   "profile_avg_us_all_dispatches": round(float(stats["conv_avg_ns"]) / 1000.0, 3),
+                                   "profile": stats["file"]})
 
     tables = [] if args.tables == "none" else [int(v) for v in args.tables.split(",") if v]
     for cfg in tables:
@@ -809,6 +918,7 @@ def main() -> int:
         rows = per_layer_table(cfg, qi.distinct(layers) if cfg in (2, 3) else layers, dev, args.layer_reps)
         entry = {"per_layer": rows}
         if cfg in (2, 3):
+            entry["proj_fused"] = proj_table(cfg, layers, dev, args.layer_reps)
             entry["chain"] = chain_time(cfg, layers, dev, max(20, args.layer_reps // 4))
             log(f"  chained network: {entry['chain']}")
             entry["chain_residual"] = chain_time(cfg, layers, dev, max(20, args.layer_reps // 4), residual=True)
@@ -820,6 +930,23 @@ def main() -> int:
             entry["bottleneck_stack"] = bottleneck_stack_time(dev, max(10, args.layer_reps // 10))
             log(f"  bottleneck stack: {entry['bottleneck_stack']}")
         result[f"workload{cfg}"] = entry
+        if cfg == 2:
+            # the stated goal: the batch-16 4-bit 3x3 stride-1 layers at >= 50 % of the int8 peak
+            tgt = [r for r in rows if "3x3" in qi_shape(layers, r["layer"]) and "s1" in qi_shape(layers, r["layer"])]
+            result["target"] = {
+                "what": "ResNet-18 4-bit 3x3 stride-1 layers at N=16, % of the 5.0 POP/s dense int8 peak",
+                "goal_pct": 50.0,
+                "layers": [{"layer": r["layer"], "shape": qi_shape(layers, r["layer"]), "us": r["us"],
+                            "tops": r["tops"], "pct_int8_peak": r["pct_int8_peak"]} for r in tgt],
+                "met": all(r["pct_int8_peak"] >= 50.0 for r in tgt) if tgt else False,
+            }
+            if "chain" in entry:
+                result["target"]["chain_graph_us"] = entry["chain"].get("graph_us")
+
+    if args.launch_floor:
+        log("launch floor: empty kernel, back to back in a replayed graph")
+        result["launch_floor"]["sweep"] = launch_floor(dev, [(b, t, l) for b in (196, 256, 512, 1024, 2048)
+                                                             for t in (256, 512) for l in (0, 48 << 10)])
 
     if args.layout_table:
         log("layouts: plain NHWC vs batch-interleaved (nb images per pixel)")

@@ -173,6 +173,17 @@ typedef struct qconv_tile_info {
 /*
  * qconv_layout -- host only, no device work.  Validates `d` exactly as
  * qconv2d does and fills `out` with the output extent and buffer sizes.
+ *   p, q, m, gemm_k, macs   the GEMM view of Sec. 2.1: M = n*p*q lowered
+ *                           rows (P, Q as in qconv_desc), depth c*r*s
+ *   x_bytes, w_bytes,       the packed layouts above (Sec. 1: eight 4-bit
+ *   y_*_bytes               values per 32-bit word)
+ *   max_abs_acc             the largest |accumulator| any input of the
+ *                           declared ranges can give, c*r*s*max|x|*max|w|;
+ *                           Sec. 3.2.1 argues that 32-bit accumulators are
+ *                           enough for reduced-precision products, and the
+ *                           descriptor is rejected (QCONV_EUNSUPPORTED) when
+ *                           this bound, times the widening factor of signed
+ *                           4-bit operands, reaches 2^31
  * Returns QCONV_EINVAL / QCONV_EUNSUPPORTED for a descriptor qconv2d would
  * reject.  `out` may be NULL (validation only).
  */
@@ -278,6 +289,45 @@ int qconv_prepare_filters(const qconv_desc *d, const void *w_packed, int32_t til
 int qconv2d_prepared(const qconv_desc *d, const void *x, const void *w_prepared, size_t w_prepared_bytes,
                      const qconv_epilogue *epi, void *y, int32_t tile_id, int32_t splits, void *workspace,
                      size_t workspace_bytes, void *stream);
+
+/*
+ * A 1x1 projection fused into a 3x3 layer.  A residual stage's first block
+ * reads one input twice: its 3x3 convolution (stride s, padding 1) and the
+ * 1x1 projection of its shortcut (stride s, no padding), whose output pixel
+ * (p, q) reads input pixel (p*s, q*s) -- exactly the pixel the 3x3 window's
+ * centre tap reads.  The fused launch stages the input band once (Sec. 3.1)
+ * and runs the projection's products on the centre tap's fragments, so the
+ * projection costs no launch and no second pass over the input; each output
+ * gets its own epilogue before its store (Sec. 3.2.2) in the packed layout
+ * the next layer reads (Sec. 3.3).  The two outputs equal qconv2d of the 3x3
+ * layer and qconv2d of the projection (d with r = s = 1 and no
+ * padding) on the same input.
+ *   d          the 3x3 layer: r == s == 3, pad_h == pad_w == 1, plain layout;
+ *              the projection has the same n, h, w, c, k, strides, bits and
+ *              signedness
+ * qconv_proj_default_tile -- host only: the built-in tile for such a layer, or
+ *   an error (QCONV_EUNSUPPORTED when no tile with a projection instance fits).
+ * qconv_proj_tile_check -- host only: QCONV_OK if `tile_id` can run it.
+ * qconv_prepared_proj_filter_bytes -- host only: size of its prepared filters.
+ * qconv_prepare_filters_proj -- device work on `stream`: packed KRSC 3x3
+ *   filters `w_packed` and packed k x 1 x 1 x c projection filters
+ *   `w_proj_packed` (16-byte aligned) -> one prepared image for `tile_id`
+ *   (the projection is its tenth tap).  Errors as qconv_prepare_filters.
+ * qconv2d_proj -- the fused launch.  `epi` and `epi_proj` must have the same
+ *   mode: raw (both NULL or QCONV_OUT_RAW_I32: y and y_proj get int32
+ *   accumulators) or requant (each with its own multipliers, shift, ReLU,
+ *   clamp and optional bias; no residual).  y and y_proj (16-byte aligned,
+ *   y_packed_bytes or y_raw_bytes each) must not overlap each other or any
+ *   input.  No split.  Errors as qconv2d_prepared.
+ */
+int qconv_proj_default_tile(const qconv_desc *d);
+int qconv_proj_tile_check(const qconv_desc *d, int32_t tile_id);
+int qconv_prepared_proj_filter_bytes(const qconv_desc *d, int32_t tile_id, size_t *bytes);
+int qconv_prepare_filters_proj(const qconv_desc *d, const void *w_packed, const void *w_proj_packed, int32_t tile_id,
+                               void *w_prepared, size_t bytes, void *stream);
+int qconv2d_proj(const qconv_desc *d, const void *x, const void *w_prepared, size_t w_prepared_bytes,
+                 const qconv_epilogue *epi, void *y, const qconv_epilogue *epi_proj, void *y_proj, int32_t tile_id,
+                 void *stream);
 
 /*
  * qconv2d_packing -- qconv_pack of the activations fused into
@@ -391,6 +441,14 @@ int qconv_tile_check(const qconv_desc *d, int32_t tile_id);
 /* The tile qconv2d uses for tile_id = -1 (a static per-shape heuristic). */
 int qconv_default_tile(const qconv_desc *d);
 
+/*
+ * qconv_build_digest -- host only: a 16-hex-digit digest of the sources and
+ * compile flags this library was built from (static string; "unknown" for a
+ * build that did not set it).  Lets a caller check that the binary it loaded
+ * is the one its sources describe.
+ */
+const char *qconv_build_digest(void);
+
 /* Static text for a status code. */
 const char *qconv_strerror(int status);
 
@@ -417,6 +475,26 @@ const char *qconv_last_error(void);
  */
 int qconv_probe_mfma_i8(int32_t blocks, int32_t iters, int32_t *sink, uint64_t *stamps, int64_t *ops,
                         void *stream);
+
+/*
+ * qconv_last_launch -- host only: the grid (workgroups), workgroup size
+ * (threads) and dynamic LDS bytes of the calling thread's most recent
+ * convolution launch (any qconv2d* entry point that returned QCONV_OK); any
+ * pointer may be NULL.  QCONV_EINVAL when the thread has launched none.
+ */
+int qconv_last_launch(int64_t *grid, int64_t *threads, int64_t *lds_bytes);
+
+/*
+ * qconv_probe_launch -- measurement aid, not part of the convolution: an
+ * empty kernel over `blocks` workgroups of `threads` threads with `lds_bytes`
+ * of dynamic LDS.  Its time per launch (back to back, or replayed from a
+ * graph) is the fixed cost of dispatching and draining a grid of that shape,
+ * the floor under any kernel launched once per layer.
+ *   blocks 1 .. 2^20; threads a multiple of 64 in 64 .. 1024; lds_bytes
+ *   0 .. 163840.  QCONV_EINVAL otherwise; QCONV_EHIP if the launch is
+ *   rejected.  Asynchronous on `stream`.
+ */
+int qconv_probe_launch(int32_t blocks, int32_t threads, int32_t lds_bytes, void *stream);
 
 /*
  * Host-only self-check of the index arithmetic the kernels use (run-time

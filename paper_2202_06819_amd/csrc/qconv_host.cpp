@@ -18,9 +18,24 @@
 
 using namespace qconv;
 
+// Digest of the sources and flags this library was built from (set by the
+// build; a build from elsewhere says "unknown").  It is also kept as a plain
+// string in the file, so a caller can check a binary without loading it.
+#ifndef QCONV_SOURCE_DIGEST
+#define QCONV_SOURCE_DIGEST "unknown"
+#endif
+__attribute__((used)) static const char kDigestMarker[] = "QCONV_SOURCE_DIGEST=" QCONV_SOURCE_DIGEST;
+
 namespace {
 
 thread_local char g_err[256] = "";
+
+// Geometry of the calling thread's most recent convolution launch.
+struct LaunchGeometry {
+    int64_t grid = 0, threads = 0, lds = 0;
+    char kernel[96] = "";
+};
+thread_local LaunchGeometry g_last_launch;
 
 int fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
 int fail(int code, const char *fmt, ...) {
@@ -221,8 +236,10 @@ int64_t per_cu_estimate(const qconv_tile_info &t, int64_t lds) {
 // a CU and their phases overlap.
 // ablation: the techniques switched off (bit 0 lowered staging, bit 1 LDS
 // epilogue), for the measurement instances of 3x3 layers.
+// proj: the filter image carries a fused 1x1 projection as one more tap, and
+// the projection's multipliers and biases sit beside the layer's.
 int plan_tile(const qconv_desc *d, const qconv_layout_info &li, const qconv_tile_info &t, Plan *out,
-              int64_t per_cu = 0, int64_t splits = 1, bool one_band = false, int ablation = 0) {
+              int64_t per_cu = 0, int64_t splits = 1, bool one_band = false, int ablation = 0, bool proj = false) {
     if (t.bits != d->bits)
         return fail(QCONV_EUNSUPPORTED, "tile %s is built for %d-bit operands", t.name, t.bits);
     if ((t.x_signed >= 0 && t.x_signed != d->x_signed) || (t.w_signed >= 0 && t.w_signed != d->w_signed))
@@ -259,12 +276,13 @@ int plan_tile(const qconv_desc *d, const qconv_layout_info &li, const qconv_tile
         // prepared filter block is copied with 1 KiB LDS-DMA instructions
         // (the lowered operand holds every tile pixel once per tap instead)
         pl.pstride_b = lowered ? round_up((int64_t)d->r * d->s * t.tile_p * 16, 256) : round_up(pl.rows * ncols * 16, 256);
-        pl.pstride_w = round_up((int64_t)d->r * d->s * t.tile_k * 16, 1024);
+        pl.pstride_w = round_up(((int64_t)d->r * d->s + (proj ? 1 : 0)) * t.tile_k * 16, 1024);
         const int64_t bbuf = planes * pl.pstride_b, wbuf = planes * pl.pstride_w;
         // buffer loads take 32-bit offsets, and offset 2^31 marks padding
         if (li.x_bytes >= (1ll << 31) || pl.ktiles * nchunks * wbuf >= (1ll << 31))
             return fail(QCONV_EUNSUPPORTED, "tile %s addresses operands with 31-bit buffer offsets", t.name);
-        const int64_t mbytes0 = round_up((int64_t)t.tile_k * 8 + 4, 16);   // multipliers, biases, split-K flag
+        // multipliers, biases, split-K flag (and the projection's multipliers and biases)
+        const int64_t mbytes0 = proj ? (int64_t)t.tile_k * 16 + 16 : round_up((int64_t)t.tile_k * 8 + 4, 16);
         const int64_t mbytes = mbytes0 + (ldsepi ? (int64_t)t.tile_p * t.tile_k * 4 : 0);   // + int32 tile
         const int64_t single = bbuf + wbuf + mbytes;
         const int64_t tiles = pl.mtiles * pl.ktiles;
@@ -363,6 +381,36 @@ int pick_default(const qconv_desc *d, const qconv_layout_info &li) {
     return best;
 }
 
+// The layer can carry a fused 1x1 projection: a 3x3 window with padding 1, so
+// its centre tap reads pixel (p*stride_h, q*stride_w), the pixel a 1x1 filter
+// at the same stride without padding reads.
+bool proj_shape_ok(const qconv_desc *d) {
+    return d->r == 3 && d->s == 3 && d->pad_h == 1 && d->pad_w == 1 && d->nb <= 1;
+}
+
+// The built-in tile for a layer with a fused projection: the static heuristic's
+// score among the tiles that have a projection instance and fit the shape.
+int pick_proj_default(const qconv_desc *d, const qconv_layout_info &li) {
+    const TileEntry *tab = tile_table();
+    int best = -1;
+    double best_score = -1.0;
+    for (int i = 0; i < tile_table_size(); ++i) {
+        const qconv_tile_info &t = tab[i].info;
+        if (t.bits != d->bits || !proj_instance(t.name)) continue;
+        Plan pl;
+        if (plan_tile(d, li, t, &pl, 0, 1, false, 0, true) != QCONV_OK) continue;
+        const double tiles = (double)pl.mtiles * pl.ktiles;
+        const double util = (double)li.m * d->k / (tiles * t.tile_p * t.tile_k);
+        const double fill = std::min(1.0, tiles * t.threads / 64.0 / (4.0 * kNumCUs));
+        const double score = util * fill * (2.0 * t.frag_p * t.frag_k / (t.frag_p + t.frag_k));
+        if (score > best_score) {
+            best_score = score;
+            best = i;
+        }
+    }
+    return best;
+}
+
 struct DevAttrCache {
     std::mutex mu;
     std::unordered_map<long long, bool> done;   // (device, tile) -> max LDS attribute set
@@ -372,6 +420,8 @@ DevAttrCache g_attr;
 }  // namespace
 
 extern "C" {
+
+const char *qconv_build_digest(void) { return kDigestMarker + sizeof("QCONV_SOURCE_DIGEST=") - 1; }
 
 const char *qconv_strerror(int status) {
     switch (status) {
@@ -556,7 +606,7 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
              const qconv_epilogue *epi, void *y, void *workspace, size_t workspace_bytes, int32_t tile_id,
              int32_t splits, void *stream, int32_t wg_per_cu = 0, int32_t band_buffers = 0,
              int32_t xcd_order = 1, int32_t ablation = 0, const int8_t *x_nchw = nullptr,
-             void *x_packed = nullptr) {
+             void *x_packed = nullptr, const qconv_epilogue *epi_proj = nullptr, void *y_proj = nullptr) {
     qconv_layout_info li;
     qconv_desc kd;
     int rc = kernel_desc(d, &kd, &li);
@@ -573,6 +623,25 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
     if ((int64_t)workspace_bytes < li.workspace_bytes)
         return fail(QCONV_EWORKSPACE, "workspace of %zu bytes, need %lld", workspace_bytes,
                     (long long)li.workspace_bytes);
+    // a fused 1x1 projection (y_proj): same input, stride, channels and mode, its own epilogue
+    const bool proj = y_proj != nullptr;
+    if (proj) {
+        if (!proj_shape_ok(d))
+            return fail(QCONV_EUNSUPPORTED, "a fused projection needs a 3x3 layer with padding 1 in the plain layout");
+        rc = check_epilogue(d, epi_proj);
+        if (rc) return rc;
+        const int m1 = epi ? epi->mode : QCONV_OUT_RAW_I32, m2 = epi_proj ? epi_proj->mode : QCONV_OUT_RAW_I32;
+        if (m1 != m2) return fail(QCONV_EINVAL, "the layer and its projection must use the same epilogue mode");
+        if ((epi && epi->residual) || (epi_proj && epi_proj->residual))
+            return fail(QCONV_EUNSUPPORTED, "a layer with a fused projection takes no residual");
+        if (!prepared || splits != 1 || ablation || x_nchw)
+            return fail(QCONV_EUNSUPPORTED, "a fused projection runs from prepared filters, without split or ablation");
+        if (!aligned16(y_proj)) return fail(QCONV_EINVAL, "y_proj must be 16-byte aligned");
+        if (tile_id == -1) {
+            tile_id = pick_proj_default(d, li);
+            if (tile_id < 0) return fail(QCONV_EUNSUPPORTED, "no tile with a projection instance fits this shape");
+        }
+    }
     rc = resolve_tile(d, li, tile_id);
     if (rc < 0) return rc;
     tile_id = rc;
@@ -580,7 +649,9 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
     Plan pl;
     if (ablation && (!prepared || te.info.variant != QCONV_VARIANT_WIDE || !ablation_instance(te.info.name, ablation)))
         return fail(QCONV_EUNSUPPORTED, "no ablation instance %d of tile %s", ablation, te.info.name);
-    rc = plan_tile(d, li, te.info, &pl, 0, splits, false, ablation);
+    const ProjInstance *pi = proj ? proj_instance(te.info.name) : nullptr;
+    if (proj && !pi) return fail(QCONV_EUNSUPPORTED, "tile %s has no projection instance", te.info.name);
+    rc = plan_tile(d, li, te.info, &pl, 0, splits, false, ablation, proj);
     if (rc) return rc;
     const int64_t wsb = split_workspace_bytes(te.info, pl);
     if (wsb > 0) {
@@ -605,6 +676,13 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
             ((uintptr_t)w < w1 && w0 < (uintptr_t)w + wb))
             return fail(QCONV_EINVAL, "workspace overlaps x, w or y");
     }
+    if (proj) {
+        const uintptr_t p0 = (uintptr_t)y_proj, p1 = p0 + ybytes;
+        if ((p0 < y1 && y0 < p1) || ((uintptr_t)x < p1 && p0 < (uintptr_t)x + xin_bytes) ||
+            ((uintptr_t)w < p1 && p0 < (uintptr_t)w + wb) ||
+            (wsb > 0 && (uintptr_t)workspace < p1 && p0 < (uintptr_t)workspace + wsb))
+            return fail(QCONV_EINVAL, "y_proj overlaps x, w, y or the workspace");
+    }
     if (requant && epi->residual) {
         // each lane reads its own output words of the residual before storing
         // them, so y itself may be the residual; any other overlap may not
@@ -618,7 +696,7 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
     // the epilogue flavour: bias and residual are compiled into separate kernels;
     // prepared filters of a 3x3 or 1x1 layer run the tile's fixed-size instance
     // (whose taps are one column apart: not for 3x3 in the interleaved layout)
-    const bool ext = requant && (epi->bias || epi->residual);
+    const bool ext = requant && (epi->bias || epi->residual || (proj && epi_proj->bias));
     if (ablation && ext) return fail(QCONV_EUNSUPPORTED, "ablation instances have no bias or residual epilogue");
     const KernelSet &ks = ext ? te.ext : te.plain;
     ConvLauncher launch = ks.launch;
@@ -634,6 +712,12 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
                 kernel = mc ? ks.fixed[i].kernel_mc : ks.fixed[i].kernel;
                 inst = mc ? (ext ? 7 : 6) : (ext ? 3 : 0) + 1 + i;
             }
+    if (pi) {
+        const FixedInstance &fi = ext ? pi->ext : pi->plain;
+        launch = fi.launch;
+        kernel = fi.kernel;
+        inst = ext ? 15 : 14;
+    }
     if (ablation) {
         const AblationInstance *ai = ablation_instance(te.info.name, ablation);
         launch = ai->launch;
@@ -674,14 +758,15 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
         // choice; band_buffers forces either)
         Plan one;
         int occ1 = 0;
-        const bool one_ok = plan_tile(d, li, te.info, &one, 0, 1, true, ablation) == QCONV_OK && one.lds < pl.lds;
+        const bool one_ok =
+            plan_tile(d, li, te.info, &one, 0, 1, true, ablation, proj) == QCONV_OK && one.lds < pl.lds;
         if (one_ok &&
             hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ1, kernel, te.info.threads, (size_t)one.lds) != hipSuccess)
             occ1 = 0;
         const bool use_one = band_buffers == 1 ? one_ok : (band_buffers == 2 ? false : one_ok && occ > 0 && occ1 > occ);
         const int pc = wg_per_cu > 0 ? wg_per_cu : (use_one ? occ1 : occ);
         if (pc > 0 || use_one) {
-            rc = plan_tile(d, li, te.info, &pl, pc > 0 ? pc : 0, 1, use_one, ablation);
+            rc = plan_tile(d, li, te.info, &pl, pc > 0 ? pc : 0, 1, use_one, ablation, proj);
             if (rc) return rc;
         }
     }
@@ -713,10 +798,25 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
         a.hi = epi->clamp_hi;
         if (a.lo > a.hi) a.lo = a.hi;   // relu with an all-negative clamp range: every value is clamp_hi
     }
+    if (proj) {
+        a.yproj = static_cast<uint8_t *>(y_proj);
+        if (requant) {
+            a.mult2 = epi_proj->mult;
+            a.bias2 = epi_proj->bias;
+            a.shift2 = epi_proj->shift;
+            a.lo2 = epi_proj->relu ? std::max(epi_proj->clamp_lo, 0) : epi_proj->clamp_lo;
+            a.hi2 = epi_proj->clamp_hi;
+            if (a.lo2 > a.hi2) a.lo2 = a.hi2;
+        }
+    }
     rc = ensure_lds_attribute(kernel, tile_id, inst, pl.lds);
     if (rc) return rc;
     hipError_t e = launch(a, dim3((unsigned)pl.grid), (size_t)pl.lds, (hipStream_t)stream);
     if (e != hipSuccess) return fail(QCONV_EHIP, "conv launch (%s): %s", te.info.name, hipGetErrorString(e));
+    g_last_launch.grid = pl.grid;
+    g_last_launch.threads = te.info.threads;
+    g_last_launch.lds = pl.lds;
+    snprintf(g_last_launch.kernel, sizeof(g_last_launch.kernel), "%s", te.info.name);
     return QCONV_OK;
 }
 
@@ -844,7 +944,7 @@ int qconv_prepare_filters(const qconv_desc *d, const void *w_packed, int32_t til
         ConvArgs a;
         fill_args(a, d, li, te, pl);
         a.wptr = static_cast<const uint8_t *>(w_packed);
-        e = te.prep(a, static_cast<uint8_t *>(w_prepared), need / 16, (hipStream_t)stream);
+        e = te.prep(a, static_cast<uint8_t *>(w_prepared), need / 16, nullptr, (hipStream_t)stream);
     } else {
         e = hipMemcpyAsync(w_prepared, w_packed, (size_t)li.w_bytes, hipMemcpyDeviceToDevice, (hipStream_t)stream);
     }
@@ -858,6 +958,99 @@ int qconv2d_prepared(const qconv_desc *d, const void *x, const void *w_prepared,
     g_err[0] = 0;
     return run_conv(d, x, w_prepared, true, w_prepared_bytes, epi, y, workspace, workspace_bytes, tile_id, splits,
                     stream);
+}
+
+// The tile a layer with a fused projection runs (tile_id, or the built-in
+// choice for -1) and its plan; the descriptor is already the kernel's.
+static int proj_tile_plan(const qconv_desc *d, const qconv_layout_info &li, int32_t tile_id, Plan *pl) {
+    if (!proj_shape_ok(d))
+        return fail(QCONV_EUNSUPPORTED, "a fused projection needs a 3x3 layer with padding 1 in the plain layout");
+    if (tile_id == -1) {
+        tile_id = pick_proj_default(d, li);
+        if (tile_id < 0) return fail(QCONV_EUNSUPPORTED, "no tile with a projection instance fits this shape");
+    }
+    if (tile_id < 0 || tile_id >= tile_table_size()) return fail(QCONV_EINVAL, "unknown tile %d", tile_id);
+    const qconv_tile_info &t = tile_table()[tile_id].info;
+    if (!proj_instance(t.name)) return fail(QCONV_EUNSUPPORTED, "tile %s has no projection instance", t.name);
+    int rc = plan_tile(d, li, t, pl, 0, 1, false, 0, true);
+    return rc ? rc : tile_id;
+}
+
+int qconv_proj_default_tile(const qconv_desc *d) {
+    g_err[0] = 0;
+    qconv_layout_info li;
+    qconv_desc kd;
+    int rc = kernel_desc(d, &kd, &li);
+    if (rc) return rc;
+    Plan pl;
+    return proj_tile_plan(&kd, li, -1, &pl);
+}
+
+int qconv_proj_tile_check(const qconv_desc *d, int32_t tile_id) {
+    g_err[0] = 0;
+    if (tile_id < 0) return fail(QCONV_EINVAL, "unknown tile %d", tile_id);
+    qconv_layout_info li;
+    qconv_desc kd;
+    int rc = kernel_desc(d, &kd, &li);
+    if (rc) return rc;
+    Plan pl;
+    rc = proj_tile_plan(&kd, li, tile_id, &pl);
+    return rc < 0 ? rc : QCONV_OK;
+}
+
+int qconv_prepared_proj_filter_bytes(const qconv_desc *d, int32_t tile_id, size_t *bytes) {
+    g_err[0] = 0;
+    qconv_layout_info li;
+    qconv_desc kd;
+    int rc = kernel_desc(d, &kd, &li);
+    if (rc) return rc;
+    if (!bytes) return fail(QCONV_EINVAL, "bytes must be non-NULL");
+    Plan pl;
+    rc = proj_tile_plan(&kd, li, tile_id, &pl);
+    if (rc < 0) return rc;
+    *bytes = (size_t)prepared_bytes(&kd, li, tile_table()[rc].info, pl);
+    return QCONV_OK;
+}
+
+int qconv_prepare_filters_proj(const qconv_desc *d, const void *w_packed, const void *w_proj_packed, int32_t tile_id,
+                               void *w_prepared, size_t bytes, void *stream) {
+    g_err[0] = 0;
+    qconv_layout_info li;
+    qconv_desc kd;
+    int rc = kernel_desc(d, &kd, &li);
+    if (rc) return rc;
+    d = &kd;
+    if (!w_packed || !w_proj_packed || !w_prepared) return fail(QCONV_EINVAL, "filter pointers must be non-NULL");
+    if (!aligned16(w_packed) || !aligned16(w_proj_packed) || !aligned16(w_prepared))
+        return fail(QCONV_EINVAL, "filters must be 16-byte aligned");
+    Plan pl;
+    rc = proj_tile_plan(d, li, tile_id, &pl);
+    if (rc < 0) return rc;
+    const TileEntry &te = tile_table()[rc];
+    const int64_t need = prepared_bytes(d, li, te.info, pl);
+    if ((int64_t)bytes < need)
+        return fail(QCONV_EINVAL, "prepared filter buffer of %zu bytes, need %lld", bytes, (long long)need);
+    const int64_t proj_bytes = li.w_bytes / (d->r * d->s);   // k x 1 x 1 x c packed
+    const uintptr_t d0 = (uintptr_t)w_prepared, d1 = d0 + need;
+    const uintptr_t s0 = (uintptr_t)w_packed, s1 = s0 + li.w_bytes;
+    const uintptr_t p0 = (uintptr_t)w_proj_packed, p1 = p0 + proj_bytes;
+    if ((s0 < d1 && d0 < s1) || (p0 < d1 && d0 < p1)) return fail(QCONV_EINVAL, "packed and prepared filters overlap");
+    ConvArgs a;
+    fill_args(a, d, li, te, pl);
+    a.wptr = static_cast<const uint8_t *>(w_packed);
+    hipError_t e = te.prep(a, static_cast<uint8_t *>(w_prepared), need / 16,
+                           static_cast<const uint8_t *>(w_proj_packed), (hipStream_t)stream);
+    if (e != hipSuccess) return fail(QCONV_EHIP, "prepare filters (%s): %s", te.info.name, hipGetErrorString(e));
+    return QCONV_OK;
+}
+
+int qconv2d_proj(const qconv_desc *d, const void *x, const void *w_prepared, size_t w_prepared_bytes,
+                 const qconv_epilogue *epi, void *y, const qconv_epilogue *epi_proj, void *y_proj, int32_t tile_id,
+                 void *stream) {
+    g_err[0] = 0;
+    if (!y_proj) return fail(QCONV_EINVAL, "y_proj must be non-NULL");
+    return run_conv(d, x, w_prepared, true, w_prepared_bytes, epi, y, nullptr, 0, tile_id, 1, stream, 0, 0, 1, 0,
+                    nullptr, nullptr, epi_proj, y_proj);
 }
 
 int qconv2d_packing(const qconv_desc *d, const int8_t *x_nchw, void *x_packed, const void *w_prepared,
@@ -913,6 +1106,24 @@ int qconv_probe_mfma_i8(int32_t blocks, int32_t iters, int32_t *sink, uint64_t *
     if (ops) *ops = mfma_probe_ops(blocks, iters);
     hipError_t e = launch_mfma_probe(blocks, iters, sink, stamps, (hipStream_t)stream);
     if (e != hipSuccess) return fail(QCONV_EHIP, "probe launch: %s", hipGetErrorString(e));
+    return QCONV_OK;
+}
+
+int qconv_last_launch(int64_t *grid, int64_t *threads, int64_t *lds_bytes) {
+    if (grid) *grid = g_last_launch.grid;
+    if (threads) *threads = g_last_launch.threads;
+    if (lds_bytes) *lds_bytes = g_last_launch.lds;
+    return g_last_launch.grid > 0 ? QCONV_OK : fail(QCONV_EINVAL, "no convolution launched on this thread yet");
+}
+
+int qconv_probe_launch(int32_t blocks, int32_t threads, int32_t lds_bytes, void *stream) {
+    g_err[0] = 0;
+    if (blocks < 1 || blocks > (1 << 20) || threads < 64 || threads > 1024 || threads % 64 != 0 || lds_bytes < 0 ||
+        lds_bytes > kLdsBytes)
+        return fail(QCONV_EINVAL, "blocks in [1, 2^20], threads a multiple of 64 in [64, 1024], lds_bytes in [0, %lld]",
+                    (long long)kLdsBytes);
+    hipError_t e = launch_empty_probe(blocks, threads, lds_bytes, (hipStream_t)stream);
+    if (e != hipSuccess) return fail(QCONV_EHIP, "empty probe launch: %s", hipGetErrorString(e));
     return QCONV_OK;
 }
 

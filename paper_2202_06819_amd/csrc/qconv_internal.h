@@ -85,6 +85,13 @@ struct ConvArgs {
     int32_t xsrc_bytes;
     uint8_t *xpk;           // packed copy of the input written on the way, or null
     FastDiv div_w, div_wq;  // by w and by its column quads
+    // a 1x1 projection at the same stride fused into a 3x3 launch (PROJ
+    // instances): its filters are tap r*s of the prepared image, its input the
+    // centre tap's pixels, its output and epilogue its own
+    uint8_t *yproj;         // its output (raw int32 or packed, as yptr)
+    const int32_t *mult2;   // its per-channel multipliers (requant mode)
+    const int32_t *bias2;   // its per-channel accumulator offsets, or null
+    int32_t shift2, lo2, hi2;
 };
 
 // Band pixels one thread of a wide tile stages per channel chunk: the 4
@@ -98,7 +105,10 @@ constexpr int wide_band_pixels_per_thread(int tile_p, int threads, int vecs_per_
 }
 
 using ConvLauncher = hipError_t (*)(const ConvArgs &, dim3 grid, size_t lds_bytes, hipStream_t);
-using PrepLauncher = hipError_t (*)(const ConvArgs &, uint8_t *image, int64_t elems, hipStream_t);
+// builds a prepared filter image; `wproj` (or null): packed K x 1 x 1 x C filters
+// of a fused projection, placed as the image's last tap
+using PrepLauncher = hipError_t (*)(const ConvArgs &, uint8_t *image, int64_t elems, const uint8_t *wproj,
+                                    hipStream_t);
 
 // A compiled instance of a tile for one fixed filter size (prepared filters).
 struct FixedInstance {
@@ -132,10 +142,21 @@ struct AblationInstance {
     const void *kernel;
 };
 
+// A 3x3 instance of a tile with a 1x1 projection at the same stride fused in
+// (prepared filters, no split).
+struct ProjInstance {
+    const char *tile;       // the tile it is a variant of
+    FixedInstance plain;    // epilogues without bias
+    FixedInstance ext;      // epilogues with per-channel biases
+};
+
 // Defined in qconv_conv.hip.
 const TileEntry *tile_table();
 int tile_table_size();
 const AblationInstance *ablation_instance(const char *tile_name, int mask);
+
+// Defined in qconv_tiles_proj.hip.
+const ProjInstance *proj_instance(const char *tile_name);
 
 // Defined in qconv_pack.hip.
 hipError_t launch_pack(const int8_t *src, void *dst, int32_t n, int32_t c, int32_t h, int32_t w, int32_t bits,
@@ -157,5 +178,6 @@ hipError_t launch_unroll(const int8_t *src, int8_t *dst, const UnrollArgs &a, hi
 // Defined in qconv_probe.hip (measurement aid).
 int64_t mfma_probe_ops(int blocks, int iters);
 hipError_t launch_mfma_probe(int blocks, int iters, int32_t *sink, uint64_t *stamps, hipStream_t stream);
+hipError_t launch_empty_probe(int blocks, int threads, int lds_bytes, hipStream_t stream);
 
 }  // namespace qconv

@@ -45,6 +45,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <type_traits>
+
 #include "qconv_device.h"
 #include "qconv_internal.h"
 
@@ -373,6 +375,16 @@ __device__ __forceinline__ void sched_lds_reads() { __builtin_amdgcn_sched_group
 template <int N>
 __device__ __forceinline__ void sched_mfmas() { __builtin_amdgcn_sched_group_barrier(0x008, N, 0); }
 
+// f(integral_constant<int, I>) for I = B .. E-1, unrolled at compile time (for
+// scheduling-group counts that differ between steps).
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(f);
+    }
+}
+
 // Workgroups are dispatched round-robin over the 8 XCDs, each with its own L2:
 // block b runs on XCD b % 8.  Renumber them so that every XCD gets one
 // contiguous range of logical blocks; neighbouring output tiles share halo
@@ -392,14 +404,19 @@ __device__ __forceinline__ int xcd_block(int b, int g) {
 // tap, as without duplicate awareness; bit 1 sends the int32 accumulators
 // through LDS to a separate requantise-and-pack pass instead of packing them
 // in registers before the store.
+// PROJ: a 1x1 projection at the same stride is fused into a 3x3 instance (pad
+// 1): its filter block is tap 9 of the prepared image, its input the centre
+// tap's band pixels -- the fragments the 3x3 already reads -- and it keeps
+// accumulators, multipliers and an output of its own (no split, no residual).
 template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC, bool EXT, int ABL = 0,
-          bool MC = false, bool NCHW = false>
+          bool MC = false, bool NCHW = false, bool PROJ = false>
 __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     constexpr bool FIXED = RC > 0 && SC > 0;
     constexpr bool LOWERED = (ABL & 1) != 0;
     constexpr bool LDSEPI = (ABL & 2) != 0;
     static_assert(!NCHW || (!LOWERED && !MC), "the fused pack stages the band itself");
     static_assert(ABL == 0 || (FIXED && !EXT), "ablation instances are fixed-size, without bias or residual");
+    static_assert(!PROJ || (RC == 3 && SC == 3 && ABL == 0 && !MC && !NCHW), "the projection rides on a plain 3x3");
     constexpr int NW = WP * WK;
     constexpr int NT = NW * 64;
     constexpr int TP = WP * FP * 16;
@@ -782,23 +799,43 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     for (int tn = 0; tn < FP; ++tn)
 #pragma unroll
         for (int tm = 0; tm < FK; ++tm) acc[tn][tm] = v4i{0, 0, 0, 0};
+    // the projection's accumulators (PROJ)
+    v4i acc2[PROJ ? FP : 1][PROJ ? FK : 1];
+#pragma unroll
+    for (int tn = 0; tn < (PROJ ? FP : 1); ++tn)
+#pragma unroll
+        for (int tm = 0; tm < (PROJ ? FK : 1); ++tm) acc2[tn][tm] = v4i{0, 0, 0, 0};
+    // the projection's epilogue reads the same fields as the main one
+    ConvArgs ap = a;
+    if constexpr (PROJ) {
+        ap.yptr = a.yproj;
+        ap.mult = a.mult2;
+        ap.bias = a.bias2;
+        ap.shift = a.shift2;
+        ap.lo = a.lo2;
+        ap.hi = a.hi2;
+        ap.res = nullptr;
+    }
 
     const int cb = k0 + wk * FK * 16 + gq * 4 * FK;
     // the workgroup's TK multipliers (and biases) go to LDS by DMA, read back
     // for the epilogue; channels past k repeat the last one and are never stored
+    // (PROJ: the projection's follow at mlds2 = mlds + 2*TK + 4)
     int32_t *mlds = reinterpret_cast<int32_t *>(smem + a.off_m);
     int32_t *blds = mlds + TK;
-    if (a.mode == QCONV_OUT_REQUANT && wave == 0) {
-        const u32x4 rm = make_rsrc(a.mult, 4 * a.k);
+    int32_t *mlds2 = mlds + 2 * TK + 4;
+    int32_t *blds2 = mlds2 + TK;
+    auto dma_channels = [&](int32_t *dst, const int32_t *src) {
+        const u32x4 r = make_rsrc(src, 4 * a.k);
         for (int e = 0; e < TK; e += 64)
             if (e + lane < TK)   // TK may be 32: only the lanes of the buffer write
-                dma4(reinterpret_cast<const uint8_t *>(mlds + e), (uint32_t)min(k0 + e + lane, a.k - 1) * 4u, rm);
-    }
-    if (EXT && a.mode == QCONV_OUT_REQUANT && a.bias && wave == (NW > 1 ? 1 : 0)) {
-        const u32x4 rb = make_rsrc(a.bias, 4 * a.k);
-        for (int e = 0; e < TK; e += 64)
-            if (e + lane < TK)
-                dma4(reinterpret_cast<const uint8_t *>(blds + e), (uint32_t)min(k0 + e + lane, a.k - 1) * 4u, rb);
+                dma4(reinterpret_cast<const uint8_t *>(dst + e), (uint32_t)min(k0 + e + lane, a.k - 1) * 4u, r);
+    };
+    if (a.mode == QCONV_OUT_REQUANT && wave == 0) dma_channels(mlds, a.mult);
+    if (EXT && a.mode == QCONV_OUT_REQUANT && a.bias && wave == (NW > 1 ? 1 : 0)) dma_channels(blds, a.bias);
+    if constexpr (PROJ) {
+        if (a.mode == QCONV_OUT_REQUANT && wave == (NW > 2 ? 2 : 0)) dma_channels(mlds2, a.mult2);
+        if (EXT && a.mode == QCONV_OUT_REQUANT && a.bias2 && wave == (NW > 3 ? 3 : 0)) dma_channels(blds2, a.bias2);
     }
 
     // ---- prologue: stage 0 (every load in flight before the first wait)
@@ -822,21 +859,28 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
 
     // the workgroup keeps one channel tile: its epilogue multipliers are read
     // from LDS and prepared once
-    EpiParams<FK> ep;
-    if (a.mode == QCONV_OUT_REQUANT) {
-        int32_t mraw[4 * FK];
+    EpiParams<FK> ep, ep2;
+    auto lds_epilogue_params = [&](const ConvArgs &aa, const int32_t *ml, EpiParams<FK> &e2) {
+        if (aa.mode == QCONV_OUT_REQUANT) {
+            int32_t mraw[4 * FK];
 #pragma unroll
-        for (int e = 0; e < 4 * FK; e += 4) {
-            const int4 q = *reinterpret_cast<const int4 *>(mlds + cb - k0 + e);
-            mraw[e] = q.x; mraw[e + 1] = q.y; mraw[e + 2] = q.z; mraw[e + 3] = q.w;
+            for (int e = 0; e < 4 * FK; e += 4) {
+                const int4 q = *reinterpret_cast<const int4 *>(ml + cb - k0 + e);
+                mraw[e] = q.x; mraw[e + 1] = q.y; mraw[e + 2] = q.z; mraw[e + 3] = q.w;
+            }
+            make_epilogue_params<FK>(aa, mraw, e2);
+        } else {
+            e2.fast = false;
         }
-        make_epilogue_params<FK>(a, mraw, ep);
-    } else {
-        ep.fast = false;
-    }
+    };
+    lds_epilogue_params(a, mlds, ep);
+    if constexpr (PROJ) lds_epilogue_params(ap, mlds2, ep2);
     // accumulators start from the bias (in the first split of a tile only)
     const bool bias_here = EXT && a.mode == QCONV_OUT_REQUANT && a.bias && sp == 0;
     if (bias_here) init_acc<FP, FK>(a, acc, blds + cb - k0, false, cb);
+    const bool bias2_here = PROJ && EXT && a.mode == QCONV_OUT_REQUANT && a.bias2;
+    if constexpr (PROJ)
+        if (bias2_here) init_acc<FP, FK>(ap, acc2, blds2 + cb - k0, false, cb);
 
     const int nit = rs * KSTEPS;
 
@@ -934,8 +978,10 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
             // every step's LDS offsets are known: filter reads use immediate
             // offsets from one base; band reads from one base per (fragment,
             // filter row, depth step) plus the column as an immediate
-            constexpr int PSW = (RC * SC * TK * 16 + 1023) / 1024 * 1024;   // filter plane stride
+            constexpr int TAPS_IMG = RC * SC + (PROJ ? 1 : 0);   // taps in the filter image
+            constexpr int PSW = (TAPS_IMG * TK * 16 + 1023) / 1024 * 1024;   // filter plane stride
             constexpr int NIT = RC * SC * KSTEPS;
+            constexpr int CT = (RC / 2) * SC + SC / 2;   // the centre tap (the projection's pixels)
             const uint8_t *wa = wb;
             const uint8_t *brow[FP][RC][KSTEPS];
 #pragma unroll
@@ -947,6 +993,7 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                         brow[tn][rr][ks] = bb + pixoff[tn] + (LOWERED ? rr * SC * TP : rr * a.ncols) * 16 +
                                            ks * 4 * a.pstride_b;
             v4i A[2][FK], B[2][FP];
+            v4i Ap[2][PROJ ? FK : 1];   // the projection's filter fragments at the centre tap
             // Multi-chunk instances (MC): the next chunk's filter block goes out
             // as 1 KiB LDS-DMA copies spread over the MFMA steps (about one per
             // step and wave); issued all at once before the loop they queue
@@ -976,6 +1023,13 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
 #pragma unroll
                 for (int tn = 0; tn < FP; ++tn)
                     B[set][tn] = *reinterpret_cast<const v4i *>(brow[tn][rr][ks] + ss * (LOWERED ? TP * 16 : 16));
+                if constexpr (PROJ) {
+                    if (tap == CT) {
+#pragma unroll
+                        for (int tm = 0; tm < FK; ++tm)
+                            Ap[set][tm] = *reinterpret_cast<const v4i *>(wa + ks * 4 * PSW + RC * SC * TK * 16 + tm * 256);
+                    }
+                }
             };
             ld(0, 0);
 #pragma unroll
@@ -988,15 +1042,35 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                     for (int tm = 0; tm < FK; ++tm)
                         acc[tn][tm] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A[it & 1][tm], B[it & 1][tn], acc[tn][tm],
                                                                             0, 0, 0);
+                if constexpr (PROJ) {
+                    if (it / KSTEPS == CT) {
+                        // the same activation fragments times the projection's filters
+#pragma unroll
+                        for (int tn = 0; tn < FP; ++tn)
+#pragma unroll
+                            for (int tm = 0; tm < FK; ++tm)
+                                acc2[tn][tm] = __builtin_amdgcn_mfma_i32_16x16x64_i8(Ap[it & 1][tm], B[it & 1][tn],
+                                                                                     acc2[tn][tm], 0, 0, 0);
+                    }
+                }
             }
             // Pin the issue order (the scheduler otherwise reuses one register
             // set and waits on every read): the LDS reads of step it+1 go out
             // before the MFMAs of step it.
-            sched_lds_reads<FK + FP>();
+            if constexpr (PROJ) {
+                sched_lds_reads<FK + FP>();   // step 0 is never the centre tap
+                static_for<0, NIT>([&](auto I) {
+                    constexpr int it = decltype(I)::value;
+                    if constexpr (it + 1 < NIT) sched_lds_reads<FK + FP + ((it + 1) / KSTEPS == CT ? FK : 0)>();
+                    sched_mfmas<FP * FK * (it / KSTEPS == CT ? 2 : 1)>();
+                });
+            } else {
+                sched_lds_reads<FK + FP>();
 #pragma unroll
-            for (int it = 0; it < NIT; ++it) {
-                if (it + 1 < NIT) sched_lds_reads<FK + FP>();
-                sched_mfmas<FP * FK>();
+                for (int it = 0; it < NIT; ++it) {
+                    if (it + 1 < NIT) sched_lds_reads<FK + FP>();
+                    sched_mfmas<FP * FK>();
+                }
             }
         } else {
             // three fragment sets in rotation: the LDS reads of step it+2 are in
@@ -1069,7 +1143,7 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         if constexpr (NCHW)
             if (a.xpk && a.off_b1 != a.off_b0) nchw_write_packed(ti, c, cur);
         if (c == c_end - 1) {
-            if (a.splits > 1) {
+            if (!PROJ && a.splits > 1) {
                 // split-K: publish this split's partial sums; the last split of the
                 // tile to arrive adds the others and runs the epilogue
                 const int tile = lt;
@@ -1120,6 +1194,17 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
 #pragma unroll
                     for (int tm = 0; tm < FK; ++tm) acc[tn][tm] = v4i{0, 0, 0, 0};
             }
+            if constexpr (PROJ) {
+                epilogue<BITS, FP, FK, EXT>(ap, acc2, (j0 + ti * gpk) * TP + wp * FP * 16, cb, l16, ep2);
+                if (bias2_here) {
+                    init_acc<FP, FK>(ap, acc2, blds2 + cb - k0, false, cb);
+                } else {
+#pragma unroll
+                    for (int tn = 0; tn < FP; ++tn)
+#pragma unroll
+                        for (int tm = 0; tm < FK; ++tm) acc2[tn][tm] = v4i{0, 0, 0, 0};
+                }
+            }
         }
         if (more) {
             __syncthreads();
@@ -1135,11 +1220,15 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
 // holds the widened int8 granule of output channel row_channel(slot) at that
 // tap -- the same bytes the gather path writes into LDS.  One thread per
 // 16-byte element; padding elements are zero.
+// With `wproj` (packed K x 1 x 1 x C filters of a fused projection) the image
+// has one more tap, rs, holding those filters.
 template <int BITS, int FK, bool WS>
-__global__ void __launch_bounds__(256) build_filter_image(ConvArgs a, int TK, int CK, uint8_t *img, int64_t total) {
+__global__ void __launch_bounds__(256) build_filter_image(ConvArgs a, int TK, int CK, uint8_t *img, int64_t total,
+                                                          const uint8_t *wproj) {
     const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (e >= total) return;
     const int rs = a.r * a.s;
+    const int taps = rs + (wproj ? 1 : 0);
     const int ng = CK / 16;
     const int64_t plane_elems = a.pstride_w / 16;
     const int64_t blk = e / (ng * plane_elems);
@@ -1149,13 +1238,14 @@ __global__ void __launch_bounds__(256) build_filter_image(ConvArgs a, int TK, in
     const int kt = (int)(blk / a.nchunks);
     const int c = (int)(blk - (int64_t)kt * a.nchunks);
     uint4 out = uint4{0u, 0u, 0u, 0u};
-    if (el < rs * TK) {
+    if (el < taps * TK) {
         const int tap = el / TK;
         const int slot = el - tap * TK;
         const int kk = kt * TK + (slot / (FK * 16)) * FK * 16 + row_channel<FK>((slot % (FK * 16)) / 16, slot % 16);
         const int ch = c * CK + 16 * g;
         if (kk < a.k && ch < a.c) {
-            const uint8_t *src = a.wptr + ((size_t)kk * rs + tap) * a.xpix + (size_t)ch * BITS / 8;
+            const uint8_t *src = tap < rs ? a.wptr + ((size_t)kk * rs + tap) * a.xpix + (size_t)ch * BITS / 8
+                                          : wproj + (size_t)kk * a.xpix + (size_t)ch * BITS / 8;
             if constexpr (BITS == 4) {
                 const uint2 v = *reinterpret_cast<const uint2 *>(src);
                 uint4 g0, g1;
@@ -1172,9 +1262,9 @@ __global__ void __launch_bounds__(256) build_filter_image(ConvArgs a, int TK, in
 // One operand signedness per kernel (the widening is compiled for it); 8-bit
 // operands are always signed.
 template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC, bool EXT, int ABL = 0,
-          bool MC = false, bool NCHW = false>
+          bool MC = false, bool NCHW = false, bool PROJ = false>
 __global__ void __launch_bounds__(WP * WK * 64) __attribute__((amdgpu_waves_per_eu(2))) conv_wide(ConvArgs a) {
-    wide_body<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC, EXT, ABL, MC, NCHW>(a);
+    wide_body<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC, EXT, ABL, MC, NCHW, PROJ>(a);
 }
 
 // ============================================================== tile registry
@@ -1186,18 +1276,19 @@ static hipError_t launch_staged(const ConvArgs &a, dim3 grid, size_t lds, hipStr
 }
 
 template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC, bool EXT, int ABL = 0,
-          bool MC = false, bool NCHW = false>
+          bool MC = false, bool NCHW = false, bool PROJ = false>
 static hipError_t launch_wide(const ConvArgs &a, dim3 grid, size_t lds, hipStream_t stream) {
-    hipLaunchKernelGGL((conv_wide<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC, EXT, ABL, MC, NCHW>), grid, dim3(WP * WK * 64),
-                       lds, stream, a);
+    hipLaunchKernelGGL((conv_wide<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC, EXT, ABL, MC, NCHW, PROJ>), grid,
+                       dim3(WP * WK * 64), lds, stream, a);
     return hipGetLastError();
 }
 
 template <int BITS, int WK, int FK, int CK, bool WS>
-static hipError_t launch_prep(const ConvArgs &a, uint8_t *img, int64_t elems, hipStream_t stream) {
+static hipError_t launch_prep(const ConvArgs &a, uint8_t *img, int64_t elems, const uint8_t *wproj,
+                              hipStream_t stream) {
     const int64_t blocks = (elems + 255) / 256;
     hipLaunchKernelGGL((build_filter_image<BITS, FK, WS>), dim3((unsigned)blocks), dim3(256), 0, stream, a, WK * FK * 16, CK,
-                       img, elems);
+                       img, elems, wproj);
     return hipGetLastError();
 }
 
@@ -1273,6 +1364,13 @@ static hipError_t launch_prep(const ConvArgs &a, uint8_t *img, int64_t elems, hi
     {3, 3, &launch_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, false, 0, false, true>,                      \
      reinterpret_cast<const void *>(&conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, false, 0, false, true>), \
      nullptr, nullptr}
+#define QCONV_PROJ_INST(B, WP, WK, FP, FK, CK, EXT)                                                               \
+    {3, 3, &launch_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, EXT, 0, false, false, true>,                \
+     reinterpret_cast<const void *>(&conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, EXT, 0, false, false, true>), \
+     nullptr, nullptr}
+#define QCONV_PROJ_ENTRY(B, WP, WK, FP, FK, CK)                                                                   \
+    {"wide_b" #B "_w" #WP "x" #WK "_f" #FP "x" #FK "_c" #CK, QCONV_PROJ_INST(B, WP, WK, FP, FK, CK, false),         \
+     QCONV_PROJ_INST(B, WP, WK, FP, FK, CK, true)},
 #define QCONV_WIDE_ENTRY(B, WP, WK, FP, FK, CK)                                                                   \
     {QCONV_TILE_INFO(QCONV_VARIANT_WIDE, "wide_b", B, WP, WK, FP, FK, CK, (B == 8), 1),                         \
      QCONV_WIDE_SET(B, WP, WK, FP, FK, CK, false), QCONV_WIDE_SET(B, WP, WK, FP, FK, CK, true),                 \

@@ -1,7 +1,8 @@
-// Measurement aid: a kernel that issues nothing but int8 MFMAs, so the rate
+// Measurement aids: a kernel that issues nothing but int8 MFMAs, so the rate
 // the matrix cores sustain on this device (and the shader clock they ran at)
-// can be measured beside the convolution kernels.  It computes nothing of the
-// convolution.
+// can be measured beside the convolution kernels; and an empty kernel, whose
+// time per launch is the fixed cost every launch of a grid pays.  Neither
+// computes anything of the convolution.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -51,7 +52,21 @@ __global__ void __launch_bounds__(256) mfma_i8_probe(int iters, int32_t *sink, u
     }
 }
 
+// Does nothing: its launches measure the cost of dispatching a grid of this
+// shape (and dynamic LDS size) and of waiting for it to drain.
+__global__ void __launch_bounds__(1024) empty_probe() {}
+
 }  // namespace
+
+hipError_t launch_empty_probe(int blocks, int threads, int lds_bytes, hipStream_t stream) {
+    if (lds_bytes > 64 * 1024) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&empty_probe),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(empty_probe, dim3((unsigned)blocks), dim3((unsigned)threads), (size_t)lds_bytes, stream);
+    return hipGetLastError();
+}
 
 int64_t mfma_probe_ops(int blocks, int iters) {
     return (int64_t)blocks * 4 * iters * kProbeChains * (2 * 16 * 16 * 64);

@@ -32,6 +32,34 @@ class LayerSpec:
     residual_signed: bool = False
 
 
+def projection_pairs(layers) -> dict[int, int]:
+    """Layers that can run as one launch: a 3x3 layer with padding 1 and a 1x1
+    layer without padding that read the same input at the same stride with the
+    same channels and operand types (a residual stage's first convolution and
+    its shortcut projection).  Returns {3x3 layer: 1x1 layer}; the 1x1 layer
+    must come later in the chain and neither may take a residual."""
+    pairs, used = {}, set()
+    for i, A in enumerate(layers):
+        d = A.desc
+        if not (d["r"] == 3 and d["s"] == 3 and d["pad_h"] == 1 and d["pad_w"] == 1) or A.residual_src is not None:
+            continue
+        if int(d.get("nb", 0)) > 1:
+            continue
+        for j in range(i + 1, len(layers)):
+            B = layers[j]
+            e = B.desc
+            if j in used or B.src != A.src or B.residual_src is not None:
+                continue
+            if (e["r"], e["s"], e["pad_h"], e["pad_w"]) != (1, 1, 0, 0):
+                continue
+            if all(e[f] == d[f] for f in ("n", "h", "w", "c", "k", "stride_h", "stride_w", "bits", "x_signed",
+                                         "w_signed")):
+                pairs[i] = j
+                used.add(j)
+                break
+    return pairs
+
+
 def branch_plan(layers) -> tuple[list[bool], list[list[int]]]:
     """Which layers of a chain run on the second stream, and the layers on the
     other stream each one must wait for.
@@ -54,27 +82,62 @@ def branch_plan(layers) -> tuple[list[bool], list[list[int]]]:
 class Chain:
     """Layers on one stream; filters are prepared once for each layer's tile.
 
-    With ``branches``, a layer that the main line of layers steps over (a
-    strided 1x1 projection beside the block's first 3x3) runs on a second
-    stream, so the two convolutions share the chip; events order it
-    after its input and before the layers that read its output, and every
-    forward pass starts and ends with the two streams joined.
+    With ``fuse_projections`` (the default), a strided 3x3 layer and the 1x1
+    projection that reads the same input (:func:`projection_pairs`) run as one
+    launch (qconv2d_proj): the projection's products ride on the 3x3 layer's
+    staged input band, and its output goes to its own buffer.
+
+    With ``branches`` (which turns the fusion off), a layer that the main line
+    of layers steps over (a strided 1x1 projection beside the block's first
+    3x3) runs on a second stream instead, so the two convolutions share the
+    chip; events order it after its input and before the layers that read its
+    output, and every forward pass starts and ends with the two streams joined.
     """
 
-    def __init__(self, layers: list[LayerSpec], x_packed: torch.Tensor, stream=None, branches: bool = False):
+    def __init__(self, layers: list[LayerSpec], x_packed: torch.Tensor, stream=None, branches: bool = False,
+                 fuse_projections: bool = True):
         self.layers = layers
         self.x = x_packed
-        self.calls = []
         self.filters = []
         self.main = stream if stream is not None else torch.cuda.current_stream(x_packed.device)
         self.on_side, self.waits = branch_plan(layers) if branches else ([False] * len(layers),
                                                                           [[] for _ in layers])
+        self.pairs = projection_pairs(layers) if fuse_projections and not branches else {}
+        fused_into = {j: i for i, j in self.pairs.items()}
         self.side = torch.cuda.Stream(device=x_packed.device) if any(self.on_side) else None
         needed = {d for w in self.waits for d in w}
         self.events = [torch.cuda.Event() if i in needed else None for i in range(len(layers))]
+        # one factory per launch: factory(stream) builds the call for that stream;
+        # layers fused into an earlier launch have none
+        self.factories = []
+        proj_out = {}   # 3x3 layer -> the output buffer of the projection fused into its launch
         outs = []
         for i, L in enumerate(layers):
+            if i in fused_into:
+                outs.append(proj_out[fused_into[i]])
+                self.factories.append(None)
+                continue
             inp = self.x if L.src < 0 else outs[L.src]
+            if i in self.pairs:
+                P = layers[self.pairs[i]]
+                tile = L.tile if L.tile != -1 else sweep.tuned_proj_tile(L.desc)
+                wprep = qconv.prepare_filters_proj(L.desc, L.w_packed, P.w_packed, tile)
+                first = qconv.ProjConv2dCall(L.desc, inp, wprep, tile=tile, requant=True, mult=L.mult,
+                                             shift=L.shift, relu=L.relu, clamp=L.clamp, bias=L.bias,
+                                             proj=dict(mult=P.mult, shift=P.shift, relu=P.relu, clamp=P.clamp,
+                                                       bias=P.bias))
+                y, yp = first.out, first.out_proj
+
+                def make(stream, L=L, P=P, inp=inp, wprep=wprep, tile=tile, y=y, yp=yp):
+                    return qconv.ProjConv2dCall(L.desc, inp, wprep, tile=tile, requant=True, mult=L.mult,
+                                                shift=L.shift, relu=L.relu, clamp=L.clamp, bias=L.bias,
+                                                proj=dict(mult=P.mult, shift=P.shift, relu=P.relu, clamp=P.clamp,
+                                                          bias=P.bias), out=y, out_proj=yp, stream=stream)
+                proj_out[i] = yp
+                self.filters.append(wprep)
+                outs.append(y)
+                self.factories.append(make)
+                continue
             tile, splits = L.tile, L.splits
             if tile == -1:
                 tile, tuned_splits = sweep.tuned_config(L.desc)
@@ -85,13 +148,21 @@ class Chain:
             res = None
             if L.residual_src is not None:
                 res = self.x if L.residual_src < 0 else outs[L.residual_src]
-            call = qconv.Conv2dCall(L.desc, inp, wprep, requant=True, mult=L.mult, shift=L.shift,
-                                    relu=L.relu, clamp=L.clamp, tile=tile, stream=self._stream_of(i, self.main),
-                                    prepared=True, splits=splits, bias=L.bias, residual=res,
-                                    residual_signed=L.residual_signed)
-            outs.append(call.out)
-            self.calls.append(call)
+            ws = qconv.make_workspace(L.desc, tile, splits, x_packed.device) if splits > 1 else None
+            first = qconv.Conv2dCall(L.desc, inp, wprep, requant=True, mult=L.mult, shift=L.shift, relu=L.relu,
+                                     clamp=L.clamp, tile=tile, prepared=True, splits=splits, workspace=ws,
+                                     bias=L.bias, residual=res, residual_signed=L.residual_signed)
+
+            def make(stream, L=L, inp=inp, wprep=wprep, tile=tile, splits=splits, ws=ws, res=res, y=first.out):
+                return qconv.Conv2dCall(L.desc, inp, wprep, requant=True, mult=L.mult, shift=L.shift, relu=L.relu,
+                                        clamp=L.clamp, tile=tile, prepared=True, splits=splits, workspace=ws,
+                                        bias=L.bias, residual=res, residual_signed=L.residual_signed, out=y,
+                                        stream=stream)
+            outs.append(first.out)
+            self.factories.append(make)
         self.outputs = outs
+        self.calls = [f(self._stream_of(i, self.main)) if f else None for i, f in enumerate(self.factories)]
+        self.launches = sum(1 for c in self.calls if c is not None)
         self.graph = None
 
     def _stream_of(self, i: int, main):
@@ -101,6 +172,8 @@ class Chain:
         if self.side is not None:
             self.side.wait_stream(main)
         for i, c in enumerate(calls):
+            if c is None:
+                continue
             s = self._stream_of(i, main)
             for d in self.waits[i]:
                 s.wait_event(self.events[d])
@@ -120,12 +193,7 @@ class Chain:
         s.wait_stream(self.main)
         with torch.cuda.stream(s):
             # calls marshal the stream at construction: rebuild them for the capture stream
-            calls = [qconv.Conv2dCall(c.desc, c.x, c.w, requant=True, mult=c.mult, shift=c.epi.shift,
-                                      relu=bool(c.epi.relu), clamp=(c.epi.clamp_lo, c.epi.clamp_hi), out=c.out,
-                                      tile=c.tile, stream=self._stream_of(i, s), prepared=c.prepared,
-                                      splits=c.splits, workspace=getattr(c, "workspace", None), bias=c.bias,
-                                      residual=c.residual, residual_signed=bool(c.epi.residual_signed))
-                     for i, c in enumerate(self.calls)]
+            calls = [f(self._stream_of(i, s)) if f else None for i, f in enumerate(self.factories)]
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g, stream=s):
                 self._run(calls, s)

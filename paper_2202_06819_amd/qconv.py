@@ -21,6 +21,7 @@ import threading
 import torch
 
 from .build import LIB as LIB_PATH
+from .build import source_digest
 
 OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP = 0, -1, -2, -3, -4
 OUT_RAW_I32, OUT_REQUANT = 0, 1
@@ -84,6 +85,12 @@ def lib() -> ctypes.CDLL:
         if not os.path.exists(LIB_PATH):
             raise QConvError(EHIP, f"{LIB_PATH} is not built; run `python -m paper_2202_06819_amd.build`")
         L = ctypes.CDLL(LIB_PATH)
+        L.qconv_build_digest.argtypes = []
+        L.qconv_build_digest.restype = ctypes.c_char_p
+        got, want = L.qconv_build_digest().decode(), source_digest()
+        if got != want:
+            raise QConvError(EHIP, f"{LIB_PATH} was built from other sources (digest {got}, sources {want}); "
+                                   "rebuild it with `python -m paper_2202_06819_amd.build`")
         P = ctypes.POINTER
         L.qconv_layout.argtypes = [P(QConvDesc), P(QConvLayoutInfo)]
         L.qconv_pack.argtypes = [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _vp]
@@ -111,10 +118,20 @@ def lib() -> ctypes.CDLL:
                                       _vp]
         L.qconv2d_scheduled.argtypes = [P(QConvDesc), _vp, _vp, ctypes.c_size_t, P(QConvEpilogue), _vp,
                                         P(QConvSchedule), _vp, ctypes.c_size_t, _vp]
+        L.qconv_probe_launch.argtypes = [_i32, _i32, _i32, _vp]
+        L.qconv_last_launch.argtypes = [P(_i64), P(_i64), P(_i64)]
+        L.qconv_proj_default_tile.argtypes = [P(QConvDesc)]
+        L.qconv_proj_tile_check.argtypes = [P(QConvDesc), _i32]
+        L.qconv_prepared_proj_filter_bytes.argtypes = [P(QConvDesc), _i32, P(ctypes.c_size_t)]
+        L.qconv_prepare_filters_proj.argtypes = [P(QConvDesc), _vp, _vp, _i32, _vp, ctypes.c_size_t, _vp]
+        L.qconv2d_proj.argtypes = [P(QConvDesc), _vp, _vp, ctypes.c_size_t, P(QConvEpilogue), _vp,
+                                   P(QConvEpilogue), _vp, _i32, _vp]
         for f in ("qconv_layout", "qconv_pack", "qconv2d", "qconv_tile_count", "qconv_tile_get", "qconv_tile_check",
                   "qconv_default_tile", "qconv_selftest", "qconv_prepared_filter_bytes", "qconv_prepare_filters",
                   "qconv2d_prepared", "qconv_workspace_bytes", "qconv_max_splits", "qconv_probe_mfma_i8", "qconv_schedule_check", "qconv2d_scheduled", "qconv_unroll", "qconv_pack_interleaved",
-                  "qconv2d_packing"):
+                  "qconv2d_packing", "qconv_probe_launch",
+                  "qconv_last_launch", "qconv_proj_default_tile", "qconv_proj_tile_check",
+                  "qconv_prepared_proj_filter_bytes", "qconv_prepare_filters_proj", "qconv2d_proj"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
         return L
@@ -162,6 +179,12 @@ def default_tile(d: dict) -> int:
 
 def selftest() -> int:
     return lib().qconv_selftest()
+
+
+def build_digest() -> str:
+    """Digest of the sources the loaded library was built from (equal to
+    build.source_digest(): lib() refuses a library built from other sources)."""
+    return lib().qconv_build_digest().decode()
 
 
 def prepared_filter_bytes(d: dict, tile: int = -1) -> int:
@@ -227,6 +250,25 @@ def probe_mfma_i8(blocks: int, iters: int, sink: torch.Tensor, stamps: torch.Ten
                                    _vp(_stream(stream)))
     _check(rc, "qconv_probe_mfma_i8")
     return int(ops.value)
+
+
+def last_launch() -> dict:
+    """Grid, threads and dynamic LDS of this thread's most recent convolution launch."""
+    g, t, l = _i64(0), _i64(0), _i64(0)
+    _check(lib().qconv_last_launch(ctypes.byref(g), ctypes.byref(t), ctypes.byref(l)), "qconv_last_launch")
+    return {"grid": int(g.value), "threads": int(t.value), "lds_bytes": int(l.value)}
+
+
+class ProbeLaunchCall:
+    """The empty-kernel launch probe (a measurement aid) with its arguments
+    marshalled once; ``()`` enqueues one launch."""
+
+    def __init__(self, blocks: int, threads: int, lds_bytes: int = 0, stream=None):
+        self._args = (int(blocks), int(threads), int(lds_bytes), _vp(_stream(stream)))
+        self._fn = lib().qconv_probe_launch
+
+    def __call__(self) -> None:
+        _check(self._fn(*self._args), "qconv_probe_launch")
 
 
 def _stream(stream) -> int:
@@ -483,6 +525,99 @@ class Conv2dCall:
     def __call__(self) -> torch.Tensor:
         _check(self._fn(*self._args), "qconv2d")
         return self.out
+
+
+def proj_default_tile(d: dict) -> int:
+    """The built-in tile for a 3x3 layer with a fused 1x1 projection."""
+    return _check(lib().qconv_proj_default_tile(ctypes.byref(make_desc(d))), "qconv_proj_default_tile")
+
+
+def proj_tile_status(d: dict, tile_id: int) -> int:
+    """QCONV_OK if `tile_id` can run the 3x3 layer `d` with a fused projection."""
+    return lib().qconv_proj_tile_check(ctypes.byref(make_desc(d)), int(tile_id))
+
+
+def proj_desc(d: dict) -> dict:
+    """The 1x1 projection a 3x3 layer can carry: same input, channels and stride, no padding."""
+    return dict(d, r=1, s=1, pad_h=0, pad_w=0)
+
+
+def prepare_filters_proj(d: dict, w_packed: torch.Tensor, w_proj_packed: torch.Tensor, tile: int = -1,
+                         out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Packed 3x3 filters and packed 1x1 projection filters -> one prepared image
+    for `tile` (the projection as its tenth tap)."""
+    desc = make_desc(d)
+    n = ctypes.c_size_t(0)
+    _check(lib().qconv_prepared_proj_filter_bytes(ctypes.byref(desc), int(tile), ctypes.byref(n)),
+           "qconv_prepared_proj_filter_bytes")
+    nbytes = int(n.value)
+    info = layout(d)
+    if out is None:
+        out = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=w_packed.device)
+    rc = lib().qconv_prepare_filters_proj(ctypes.byref(desc), _dev_ptr(w_packed, "w_packed", info["w_bytes"]),
+                                          _dev_ptr(w_proj_packed, "w_proj_packed", info["w_bytes"] // (desc.r * desc.s)),
+                                          int(tile), _dev_ptr(out, "w_prepared", nbytes),
+                                          out.numel() * out.element_size(), _vp(_stream(stream)))
+    _check(rc, "qconv_prepare_filters_proj")
+    return out
+
+
+def _requant_epilogue(desc: QConvDesc, info: dict, mult, shift, relu, clamp, bias=None) -> QConvEpilogue:
+    epi = QConvEpilogue()
+    if mult is None or mult.dtype != torch.int32 or mult.numel() != desc.k:
+        raise QConvError(EINVAL, "requant needs an int32 multiplier per output channel")
+    epi.mode, epi.mult = OUT_REQUANT, _dev_ptr(mult, "mult", 4 * desc.k)
+    epi.shift, epi.relu, epi.clamp_lo, epi.clamp_hi = int(shift), int(bool(relu)), int(clamp[0]), int(clamp[1])
+    _epilogue_extras(epi, desc, info["y_packed_bytes"], bias, None, False)
+    return epi
+
+
+class ProjConv2dCall:
+    """A qconv2d_proj call (a 3x3 layer with its 1x1 projection fused in) with
+    its arguments marshalled once; ``()`` enqueues it and returns (y, y_proj).
+
+    `w_prepared` comes from :func:`prepare_filters_proj` for `tile`.  Raw mode
+    (requant=False) gives both int32 accumulator tensors; requant mode takes
+    each output's own multipliers, shift, ReLU, clamp and optional bias
+    (``proj`` holds the projection's: dict(mult=, shift=, relu=, clamp=, bias=)).
+    """
+
+    def __init__(self, d: dict, x: torch.Tensor, w_prepared: torch.Tensor, *, tile: int = -1, requant: bool = False,
+                 mult: torch.Tensor | None = None, shift: int = 20, relu: bool = True, clamp: tuple = (0, 15),
+                 bias: torch.Tensor | None = None, proj: dict | None = None, out: torch.Tensor | None = None,
+                 out_proj: torch.Tensor | None = None, stream=None):
+        self.desc = make_desc(d)
+        info = layout(d)
+        bits = self.desc.bits
+        shape = (packed_shape(self.desc.n, info["p"], info["q"], self.desc.k, bits) if requant
+                 else raw_shape(self.desc, info))
+        dtype = packed_dtype(bits) if requant else torch.int32
+        out = torch.empty(shape, dtype=dtype, device=x.device) if out is None else out
+        out_proj = torch.empty(shape, dtype=dtype, device=x.device) if out_proj is None else out_proj
+        if requant:
+            pj = proj or {}
+            self.epi = _requant_epilogue(self.desc, info, mult, shift, relu, clamp, bias)
+            self.epi_proj = _requant_epilogue(self.desc, info, pj.get("mult"), pj.get("shift", 20),
+                                              pj.get("relu", True), pj.get("clamp", (0, 15)), pj.get("bias"))
+        else:
+            self.epi, self.epi_proj = QConvEpilogue(), QConvEpilogue()
+            self.epi.mode = self.epi_proj.mode = OUT_RAW_I32
+        self.tile = proj_default_tile(d) if tile == -1 else int(tile)
+        n = ctypes.c_size_t(0)
+        _check(lib().qconv_prepared_proj_filter_bytes(ctypes.byref(self.desc), self.tile, ctypes.byref(n)),
+               "qconv_prepared_proj_filter_bytes")
+        y_bytes = info["y_packed_bytes"] if requant else info["y_raw_bytes"]
+        self.x, self.w, self.out, self.out_proj, self.info = x, w_prepared, out, out_proj, info
+        self.keep = (mult, bias, proj)
+        self._args = (ctypes.byref(self.desc), _dev_ptr(x, "x", info["x_bytes"]),
+                      _dev_ptr(w_prepared, "w", int(n.value)), w_prepared.numel() * w_prepared.element_size(),
+                      ctypes.byref(self.epi), _dev_ptr(out, "y", y_bytes), ctypes.byref(self.epi_proj),
+                      _dev_ptr(out_proj, "y_proj", y_bytes), self.tile, _vp(_stream(stream)))
+        self._fn = lib().qconv2d_proj
+
+    def __call__(self):
+        _check(self._fn(*self._args), "qconv2d_proj")
+        return self.out, self.out_proj
 
 
 class PackingConv2dCall:

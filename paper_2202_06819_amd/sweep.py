@@ -65,6 +65,22 @@ def tuned_tile(d: dict, requant: bool = True) -> int:
     return tuned_config(d, requant)[0]
 
 
+def proj_key(d: dict, requant: bool = True) -> str:
+    """Tuned-table key of a 3x3 layer with its 1x1 projection fused in."""
+    return shape_key(d, requant) + "_proj"
+
+
+def tuned_proj_tile(d: dict, requant: bool = True) -> int:
+    """The swept best tile for the 3x3 layer `d` with a fused projection (the
+    library's built-in choice when unswept)."""
+    entry = tuned_table().get(proj_key(d, requant))
+    if entry:
+        for t in qconv.tiles():
+            if t["name"] == entry["tile"] and qconv.proj_tile_status(d, t["id"]) == 0:
+                return t["id"]
+    return qconv.proj_default_tile(d)
+
+
 def split_choices(d: dict, tile: int) -> list[int]:
     """Split-K factors worth timing: 1 and the powers of two up to the chunk count."""
     top = max(1, qconv.max_splits(d, tile))
@@ -103,16 +119,22 @@ def _time(make_call, reps: int, rounds: int) -> float:
 
 
 def sweep_layer(d: dict, x: torch.Tensor, w: torch.Tensor, mult: torch.Tensor | None, *, shift=20, relu=True,
-                clamp=(0, 15), reps=100, rounds=5, done=frozenset(), log=print) -> list[dict]:
-    """Measure every valid tile on one shape; returns result rows."""
+                clamp=(0, 15), reps=100, rounds=5, done=frozenset(), log=print,
+                expected: torch.Tensor | None = None) -> list[dict]:
+    """Measure every valid tile on one shape; returns result rows.  Every
+    candidate's output must equal `expected` (a caller's reference output, e.g.
+    a test's), or else the built-in tile's output from the packed filters."""
     requant = mult is not None
     key = shape_key(d, requant)
     info = qconv.layout(d)
     ops = 2 * info["macs"]
     default = qconv.default_tile(d)
-    ref_call = qconv.Conv2dCall(d, x, w, requant=requant, mult=mult, shift=shift, relu=relu, clamp=clamp,
-                                tile=default)
-    ref = ref_call().clone()   # packed filters, default tile
+    if expected is None:
+        ref_call = qconv.Conv2dCall(d, x, w, requant=requant, mult=mult, shift=shift, relu=relu, clamp=clamp,
+                                    tile=default)
+        ref = ref_call().clone()   # packed filters, default tile
+    else:
+        ref = expected.to(x.device)
     rows = []
     for t in qconv.tiles():
         if qconv.tile_status(d, t["id"]) != 0:
@@ -130,7 +152,7 @@ def sweep_layer(d: dict, x: torch.Tensor, w: torch.Tensor, mult: torch.Tensor | 
 
             out = make()()
             torch.cuda.synchronize()
-            same = bool(torch.equal(out, ref))
+            same = out.shape == ref.shape and bool(torch.equal(out.view(ref.dtype), ref))
             us = _time(make, reps, rounds)
             tops = ops / (us * 1e-6) / 1e12
             row = {"shape": key, "tile": t["name"], "tile_id": t["id"], "splits": splits,
@@ -139,7 +161,48 @@ def sweep_layer(d: dict, x: torch.Tensor, w: torch.Tensor, mult: torch.Tensor | 
             rows.append(row)
             log(json.dumps(row))
             if not same:
-                raise RuntimeError(f"tile {t['name']} splits {splits} output differs from tile {default} on {key}")
+                raise RuntimeError(f"tile {t['name']} splits {splits} output differs from the reference on {key}")
+    return rows
+
+
+def sweep_proj_layer(d: dict, x: torch.Tensor, w3: torch.Tensor, w1: torch.Tensor, mult: torch.Tensor | None,
+                     mult2: torch.Tensor | None, *, shift=20, shift2=20, relu=True, relu2=False, clamp=(0, 15),
+                     reps=100, rounds=5, done=frozenset(), log=print, expected=None) -> list[dict]:
+    """Every tile with a projection instance on a 3x3 layer with its 1x1
+    projection fused in (packed filters w3 and w1); both outputs of each must
+    equal `expected` = (y, y_proj), or else the built-in tile's."""
+    requant = mult is not None
+    key = proj_key(d, requant)
+    ops = 2 * qconv.layout(d)["macs"] + 2 * qconv.layout(qconv.proj_desc(d))["macs"]
+    default = qconv.proj_default_tile(d)
+    kw = dict(requant=True, mult=mult, shift=shift, relu=relu, clamp=clamp,
+              proj=dict(mult=mult2, shift=shift2, relu=relu2, clamp=clamp)) if requant else {}
+
+    def make_for(tid, wprep, stream=None):
+        return qconv.ProjConv2dCall(d, x, wprep, tile=tid, stream=stream, **kw)
+
+    if expected is None:
+        y, yp = make_for(default, qconv.prepare_filters_proj(d, w3, w1, default))()
+        ref = (y.clone(), yp.clone())
+    else:
+        ref = tuple(e.to(x.device) for e in expected)
+    rows = []
+    for t in qconv.tiles():
+        if qconv.proj_tile_status(d, t["id"]) != 0 or (key, t["name"], 1) in done:
+            continue
+        wprep = qconv.prepare_filters_proj(d, w3, w1, t["id"])
+        y, yp = make_for(t["id"], wprep)()
+        torch.cuda.synchronize()
+        same = all(o.shape == r.shape and bool(torch.equal(o.view(r.dtype), r)) for o, r in zip((y, yp), ref))
+        us = _time(lambda stream, tid=t["id"], wprep=wprep: make_for(tid, wprep, stream), reps, rounds)
+        tops = ops / (us * 1e-6) / 1e12
+        row = {"shape": key, "tile": t["name"], "tile_id": t["id"], "splits": 1, "default": t["id"] == default,
+               "us": round(us, 3), "tops": round(tops, 2), "pct_int8_peak": round(100 * tops / INT8_PEAK_TOPS, 3),
+               "identical": same}
+        rows.append(row)
+        log(json.dumps(row))
+        if not same:
+            raise RuntimeError(f"tile {t['name']} (fused projection) output differs from the reference on {key}")
     return rows
 
 
@@ -161,6 +224,9 @@ def main(argv=None) -> int:
     ap.add_argument("--reps", type=int, default=100)
     ap.add_argument("--rounds", type=int, default=5)
     ap.add_argument("--write-tuned", action="store_true", help="merge the best tiles into tuned_tiles.json")
+    ap.add_argument("--proj", action="store_true",
+                    help="also sweep the stage entries of workloads 2 and 3 with their projections fused in")
+    ap.add_argument("--proj-only", action="store_true", help="sweep only those fused stage entries")
     args = ap.parse_args(argv)
 
     done = set()
@@ -181,7 +247,7 @@ def main(argv=None) -> int:
             layers = qi.WORKLOADS[cfg]()
             if cfg in (2, 3):
                 layers = qi.distinct(layers)
-            for lid, L in enumerate(layers):
+            for lid, L in enumerate([] if args.proj_only else layers):
                 t = qi.layer_tensors(cfg, lid, L)
                 x = qconv.pack(torch.from_numpy(t["x"]).to(dev), L.bits, L.x_signed)
                 w = qconv.pack(torch.from_numpy(t["w"]).to(dev), L.bits, L.w_signed)
@@ -191,6 +257,24 @@ def main(argv=None) -> int:
                 rows += sweep_layer(L.desc(), x, w, mult, shift=e.shift if e else 20, relu=e.relu if e else False,
                                     clamp=(e.lo, e.hi) if e else (0, 15), reps=args.reps, rounds=args.rounds,
                                     done=frozenset(done), log=log)
+            if (args.proj or args.proj_only) and cfg in (2, 3):
+                full = qi.WORKLOADS[cfg]()
+                names = [L.name for L in full]
+                for i, L in enumerate(full):
+                    if not (L.name.endswith(".0.conv1") and L.stride == 2):
+                        continue
+                    j = names.index(L.name.replace("conv1", "downsample"))
+                    P = full[j]
+                    t, tp = qi.layer_tensors(cfg, i, L), qi.layer_tensors(cfg, j, P)
+                    x = qconv.pack(torch.from_numpy(t["x"]).to(dev), L.bits, L.x_signed)
+                    w3 = qconv.pack(torch.from_numpy(t["w"]).to(dev), L.bits, L.w_signed)
+                    w1 = qconv.pack(torch.from_numpy(tp["w"]).to(dev), P.bits, P.w_signed)
+                    e, ep = L.epilogue, P.epilogue
+                    print(f"# workload {cfg} fused {L.name} + {P.name}", flush=True)
+                    rows += sweep_proj_layer(L.desc(), x, w3, w1, torch.from_numpy(t["mult"]).to(dev),
+                                             torch.from_numpy(tp["mult"]).to(dev), shift=e.shift, shift2=ep.shift,
+                                             relu=e.relu, relu2=ep.relu, clamp=(e.lo, e.hi), reps=args.reps,
+                                             rounds=args.rounds, done=frozenset(done), log=log)
     best = best_per_shape(rows)
     for key, r in sorted(best.items()):
         dflt = [x for x in rows if x["shape"] == key and x["default"]]

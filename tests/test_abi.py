@@ -21,8 +21,7 @@ HEADER = os.path.join(ROOT, "include", "qconv.h")
 @pytest.fixture(scope="module")
 def q():
     from paper_2202_06819_amd import build, qconv
-    if not os.path.exists(build.LIB):
-        build.build()
+    build.ensure_built()
     return qconv
 
 
@@ -46,6 +45,12 @@ def test_library_exports_every_declared_symbol(q):
 
 def test_selftest(q):
     assert q.selftest() == 0
+
+
+def test_build_digest_matches_sources(q):
+    from paper_2202_06819_amd import build
+    assert q.build_digest() == build.source_digest() == build.built_digest()
+    assert re.fullmatch(r"[0-9a-f]{16}", q.build_digest())
 
 
 def D(**kw):
@@ -465,3 +470,34 @@ def test_fused_pack_argument_errors(q):
     assert call(D(n=2, stride_h=4, stride_w=4)) == -2                    # bands skip rows: no packed copy
     assert call(D(n=2), xp_=xp + 8) == -1                                # misaligned packed copy
     assert call(D(n=2), xp_=x + 64) == -1                                # packed copy overlaps x
+
+
+def test_projection_entry_points_validate_on_the_host(q):
+    """Shapes a fused projection cannot ride on are refused before any launch."""
+    d = D(n=2, h=9, w=9, stride_h=2, stride_w=2)
+    t = q.proj_default_tile(d)
+    assert q.proj_tile_status(d, t) == q.OK
+    assert q.tiles()[t]["name"] in {"wide_b4_w4x2_f2x2_c64", "wide_b4_w2x2_f2x2_c64", "wide_b4_w4x1_f2x4_c64",
+                                    "wide_b4_w4x2_f2x2_c128"}
+    assert q.proj_tile_status(D(pad_h=0, pad_w=0), t) == q.EUNSUPPORTED        # the centre tap moves
+    assert q.proj_tile_status(D(r=1, s=1, pad_h=0, pad_w=0), t) == q.EUNSUPPORTED
+    assert q.proj_tile_status(D(nb=2), t) == q.EUNSUPPORTED
+    staged = next(tt["id"] for tt in q.tiles() if tt["variant"] == 0 and tt["bits"] == 4)
+    assert q.proj_tile_status(d, staged) == q.EUNSUPPORTED
+    # the image carries one more tap than the plain 3x3 image of the same tile
+    plain = q.prepared_filter_bytes(d, t)
+    n = ctypes.c_size_t(0)
+    assert q.lib().qconv_prepared_proj_filter_bytes(ctypes.byref(q.make_desc(d)), t, ctypes.byref(n)) == q.OK
+    assert n.value >= plain
+    # mismatched epilogue modes and residuals are refused
+    desc = q.make_desc(d)
+    raw, rq = q.QConvEpilogue(), q.QConvEpilogue()
+    raw.mode = q.OUT_RAW_I32
+    rq.mode, rq.mult, rq.shift, rq.relu, rq.clamp_lo, rq.clamp_hi = q.OUT_REQUANT, 1 << 20, 20, 1, 0, 15
+    args = (ctypes.byref(desc), 1 << 20, 2 << 20, 1 << 30)
+    assert q.lib().qconv2d_proj(*args, ctypes.byref(raw), 3 << 20, ctypes.byref(rq), 4 << 20, t, None) == q.EINVAL
+    rq2 = q.QConvEpilogue.from_buffer_copy(rq)
+    rq2.residual = 5 << 20
+    assert q.lib().qconv2d_proj(*args, ctypes.byref(rq), 3 << 20, ctypes.byref(rq2), 4 << 20, t, None) \
+        == q.EUNSUPPORTED
+    assert q.lib().qconv2d_proj(*args, ctypes.byref(rq), 3 << 20, ctypes.byref(rq), None, t, None) == q.EINVAL

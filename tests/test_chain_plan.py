@@ -66,3 +66,37 @@ def test_layer_feeding_the_next_stays_on_the_first_stream():
     specs = [SimpleNamespace(src=-1, residual_src=None), SimpleNamespace(src=0, residual_src=None),
              SimpleNamespace(src=0, residual_src=1)]
     assert branch_plan(specs)[0] == [False, False, False]
+
+
+def _desc_specs(plan):
+    return [SimpleNamespace(name=L.name, desc=L.desc(), src=src, residual_src=short) for L, src, short, _ in plan]
+
+
+def test_resnet18_stage_entries_pair_with_their_projections():
+    """Each stage's strided 3x3 and its 1x1 projection read the block input:
+    they form the three fused launches, in plain and in residual order."""
+    from paper_2202_06819_amd.nets import projection_pairs
+    for layers in (qi.workload2(), qi.workload3()):
+        for specs in (_desc_specs([(L, L.src, None, i) for i, L in enumerate(layers)]),
+                      _desc_specs(bench.residual_order(layers))):
+            pairs = projection_pairs(specs)
+            assert sorted((specs[i].name, specs[j].name) for i, j in pairs.items()) == \
+                [(f"l{k}.0.conv1", f"l{k}.0.downsample") for k in (2, 3, 4)]
+            for i, j in pairs.items():
+                assert i < j and specs[i].src == specs[j].src
+            assert len(specs) - len(pairs) == 16   # launches per forward pass
+
+
+def test_projection_pairs_need_the_same_input_and_stride():
+    from paper_2202_06819_amd.nets import projection_pairs
+    d3 = dict(n=2, h=8, w=8, c=64, k=64, r=3, s=3, stride_h=2, stride_w=2, pad_h=1, pad_w=1, bits=4, x_signed=0,
+              w_signed=1)
+    d1 = dict(d3, r=1, s=1, pad_h=0, pad_w=0)
+    mk = lambda d, src, res=None: SimpleNamespace(desc=d, src=src, residual_src=res)
+    assert projection_pairs([mk(d3, -1), mk(d1, -1)]) == {0: 1}
+    assert projection_pairs([mk(d3, -1), mk(d1, 0)]) == {}                          # other input
+    assert projection_pairs([mk(d3, -1), mk(dict(d1, stride_h=1, stride_w=1), -1)]) == {}   # other stride
+    assert projection_pairs([mk(d3, -1), mk(dict(d1, k=128), -1)]) == {}            # other channels
+    assert projection_pairs([mk(dict(d3, pad_h=0, pad_w=0), -1), mk(d1, -1)]) == {}  # centre tap moves
+    assert projection_pairs([mk(d3, -1), mk(d1, -1, res=0)]) == {}                  # projection with a residual
+    assert projection_pairs([mk(d1, -1), mk(d3, -1)]) == {}                         # the 1x1 must come later
