@@ -374,6 +374,34 @@ int qconv_max_splits(const qconv_desc *d, int32_t tile_id);
 int qconv_workspace_bytes(const qconv_desc *d, int32_t tile_id, int32_t splits, size_t *bytes);
 
 /*
+ * qconv2d_prepared_noalloc -- for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): qconv2d_prepared without a workspace argument.  A split-K call
+ * keeps its partial sums and arrival counters in a scratch array the library
+ * holds in each GPU's memory (a static device array, present from the load of
+ * the library to the end of the process), so nothing is allocated, freed or
+ * memset by the call; the caller still passes x, the prepared filters and y.
+ * Results are identical to qconv2d_prepared with the same tile and splits.
+ *   Limit: the split-K partial sums (tiles x splits x tile_p x tile_k int32)
+ *   must fit the scratch, and the output tiles its counters; qconv_noalloc_limits
+ *   gives both (16 MiB minus 64 KiB, 16384 tiles).  Larger requests return
+ *   QCONV_EWORKSPACE before anything is enqueued.  splits == 1 uses no scratch.
+ *   Set-up: the first call on a device looks up that device's copy of the
+ *   array and enqueues, on `stream`, the clearing of its counters (a small
+ *   kernel, no memset); every split-K launch leaves them at zero again.
+ *   Concurrency: all calls on one GPU share its scratch, which keeps the last
+ *   call's contents; split-K calls that overlap in time on one GPU (other
+ *   streams, other threads) race and give wrong results.  Serialise them.
+ * Errors as qconv2d_prepared.
+ */
+int qconv2d_prepared_noalloc(const qconv_desc *d, const void *x, const void *w_prepared, size_t w_prepared_bytes,
+                             const qconv_epilogue *epi, void *y, int32_t tile_id, int32_t splits, void *stream);
+
+/* Host only: the no-alloc scratch's capacity for split-K partial sums (bytes) and
+ * output tiles (counters); either pointer may be NULL.  Returns QCONV_OK. */
+int qconv_noalloc_limits(int64_t *scratch_bytes, int64_t *max_tiles);
+
+/*
  * Schedules.  The knobs of the schedule search space (Sec. 4.1: warps per
  * block along M and N, MMA tiles per warp along M and N, the input-channel
  * chunk -- here fixed per compiled tile -- and the loop order), as they exist

@@ -419,6 +419,57 @@ DevAttrCache g_attr;
 
 }  // namespace
 
+// ---- the device scratch of qconv2d_prepared_noalloc: the split-K workspace
+// for callers that cannot allocate.  One array per device (each GPU the
+// library runs on holds its own copy until the process ends).  Layout: the
+// arrival counters first, at a fixed place, then the partial sums.  The
+// array's name is only a host-side stand-in: host code uses the address
+// hipGetSymbolAddress gives for the current device, never the name itself.
+constexpr int64_t kScratchBytes = 16ll << 20;
+constexpr int64_t kScratchCounterBytes = 64ll << 10;   // up to 16384 output tiles
+__device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+__global__ void __launch_bounds__(256) clear_words(uint32_t *p, int32_t n) {
+    const int32_t i = (int32_t)(blockIdx.x * 256 + threadIdx.x);
+    if (i < n) p[i] = 0u;   // a vector store (no scalar-cache writes)
+}
+
+namespace {
+
+struct ScratchCache {
+    std::mutex mu;
+    std::unordered_map<int, uint8_t *> ptr;   // device -> its copy of `scratch`
+};
+ScratchCache g_scratch;
+
+// The current device's scratch address; on the first call on a device, also
+// enqueues (on `stream`) the clearing of its arrival counters, which every
+// split-K launch then leaves at zero again.
+int scratch_for_current_device(hipStream_t stream, uint8_t **out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return fail(QCONV_EHIP, "hipGetDevice failed");
+    std::lock_guard<std::mutex> g(g_scratch.mu);
+    auto it = g_scratch.ptr.find(dev);
+    if (it != g_scratch.ptr.end()) {
+        *out = it->second;
+        return QCONV_OK;
+    }
+    void *p = nullptr;
+    hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+        return fail(QCONV_EHIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    const int32_t words = (int32_t)(kScratchCounterBytes / 4);
+    hipLaunchKernelGGL(clear_words, dim3((unsigned)((words + 255) / 256)), dim3(256), 0, stream,
+                       static_cast<uint32_t *>(p), words);
+    e = hipGetLastError();
+    if (e != hipSuccess) return fail(QCONV_EHIP, "scratch clear launch: %s", hipGetErrorString(e));
+    g_scratch.ptr[dev] = static_cast<uint8_t *>(p);
+    *out = static_cast<uint8_t *>(p);
+    return QCONV_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 const char *qconv_build_digest(void) { return kDigestMarker + sizeof("QCONV_SOURCE_DIGEST=") - 1; }
@@ -606,7 +657,8 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
              const qconv_epilogue *epi, void *y, void *workspace, size_t workspace_bytes, int32_t tile_id,
              int32_t splits, void *stream, int32_t wg_per_cu = 0, int32_t band_buffers = 0,
              int32_t xcd_order = 1, int32_t ablation = 0, const int8_t *x_nchw = nullptr,
-             void *x_packed = nullptr, const qconv_epilogue *epi_proj = nullptr, void *y_proj = nullptr) {
+             void *x_packed = nullptr, bool noalloc = false, const qconv_epilogue *epi_proj = nullptr,
+             void *y_proj = nullptr) {
     qconv_layout_info li;
     qconv_desc kd;
     int rc = kernel_desc(d, &kd, &li);
@@ -653,7 +705,24 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
     if (proj && !pi) return fail(QCONV_EUNSUPPORTED, "tile %s has no projection instance", te.info.name);
     rc = plan_tile(d, li, te.info, &pl, 0, splits, false, ablation, proj);
     if (rc) return rc;
-    const int64_t wsb = split_workspace_bytes(te.info, pl);
+    int64_t wsb = split_workspace_bytes(te.info, pl);
+    uint8_t *ws_cnt = nullptr;   // noalloc: the scratch's counters (its partial sums are `workspace`)
+    if (noalloc && wsb > 0) {
+        // the library's own scratch: counters at its start, partial sums after them
+        const int64_t part = split_part_bytes(te.info, pl), tiles = pl.mtiles * pl.ktiles;
+        if (tiles * 4 > kScratchCounterBytes || part > kScratchBytes - kScratchCounterBytes)
+            return fail(QCONV_EWORKSPACE, "split-K of %lld tiles x %lld splits needs %lld bytes of partial sums and "
+                        "%lld counters; the no-alloc scratch holds %lld bytes and %lld counters",
+                        (long long)tiles, (long long)pl.splits, (long long)part, (long long)tiles,
+                        (long long)(kScratchBytes - kScratchCounterBytes), (long long)(kScratchCounterBytes / 4));
+        uint8_t *base = nullptr;
+        rc = scratch_for_current_device((hipStream_t)stream, &base);
+        if (rc) return rc;
+        ws_cnt = base;
+        workspace = base + kScratchCounterBytes;
+        workspace_bytes = (size_t)part;
+        wsb = part;
+    }
     if (wsb > 0) {
         if (!workspace || (int64_t)workspace_bytes < wsb)
             return fail(QCONV_EWORKSPACE, "split-K workspace of %zu bytes, need %lld", workspace ? workspace_bytes : 0,
@@ -785,7 +854,8 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
     a.xcd_order = xcd_order;
     if (wsb > 0) {
         a.ws_part = static_cast<int32_t *>(workspace);
-        a.ws_cnt = reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(workspace) + split_part_bytes(te.info, pl));
+        a.ws_cnt = reinterpret_cast<uint32_t *>(ws_cnt ? ws_cnt
+                                                       : static_cast<uint8_t *>(workspace) + split_part_bytes(te.info, pl));
     }
     if (a.w_image) a.wbytes = (int32_t)wb;
     a.mode = requant ? QCONV_OUT_REQUANT : QCONV_OUT_RAW_I32;
@@ -960,6 +1030,13 @@ int qconv2d_prepared(const qconv_desc *d, const void *x, const void *w_prepared,
                     stream);
 }
 
+int qconv2d_prepared_noalloc(const qconv_desc *d, const void *x, const void *w_prepared, size_t w_prepared_bytes,
+                             const qconv_epilogue *epi, void *y, int32_t tile_id, int32_t splits, void *stream) {
+    g_err[0] = 0;
+    return run_conv(d, x, w_prepared, true, w_prepared_bytes, epi, y, nullptr, 0, tile_id, splits, stream, 0, 0, 1, 0,
+                    nullptr, nullptr, true);
+}
+
 // The tile a layer with a fused projection runs (tile_id, or the built-in
 // choice for -1) and its plan; the descriptor is already the kernel's.
 static int proj_tile_plan(const qconv_desc *d, const qconv_layout_info &li, int32_t tile_id, Plan *pl) {
@@ -1050,7 +1127,14 @@ int qconv2d_proj(const qconv_desc *d, const void *x, const void *w_prepared, siz
     g_err[0] = 0;
     if (!y_proj) return fail(QCONV_EINVAL, "y_proj must be non-NULL");
     return run_conv(d, x, w_prepared, true, w_prepared_bytes, epi, y, nullptr, 0, tile_id, 1, stream, 0, 0, 1, 0,
-                    nullptr, nullptr, epi_proj, y_proj);
+                    nullptr, nullptr, false, epi_proj, y_proj);
+}
+
+int qconv_noalloc_limits(int64_t *scratch_bytes, int64_t *max_tiles) {
+    g_err[0] = 0;
+    if (scratch_bytes) *scratch_bytes = kScratchBytes - kScratchCounterBytes;
+    if (max_tiles) *max_tiles = kScratchCounterBytes / 4;
+    return QCONV_OK;
 }
 
 int qconv2d_packing(const qconv_desc *d, const int8_t *x_nchw, void *x_packed, const void *w_prepared,

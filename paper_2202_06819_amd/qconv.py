@@ -118,6 +118,9 @@ def lib() -> ctypes.CDLL:
                                       _vp]
         L.qconv2d_scheduled.argtypes = [P(QConvDesc), _vp, _vp, ctypes.c_size_t, P(QConvEpilogue), _vp,
                                         P(QConvSchedule), _vp, ctypes.c_size_t, _vp]
+        L.qconv2d_prepared_noalloc.argtypes = [P(QConvDesc), _vp, _vp, ctypes.c_size_t, P(QConvEpilogue), _vp,
+                                               _i32, _i32, _vp]
+        L.qconv_noalloc_limits.argtypes = [P(_i64), P(_i64)]
         L.qconv_probe_launch.argtypes = [_i32, _i32, _i32, _vp]
         L.qconv_last_launch.argtypes = [P(_i64), P(_i64), P(_i64)]
         L.qconv_proj_default_tile.argtypes = [P(QConvDesc)]
@@ -129,7 +132,7 @@ def lib() -> ctypes.CDLL:
         for f in ("qconv_layout", "qconv_pack", "qconv2d", "qconv_tile_count", "qconv_tile_get", "qconv_tile_check",
                   "qconv_default_tile", "qconv_selftest", "qconv_prepared_filter_bytes", "qconv_prepare_filters",
                   "qconv2d_prepared", "qconv_workspace_bytes", "qconv_max_splits", "qconv_probe_mfma_i8", "qconv_schedule_check", "qconv2d_scheduled", "qconv_unroll", "qconv_pack_interleaved",
-                  "qconv2d_packing", "qconv_probe_launch",
+                  "qconv2d_packing", "qconv2d_prepared_noalloc", "qconv_noalloc_limits", "qconv_probe_launch",
                   "qconv_last_launch", "qconv_proj_default_tile", "qconv_proj_tile_check",
                   "qconv_prepared_proj_filter_bytes", "qconv_prepare_filters_proj", "qconv2d_proj"):
             getattr(L, f).restype = ctypes.c_int
@@ -214,6 +217,14 @@ def workspace_bytes(d: dict, tile: int = -1, splits: int = 1) -> int:
     _check(lib().qconv_workspace_bytes(ctypes.byref(make_desc(d)), int(tile), int(splits), ctypes.byref(n)),
            "qconv_workspace_bytes")
     return int(n.value)
+
+
+def noalloc_limits() -> dict:
+    """Capacity of qconv2d_prepared_noalloc's device scratch: bytes of split-K
+    partial sums and output tiles (arrival counters)."""
+    b, t = _i64(0), _i64(0)
+    _check(lib().qconv_noalloc_limits(ctypes.byref(b), ctypes.byref(t)), "qconv_noalloc_limits")
+    return {"scratch_bytes": int(b.value), "max_tiles": int(t.value)}
 
 
 def make_workspace(d: dict, tile: int, splits: int, device) -> torch.Tensor | None:
@@ -396,12 +407,15 @@ def conv2d(d: dict, x: torch.Tensor, w: torch.Tensor, *, requant: bool = False, 
            shift: int = 20, relu: bool = True, clamp: tuple = (0, 15), out: torch.Tensor | None = None,
            tile: int = -1, workspace: torch.Tensor | None = None, stream=None,
            prepared: bool = False, splits: int = 1, bias: torch.Tensor | None = None,
-           residual: torch.Tensor | None = None, residual_signed: bool = False) -> torch.Tensor:
+           residual: torch.Tensor | None = None, residual_signed: bool = False,
+           noalloc: bool = False) -> torch.Tensor:
     """The convolution with its fused epilogue; returns the output tensor.
 
     Raw mode: int32 N x P x Q x K accumulators.  Requant mode: the packed
     b-bit output (the next layer's input layout).  With ``prepared`` the
-    filters `w` come from :func:`prepare_filters` for the same `tile`.
+    filters `w` come from :func:`prepare_filters` for the same `tile`; with
+    ``noalloc`` as well, the call goes through qconv2d_prepared_noalloc (a
+    split-K uses the library's device scratch instead of `workspace`).
     """
     desc = make_desc(d)
     info = layout(d)
@@ -424,6 +438,15 @@ def conv2d(d: dict, x: torch.Tensor, w: torch.Tensor, *, requant: bool = False, 
     ws_ptr, ws_bytes = (None, 0) if workspace is None else (_dev_ptr(workspace, "workspace"),
                                                            workspace.numel() * workspace.element_size())
     y_bytes = info["y_packed_bytes"] if requant else info["y_raw_bytes"]
+    if noalloc:
+        if not prepared or workspace is not None:
+            raise QConvError(EINVAL, "noalloc runs prepared filters and takes no workspace")
+        wb = prepared_filter_bytes(d, tile)
+        rc = lib().qconv2d_prepared_noalloc(ctypes.byref(desc), _dev_ptr(x, "x", info["x_bytes"]),
+                                            _dev_ptr(w, "w", wb), w.numel() * w.element_size(), ctypes.byref(epi),
+                                            _dev_ptr(out, "y", y_bytes), int(tile), int(splits), _vp(_stream(stream)))
+        _check(rc, "qconv2d_prepared_noalloc")
+        return out
     if prepared:
         wb = prepared_filter_bytes(d, tile)
         rc = lib().qconv2d_prepared(ctypes.byref(desc), _dev_ptr(x, "x", info["x_bytes"]), _dev_ptr(w, "w", wb),

@@ -53,6 +53,23 @@ def test_build_digest_matches_sources(q):
     assert re.fullmatch(r"[0-9a-f]{16}", q.build_digest())
 
 
+def test_noalloc_limits_and_oversized_split(q):
+    """The no-alloc entry point states its scratch capacity and rejects a
+    split-K whose partial sums exceed it on the host, before any device call."""
+    lim = q.noalloc_limits()
+    assert lim == {"scratch_bytes": (16 << 20) - (64 << 10), "max_tiles": 16384}
+    d = q.make_desc(D(n=64, c=256, k=256))
+    e = q.QConvEpilogue()
+    e.mode = q.OUT_RAW_I32
+    t = next(t["id"] for t in q.tiles() if t["variant"] == 2 and t["bits"] == 4 and q.tile_status(D(n=64, c=256, k=256), t["id"]) == 0)
+    splits = q.max_splits(D(n=64, c=256, k=256), t)
+    assert splits >= 2
+    rc = q.lib().qconv2d_prepared_noalloc(ctypes.byref(d), 1 << 20, 2 << 20, 1 << 40, ctypes.byref(e), 1 << 40,
+                                           t, splits, None)
+    assert rc == q.EWORKSPACE, q.lib().qconv_last_error()
+    assert b"no-alloc scratch" in q.lib().qconv_last_error()
+
+
 def D(**kw):
     base = dict(n=8, h=56, w=56, c=64, k=64, r=3, s=3, stride_h=1, stride_w=1, pad_h=1, pad_w=1, bits=4,
                 x_signed=0, w_signed=1)
