@@ -428,7 +428,10 @@ int qconv_noalloc_limits(int64_t *scratch_bytes, int64_t *max_tiles);
  *                 pixel is staged once per filter tap, as the lowered matrix;
  *                 2 = register-level packing (Sec. 3.2) -- the int32
  *                 accumulators pass through LDS to a separate requantise and
- *                 pack step.  Compiled for 4-bit 3x3 layers on the tiles
+ *                 pack step; 4 = widening at staging -- the 4-bit activations
+ *                 stay packed in LDS and every fragment is widened to int8
+ *                 after its LDS read, inside the MFMA loop.  Every subset
+ *                 (1 .. 7) is compiled for 4-bit 3x3 layers on the tiles
  *                 wide_b4_w4x1_f1x4_c64, wide_b4_w8x1_f1x4_c64 and
  *                 wide_b4_w4x1_f2x4_c64, without split, bias or residual;
  *                 QCONV_EUNSUPPORTED otherwise.  Results are identical.

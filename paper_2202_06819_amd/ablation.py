@@ -1,17 +1,21 @@
 """Ablation of the techniques on one MI355X (the study of Sec. 4.4, restated).
 
 For each layer and each tile that has ablation instances, the same schedule
-is timed with techniques switched off (``qconv_schedule.ablation``):
+is timed with techniques switched off (``qconv_schedule.ablation``, a bit
+mask of the techniques switched off):
 
-    3  baseline: lowered staging (every pixel once per filter tap) and int32
-       accumulators through LDS to a separate requantise-and-pack step
-    2  + duplicate-aware loading (Sec. 3.1): the input band, staged once
-    1  + register-level packing (Sec. 3.2) alone, lowered staging kept
-    0  both techniques (the normal kernels)
+    1  duplicate-aware loading (Sec. 3.1): without it every tile pixel is
+       staged once per filter tap, as the lowered matrix
+    2  register-level packing (Sec. 3.2): without it the int32 accumulators go
+       through LDS to a separate requantise-and-pack step
+    4  widening at staging: without it the 4-bit activations stay packed in
+       LDS and every fragment is widened inside the MFMA loop
 
-Accumulated speedup (Fig. 15): 3 -> 2 -> 0.  Marginal speedup of a technique
-(Fig. 16): the time with only that technique switched off over the time
-with both on.  Every output is checked against the default schedule's.
+Accumulated speedup (Fig. 15): 7 (all off) -> 6 (+ duplicate-aware) -> 4
+(+ register packing) -> 0 (+ widening at staging: the normal kernels).
+Marginal speedup of a technique (Fig. 16): the time with only that technique
+switched off (mask 1, 2 or 4) over the time with all on.  Every output is
+checked against the default schedule's.
 
     python -m paper_2202_06819_amd.ablation --workload table1 --out ablation.jsonl
 """
@@ -23,7 +27,8 @@ import os
 import sys
 
 ABLATION_TILES = ("wide_b4_w4x1_f1x4_c64", "wide_b4_w8x1_f1x4_c64", "wide_b4_w4x1_f2x4_c64")
-MASKS = (3, 2, 1, 0)
+MASKS = (7, 6, 4, 0, 1, 2)
+TECHNIQUES = ((1, "duplicate-aware"), (2, "register packing"), (4, "widening at staging"))
 
 
 def ablate_layer(L, dev, reps: int = 50, rounds: int = 5, log=print) -> list[dict]:
@@ -65,22 +70,26 @@ def ablate_layer(L, dev, reps: int = 50, rounds: int = 5, log=print) -> list[dic
 
 
 def summarize(rows: list[dict]) -> list[str]:
-    """Accumulated and marginal speedups per (layer, tile) with all four masks."""
+    """Accumulated and marginal speedups per (layer, tile)."""
     by = {}
     for r in rows:
         by.setdefault((r["layer"], r["tile"]), {})[r["ablation"]] = r["us"]
-    out = ["| layer | tile | baseline us | + duplicate-aware | + register packing | marginal: duplicate-aware | "
-           "marginal: register packing |", "|---|---|---|---|---|---|---|"]
+    out = ["| layer | tile | all off (mask 7) | + duplicate-aware (6) | + register packing (4) | "
+           "+ widening at staging (0) | marginal: " + " | marginal: ".join(n for _, n in TECHNIQUES) + " |",
+           "|---|---|---|---|---|---|---|---|---|"]
+
+    def cell(m, mask, base):
+        if mask not in m:
+            return "n/a"
+        return f"{m[mask]:.2f} us" + (f" ({base / m[mask]:.2f}x)" if base and mask != 7 else "")
+
     for (layer, tile), m in by.items():
         if 0 not in m:
             continue
-        base = m.get(3)
-        base_s = f"{base:.2f}" if base else "n/a"
-        acc1 = f"{base / m[2]:.2f}x ({m[2]:.2f} us)" if base and 2 in m else "n/a"
-        acc2 = f"{base / m[0]:.2f}x ({m[0]:.2f} us)" if base else f"({m[0]:.2f} us)"
-        dup = f"{m[1] / m[0]:.2f}x" if 1 in m else "n/a (lowered operand exceeds LDS)"
-        pack = f"{m[2] / m[0]:.2f}x" if 2 in m else "n/a"
-        out.append(f"| `{layer}` | `{tile}` | {base_s} | {acc1} | {acc2} | {dup} | {pack} |")
+        base = m.get(7)
+        acc = " | ".join(cell(m, k, base) for k in (7, 6, 4, 0))
+        marg = " | ".join(f"{m[b] / m[0]:.2f}x" if b in m else "n/a" for b, _ in TECHNIQUES)
+        out.append(f"| `{layer}` | `{tile}` | {acc} | {marg} |")
     return out
 
 

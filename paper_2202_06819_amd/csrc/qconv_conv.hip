@@ -1,10 +1,9 @@
 // Tile registry of the convolution kernels of qconv_kernels.h.  The staged
-// tiles, the ablation instances and the first group of wide tiles are
-// compiled here; the other wide groups each in a translation unit of its own
-// (qconv_tiles_*.hip), so the build compiles them in parallel.  Tile ids
+// tiles and the first group of wide tiles are compiled here; the other wide
+// groups, the ablation instances and the projection instances each in a
+// translation unit of its own (qconv_tiles_*.hip), so the build compiles them
+// in parallel.  Tile ids
 // follow the lists' order: staged tiles, then wide groups A to D.
-#include <string.h>
-
 #include <vector>
 
 #include "qconv_kernels.h"
@@ -31,20 +30,5 @@ static const std::vector<TileEntry> &all_tiles() {
 const TileEntry *tile_table() { return all_tiles().data(); }
 
 int tile_table_size() { return (int)all_tiles().size(); }
-
-// Ablation instances (4-bit, 3x3, prepared filters): each technique switched
-// off alone and both together, for three tiles.
-#define QCONV_ABL(WP, WK, FP, FK, MASK)                                                                           \
-    {"wide_b4_w" #WP "x" #WK "_f" #FP "x" #FK "_c64", MASK,                                                        \
-     &launch_wide<4, WP, WK, FP, FK, 64, false, true, 3, 3, false, MASK>,                                         \
-     reinterpret_cast<const void *>(&conv_wide<4, WP, WK, FP, FK, 64, false, true, 3, 3, false, MASK>)}
-#define QCONV_ABL3(WP, WK, FP, FK) QCONV_ABL(WP, WK, FP, FK, 1), QCONV_ABL(WP, WK, FP, FK, 2), QCONV_ABL(WP, WK, FP, FK, 3)
-static const AblationInstance g_ablation[] = {QCONV_ABL3(4, 1, 1, 4), QCONV_ABL3(8, 1, 1, 4), QCONV_ABL3(4, 1, 2, 4)};
-
-const AblationInstance *ablation_instance(const char *tile_name, int mask) {
-    for (const AblationInstance &e : g_ablation)
-        if (e.mask == mask && strcmp(e.tile, tile_name) == 0) return &e;
-    return nullptr;
-}
 
 }  // namespace qconv

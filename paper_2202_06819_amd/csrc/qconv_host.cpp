@@ -263,9 +263,12 @@ int plan_tile(const qconv_desc *d, const qconv_layout_info &li, const qconv_tile
             return fail(QCONV_EUNSUPPORTED, "tile %s needs c*bits %% 128 == 0 (whole 16-byte vectors)", t.name);
         const int64_t vpp = (int64_t)t.chunk_c * d->bits / 128;
         const int64_t pj = wide_band_pixels_per_thread(t.tile_p, t.threads, (int)vpp);
-        const bool lowered = (ablation & 1) != 0, ldsepi = (ablation & 2) != 0;
+        const bool lowered = (ablation & 1) != 0, ldsepi = (ablation & 2) != 0, packed_lds = (ablation & 4) != 0;
         if (ablation && (d->r != 3 || d->s != 3 || splits != 1 || d->nb > 1))
             return fail(QCONV_EUNSUPPORTED, "ablation instances run 3x3 filters without a split, plain layout");
+        if (packed_lds && d->bits != 4)
+            return fail(QCONV_EUNSUPPORTED, "only 4-bit activations are kept packed in LDS");
+        const int64_t bpix = packed_lds ? 8 : 16;   // band bytes per pixel and granule plane
         const int64_t rounds = d->bits == 8 ? kBandRounds : 1;
         if (!lowered && pl.rows * ncols > rounds * (int64_t)t.threads * pj)
             return fail(QCONV_EUNSUPPORTED, "tile %s: the input band of this shape exceeds %d staging round(s)", t.name,
@@ -275,7 +278,8 @@ int plan_tile(const qconv_desc *d, const qconv_layout_info &li, const qconv_tile
         // 16-byte LDS read in distinct banks; filter planes are whole KiB so a
         // prepared filter block is copied with 1 KiB LDS-DMA instructions
         // (the lowered operand holds every tile pixel once per tap instead)
-        pl.pstride_b = lowered ? round_up((int64_t)d->r * d->s * t.tile_p * 16, 256) : round_up(pl.rows * ncols * 16, 256);
+        pl.pstride_b = lowered ? round_up((int64_t)d->r * d->s * t.tile_p * bpix, 256)
+                               : round_up(pl.rows * ncols * bpix, 256);
         pl.pstride_w = round_up(((int64_t)d->r * d->s + (proj ? 1 : 0)) * t.tile_k * 16, 1024);
         const int64_t bbuf = planes * pl.pstride_b, wbuf = planes * pl.pstride_w;
         // buffer loads take 32-bit offsets, and offset 2^31 marks padding
@@ -630,7 +634,8 @@ void fill_args(ConvArgs &a, const qconv_desc *d, const qconv_layout_info &li, co
 
 // inst: 0 = the tile's generic kernel, 1 + i = its fixed-size instance i; 3 + the same for
 // the kernels with the bias and residual epilogue; 6 / 7 the multi-chunk 3x3 instance
-// (plain / with bias and residual); 8 + mask for an ablation instance.
+// (plain / with bias and residual); 8 + mask for an ablation instance (masks 1..3; 16 + mask
+// for masks 4..7); 12 the fused pack; 14 / 15 the fused projection (plain / with biases).
 int ensure_lds_attribute(const void *kernel, int tile_id, int inst, int64_t lds) {
     if (lds <= 64 * 1024) return QCONV_OK;
     int dev = 0;
@@ -791,7 +796,7 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
         const AblationInstance *ai = ablation_instance(te.info.name, ablation);
         launch = ai->launch;
         kernel = ai->kernel;
-        inst = 8 + ablation;
+        inst = ablation < 4 ? 8 + ablation : 16 + ablation;
     }
     if (fused) {
         if (!prepared || !te.fused.launch || d->r != te.fused.r || d->s != te.fused.s || ext || ablation || d->nb != 1)
@@ -905,7 +910,7 @@ static int check_schedule_knobs(const qconv_schedule *s) {
     if (s->wg_per_cu < 0 || s->wg_per_cu > 16) return fail(QCONV_EINVAL, "wg_per_cu must be in [0, 16]");
     if (s->band_buffers < 0 || s->band_buffers > 2) return fail(QCONV_EINVAL, "band_buffers must be 0, 1 or 2");
     if (s->xcd_order != 0 && s->xcd_order != 1) return fail(QCONV_EINVAL, "xcd_order must be 0 or 1");
-    if (s->ablation < 0 || s->ablation > 3) return fail(QCONV_EINVAL, "ablation must be in [0, 3]");
+    if (s->ablation < 0 || s->ablation > 7) return fail(QCONV_EINVAL, "ablation must be in [0, 7]");
     if (s->splits < 1) return fail(QCONV_EUNSUPPORTED, "splits must be >= 1");
     return QCONV_OK;
 }

@@ -137,7 +137,7 @@ struct TileEntry {
 // A kernel with some of the techniques switched off (for measurement).
 struct AblationInstance {
     const char *tile;       // the tile it is a variant of
-    int mask;               // 1: lowered staging, 2: LDS epilogue, 3: both
+    int mask;               // bits: 1 lowered staging, 2 LDS epilogue, 4 packed activations in LDS
     ConvLauncher launch;
     const void *kernel;
 };
@@ -153,6 +153,8 @@ struct ProjInstance {
 // Defined in qconv_conv.hip.
 const TileEntry *tile_table();
 int tile_table_size();
+
+// Defined in qconv_tiles_abl.hip.
 const AblationInstance *ablation_instance(const char *tile_name, int mask);
 
 // Defined in qconv_tiles_proj.hip.

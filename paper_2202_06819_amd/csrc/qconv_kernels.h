@@ -403,7 +403,9 @@ __device__ __forceinline__ int xcd_block(int b, int g) {
 // (im2col) operand instead of the band -- one copy of every pixel per filter
 // tap, as without duplicate awareness; bit 1 sends the int32 accumulators
 // through LDS to a separate requantise-and-pack pass instead of packing them
-// in registers before the store.
+// in registers before the store; bit 2 (4-bit) keeps the staged activations
+// packed in LDS and widens every fragment after its LDS read, inside the
+// MFMA loop, instead of once when the band is written.
 // PROJ: a 1x1 projection at the same stride is fused into a 3x3 instance (pad
 // 1): its filter block is tap 9 of the prepared image, its input the centre
 // tap's band pixels -- the fragments the 3x3 already reads -- and it keeps
@@ -414,6 +416,9 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     constexpr bool FIXED = RC > 0 && SC > 0;
     constexpr bool LOWERED = (ABL & 1) != 0;
     constexpr bool LDSEPI = (ABL & 2) != 0;
+    constexpr bool PACKEDLDS = (ABL & 4) != 0;
+    constexpr int BPIX = PACKEDLDS ? 8 : 16;   // band bytes per pixel (or lowered entry) and granule plane
+    static_assert(!PACKEDLDS || BITS == 4, "only 4-bit activations are packed");
     static_assert(!NCHW || (!LOWERED && !MC), "the fused pack stages the band itself");
     static_assert(ABL == 0 || (FIXED && !EXT), "ablation instances are fixed-size, without bias or residual");
     static_assert(!PROJ || (RC == 3 && SC == 3 && ABL == 0 && !MC && !NCHW), "the projection rides on a plain 3x3");
@@ -534,11 +539,18 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
             if (pix >= npix) continue;
 #pragma unroll
             for (int p = 0; p < VPP; ++p) {
-                uint4 g0, g1;
-                widen_vec<BITS, XS>(f.v[j][p], g0, g1);
-                *reinterpret_cast<uint4 *>(bb + (size_t)(p * GPV) * a.pstride_b + pix * 16) = g0;
-                if constexpr (GPV == 2)
-                    *reinterpret_cast<uint4 *>(bb + (size_t)(p * GPV + 1) * a.pstride_b + pix * 16) = g1;
+                if constexpr (PACKEDLDS) {
+                    // each 16-channel granule stays two packed words (widened in the MFMA loop)
+                    const uint4 v = f.v[j][p];
+                    *reinterpret_cast<uint2 *>(bb + (size_t)(p * GPV) * a.pstride_b + pix * 8) = uint2{v.x, v.y};
+                    *reinterpret_cast<uint2 *>(bb + (size_t)(p * GPV + 1) * a.pstride_b + pix * 8) = uint2{v.z, v.w};
+                } else {
+                    uint4 g0, g1;
+                    widen_vec<BITS, XS>(f.v[j][p], g0, g1);
+                    *reinterpret_cast<uint4 *>(bb + (size_t)(p * GPV) * a.pstride_b + pix * 16) = g0;
+                    if constexpr (GPV == 2)
+                        *reinterpret_cast<uint4 *>(bb + (size_t)(p * GPV + 1) * a.pstride_b + pix * 16) = g1;
+                }
             }
         }
     };
@@ -780,7 +792,7 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         const int m0 = (j0 + ti * gpk) * TP;
         if constexpr (LOWERED) {
 #pragma unroll
-            for (int tn = 0; tn < FP; ++tn) pixoff[tn] = (wp * FP * 16 + tn * 16 + l16) * 16 + lane_b;
+            for (int tn = 0; tn < FP; ++tn) pixoff[tn] = (wp * FP * 16 + tn * 16 + l16) * BPIX + lane_b;
             return;
         }
         int vlo, cu;
@@ -790,7 +802,7 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
             int m = min(m0 + wp * FP * 16 + tn * 16 + l16, a.m - 1);
             int vr, cl;
             pixel_origin(a, m, vr, cl);
-            pixoff[tn] = ((vr - vlo) * a.ncols + cl) * 16 + lane_b;
+            pixoff[tn] = ((vr - vlo) * a.ncols + cl) * BPIX + lane_b;
         }
     };
 
@@ -990,7 +1002,7 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                 for (int rr = 0; rr < RC; ++rr)
 #pragma unroll
                     for (int ks = 0; ks < KSTEPS; ++ks)
-                        brow[tn][rr][ks] = bb + pixoff[tn] + (LOWERED ? rr * SC * TP : rr * a.ncols) * 16 +
+                        brow[tn][rr][ks] = bb + pixoff[tn] + (LOWERED ? rr * SC * TP : rr * a.ncols) * BPIX +
                                            ks * 4 * a.pstride_b;
             v4i A[2][FK], B[2][FP];
             v4i Ap[2][PROJ ? FK : 1];   // the projection's filter fragments at the centre tap
@@ -1021,8 +1033,17 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                 for (int tm = 0; tm < FK; ++tm)
                     A[set][tm] = *reinterpret_cast<const v4i *>(wa + ks * 4 * PSW + tap * TK * 16 + tm * 256);
 #pragma unroll
-                for (int tn = 0; tn < FP; ++tn)
-                    B[set][tn] = *reinterpret_cast<const v4i *>(brow[tn][rr][ks] + ss * (LOWERED ? TP * 16 : 16));
+                for (int tn = 0; tn < FP; ++tn) {
+                    const uint8_t *bp = brow[tn][rr][ks] + ss * (LOWERED ? TP : 1) * BPIX;
+                    if constexpr (PACKEDLDS) {
+                        const uint2 v = *reinterpret_cast<const uint2 *>(bp);
+                        uint4 g0, g1;
+                        widen_vec<BITS, XS>(uint4{v.x, v.y, 0u, 0u}, g0, g1);
+                        B[set][tn] = v4i{(int)g0.x, (int)g0.y, (int)g0.z, (int)g0.w};
+                    } else {
+                        B[set][tn] = *reinterpret_cast<const v4i *>(bp);
+                    }
+                }
                 if constexpr (PROJ) {
                     if (tap == CT) {
 #pragma unroll

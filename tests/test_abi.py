@@ -368,10 +368,17 @@ def test_ablation_schedules(q):
     d = D(n=2)
     names = {t["name"]: t["id"] for t in q.tiles()}
     for name in ("wide_b4_w4x1_f1x4_c64", "wide_b4_w8x1_f1x4_c64", "wide_b4_w4x1_f2x4_c64"):
-        for mask in (1, 2, 3):
+        for mask in range(1, 8):
             assert q.schedule_status(d, {"tile_id": names[name], "ablation": mask}) == 0, (name, mask)
     assert q.schedule_status(d, {"tile_id": names["wide_b4_w4x1_f4x4_c64"], "ablation": 1}) == -2   # not compiled
-    assert q.schedule_status(d, {"tile_id": names["wide_b4_w4x1_f1x4_c64"], "ablation": 4}) == -1
+    assert q.schedule_status(d, {"tile_id": names["wide_b4_w4x1_f1x4_c64"], "ablation": 8}) == -1
+    # keeping the band packed halves its LDS: with the int32 tile also in LDS,
+    # the lowered operand of a deeper layer fits only packed
+    deep = D(n=2, h=28, w=28, c=128, k=128)
+    t = names["wide_b4_w8x1_f1x4_c64"]
+    assert q.schedule_status(deep, {"tile_id": t, "ablation": 3}) == -2
+    assert q.schedule_status(deep, {"tile_id": t, "ablation": 7}) == 0
+    assert q.schedule_status(D(bits=8, x_signed=1), {"tile_id": t, "ablation": 4}) == -2
     assert q.schedule_status(D(r=1, s=1, pad_h=0, pad_w=0), {"tile_id": names["wide_b4_w4x1_f1x4_c64"],
                                                            "ablation": 1}) == -2              # 3x3 only
 
