@@ -419,9 +419,15 @@ int qconv_noalloc_limits(int64_t *scratch_bytes, int64_t *max_tiles);
  *   band_buffers  LDS band buffers of a persistent single-chunk plan: 1 (one
  *                 more barrier per stage, less LDS), 2, or 0 = whichever lets
  *                 more workgroups share a CU.  Ignored where it does not apply.
- *   xcd_order     1 = consecutive workgroup tiles are placed on one XCD so
- *                 neighbouring tiles share its L2 (the default elsewhere);
- *                 0 = the hardware's round-robin order
+ *   xcd_order     1 = consecutive workgroup tiles are placed on one XCD,
+ *                 pixel tiles outermost, so neighbouring tiles share its L2
+ *                 (halo rows) while it reads every channel tile's filters;
+ *                 2 = the same with channel tiles outermost, so an XCD reads
+ *                 only its channel tiles' filters (deep layers, whose filters
+ *                 outweigh their input); 0 = the hardware's round-robin
+ *                 order; -1 = the library's choice (what qconv2d and
+ *                 qconv2d_prepared use): the order whose bytes read into the
+ *                 eight L2s, filters and input, are fewer
  *   ablation      0 for normal use.  For measuring the techniques (the
  *                 ablation of Sec. 4.4), a bit mask of techniques switched
  *                 off: 1 = duplicate-aware loading (Sec. 3.1) -- every tile
@@ -440,7 +446,7 @@ int qconv_noalloc_limits(int64_t *scratch_bytes, int64_t *max_tiles);
  * qconv2d_scheduled -- qconv2d_prepared with every knob given; the prepared
  *   filters must be those of s->tile_id; `workspace` as for split-K above.
  *   qconv2d_prepared(..., tile_id, splits, ...) is the schedule
- *   {tile_id, splits, 0, 0, 1, 0}.
+ *   {tile_id, splits, 0, 0, -1, 0}.
  */
 typedef struct {
     int32_t tile_id;

@@ -650,6 +650,21 @@ int ensure_lds_attribute(const void *kernel, int tile_id, int inst, int64_t lds)
     return QCONV_OK;
 }
 
+// The workgroup order of xcd_order -1 (the library's choice).  Each XCD has
+// its own L2, so bytes are fetched once per XCD that reads them.  Ordered
+// pixel tile by pixel tile, every XCD reads every channel tile's filters and
+// an eighth of the input; ordered channel tile by channel tile, every XCD
+// reads its channel tiles' filters and (with at least eight channel tiles)
+// all of the input.  The order with fewer such bytes wins: channel tiles for
+// deep layers, whose filters outweigh their input.
+int auto_xcd_order(const qconv_layout_info &li, const Plan &pl, int64_t filter_bytes) {
+    if (pl.ktiles < 2) return 1;
+    const int64_t k = std::min<int64_t>(pl.ktiles, 8);
+    const int64_t pixel_major = 8 * filter_bytes + li.x_bytes;
+    const int64_t channel_major = filter_bytes + k * li.x_bytes;
+    return channel_major < pixel_major ? 2 : 1;
+}
+
 // The convolution; w is packed KRSC filters (prepared == false) or the
 // prepared filters of tile_id (prepared == true, w_bytes_given bytes).
 // splits > 1 (prepared filters only): split-K over channel chunks with its
@@ -661,7 +676,7 @@ int ensure_lds_attribute(const void *kernel, int tile_id, int inst, int64_t lds)
 int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, size_t w_bytes_given,
              const qconv_epilogue *epi, void *y, void *workspace, size_t workspace_bytes, int32_t tile_id,
              int32_t splits, void *stream, int32_t wg_per_cu = 0, int32_t band_buffers = 0,
-             int32_t xcd_order = 1, int32_t ablation = 0, const int8_t *x_nchw = nullptr,
+             int32_t xcd_order = -1, int32_t ablation = 0, const int8_t *x_nchw = nullptr,
              void *x_packed = nullptr, bool noalloc = false, const qconv_epilogue *epi_proj = nullptr,
              void *y_proj = nullptr) {
     qconv_layout_info li;
@@ -856,7 +871,7 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
     a.yptr = static_cast<uint8_t *>(y);
     a.mult = requant ? epi->mult : nullptr;
     a.w_image = (prepared && te.info.variant == QCONV_VARIANT_WIDE) ? 1 : 0;
-    a.xcd_order = xcd_order;
+    a.xcd_order = xcd_order >= 0 ? xcd_order : auto_xcd_order(li, pl, a.w_image ? wb : li.w_bytes);
     if (wsb > 0) {
         a.ws_part = static_cast<int32_t *>(workspace);
         a.ws_cnt = reinterpret_cast<uint32_t *>(ws_cnt ? ws_cnt
@@ -909,7 +924,7 @@ static int check_schedule_knobs(const qconv_schedule *s) {
     if (!s) return fail(QCONV_EINVAL, "schedule must be non-NULL");
     if (s->wg_per_cu < 0 || s->wg_per_cu > 16) return fail(QCONV_EINVAL, "wg_per_cu must be in [0, 16]");
     if (s->band_buffers < 0 || s->band_buffers > 2) return fail(QCONV_EINVAL, "band_buffers must be 0, 1 or 2");
-    if (s->xcd_order != 0 && s->xcd_order != 1) return fail(QCONV_EINVAL, "xcd_order must be 0 or 1");
+    if (s->xcd_order < -1 || s->xcd_order > 2) return fail(QCONV_EINVAL, "xcd_order must be -1, 0, 1 or 2");
     if (s->ablation < 0 || s->ablation > 7) return fail(QCONV_EINVAL, "ablation must be in [0, 7]");
     if (s->splits < 1) return fail(QCONV_EUNSUPPORTED, "splits must be >= 1");
     return QCONV_OK;
@@ -1038,7 +1053,7 @@ int qconv2d_prepared(const qconv_desc *d, const void *x, const void *w_prepared,
 int qconv2d_prepared_noalloc(const qconv_desc *d, const void *x, const void *w_prepared, size_t w_prepared_bytes,
                              const qconv_epilogue *epi, void *y, int32_t tile_id, int32_t splits, void *stream) {
     g_err[0] = 0;
-    return run_conv(d, x, w_prepared, true, w_prepared_bytes, epi, y, nullptr, 0, tile_id, splits, stream, 0, 0, 1, 0,
+    return run_conv(d, x, w_prepared, true, w_prepared_bytes, epi, y, nullptr, 0, tile_id, splits, stream, 0, 0, -1, 0,
                     nullptr, nullptr, true);
 }
 
@@ -1131,7 +1146,7 @@ int qconv2d_proj(const qconv_desc *d, const void *x, const void *w_prepared, siz
                  void *stream) {
     g_err[0] = 0;
     if (!y_proj) return fail(QCONV_EINVAL, "y_proj must be non-NULL");
-    return run_conv(d, x, w_prepared, true, w_prepared_bytes, epi, y, nullptr, 0, tile_id, 1, stream, 0, 0, 1, 0,
+    return run_conv(d, x, w_prepared, true, w_prepared_bytes, epi, y, nullptr, 0, tile_id, 1, stream, 0, 0, -1, 0,
                     nullptr, nullptr, false, epi_proj, y_proj);
 }
 
@@ -1146,7 +1161,7 @@ int qconv2d_packing(const qconv_desc *d, const int8_t *x_nchw, void *x_packed, c
                     size_t w_prepared_bytes, const qconv_epilogue *epi, void *y, int32_t tile_id, void *stream) {
     g_err[0] = 0;
     if (!x_nchw) return fail(QCONV_EINVAL, "x_nchw must be non-NULL");
-    return run_conv(d, nullptr, w_prepared, true, w_prepared_bytes, epi, y, nullptr, 0, tile_id, 1, stream, 0, 0, 1,
+    return run_conv(d, nullptr, w_prepared, true, w_prepared_bytes, epi, y, nullptr, 0, tile_id, 1, stream, 0, 0, -1,
                     0, x_nchw, x_packed);
 }
 

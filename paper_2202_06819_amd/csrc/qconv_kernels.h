@@ -450,11 +450,16 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     // j0 + gpk, ... of one channel tile over all channel chunks.  With a split
     // (a.splits > 1) it owns one output tile and the chunk range of its split;
     // the splits of a tile have consecutive logical numbers (one XCD).
+    // Logical tiles lt are numbered channel tile fastest (xcd_order 0, 1:
+    // consecutive workgroups share pixels, so an XCD reads its share of the
+    // input and every channel tile's filters) or pixel tile fastest
+    // (xcd_order 2: an XCD takes one channel tile's filters and the pixels).
     const int lb = a.xcd_order ? xcd_block(blockIdx.x, gridDim.x) : (int)blockIdx.x;
     const int sp = a.splits > 1 ? lb % a.splits : 0;
     const int lt = a.splits > 1 ? lb / a.splits : lb;
-    const int kt = lt % a.ktiles;
-    const int j0 = lt / a.ktiles;
+    const int per_kt = a.splits > 1 ? a.mtiles : (int)gridDim.x / a.ktiles;   // logical tiles per channel tile
+    const int kt = a.xcd_order == 2 ? lt / per_kt : lt % a.ktiles;
+    const int j0 = a.xcd_order == 2 ? lt - kt * per_kt : lt / a.ktiles;
     const int gpk = a.splits > 1 ? a.mtiles : gridDim.x / a.ktiles;   // workgroups sharing this channel tile
     const int my_tiles = (a.mtiles - j0 + gpk - 1) / gpk;              // tiles j0, j0 + gpk, ...
     const int c_begin = sp * a.cps;                                     // chunks [c_begin, c_end)

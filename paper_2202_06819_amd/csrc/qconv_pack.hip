@@ -3,14 +3,16 @@
 // axis; Sec. 3.3: channels innermost so consumers read it coalesced).
 //
 // The operation is a transpose of each image's C x (H*W) plane.  A workgroup
-// owns a tile of 64 channels x 128 pixels.  It reads the tile row by row
-// (each channel's pixels are contiguous in NCHW: 32 bytes per lane, whole
-// 128-byte lines per row), saturates every value into the target range and
-// parks it in LDS; it then reads 8 channels x 4 pixels per lane as dwords,
-// transposes the bytes in registers, packs nibbles and writes each pixel's
-// words.  The LDS row pitch of 33 dwords keeps the column reads free of bank
-// conflicts.  The kernel is HBM-bound: every input byte is read once and
-// every output byte written once.
+// of 128 threads owns a tile of 64 channels x 64 pixels (small tiles, so even
+// a batch-8 56x56 tensor spreads over more than twice as many workgroups as
+// there are CUs).  It reads the tile row by row (each channel's pixels are
+// contiguous in NCHW: 32 bytes per lane, two lanes per 64-byte row segment),
+// saturates every value into the target range and parks it in LDS; it then
+// reads 8 channels x 4 pixels per lane as dwords, transposes the bytes in
+// registers, packs nibbles and writes each pixel's words.  The LDS row pitch
+// of 17 dwords keeps the column reads of a wave (8 channel groups x 8 pixel
+// quads) free of bank conflicts.  The kernel is HBM-bound: every input byte
+// is read once and every output byte written once.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -19,9 +21,9 @@
 namespace qconv {
 
 constexpr int PK_C = 64;          // channels per tile
-constexpr int PK_P = 128;         // pixels per tile: whole 128-byte lines of each channel row
-constexpr int PK_PITCH = 132;     // LDS row pitch in bytes (33 dwords: conflict-free column reads)
-constexpr int PK_THREADS = 256;
+constexpr int PK_P = 64;          // pixels per tile (64-byte segments of each channel row)
+constexpr int PK_PITCH = 68;      // LDS row pitch in bytes (17 dwords: conflict-free column reads)
+constexpr int PK_THREADS = 128;   // phase 2: 8 channel groups x 16 pixel quads
 
 // Same renumbering as the convolution kernels: block b runs on XCD b % 8;
 // give every XCD a contiguous range so neighbouring pixel tiles (which share
@@ -59,11 +61,11 @@ __global__ void __launch_bounds__(PK_THREADS)
     const size_t obase = (size_t)(img / nb) * hw * nb + img % nb;
     auto out_pixel = [&](int px) { return obase + (size_t)px * nb; };
 
-    // ---- phase 1: 64 channel rows x 128 pixels; a lane reads 32 consecutive
+    // ---- phase 1: 64 channel rows x 64 pixels; a lane reads 32 consecutive
     // pixels of one row, saturates them and parks them in LDS
     {
-        const int row = tid >> 2;
-        const int seg = (tid & 3) * 32;
+        const int row = tid >> 1;
+        const int seg = (tid & 1) * 32;
         const int ch = c0 + row;
         uint32_t v[8];
         const int8_t *rp = plane + (size_t)ch * hw + p0 + seg;

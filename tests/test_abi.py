@@ -330,7 +330,10 @@ def test_schedule_check_and_errors(q):
     assert q.schedule_status(d, dict(base, wg_per_cu=17)) == -1
     assert q.schedule_status(d, dict(base, wg_per_cu=-1)) == -1
     assert q.schedule_status(d, dict(base, band_buffers=3)) == -1
-    assert q.schedule_status(d, dict(base, xcd_order=2)) == -1
+    assert q.schedule_status(d, dict(base, xcd_order=2)) == 0
+    assert q.schedule_status(d, dict(base, xcd_order=-1)) == 0
+    assert q.schedule_status(d, dict(base, xcd_order=3)) == -1
+    assert q.schedule_status(d, dict(base, xcd_order=-2)) == -1
     assert q.schedule_status(d, dict(base, splits=0)) == -2
     assert q.schedule_status(d, dict(base, splits=q.max_splits(d, tid) + 1)) == -2
     assert q.schedule_status(d, {"tile_id": staged, "splits": 2}) == -2

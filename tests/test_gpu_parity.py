@@ -838,3 +838,43 @@ def test_persistent_3x3_requant_every_tile(case):
         assert_same(y_np, want, f"{name} tile {tt['name']} vs the oracle")
         ran += 1
     assert ran >= 3
+
+
+@pytest.mark.parametrize("shape", [
+    # name, n, h, c, k, r, splits, wg_per_cu -- deep layers with several channel tiles
+    ("x_4x14_256to256_3x3_split2", 4, 14, 256, 256, 3, 2, 0),
+    ("x_2x7_512to512_3x3_persistent", 2, 7, 512, 512, 3, 1, 1),
+    ("x_3x7_512to384_1x1", 3, 7, 512, 384, 1, 1, 0),
+], ids=lambda v: v[0])
+def test_xcd_orders_match_oracle(shape):
+    """Every workgroup order (hardware, pixel tiles outermost, channel tiles
+    outermost, the library's choice) computes the same bytes, with split-K and
+    with persistent grids."""
+    torch, q = _torch(), _qconv()
+    name, n, h, c, k, r, splits, wg = shape
+    L = qi.Layer(name, n, h, h, c, k, r, r, 1, r // 2, w_range=(-7, 7))
+    t = qi.layer_tensors(980, c + k + r, L)
+    sh = stress_shift(L, L.x_range, L.w_range)
+    ref = ref_layer(L, t, requant=True, shift=sh)
+    dev = torch.device("cuda:0")
+    xp = q.pack(torch.from_numpy(t["x"]).to(dev), 4, False)
+    wp = q.pack(torch.from_numpy(t["w"]).to(dev), 4, True)
+    mult = torch.from_numpy(t["mult"]).to(dev)
+    ran = 0
+    for tt in q.tiles():
+        if tt["variant"] != 2 or q.tile_status(L.desc(), tt["id"]) != 0 or -(-k // tt["tile_k"]) < 2:
+            continue
+        if splits > q.max_splits(L.desc(), tt["id"]):
+            continue
+        wprep = q.prepare_filters(L.desc(), wp, tt["id"])
+        ws = q.make_workspace(L.desc(), tt["id"], splits, dev)
+        for xo in (-1, 0, 1, 2):
+            sch = {"tile_id": tt["id"], "splits": splits, "wg_per_cu": wg, "xcd_order": xo}
+            announce(f"{name} tile {tt['name']} xcd_order {xo}")
+            y = q.Conv2dCall(L.desc(), xp, wprep, schedule=sch, workspace=ws, requant=True, mult=mult, shift=sh)()
+            torch.cuda.synchronize()
+            assert_same(y.cpu().numpy(), ref["y_packed"], f"{name} {tt['name']} xcd_order {xo}")
+        ran += 1
+        if ran == 4:
+            break
+    assert ran >= 2
