@@ -401,14 +401,16 @@ def proj_table(cfg: int, layers, dev, reps: int) -> list[dict]:
         w1 = qconv.pack(torch.from_numpy(tp["w"]).to(dev), P.bits, P.w_signed)
         m3, m1 = torch.from_numpy(t["mult"]).to(dev), torch.from_numpy(tp["mult"]).to(dev)
         e, ep = L.epilogue, P.epilogue
-        tile = sweep.tuned_proj_tile(L.desc())
+        tile, psplits = sweep.tuned_proj_config(L.desc())
         wprep = qconv.prepare_filters_proj(L.desc(), w3, w1, tile)
+        nws = qconv.proj_workspace_bytes(L.desc(), tile, psplits)
+        pws = torch.zeros(nws, dtype=torch.uint8, device=dev) if nws else None
 
         def make(stream=None):
             return qconv.ProjConv2dCall(L.desc(), xp, wprep, tile=tile, requant=True, mult=m3, shift=e.shift,
                                         relu=e.relu, clamp=(e.lo, e.hi),
                                         proj=dict(mult=m1, shift=ep.shift, relu=ep.relu, clamp=(ep.lo, ep.hi)),
-                                        stream=stream)
+                                        splits=psplits, workspace=pws, stream=stream)
 
         g, _ = captured(lambda s: [make(s)], reps)
         per = sorted(time_graph(g, 1) * 1000.0 / reps for _ in range(5))
@@ -426,12 +428,12 @@ def proj_table(cfg: int, layers, dev, reps: int) -> list[dict]:
             gs, _ = captured(lambda s, mk=mk: [mk(s)], reps)
             sep.append(sorted(time_graph(gs, 1) * 1000.0 / reps for _ in range(5))[2])
         ops = L.ops + P.ops
-        rows.append({"layers": f"{L.name} + {P.name}", "tile": qconv.tiles()[tile]["name"],
+        rows.append({"layers": f"{L.name} + {P.name}", "tile": qconv.tiles()[tile]["name"], "splits": psplits,
                      "fused_us": round(per[2], 3), "separate_us": round(sum(sep), 3),
                      "conv3x3_us": round(sep[0], 3), "proj_us": round(sep[1], 3),
                      "gops": round(ops / 1e9, 4), "tops": round(ops / (per[2] * 1e-6) / 1e12, 2)})
         log(f"  fused {L.name} + {P.name}: {per[2]:.2f} us vs {sum(sep):.2f} us as two launches "
-            f"(tile {rows[-1]['tile']})")
+            f"(tile {rows[-1]['tile']} splits {psplits})")
     return rows
 
 

@@ -313,21 +313,28 @@ int qconv2d_prepared(const qconv_desc *d, const void *x, const void *w_prepared,
  *   filters `w_packed` and packed k x 1 x 1 x c projection filters
  *   `w_proj_packed` (16-byte aligned) -> one prepared image for `tile_id`
  *   (the projection is its tenth tap).  Errors as qconv_prepare_filters.
+ * qconv_proj_workspace_bytes -- host only: split-K workspace of the fused
+ *   launch for (tile_id, splits) (the projection's partial sums double it; 0
+ *   when splits == 1); errors as qconv_workspace_bytes.
  * qconv2d_proj -- the fused launch.  `epi` and `epi_proj` must have the same
  *   mode: raw (both NULL or QCONV_OUT_RAW_I32: y and y_proj get int32
  *   accumulators) or requant (each with its own multipliers, shift, ReLU,
  *   clamp and optional bias; no residual).  y and y_proj (16-byte aligned,
  *   y_packed_bytes or y_raw_bytes each) must not overlap each other or any
- *   input.  No split.  Errors as qconv2d_prepared.
+ *   input.  `splits`, `workspace` and `workspace_bytes` as for split-K below
+ *   (qconv_max_splits bounds `splits`; the workspace is
+ *   qconv_proj_workspace_bytes long, under the same contract).  Errors as
+ *   qconv2d_prepared.
  */
 int qconv_proj_default_tile(const qconv_desc *d);
 int qconv_proj_tile_check(const qconv_desc *d, int32_t tile_id);
 int qconv_prepared_proj_filter_bytes(const qconv_desc *d, int32_t tile_id, size_t *bytes);
 int qconv_prepare_filters_proj(const qconv_desc *d, const void *w_packed, const void *w_proj_packed, int32_t tile_id,
                                void *w_prepared, size_t bytes, void *stream);
+int qconv_proj_workspace_bytes(const qconv_desc *d, int32_t tile_id, int32_t splits, size_t *bytes);
 int qconv2d_proj(const qconv_desc *d, const void *x, const void *w_prepared, size_t w_prepared_bytes,
                  const qconv_epilogue *epi, void *y, const qconv_epilogue *epi_proj, void *y_proj, int32_t tile_id,
-                 void *stream);
+                 int32_t splits, void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * qconv2d_packing -- qconv_pack of the activations fused into

@@ -218,6 +218,7 @@ struct Plan {
     int64_t off_b0 = 0, off_b1 = 0, off_w0 = 0, off_w1 = 0, off_m = 0, off_e = 0;
     int64_t mtiles = 0, ktiles = 0, grid = 0;
     int64_t splits = 1, cps = 0;   // split-K: splits of the chunk range, chunks per split
+    bool proj = false;             // a fused projection (its own accumulators and partial sums)
 };
 
 int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
@@ -247,6 +248,7 @@ int plan_tile(const qconv_desc *d, const qconv_layout_info &li, const qconv_tile
     const int64_t ncols = d->w + 2 * d->pad_w;
     const int64_t nchunks = (d->c + t.chunk_c - 1) / t.chunk_c;
     Plan pl;
+    pl.proj = proj;
     pl.rows = band_rows(d, li.p, li.q, t.tile_p);
     pl.mtiles = (li.m + t.tile_p - 1) / t.tile_p;
     pl.ktiles = (d->k + t.tile_k - 1) / t.tile_k;
@@ -577,9 +579,12 @@ int64_t prepared_bytes(const qconv_desc *d, const qconv_layout_info &li, const q
 }
 
 // Split-K workspace: int32 partial sums of every (tile, split) block in the
-// kernel's register order, then one arrival counter per output tile.
+// kernel's register order (a fused projection's after the layer's, in each
+// block), then one arrival counter per output tile.
 int64_t split_part_bytes(const qconv_tile_info &t, const Plan &pl) {
-    return pl.splits > 1 ? round_up(pl.mtiles * pl.ktiles * pl.splits * (int64_t)t.tile_p * t.tile_k * 4, 256) : 0;
+    return pl.splits > 1 ? round_up(pl.mtiles * pl.ktiles * pl.splits * (int64_t)t.tile_p * t.tile_k * 4 *
+                                        (pl.proj ? 2 : 1), 256)
+                         : 0;
 }
 int64_t split_workspace_bytes(const qconv_tile_info &t, const Plan &pl) {
     return pl.splits > 1 ? split_part_bytes(t, pl) + round_up(pl.mtiles * pl.ktiles * 4, 256) : 0;
@@ -706,8 +711,8 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
         if (m1 != m2) return fail(QCONV_EINVAL, "the layer and its projection must use the same epilogue mode");
         if ((epi && epi->residual) || (epi_proj && epi_proj->residual))
             return fail(QCONV_EUNSUPPORTED, "a layer with a fused projection takes no residual");
-        if (!prepared || splits != 1 || ablation || x_nchw)
-            return fail(QCONV_EUNSUPPORTED, "a fused projection runs from prepared filters, without split or ablation");
+        if (!prepared || ablation || x_nchw)
+            return fail(QCONV_EUNSUPPORTED, "a fused projection runs from prepared filters, without ablation");
         if (!aligned16(y_proj)) return fail(QCONV_EINVAL, "y_proj must be 16-byte aligned");
         if (tile_id == -1) {
             tile_id = pick_proj_default(d, li);
@@ -1059,7 +1064,8 @@ int qconv2d_prepared_noalloc(const qconv_desc *d, const void *x, const void *w_p
 
 // The tile a layer with a fused projection runs (tile_id, or the built-in
 // choice for -1) and its plan; the descriptor is already the kernel's.
-static int proj_tile_plan(const qconv_desc *d, const qconv_layout_info &li, int32_t tile_id, Plan *pl) {
+static int proj_tile_plan(const qconv_desc *d, const qconv_layout_info &li, int32_t tile_id, Plan *pl,
+                          int32_t splits = 1) {
     if (!proj_shape_ok(d))
         return fail(QCONV_EUNSUPPORTED, "a fused projection needs a 3x3 layer with padding 1 in the plain layout");
     if (tile_id == -1) {
@@ -1069,8 +1075,22 @@ static int proj_tile_plan(const qconv_desc *d, const qconv_layout_info &li, int3
     if (tile_id < 0 || tile_id >= tile_table_size()) return fail(QCONV_EINVAL, "unknown tile %d", tile_id);
     const qconv_tile_info &t = tile_table()[tile_id].info;
     if (!proj_instance(t.name)) return fail(QCONV_EUNSUPPORTED, "tile %s has no projection instance", t.name);
-    int rc = plan_tile(d, li, t, pl, 0, 1, false, 0, true);
+    int rc = plan_tile(d, li, t, pl, 0, splits, false, 0, true);
     return rc ? rc : tile_id;
+}
+
+int qconv_proj_workspace_bytes(const qconv_desc *d, int32_t tile_id, int32_t splits, size_t *bytes) {
+    g_err[0] = 0;
+    qconv_layout_info li;
+    qconv_desc kd;
+    int rc = kernel_desc(d, &kd, &li);
+    if (rc) return rc;
+    if (!bytes) return fail(QCONV_EINVAL, "bytes must be non-NULL");
+    Plan pl;
+    rc = proj_tile_plan(&kd, li, tile_id, &pl, splits);
+    if (rc < 0) return rc;
+    *bytes = (size_t)split_workspace_bytes(tile_table()[rc].info, pl);
+    return QCONV_OK;
 }
 
 int qconv_proj_default_tile(const qconv_desc *d) {
@@ -1143,11 +1163,11 @@ int qconv_prepare_filters_proj(const qconv_desc *d, const void *w_packed, const 
 
 int qconv2d_proj(const qconv_desc *d, const void *x, const void *w_prepared, size_t w_prepared_bytes,
                  const qconv_epilogue *epi, void *y, const qconv_epilogue *epi_proj, void *y_proj, int32_t tile_id,
-                 void *stream) {
+                 int32_t splits, void *workspace, size_t workspace_bytes, void *stream) {
     g_err[0] = 0;
     if (!y_proj) return fail(QCONV_EINVAL, "y_proj must be non-NULL");
-    return run_conv(d, x, w_prepared, true, w_prepared_bytes, epi, y, nullptr, 0, tile_id, 1, stream, 0, 0, -1, 0,
-                    nullptr, nullptr, false, epi_proj, y_proj);
+    return run_conv(d, x, w_prepared, true, w_prepared_bytes, epi, y, workspace, workspace_bytes, tile_id, splits,
+                    stream, 0, 0, -1, 0, nullptr, nullptr, false, epi_proj, y_proj);
 }
 
 int qconv_noalloc_limits(int64_t *scratch_bytes, int64_t *max_tiles) {

@@ -262,6 +262,14 @@ __device__ __forceinline__ void widen_vec(uint4 v, uint4 &g0, uint4 &g1) {
 }
 
 constexpr int kWideMaxV = 4;   // packed 16-byte filter vectors a thread gathers per batch
+// MFMA steps whose LDS fragment reads are in flight ahead of the step being
+// multiplied (fixed-size instances).  A wave's step of 2x2 fragments is 64
+// MFMA cycles, well under an LDS read's latency with the CU's other waves
+// reading too, so one step ahead leaves the wave waiting on LDS.
+#ifndef QCONV_LDS_LOOKAHEAD
+#define QCONV_LDS_LOOKAHEAD 2
+#endif
+constexpr int kLdsLookahead = QCONV_LDS_LOOKAHEAD;
 
 // ---- the pack fused into the convolution (int8 N x C x H x W activations).
 // Four int8 values of one channel -> the int8 MFMA operand bytes that
@@ -319,6 +327,9 @@ __device__ __forceinline__ u32x4 make_rsrc(const void *base, int32_t bytes) {
 }
 
 constexpr uint32_t kOutOfRange = 0x80000000u;   // a buffer offset past every tensor: loads return 0
+// Cache-policy operand of a buffer access that is coherent across the device
+// (sc1): it is written through to, and read from, past the XCD's L2.
+constexpr int kCoherentAux = 16;
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_brsrc(const void *base, int32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, bytes, (int)kRsrcWord3);
@@ -409,7 +420,8 @@ __device__ __forceinline__ int xcd_block(int b, int g) {
 // PROJ: a 1x1 projection at the same stride is fused into a 3x3 instance (pad
 // 1): its filter block is tap 9 of the prepared image, its input the centre
 // tap's band pixels -- the fragments the 3x3 already reads -- and it keeps
-// accumulators, multipliers and an output of its own (no split, no residual).
+// accumulators (split-K partial sums too), multipliers and an output of its
+// own (no residual).
 template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC, bool EXT, int ABL = 0,
           bool MC = false, bool NCHW = false, bool PROJ = false>
 __device__ __forceinline__ void wide_body(const ConvArgs &a) {
@@ -895,7 +907,7 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     // accumulators start from the bias (in the first split of a tile only)
     const bool bias_here = EXT && a.mode == QCONV_OUT_REQUANT && a.bias && sp == 0;
     if (bias_here) init_acc<FP, FK>(a, acc, blds + cb - k0, false, cb);
-    const bool bias2_here = PROJ && EXT && a.mode == QCONV_OUT_REQUANT && a.bias2;
+    const bool bias2_here = PROJ && EXT && a.mode == QCONV_OUT_REQUANT && a.bias2 && sp == 0;
     if constexpr (PROJ)
         if (bias2_here) init_acc<FP, FK>(ap, acc2, blds2 + cb - k0, false, cb);
 
@@ -1009,8 +1021,14 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                     for (int ks = 0; ks < KSTEPS; ++ks)
                         brow[tn][rr][ks] = bb + pixoff[tn] + (LOWERED ? rr * SC * TP : rr * a.ncols) * BPIX +
                                            ks * 4 * a.pstride_b;
-            v4i A[2][FK], B[2][FP];
-            v4i Ap[2][PROJ ? FK : 1];   // the projection's filter fragments at the centre tap
+            // LA steps of fragments in flight: register sets rotate over NS = LA + 1
+            // (larger sets -- 4x4 fragments, or 2x4 with a projection -- keep
+            // one: their steps are longer and their registers are spoken for)
+            constexpr int LA0 = FK + FP + (PROJ ? FK : 0) <= 6 ? kLdsLookahead : 1;
+            constexpr int LA = LA0 < NIT ? LA0 : NIT;
+            constexpr int NS = LA + 1;
+            v4i A[NS][FK], B[NS][FP];
+            v4i Ap[NS][PROJ ? FK : 1];   // the projection's filter fragments at the centre tap
             // Multi-chunk instances (MC): the next chunk's filter block goes out
             // as 1 KiB LDS-DMA copies spread over the MFMA steps (about one per
             // step and wave); issued all at once before the loop they queue
@@ -1057,16 +1075,17 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                     }
                 }
             };
-            ld(0, 0);
+#pragma unroll
+            for (int it = 0; it < LA; ++it) ld(it, it);
 #pragma unroll
             for (int it = 0; it < NIT; ++it) {
                 if constexpr (MC) dma_step(it);
-                if (it + 1 < NIT) ld(it + 1, (it + 1) & 1);
+                if (it + LA < NIT) ld(it + LA, (it + LA) % NS);
 #pragma unroll
                 for (int tn = 0; tn < FP; ++tn)
 #pragma unroll
                     for (int tm = 0; tm < FK; ++tm)
-                        acc[tn][tm] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A[it & 1][tm], B[it & 1][tn], acc[tn][tm],
+                        acc[tn][tm] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A[it % NS][tm], B[it % NS][tn], acc[tn][tm],
                                                                             0, 0, 0);
                 if constexpr (PROJ) {
                     if (it / KSTEPS == CT) {
@@ -1075,29 +1094,22 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                         for (int tn = 0; tn < FP; ++tn)
 #pragma unroll
                             for (int tm = 0; tm < FK; ++tm)
-                                acc2[tn][tm] = __builtin_amdgcn_mfma_i32_16x16x64_i8(Ap[it & 1][tm], B[it & 1][tn],
+                                acc2[tn][tm] = __builtin_amdgcn_mfma_i32_16x16x64_i8(Ap[it % NS][tm], B[it % NS][tn],
                                                                                      acc2[tn][tm], 0, 0, 0);
                     }
                 }
             }
             // Pin the issue order (the scheduler otherwise reuses one register
-            // set and waits on every read): the LDS reads of step it+1 go out
-            // before the MFMAs of step it.
-            if constexpr (PROJ) {
-                sched_lds_reads<FK + FP>();   // step 0 is never the centre tap
-                static_for<0, NIT>([&](auto I) {
-                    constexpr int it = decltype(I)::value;
-                    if constexpr (it + 1 < NIT) sched_lds_reads<FK + FP + ((it + 1) / KSTEPS == CT ? FK : 0)>();
-                    sched_mfmas<FP * FK * (it / KSTEPS == CT ? 2 : 1)>();
-                });
-            } else {
-                sched_lds_reads<FK + FP>();
-#pragma unroll
-                for (int it = 0; it < NIT; ++it) {
-                    if (it + 1 < NIT) sched_lds_reads<FK + FP>();
-                    sched_mfmas<FP * FK>();
-                }
-            }
+            // set and waits on every read): the LDS reads of step it+LA go out
+            // before the MFMAs of step it.  (PROJ: the centre tap's steps read
+            // and multiply the projection's fragments too.)
+            constexpr auto centre = [](int it) { return PROJ && it / KSTEPS == CT; };
+            static_for<0, LA>([&](auto J) { sched_lds_reads<FK + FP + (centre(decltype(J)::value) ? FK : 0)>(); });
+            static_for<0, NIT>([&](auto I) {
+                constexpr int it = decltype(I)::value;
+                if constexpr (it + LA < NIT) sched_lds_reads<FK + FP + (centre(it + LA) ? FK : 0)>();
+                sched_mfmas<FP * FK * (centre(it) ? 2 : 1)>();
+            });
         } else {
             // three fragment sets in rotation: the LDS reads of step it+2 are in
             // flight while the MFMAs of step it run
@@ -1169,44 +1181,65 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         if constexpr (NCHW)
             if (a.xpk && a.off_b1 != a.off_b0) nchw_write_packed(ti, c, cur);
         if (c == c_end - 1) {
-            if (!PROJ && a.splits > 1) {
+            if (a.splits > 1) {
                 // split-K: publish this split's partial sums; the last split of the
-                // tile to arrive adds the others and runs the epilogue
+                // tile to arrive adds the others and runs the epilogue.  Partial
+                // sums move with device-coherent loads and stores (sc1, the form
+                // of monotonic agent-scope atomics), so no L2 write-back or
+                // invalidation is needed: the stores are complete (waited for)
+                // before the arrival count is bumped, and the last arrival reads
+                // them past the caches.  (A release/acquire pair would write back
+                // and invalidate the whole L2 of the XCD in every workgroup.)
+                // (PROJ: the projection's partial sums follow the layer's)
                 const int tile = lt;
-                int4 *mine = reinterpret_cast<int4 *>(a.ws_part) +
-                             ((size_t)(tile * a.splits + sp) * NW + wave) * (FP * FK * 64) + lane;
+                constexpr int kFrag = 64 * 16;                      // one fragment of a wave: 64 lanes x int4
+                constexpr int kAccBytes = NW * FP * FK * kFrag;      // one accumulator set of a tile
+                constexpr int kSplitBytes = (PROJ ? 2 : 1) * kAccBytes;   // one split's partial sums of a tile
+                const __amdgpu_buffer_rsrc_t rws = make_brsrc(
+                    reinterpret_cast<const uint8_t *>(a.ws_part) + (size_t)tile * a.splits * kSplitBytes,
+                    a.splits * kSplitBytes);
+                const int lane_off = (wave * FP * FK) * kFrag + lane * 16;
 #pragma unroll
                 for (int tn = 0; tn < FP; ++tn)
 #pragma unroll
                     for (int tm = 0; tm < FK; ++tm) {
                         const v4i v = acc[tn][tm];
-                        mine[(tn * FK + tm) * 64] = int4{v[0], v[1], v[2], v[3]};
+                        __builtin_amdgcn_raw_buffer_store_b128(u32x4{(uint32_t)v[0], (uint32_t)v[1], (uint32_t)v[2], (uint32_t)v[3]},
+                                                               rws, sp * kSplitBytes + lane_off + (tn * FK + tm) * kFrag, 0,
+                                                               kCoherentAux);
+                        if constexpr (PROJ) {
+                            const v4i v2 = acc2[tn][tm];
+                            __builtin_amdgcn_raw_buffer_store_b128(
+                                u32x4{(uint32_t)v2[0], (uint32_t)v2[1], (uint32_t)v2[2], (uint32_t)v2[3]}, rws,
+                                sp * kSplitBytes + kAccBytes + lane_off + (tn * FK + tm) * kFrag, 0, kCoherentAux);
+                        }
                     }
-                // every wave's partial stores are complete before the one
-                // agent-scope release (an L2 write-back) that publishes them;
-                // the same atomic's acquire side invalidates the caches the
-                // workgroup then reads the other partial sums through
-                __builtin_amdgcn_s_waitcnt(0);
+                __builtin_amdgcn_s_waitcnt(0);   // every wave's partial stores are complete
                 __syncthreads();
                 uint32_t *flag = reinterpret_cast<uint32_t *>(smem + a.off_m) + 2 * TK;   // past multipliers and biases
                 if (tid == 0)
-                    *flag = __hip_atomic_fetch_add(a.ws_cnt + tile, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+                    *flag = __hip_atomic_fetch_add(a.ws_cnt + tile, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 __syncthreads();
                 const bool last = *flag == (uint32_t)(a.splits - 1);
                 if (!last) return;   // uniform over the workgroup
                 for (int o = 0; o < a.splits; ++o) {
                     if (o == sp) continue;
-                    const int4 *other = reinterpret_cast<const int4 *>(a.ws_part) +
-                                        ((size_t)(tile * a.splits + o) * NW + wave) * (FP * FK * 64) + lane;
 #pragma unroll
                     for (int tn = 0; tn < FP; ++tn)
 #pragma unroll
                         for (int tm = 0; tm < FK; ++tm) {
-                            const int4 q = other[(tn * FK + tm) * 64];
-                            acc[tn][tm] += v4i{q.x, q.y, q.z, q.w};
+                            const u32x4 q = __builtin_amdgcn_raw_buffer_load_b128(
+                                rws, o * kSplitBytes + lane_off + (tn * FK + tm) * kFrag, 0, kCoherentAux);
+                            acc[tn][tm] += v4i{(int)q[0], (int)q[1], (int)q[2], (int)q[3]};
+                            if constexpr (PROJ) {
+                                const u32x4 q2 = __builtin_amdgcn_raw_buffer_load_b128(
+                                    rws, o * kSplitBytes + kAccBytes + lane_off + (tn * FK + tm) * kFrag, 0, kCoherentAux);
+                                acc2[tn][tm] += v4i{(int)q2[0], (int)q2[1], (int)q2[2], (int)q2[3]};
+                            }
                         }
                 }
-                if (tid == 0) a.ws_cnt[tile] = 0u;   // ready for the next call
+                if (tid == 0)   // ready for the next call
+                    __hip_atomic_store(a.ws_cnt + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
             if constexpr (LDSEPI)
                 lds_epilogue(ti);

@@ -120,19 +120,26 @@ class Chain:
             inp = self.x if L.src < 0 else outs[L.src]
             if i in self.pairs:
                 P = layers[self.pairs[i]]
-                tile = L.tile if L.tile != -1 else sweep.tuned_proj_tile(L.desc)
+                tile, splits = L.tile, L.splits
+                if tile == -1:
+                    tile, tuned_splits = sweep.tuned_proj_config(L.desc)
+                    splits = splits or tuned_splits
+                splits = splits or 1
                 wprep = qconv.prepare_filters_proj(L.desc, L.w_packed, P.w_packed, tile)
+                nws = qconv.proj_workspace_bytes(L.desc, tile, splits)
+                ws = torch.zeros(nws, dtype=torch.uint8, device=x_packed.device) if nws else None
                 first = qconv.ProjConv2dCall(L.desc, inp, wprep, tile=tile, requant=True, mult=L.mult,
                                              shift=L.shift, relu=L.relu, clamp=L.clamp, bias=L.bias,
                                              proj=dict(mult=P.mult, shift=P.shift, relu=P.relu, clamp=P.clamp,
-                                                       bias=P.bias))
+                                                       bias=P.bias), splits=splits, workspace=ws)
                 y, yp = first.out, first.out_proj
 
-                def make(stream, L=L, P=P, inp=inp, wprep=wprep, tile=tile, y=y, yp=yp):
+                def make(stream, L=L, P=P, inp=inp, wprep=wprep, tile=tile, splits=splits, ws=ws, y=y, yp=yp):
                     return qconv.ProjConv2dCall(L.desc, inp, wprep, tile=tile, requant=True, mult=L.mult,
                                                 shift=L.shift, relu=L.relu, clamp=L.clamp, bias=L.bias,
                                                 proj=dict(mult=P.mult, shift=P.shift, relu=P.relu, clamp=P.clamp,
-                                                          bias=P.bias), out=y, out_proj=yp, stream=stream)
+                                                          bias=P.bias), out=y, out_proj=yp, splits=splits,
+                                                workspace=ws, stream=stream)
                 proj_out[i] = yp
                 self.filters.append(wprep)
                 outs.append(y)

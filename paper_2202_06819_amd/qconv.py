@@ -127,14 +127,16 @@ def lib() -> ctypes.CDLL:
         L.qconv_proj_tile_check.argtypes = [P(QConvDesc), _i32]
         L.qconv_prepared_proj_filter_bytes.argtypes = [P(QConvDesc), _i32, P(ctypes.c_size_t)]
         L.qconv_prepare_filters_proj.argtypes = [P(QConvDesc), _vp, _vp, _i32, _vp, ctypes.c_size_t, _vp]
+        L.qconv_proj_workspace_bytes.argtypes = [P(QConvDesc), _i32, _i32, P(ctypes.c_size_t)]
         L.qconv2d_proj.argtypes = [P(QConvDesc), _vp, _vp, ctypes.c_size_t, P(QConvEpilogue), _vp,
-                                   P(QConvEpilogue), _vp, _i32, _vp]
+                                   P(QConvEpilogue), _vp, _i32, _i32, _vp, ctypes.c_size_t, _vp]
         for f in ("qconv_layout", "qconv_pack", "qconv2d", "qconv_tile_count", "qconv_tile_get", "qconv_tile_check",
                   "qconv_default_tile", "qconv_selftest", "qconv_prepared_filter_bytes", "qconv_prepare_filters",
                   "qconv2d_prepared", "qconv_workspace_bytes", "qconv_max_splits", "qconv_probe_mfma_i8", "qconv_schedule_check", "qconv2d_scheduled", "qconv_unroll", "qconv_pack_interleaved",
                   "qconv2d_packing", "qconv2d_prepared_noalloc", "qconv_noalloc_limits", "qconv_probe_launch",
                   "qconv_last_launch", "qconv_proj_default_tile", "qconv_proj_tile_check",
-                  "qconv_prepared_proj_filter_bytes", "qconv_prepare_filters_proj", "qconv2d_proj"):
+                  "qconv_prepared_proj_filter_bytes", "qconv_prepare_filters_proj", "qconv_proj_workspace_bytes",
+                  "qconv2d_proj"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
         return L
@@ -560,6 +562,14 @@ def proj_tile_status(d: dict, tile_id: int) -> int:
     return lib().qconv_proj_tile_check(ctypes.byref(make_desc(d)), int(tile_id))
 
 
+def proj_workspace_bytes(d: dict, tile: int = -1, splits: int = 1) -> int:
+    """Split-K workspace bytes of the fused projection launch; 0 without a split."""
+    n = ctypes.c_size_t(0)
+    _check(lib().qconv_proj_workspace_bytes(ctypes.byref(make_desc(d)), int(tile), int(splits), ctypes.byref(n)),
+           "qconv_proj_workspace_bytes")
+    return int(n.value)
+
+
 def proj_desc(d: dict) -> dict:
     """The 1x1 projection a 3x3 layer can carry: same input, channels and stride, no padding."""
     return dict(d, r=1, s=1, pad_h=0, pad_w=0)
@@ -603,12 +613,15 @@ class ProjConv2dCall:
     (requant=False) gives both int32 accumulator tensors; requant mode takes
     each output's own multipliers, shift, ReLU, clamp and optional bias
     (``proj`` holds the projection's: dict(mult=, shift=, relu=, clamp=, bias=)).
+    `splits` > 1 is split-K, with a zero-filled `workspace` of
+    :func:`proj_workspace_bytes` (made here when not given).
     """
 
     def __init__(self, d: dict, x: torch.Tensor, w_prepared: torch.Tensor, *, tile: int = -1, requant: bool = False,
                  mult: torch.Tensor | None = None, shift: int = 20, relu: bool = True, clamp: tuple = (0, 15),
                  bias: torch.Tensor | None = None, proj: dict | None = None, out: torch.Tensor | None = None,
-                 out_proj: torch.Tensor | None = None, stream=None):
+                 out_proj: torch.Tensor | None = None, splits: int = 1, workspace: torch.Tensor | None = None,
+                 stream=None):
         self.desc = make_desc(d)
         info = layout(d)
         bits = self.desc.bits
@@ -632,10 +645,18 @@ class ProjConv2dCall:
         y_bytes = info["y_packed_bytes"] if requant else info["y_raw_bytes"]
         self.x, self.w, self.out, self.out_proj, self.info = x, w_prepared, out, out_proj, info
         self.keep = (mult, bias, proj)
+        self.splits = int(splits)
+        if workspace is None and self.splits > 1:
+            nws = proj_workspace_bytes(d, self.tile, self.splits)
+            workspace = torch.zeros(nws, dtype=torch.uint8, device=x.device) if nws else None
+        self.workspace = workspace
+        ws_ptr, ws_bytes = (None, 0) if workspace is None else (_dev_ptr(workspace, "workspace"),
+                                                               workspace.numel() * workspace.element_size())
         self._args = (ctypes.byref(self.desc), _dev_ptr(x, "x", info["x_bytes"]),
                       _dev_ptr(w_prepared, "w", int(n.value)), w_prepared.numel() * w_prepared.element_size(),
                       ctypes.byref(self.epi), _dev_ptr(out, "y", y_bytes), ctypes.byref(self.epi_proj),
-                      _dev_ptr(out_proj, "y_proj", y_bytes), self.tile, _vp(_stream(stream)))
+                      _dev_ptr(out_proj, "y_proj", y_bytes), self.tile, self.splits, ws_ptr, ws_bytes,
+                      _vp(_stream(stream)))
         self._fn = lib().qconv2d_proj
 
     def __call__(self):

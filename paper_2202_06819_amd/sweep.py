@@ -70,15 +70,23 @@ def proj_key(d: dict, requant: bool = True) -> str:
     return shape_key(d, requant) + "_proj"
 
 
-def tuned_proj_tile(d: dict, requant: bool = True) -> int:
-    """The swept best tile for the 3x3 layer `d` with a fused projection (the
-    library's built-in choice when unswept)."""
+def tuned_proj_config(d: dict, requant: bool = True) -> tuple[int, int]:
+    """(tile id, split-K factor) the sweep found fastest for the 3x3 layer `d`
+    with a fused projection (the library's built-in tile without a split when
+    unswept)."""
     entry = tuned_table().get(proj_key(d, requant))
     if entry:
         for t in qconv.tiles():
             if t["name"] == entry["tile"] and qconv.proj_tile_status(d, t["id"]) == 0:
-                return t["id"]
-    return qconv.proj_default_tile(d)
+                splits = int(entry.get("splits", 1))
+                if splits <= max(1, qconv.max_splits(d, t["id"])):
+                    return t["id"], splits
+    return qconv.proj_default_tile(d), 1
+
+
+def tuned_proj_tile(d: dict, requant: bool = True) -> int:
+    """The swept best tile for the 3x3 layer `d` with a fused projection."""
+    return tuned_proj_config(d, requant)[0]
 
 
 def split_choices(d: dict, tile: int) -> list[int]:
@@ -168,9 +176,10 @@ def sweep_layer(d: dict, x: torch.Tensor, w: torch.Tensor, mult: torch.Tensor | 
 def sweep_proj_layer(d: dict, x: torch.Tensor, w3: torch.Tensor, w1: torch.Tensor, mult: torch.Tensor | None,
                      mult2: torch.Tensor | None, *, shift=20, shift2=20, relu=True, relu2=False, clamp=(0, 15),
                      reps=100, rounds=5, done=frozenset(), log=print, expected=None) -> list[dict]:
-    """Every tile with a projection instance on a 3x3 layer with its 1x1
-    projection fused in (packed filters w3 and w1); both outputs of each must
-    equal `expected` = (y, y_proj), or else the built-in tile's."""
+    """Every tile with a projection instance, and each of its split-K factors,
+    on a 3x3 layer with its 1x1 projection fused in (packed filters w3 and w1);
+    both outputs of each must equal `expected` = (y, y_proj), or else the
+    built-in tile's."""
     requant = mult is not None
     key = proj_key(d, requant)
     ops = 2 * qconv.layout(d)["macs"] + 2 * qconv.layout(qconv.proj_desc(d))["macs"]
@@ -178,8 +187,8 @@ def sweep_proj_layer(d: dict, x: torch.Tensor, w3: torch.Tensor, w1: torch.Tenso
     kw = dict(requant=True, mult=mult, shift=shift, relu=relu, clamp=clamp,
               proj=dict(mult=mult2, shift=shift2, relu=relu2, clamp=clamp)) if requant else {}
 
-    def make_for(tid, wprep, stream=None):
-        return qconv.ProjConv2dCall(d, x, wprep, tile=tid, stream=stream, **kw)
+    def make_for(tid, wprep, stream=None, splits=1, ws=None):
+        return qconv.ProjConv2dCall(d, x, wprep, tile=tid, stream=stream, splits=splits, workspace=ws, **kw)
 
     if expected is None:
         y, yp = make_for(default, qconv.prepare_filters_proj(d, w3, w1, default))()
@@ -188,21 +197,30 @@ def sweep_proj_layer(d: dict, x: torch.Tensor, w3: torch.Tensor, w1: torch.Tenso
         ref = tuple(e.to(x.device) for e in expected)
     rows = []
     for t in qconv.tiles():
-        if qconv.proj_tile_status(d, t["id"]) != 0 or (key, t["name"], 1) in done:
+        if qconv.proj_tile_status(d, t["id"]) != 0:
             continue
-        wprep = qconv.prepare_filters_proj(d, w3, w1, t["id"])
-        y, yp = make_for(t["id"], wprep)()
-        torch.cuda.synchronize()
-        same = all(o.shape == r.shape and bool(torch.equal(o.view(r.dtype), r)) for o, r in zip((y, yp), ref))
-        us = _time(lambda stream, tid=t["id"], wprep=wprep: make_for(tid, wprep, stream), reps, rounds)
-        tops = ops / (us * 1e-6) / 1e12
-        row = {"shape": key, "tile": t["name"], "tile_id": t["id"], "splits": 1, "default": t["id"] == default,
-               "us": round(us, 3), "tops": round(tops, 2), "pct_int8_peak": round(100 * tops / INT8_PEAK_TOPS, 3),
-               "identical": same}
-        rows.append(row)
-        log(json.dumps(row))
-        if not same:
-            raise RuntimeError(f"tile {t['name']} (fused projection) output differs from the reference on {key}")
+        wprep = None
+        for splits in split_choices(d, t["id"]):
+            if (key, t["name"], splits) in done:
+                continue
+            if wprep is None:
+                wprep = qconv.prepare_filters_proj(d, w3, w1, t["id"])
+            nws = qconv.proj_workspace_bytes(d, t["id"], splits)
+            ws = torch.zeros(nws, dtype=torch.uint8, device=x.device) if nws else None
+            y, yp = make_for(t["id"], wprep, splits=splits, ws=ws)()
+            torch.cuda.synchronize()
+            same = all(o.shape == r.shape and bool(torch.equal(o.view(r.dtype), r)) for o, r in zip((y, yp), ref))
+            us = _time(lambda stream, tid=t["id"], wprep=wprep, splits=splits, ws=ws:
+                       make_for(tid, wprep, stream, splits, ws), reps, rounds)
+            tops = ops / (us * 1e-6) / 1e12
+            row = {"shape": key, "tile": t["name"], "tile_id": t["id"], "splits": splits,
+                   "default": t["id"] == default and splits == 1, "us": round(us, 3), "tops": round(tops, 2),
+                   "pct_int8_peak": round(100 * tops / INT8_PEAK_TOPS, 3), "identical": same}
+            rows.append(row)
+            log(json.dumps(row))
+            if not same:
+                raise RuntimeError(f"tile {t['name']} splits {splits} (fused projection) output differs from the "
+                                   f"reference on {key}")
     return rows
 
 

@@ -522,9 +522,26 @@ def test_projection_entry_points_validate_on_the_host(q):
     raw.mode = q.OUT_RAW_I32
     rq.mode, rq.mult, rq.shift, rq.relu, rq.clamp_lo, rq.clamp_hi = q.OUT_REQUANT, 1 << 20, 20, 1, 0, 15
     args = (ctypes.byref(desc), 1 << 20, 2 << 20, 1 << 30)
-    assert q.lib().qconv2d_proj(*args, ctypes.byref(raw), 3 << 20, ctypes.byref(rq), 4 << 20, t, None) == q.EINVAL
+    assert q.lib().qconv2d_proj(*args, ctypes.byref(raw), 3 << 20, ctypes.byref(rq), 4 << 20, t, 1, None, 0,
+                                None) == q.EINVAL
     rq2 = q.QConvEpilogue.from_buffer_copy(rq)
     rq2.residual = 5 << 20
-    assert q.lib().qconv2d_proj(*args, ctypes.byref(rq), 3 << 20, ctypes.byref(rq2), 4 << 20, t, None) \
-        == q.EUNSUPPORTED
-    assert q.lib().qconv2d_proj(*args, ctypes.byref(rq), 3 << 20, ctypes.byref(rq), None, t, None) == q.EINVAL
+    assert q.lib().qconv2d_proj(*args, ctypes.byref(rq), 3 << 20, ctypes.byref(rq2), 4 << 20, t, 1, None, 0,
+                                None) == q.EUNSUPPORTED
+    assert q.lib().qconv2d_proj(*args, ctypes.byref(rq), 3 << 20, ctypes.byref(rq), None, t, 1, None, 0,
+                                None) == q.EINVAL
+    # split-K (over 64-channel chunks): the projection's partial sums double the
+    # workspace; a missing one is refused
+    d2 = D(n=2, h=9, w=9, c=256, stride_h=2, stride_w=2)
+    t2 = next(tt["id"] for tt in q.tiles() if tt["name"] == "wide_b4_w4x2_f2x2_c64")
+    assert q.proj_tile_status(d2, t2) == q.OK
+    assert q.proj_workspace_bytes(d2, t2, 1) == 0
+    assert q.max_splits(d2, t2) == 4
+    plain_ws, proj_ws = q.workspace_bytes(d2, t2, 2), q.proj_workspace_bytes(d2, t2, 2)
+    assert plain_ws < proj_ws < 2 * plain_ws
+    desc2 = q.make_desc(d2)
+    args2 = (ctypes.byref(desc2), 1 << 20, 2 << 20, 1 << 30)
+    assert q.lib().qconv2d_proj(*args2, ctypes.byref(rq), 3 << 20, ctypes.byref(rq), 4 << 20, t2, 2, None, 0,
+                                None) == q.EWORKSPACE
+    with pytest.raises(q.QConvError):
+        q.proj_workspace_bytes(d2, t2, 5)

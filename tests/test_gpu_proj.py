@@ -2,7 +2,8 @@
 element by element: both outputs -- the 3x3 layer's and the projection's --
 as raw int32 accumulators and requantised (each with its own multipliers,
 shift, clamp and optional bias), on every tile that has a projection
-instance, on small ragged shapes (odd sizes, several channel chunks, 4-bit
+instance, without and with split-K (each split call made twice on one
+workspace), on small ragged shapes (odd sizes, several channel chunks, 4-bit
 and 8-bit, stride 2 and 1) and on the three stage entries of the ResNet-18
 stacks at full size in the configuration the chain runs."""
 import numpy as np
@@ -54,7 +55,7 @@ def _refs(L, t, shift, shift2, bias):
     return r3, r1
 
 
-def _check_layer(L, t, tile, shifts, label):
+def _check_layer(L, t, tile, shifts, label, splits=(1,)):
     import torch
     from paper_2202_06819_amd import qconv
     dev = torch.device("cuda:0")
@@ -65,24 +66,40 @@ def _check_layer(L, t, tile, shifts, label):
     w1 = qconv.pack(torch.from_numpy(t["w1"]).to(dev), L.bits, L.w_signed)
     wprep = qconv.prepare_filters_proj(d, w3, w1, tile)
     dv = {k: torch.from_numpy(t[k]).to(dev) for k in ("mult", "mult2", "bias", "bias2")}
-    announce(f"proj {label} {L.name} tile {tile} raw")
-    y, yp = qconv.ProjConv2dCall(d, xp, wprep, tile=tile)()
-    torch.cuda.synchronize()
-    r3, r1 = _refs(L, t, shifts[0][0], shifts[0][1], False)
-    assert_same(y.cpu().numpy(), r3["acc"], f"{L.name} tile {tile}: 3x3 accumulators")
-    assert_same(yp.cpu().numpy(), r1["acc"], f"{L.name} tile {tile}: projection accumulators")
-    for shift, shift2 in shifts:
-        for bias in (False, True):
-            announce(f"proj {label} {L.name} tile {tile} shifts {shift}/{shift2} bias {bias}")
-            call = qconv.ProjConv2dCall(d, xp, wprep, tile=tile, requant=True, mult=dv["mult"], shift=shift,
-                                        relu=e.relu, clamp=(e.lo, e.hi), bias=dv["bias"] if bias else None,
-                                        proj=dict(mult=dv["mult2"], shift=shift2, relu=False, clamp=(e.lo, e.hi),
-                                                  bias=dv["bias2"] if bias else None))
+    refs = {}
+
+    def ref(shift, shift2, bias):
+        if (shift, shift2, bias) not in refs:
+            refs[(shift, shift2, bias)] = _refs(L, t, shift, shift2, bias)
+        return refs[(shift, shift2, bias)]
+
+    for sp in splits:
+        nws = qconv.proj_workspace_bytes(d, tile, sp)
+        ws = torch.zeros(nws, dtype=torch.uint8, device=dev) if nws else None
+        rounds = 2 if sp > 1 else 1   # a split call leaves its workspace ready for the next
+        announce(f"proj {label} {L.name} tile {tile} splits {sp} raw")
+        call = qconv.ProjConv2dCall(d, xp, wprep, tile=tile, splits=sp, workspace=ws)
+        r3, r1 = ref(shifts[0][0], shifts[0][1], False)
+        for rnd in range(rounds):
             y, yp = call()
             torch.cuda.synchronize()
-            r3, r1 = _refs(L, t, shift, shift2, bias)
-            assert_same(y.cpu().numpy(), r3["y_packed"], f"{L.name} tile {tile} shift {shift} bias {bias}: 3x3")
-            assert_same(yp.cpu().numpy(), r1["y_packed"], f"{L.name} tile {tile} shift {shift2} bias {bias}: proj")
+            assert_same(y.cpu().numpy(), r3["acc"], f"{L.name} tile {tile} splits {sp} ({rnd}): 3x3 accumulators")
+            assert_same(yp.cpu().numpy(), r1["acc"], f"{L.name} tile {tile} splits {sp} ({rnd}): projection "
+                                                     f"accumulators")
+        for shift, shift2 in shifts:
+            for bias in (False, True):
+                announce(f"proj {label} {L.name} tile {tile} splits {sp} shifts {shift}/{shift2} bias {bias}")
+                call = qconv.ProjConv2dCall(d, xp, wprep, tile=tile, requant=True, mult=dv["mult"], shift=shift,
+                                            relu=e.relu, clamp=(e.lo, e.hi), bias=dv["bias"] if bias else None,
+                                            proj=dict(mult=dv["mult2"], shift=shift2, relu=False, clamp=(e.lo, e.hi),
+                                                      bias=dv["bias2"] if bias else None), splits=sp, workspace=ws)
+                r3, r1 = ref(shift, shift2, bias)
+                for rnd in range(rounds):
+                    y, yp = call()
+                    torch.cuda.synchronize()
+                    what = f"{L.name} tile {tile} splits {sp} ({rnd}) shift {shift}/{shift2} bias {bias}"
+                    assert_same(y.cpu().numpy(), r3["y_packed"], f"{what}: 3x3")
+                    assert_same(yp.cpu().numpy(), r1["y_packed"], f"{what}: proj")
 
 
 @pytest.mark.parametrize("lid", range(len(SMALL)))
@@ -95,7 +112,8 @@ def test_proj_every_tile_small(lid):
     tiles = [tt["id"] for tt in qconv.tiles() if qconv.proj_tile_status(L.desc(), tt["id"]) == 0]
     assert tiles, f"no projection tile fits {L.name}"
     for tile in tiles:
-        _check_layer(L, t, tile, [(s3, s1)], "small")
+        chunks = qconv.max_splits(L.desc(), tile)
+        _check_layer(L, t, tile, [(s3, s1)], "small", splits=sorted({1, 2, chunks} & set(range(1, chunks + 1))))
 
 
 def _stage_entries(cfg):
@@ -116,7 +134,7 @@ def test_proj_stage_entries_full_size(cfg):
     inputs (the 3x3 layer's x, filters and multipliers; the projection's
     filters and multipliers), the tuned tile, the literal epilogues and ones
     that spread outputs over the clamp range."""
-    from paper_2202_06819_amd import sweep
+    from paper_2202_06819_amd import qconv, sweep
     for L, P, i, j in _stage_entries(cfg):
         t = qi.layer_tensors(cfg, i, L)
         tp = qi.layer_tensors(cfg, j, P)
@@ -124,11 +142,12 @@ def test_proj_stage_entries_full_size(cfg):
         g = np.random.default_rng([cfg, i, 9])
         t["bias"] = g.integers(-256, 256, size=L.k).astype(np.int32)
         t["bias2"] = g.integers(-256, 256, size=L.k).astype(np.int32)
-        tile = sweep.tuned_proj_tile(L.desc())
+        tile, splits = sweep.tuned_proj_config(L.desc())
         e = L.epilogue
         shifts = [(e.shift, P.epilogue.shift),
                   (stress_shift(L, L.x_range, L.w_range), stress_shift(P, P.x_range, P.w_range))]
-        _check_layer(L, t, tile, shifts, f"workload {cfg}")
+        other = 2 if splits == 1 and qconv.max_splits(L.desc(), tile) >= 2 else 1
+        _check_layer(L, t, tile, shifts, f"workload {cfg}", splits=sorted({splits, other}))
 
 
 def test_proj_rejects_what_it_does_not_run():
