@@ -149,6 +149,20 @@ __device__ __forceinline__ void init_acc(const ConvArgs &a, v4i (&acc)[FP][FK], 
     }
 }
 
+// Adds bias * 2^acc_shift of this lane's channels (4*FK readable entries at
+// bsrc) to finished accumulators: the sums init_acc's start values give, since
+// the bias contract keeps every result inside int32.
+template <int FP, int FK>
+__device__ __forceinline__ void add_bias(const ConvArgs &a, v4i (&acc)[FP][FK], const int32_t *bsrc) {
+#pragma unroll
+    for (int tm = 0; tm < FK; ++tm) {
+        const int4 q = *reinterpret_cast<const int4 *>(bsrc + 4 * tm);
+        const v4i b = (v4i)((__attribute__((ext_vector_type(4))) unsigned)v4i{q.x, q.y, q.z, q.w} << (unsigned)a.acc_shift);
+#pragma unroll
+        for (int tn = 0; tn < FP; ++tn) acc[tn][tm] += b;
+    }
+}
+
 // The residual words of one pixel's channel run (the same words store_run
 // writes); zeros for a pixel past the output.
 template <int BITS, int FK>

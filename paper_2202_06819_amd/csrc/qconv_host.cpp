@@ -11,6 +11,7 @@
 #include <initializer_list>
 #include <mutex>
 #include <string>
+#include <set>
 #include <unordered_map>
 
 #include "qconv.h"
@@ -419,7 +420,7 @@ int pick_proj_default(const qconv_desc *d, const qconv_layout_info &li) {
 
 struct DevAttrCache {
     std::mutex mu;
-    std::unordered_map<long long, bool> done;   // (device, tile) -> max LDS attribute set
+    std::set<std::pair<int, const void *>> done;   // (device, kernel) whose max LDS attribute is set
 };
 DevAttrCache g_attr;
 
@@ -637,20 +638,16 @@ void fill_args(ConvArgs &a, const qconv_desc *d, const qconv_layout_info &li, co
     a.acc_shift = d->bits == 4 ? 4 * (d->x_signed + d->w_signed) : 0;
 }
 
-// inst: 0 = the tile's generic kernel, 1 + i = its fixed-size instance i; 3 + the same for
-// the kernels with the bias and residual epilogue; 6 / 7 the multi-chunk 3x3 instance
-// (plain / with bias and residual); 8 + mask for an ablation instance (masks 1..3; 16 + mask
-// for masks 4..7); 12 the fused pack; 14 / 15 the fused projection (plain / with biases).
-int ensure_lds_attribute(const void *kernel, int tile_id, int inst, int64_t lds) {
+// Kernels that stage more than 64 KiB of LDS must opt in, once per device.
+int ensure_lds_attribute(const void *kernel, int64_t lds) {
     if (lds <= 64 * 1024) return QCONV_OK;
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return fail(QCONV_EHIP, "hipGetDevice failed");
-    const long long key = ((long long)dev * 4096 + tile_id) * 16 + inst;
     std::lock_guard<std::mutex> g(g_attr.mu);
-    if (!g_attr.done[key]) {
+    if (!g_attr.done.count({dev, kernel})) {
         hipError_t e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
         if (e != hipSuccess) return fail(QCONV_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
-        g_attr.done[key] = true;
+        g_attr.done.insert({dev, kernel});
     }
     return QCONV_OK;
 }
@@ -795,7 +792,7 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
     const KernelSet &ks = ext ? te.ext : te.plain;
     ConvLauncher launch = ks.launch;
     const void *kernel = ks.kernel;
-    int inst = ext ? 3 : 0;
+    const FixedInstance *single = nullptr;   // the fixed-size instance whose single-stage copy may run
     if (prepared && te.info.variant == QCONV_VARIANT_WIDE)
         for (int i = 0; i < 2; ++i)
             if (ks.fixed[i].launch && ks.fixed[i].r == d->r && ks.fixed[i].s == d->s && (d->nb == 1 || d->s == 1)) {
@@ -804,19 +801,19 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
                 const bool mc = pl.cps > 1 && ks.fixed[i].launch_mc;
                 launch = mc ? ks.fixed[i].launch_mc : ks.fixed[i].launch;
                 kernel = mc ? ks.fixed[i].kernel_mc : ks.fixed[i].kernel;
-                inst = mc ? (ext ? 7 : 6) : (ext ? 3 : 0) + 1 + i;
+                single = mc ? nullptr : &ks.fixed[i];
             }
     if (pi) {
         const FixedInstance &fi = ext ? pi->ext : pi->plain;
         launch = fi.launch;
         kernel = fi.kernel;
-        inst = ext ? 15 : 14;
+        single = &fi;
     }
     if (ablation) {
         const AblationInstance *ai = ablation_instance(te.info.name, ablation);
         launch = ai->launch;
         kernel = ai->kernel;
-        inst = ablation < 4 ? 8 + ablation : 16 + ablation;
+        single = nullptr;
     }
     if (fused) {
         if (!prepared || !te.fused.launch || d->r != te.fused.r || d->s != te.fused.s || ext || ablation || d->nb != 1)
@@ -838,11 +835,11 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
         }
         launch = te.fused.launch;
         kernel = te.fused.kernel;
-        inst = 12;
+        single = nullptr;
     }
     if (te.info.variant == QCONV_VARIANT_WIDE && pl.splits == 1 && pl.off_b1 != pl.off_b0) {
         // persistent grid: size it by the occupancy the runtime reports for this kernel
-        rc = ensure_lds_attribute(kernel, tile_id, inst, pl.lds);
+        rc = ensure_lds_attribute(kernel, pl.lds);
         if (rc) return rc;
         int occ = 0;
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, te.info.threads, (size_t)pl.lds) != hipSuccess)
@@ -904,7 +901,13 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
             if (a.lo2 > a.hi2) a.lo2 = a.hi2;
         }
     }
-    rc = ensure_lds_attribute(kernel, tile_id, inst, pl.lds);
+    // every workgroup runs one stage (at most one tile, one chunk): the
+    // instance's single-stage copy
+    if (single && single->launch_one && pl.cps == 1 && (pl.splits > 1 || pl.grid >= pl.mtiles * pl.ktiles)) {
+        launch = single->launch_one;
+        kernel = single->kernel_one;
+    }
+    rc = ensure_lds_attribute(kernel, pl.lds);
     if (rc) return rc;
     hipError_t e = launch(a, dim3((unsigned)pl.grid), (size_t)pl.lds, (hipStream_t)stream);
     if (e != hipSuccess) return fail(QCONV_EHIP, "conv launch (%s): %s", te.info.name, hipGetErrorString(e));

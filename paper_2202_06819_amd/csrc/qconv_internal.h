@@ -118,6 +118,8 @@ struct FixedInstance {
     const void *kernel;
     ConvLauncher launch_mc; // variant for plans with several channel chunks per workgroup, or null
     const void *kernel_mc;
+    ConvLauncher launch_one;   // variant for plans whose workgroups each run one stage, or null
+    const void *kernel_one;
 };
 
 // The kernels of one tile for one epilogue flavour.

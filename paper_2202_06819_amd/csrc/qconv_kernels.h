@@ -422,8 +422,12 @@ __device__ __forceinline__ int xcd_block(int b, int g) {
 // tap's band pixels -- the fragments the 3x3 already reads -- and it keeps
 // accumulators (split-K partial sums too), multipliers and an output of its
 // own (no residual).
+// ONE: the instance for plans whose workgroups each run a single stage (one
+// tile, one chunk): it carries a copy of the stage compiled without the
+// prefetch machinery (a workgroup with more stages still takes the general
+// loop, so the instance is correct for any plan).
 template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC, bool EXT, int ABL = 0,
-          bool MC = false, bool NCHW = false, bool PROJ = false>
+          bool MC = false, bool NCHW = false, bool PROJ = false, bool ONE = false>
 __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     constexpr bool FIXED = RC > 0 && SC > 0;
     constexpr bool LOWERED = (ABL & 1) != 0;
@@ -434,6 +438,7 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     static_assert(!NCHW || (!LOWERED && !MC), "the fused pack stages the band itself");
     static_assert(ABL == 0 || (FIXED && !EXT), "ablation instances are fixed-size, without bias or residual");
     static_assert(!PROJ || (RC == 3 && SC == 3 && ABL == 0 && !MC && !NCHW), "the projection rides on a plain 3x3");
+    static_assert(!ONE || (FIXED && !MC && !NCHW), "single-stage copies are made of the fixed-size instances");
     constexpr int NW = WP * WK;
     constexpr int NT = NW * 64;
     constexpr int TP = WP * FP * 16;
@@ -902,14 +907,18 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
             e2.fast = false;
         }
     };
-    lds_epilogue_params(a, mlds, ep);
-    if constexpr (PROJ) lds_epilogue_params(ap, mlds2, ep2);
     // accumulators start from the bias (in the first split of a tile only)
     const bool bias_here = EXT && a.mode == QCONV_OUT_REQUANT && a.bias && sp == 0;
-    if (bias_here) init_acc<FP, FK>(a, acc, blds + cb - k0, false, cb);
     const bool bias2_here = PROJ && EXT && a.mode == QCONV_OUT_REQUANT && a.bias2 && sp == 0;
-    if constexpr (PROJ)
-        if (bias2_here) init_acc<FP, FK>(ap, acc2, blds2 + cb - k0, false, cb);
+    if (!ONE || nst != 1) {
+        lds_epilogue_params(a, mlds, ep);
+        if constexpr (PROJ) lds_epilogue_params(ap, mlds2, ep2);
+        if (bias_here) init_acc<FP, FK>(a, acc, blds + cb - k0, false, cb);
+        if constexpr (PROJ)
+            if (bias2_here) init_acc<FP, FK>(ap, acc2, blds2 + cb - k0, false, cb);
+    }
+    // (a single stage prepares them once its MFMAs are issued, and adds the
+    // bias to the finished sums in the workgroup that runs the epilogue)
 
     const int nit = rs * KSTEPS;
 
@@ -965,15 +974,25 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         __syncthreads();
     };
 
+    // One stage: the MFMAs over the staged chunk (with the next stage's
+    // operands in flight), then the tile's epilogue after its last chunk.  In
+    // ONE instances a workgroup with a single stage (one tile, one chunk: most
+    // single-chunk layers) runs a copy compiled without the prefetch
+    // machinery, so none of its set-up -- which the compiler hoists ahead of
+    // the loop -- sits between the first barrier and the first MFMA, and its
+    // epilogue multipliers are prepared after the MFMAs are issued.  (Kept in
+    // instances of their own: the second copy changes the general loop's
+    // register allocation.)
     int ti = 0, c = c_begin;
-    for (int st = 0; st < nst; ++st) {
+    auto stage = [&](int st, auto single) {
+        constexpr bool SINGLE = decltype(single)::value;
         int nti = ti, nc = c + 1;
         if (nc == c_end) {
             nc = c_begin;
             ++nti;
         }
-        const int cur = st & 1;
-        const bool more = st + 1 < nst;
+        const int cur = SINGLE ? 0 : st & 1;
+        const bool more = !SINGLE && st + 1 < nst;
         // prefetch the next stage; it lands while the MFMAs run
         Fetch fb;
         WFetch fw;
@@ -1241,27 +1260,38 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                 if (tid == 0)   // ready for the next call
                     __hip_atomic_store(a.ws_cnt + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
+            if constexpr (SINGLE) {
+                lds_epilogue_params(a, mlds, ep);
+                if constexpr (PROJ) lds_epilogue_params(ap, mlds2, ep2);
+                if (EXT && a.mode == QCONV_OUT_REQUANT && a.bias) add_bias<FP, FK>(a, acc, blds + cb - k0);
+                if constexpr (PROJ)
+                    if (EXT && a.mode == QCONV_OUT_REQUANT && a.bias2) add_bias<FP, FK>(ap, acc2, blds2 + cb - k0);
+            }
             if constexpr (LDSEPI)
                 lds_epilogue(ti);
             else
                 epilogue<BITS, FP, FK, EXT>(a, acc, (j0 + ti * gpk) * TP + wp * FP * 16, cb, l16, ep);
-            if (bias_here) {
-                init_acc<FP, FK>(a, acc, blds + cb - k0, false, cb);
-            } else {
-#pragma unroll
-                for (int tn = 0; tn < FP; ++tn)
-#pragma unroll
-                    for (int tm = 0; tm < FK; ++tm) acc[tn][tm] = v4i{0, 0, 0, 0};
-            }
-            if constexpr (PROJ) {
-                epilogue<BITS, FP, FK, EXT>(ap, acc2, (j0 + ti * gpk) * TP + wp * FP * 16, cb, l16, ep2);
-                if (bias2_here) {
-                    init_acc<FP, FK>(ap, acc2, blds2 + cb - k0, false, cb);
+            if constexpr (!SINGLE) {   // the accumulators of the next tile
+                if (bias_here) {
+                    init_acc<FP, FK>(a, acc, blds + cb - k0, false, cb);
                 } else {
 #pragma unroll
                     for (int tn = 0; tn < FP; ++tn)
 #pragma unroll
-                        for (int tm = 0; tm < FK; ++tm) acc2[tn][tm] = v4i{0, 0, 0, 0};
+                        for (int tm = 0; tm < FK; ++tm) acc[tn][tm] = v4i{0, 0, 0, 0};
+                }
+            }
+            if constexpr (PROJ) {
+                epilogue<BITS, FP, FK, EXT>(ap, acc2, (j0 + ti * gpk) * TP + wp * FP * 16, cb, l16, ep2);
+                if constexpr (!SINGLE) {
+                    if (bias2_here) {
+                        init_acc<FP, FK>(ap, acc2, blds2 + cb - k0, false, cb);
+                    } else {
+#pragma unroll
+                        for (int tn = 0; tn < FP; ++tn)
+#pragma unroll
+                            for (int tm = 0; tm < FK; ++tm) acc2[tn][tm] = v4i{0, 0, 0, 0};
+                    }
                 }
             }
         }
@@ -1271,6 +1301,11 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         }
         ti = nti;
         c = nc;
+    };
+    if (ONE && nst == 1) {
+        stage(0, std::bool_constant<ONE>{});
+    } else {
+        for (int st = 0; st < nst; ++st) stage(st, std::false_type{});
     }
 }
 
@@ -1321,9 +1356,9 @@ __global__ void __launch_bounds__(256) build_filter_image(ConvArgs a, int TK, in
 // One operand signedness per kernel (the widening is compiled for it); 8-bit
 // operands are always signed.
 template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC, bool EXT, int ABL = 0,
-          bool MC = false, bool NCHW = false, bool PROJ = false>
+          bool MC = false, bool NCHW = false, bool PROJ = false, bool ONE = false>
 __global__ void __launch_bounds__(WP * WK * 64) __attribute__((amdgpu_waves_per_eu(2))) conv_wide(ConvArgs a) {
-    wide_body<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC, EXT, ABL, MC, NCHW, PROJ>(a);
+    wide_body<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC, EXT, ABL, MC, NCHW, PROJ, ONE>(a);
 }
 
 // ============================================================== tile registry
@@ -1335,9 +1370,9 @@ static hipError_t launch_staged(const ConvArgs &a, dim3 grid, size_t lds, hipStr
 }
 
 template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC, bool EXT, int ABL = 0,
-          bool MC = false, bool NCHW = false, bool PROJ = false>
+          bool MC = false, bool NCHW = false, bool PROJ = false, bool ONE = false>
 static hipError_t launch_wide(const ConvArgs &a, dim3 grid, size_t lds, hipStream_t stream) {
-    hipLaunchKernelGGL((conv_wide<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC, EXT, ABL, MC, NCHW, PROJ>), grid,
+    hipLaunchKernelGGL((conv_wide<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC, EXT, ABL, MC, NCHW, PROJ, ONE>), grid,
                        dim3(WP * WK * 64), lds, stream, a);
     return hipGetLastError();
 }
@@ -1415,10 +1450,16 @@ static hipError_t launch_prep(const ConvArgs &a, uint8_t *img, int64_t elems, co
 #define QCONV_WIDE_MC(B, WP, WK, FP, FK, CK, R, S, EXT)                                                           \
     &launch_wide<B, WP, WK, FP, FK, CK, (B == 8), true, R, S, EXT, 0, true>,                                      \
         reinterpret_cast<const void *>(&conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true, R, S, EXT, 0, true>)
+#define QCONV_WIDE_ONE(B, WP, WK, FP, FK, CK, R, S, EXT)                                                          \
+    &launch_wide<B, WP, WK, FP, FK, CK, (B == 8), true, R, S, EXT, 0, false, false, false, true>,                 \
+        reinterpret_cast<const void *>(                                                                           \
+            &conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true, R, S, EXT, 0, false, false, false, true>)
 #define QCONV_WIDE_SET(B, WP, WK, FP, FK, CK, EXT)                                                                \
     {QCONV_WIDE_INST(B, WP, WK, FP, FK, CK, 0, 0, EXT),                                                           \
-     {{3, 3, QCONV_WIDE_INST(B, WP, WK, FP, FK, CK, 3, 3, EXT), QCONV_WIDE_MC(B, WP, WK, FP, FK, CK, 3, 3, EXT)}, \
-      {1, 1, QCONV_WIDE_INST(B, WP, WK, FP, FK, CK, 1, 1, EXT), nullptr, nullptr}}}
+     {{3, 3, QCONV_WIDE_INST(B, WP, WK, FP, FK, CK, 3, 3, EXT), QCONV_WIDE_MC(B, WP, WK, FP, FK, CK, 3, 3, EXT),  \
+       QCONV_WIDE_ONE(B, WP, WK, FP, FK, CK, 3, 3, EXT)},                                                         \
+      {1, 1, QCONV_WIDE_INST(B, WP, WK, FP, FK, CK, 1, 1, EXT), nullptr, nullptr,                                 \
+       QCONV_WIDE_ONE(B, WP, WK, FP, FK, CK, 1, 1, EXT)}}}
 #define QCONV_WIDE_FUSED(B, WP, WK, FP, FK, CK)                                                                   \
     {3, 3, &launch_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, false, 0, false, true>,                      \
      reinterpret_cast<const void *>(&conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, false, 0, false, true>), \
@@ -1426,7 +1467,9 @@ static hipError_t launch_prep(const ConvArgs &a, uint8_t *img, int64_t elems, co
 #define QCONV_PROJ_INST(B, WP, WK, FP, FK, CK, EXT)                                                               \
     {3, 3, &launch_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, EXT, 0, false, false, true>,                \
      reinterpret_cast<const void *>(&conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, EXT, 0, false, false, true>), \
-     nullptr, nullptr}
+     nullptr, nullptr, &launch_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, EXT, 0, false, false, true, true>, \
+     reinterpret_cast<const void *>(                                                                              \
+         &conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, EXT, 0, false, false, true, true>)}
 #define QCONV_PROJ_ENTRY(B, WP, WK, FP, FK, CK)                                                                   \
     {"wide_b" #B "_w" #WP "x" #WK "_f" #FP "x" #FK "_c" #CK, QCONV_PROJ_INST(B, WP, WK, FP, FK, CK, false),         \
      QCONV_PROJ_INST(B, WP, WK, FP, FK, CK, true)},
