@@ -626,6 +626,7 @@ void fill_args(ConvArgs &a, const qconv_desc *d, const qconv_layout_info &li, co
     a.div_s = make_fastdiv((uint32_t)d->s);
     a.div_w = make_fastdiv((uint32_t)d->w);
     a.div_wq = make_fastdiv((uint32_t)((d->w + 3) / 4));
+    a.div_brows = make_fastdiv((uint32_t)std::max<int64_t>(pl.rows, 1));
     a.x_signed = d->x_signed;
     a.w_signed = d->w_signed;
     // widening: unsigned nibble -> low half of a byte; signed nibble -> high half (value * 16)
@@ -835,7 +836,7 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
         }
         launch = te.fused.launch;
         kernel = te.fused.kernel;
-        single = nullptr;
+        single = &te.fused;
     }
     if (te.info.variant == QCONV_VARIANT_WIDE && pl.splits == 1 && pl.off_b1 != pl.off_b0) {
         // persistent grid: size it by the occupancy the runtime reports for this kernel

@@ -86,6 +86,7 @@ struct ConvArgs {
     int32_t xsrc_bytes;
     uint8_t *xpk;           // packed copy of the input written on the way, or null
     FastDiv div_w, div_wq;  // by w and by its column quads
+    FastDiv div_brows;      // by band_rows
     // a 1x1 projection at the same stride fused into a 3x3 launch (PROJ
     // instances): its filters are tap r*s of the prepared image, its input the
     // centre tap's pixels, its output and epilogue its own

@@ -438,7 +438,7 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     static_assert(!NCHW || (!LOWERED && !MC), "the fused pack stages the band itself");
     static_assert(ABL == 0 || (FIXED && !EXT), "ablation instances are fixed-size, without bias or residual");
     static_assert(!PROJ || (RC == 3 && SC == 3 && ABL == 0 && !MC && !NCHW), "the projection rides on a plain 3x3");
-    static_assert(!ONE || (FIXED && !MC && !NCHW), "single-stage copies are made of the fixed-size instances");
+    static_assert(!ONE || (FIXED && !MC), "single-stage copies are made of the fixed-size instances");
     constexpr int NW = WP * WK;
     constexpr int NT = NW * 64;
     constexpr int TP = WP * FP * 16;
@@ -635,7 +635,9 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
             vend_own = min(vend_own, vnext);
         }
     };
-    auto nchw_stage = [&](int ti, int c, int buf) {
+    // (`issued` runs once the first round's loads are out: the prologue puts
+    // its filter and channel copies behind them)
+    auto nchw_stage = [&](int ti, int c, int buf, auto &&issued) {
         uint8_t *bb = smem + (buf ? a.off_b1 : a.off_b0);
         int vlo, nrows, vend_own;
         band_rows_of(ti, vlo, nrows, vend_own);
@@ -649,8 +651,12 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         }
         constexpr int NCO = CK / 8;   // channel octets of a chunk
         constexpr int IB = 2;         // items a thread has in flight at once
+        // items run column quad fastest, then band row, then channel octet:
+        // a channel's band rows are contiguous in NCHW, so the lanes of one
+        // load instruction read one contiguous run (rows up to band_rows, the
+        // most any tile's band has; this tile's extra ones are skipped)
         const int nwq = (a.w + 3) >> 2;
-        const int items = nrows * NCO * nwq;
+        const int items = NCO * a.band_rows * nwq;
         const bool dwords = (a.w & 3) == 0;
         for (int base = 0; base < items; base += NT * IB) {
             uint32_t L[IB][8];
@@ -660,23 +666,29 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                 const int it = base + u * NT + tid;
                 const int t = (int)fdiv((uint32_t)it, a.div_wq);
                 const int wq = it - t * nwq;
-                const int co = t % NCO, rowl = t / NCO;
+                const int co = (int)fdiv((uint32_t)t, a.div_brows), rowl = t - co * a.band_rows;
+                const bool in_band = it < items && rowl < nrows;
                 const int vrow = vlo + rowl;
                 const int img = (int)fdiv((uint32_t)vrow, a.div_vh);
                 const int hh = vrow - img * a.vh - a.ph;
-                const bool row_ok = it < items && img < a.n && hh >= 0 && hh < a.h;
+                const bool row_ok = in_band && img < a.n && hh >= 0 && hh < a.h;
                 const int ww0 = wq * 4;
                 const int ch0 = c * CK + co * 8;
-                pix0[u] = it < items ? rowl * a.ncols + a.pw + ww0 : -1;
+                pix0[u] = in_band ? rowl * a.ncols + a.pw + ww0 : -1;
                 nvalid[u] = min(4, a.w - ww0);
                 plane[u] = co >> 1;
                 half[u] = (co & 1) * 8;
+                // channel ch0 + k lies k planes on: one vector offset for the
+                // octet, the plane step as the scalar offset (c is a multiple of
+                // 8, so the octet is in range or out as a whole; an offset from
+                // kOutOfRange stays past the tensor)
+                const int off0 = row_ok && ch0 < a.c ? (((img * a.c + ch0) * a.h + hh) * a.w) + ww0 : (int)kOutOfRange;
 #pragma unroll
                 for (int k = 0; k < 8; ++k) {
                     const bool ok = row_ok && ch0 + k < a.c;
                     const uint32_t off = (uint32_t)((((img * a.c + ch0 + k) * a.h + hh) * a.w) + ww0);
                     if (dwords) {
-                        L[u][k] = __builtin_amdgcn_raw_buffer_load_b32(rsx, ok ? (int)off : (int)kOutOfRange, 0, 0);
+                        L[u][k] = __builtin_amdgcn_raw_buffer_load_b32(rsx, off0, k * a.h * a.w, 0);
                     } else {
                         uint32_t v = 0u;
 #pragma unroll
@@ -688,11 +700,19 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                     }
                 }
             }
+            if (base == 0) issued();
 #pragma unroll
             for (int u = 0; u < IB; ++u) {
                 if (pix0[u] < 0) continue;
+                // (4-bit unsigned: one test for the common case of an octet
+                // already in range)
+                uint32_t any = 0u;
 #pragma unroll
-                for (int k = 0; k < 8; ++k) L[u][k] = saturate_operand<BITS, XS>(L[u][k]);
+                for (int k = 0; k < 8; ++k) any |= L[u][k];
+                if (BITS == 8 || XS || (any & 0xF0F0F0F0u) != 0u) {
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) L[u][k] = saturate_operand<BITS, XS>(L[u][k]);
+                }
                 uint32_t d0[4], d1[4];
                 if constexpr (BITS == 4) {
                     transpose4x4(L[u][0], L[u][2], L[u][4], L[u][6], d0);
@@ -865,23 +885,33 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
             if (e + lane < TK)   // TK may be 32: only the lanes of the buffer write
                 dma4(reinterpret_cast<const uint8_t *>(dst + e), (uint32_t)min(k0 + e + lane, a.k - 1) * 4u, r);
     };
-    if (a.mode == QCONV_OUT_REQUANT && wave == 0) dma_channels(mlds, a.mult);
-    if (EXT && a.mode == QCONV_OUT_REQUANT && a.bias && wave == (NW > 1 ? 1 : 0)) dma_channels(blds, a.bias);
-    if constexpr (PROJ) {
-        if (a.mode == QCONV_OUT_REQUANT && wave == (NW > 2 ? 2 : 0)) dma_channels(mlds2, a.mult2);
-        if (EXT && a.mode == QCONV_OUT_REQUANT && a.bias2 && wave == (NW > 3 ? 3 : 0)) dma_channels(blds2, a.bias2);
-    }
+    auto channel_dmas = [&] {
+        if (a.mode == QCONV_OUT_REQUANT && wave == 0) dma_channels(mlds, a.mult);
+        if (EXT && a.mode == QCONV_OUT_REQUANT && a.bias && wave == (NW > 1 ? 1 : 0)) dma_channels(blds, a.bias);
+        if constexpr (PROJ) {
+            if (a.mode == QCONV_OUT_REQUANT && wave == (NW > 2 ? 2 : 0)) dma_channels(mlds2, a.mult2);
+            if (EXT && a.mode == QCONV_OUT_REQUANT && a.bias2 && wave == (NW > 3 ? 3 : 0))
+                dma_channels(blds2, a.bias2);
+        }
+    };
 
-    // ---- prologue: stage 0 (every load in flight before the first wait)
+    // ---- prologue: stage 0 (every load in flight before the first wait).
+    // The band's loads go out first: they come from HBM, while the filter
+    // image and the channel parameters, read by every workgroup of the
+    // channel tile, mostly come from L2.
     if (nst > 0) {
-        if (w_image) w_dma(c_begin, 0);
         if constexpr (NCHW) {
-            nchw_stage(0, c_begin, 0);
+            nchw_stage(0, c_begin, 0, [&] {
+                if (w_image) w_dma(c_begin, 0);
+                channel_dmas();
+            });
             __builtin_amdgcn_s_waitcnt(0);
         } else {
             set_band(0);
             Fetch fb;
             band_fetch(c_begin, fb);
+            if (w_image) w_dma(c_begin, 0);
+            channel_dmas();
             if (!w_image) w_load_all(c_begin, 0);
             __builtin_amdgcn_s_waitcnt(0);
             band_store(fb, 0);
@@ -1183,7 +1213,7 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
             if (a.off_b1 == a.off_b0) __syncthreads();
             __builtin_amdgcn_s_waitcnt(0);   // prefetched band (and filter DMA) have landed
             if constexpr (NCHW) {
-                nchw_stage(nti, nc, cur ^ 1);
+                nchw_stage(nti, nc, cur ^ 1, [] {});
             } else {
                 band_store(fb, cur ^ 1);
                 band_rest(nc, cur ^ 1);
@@ -1463,7 +1493,9 @@ static hipError_t launch_prep(const ConvArgs &a, uint8_t *img, int64_t elems, co
 #define QCONV_WIDE_FUSED(B, WP, WK, FP, FK, CK)                                                                   \
     {3, 3, &launch_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, false, 0, false, true>,                      \
      reinterpret_cast<const void *>(&conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, false, 0, false, true>), \
-     nullptr, nullptr}
+     nullptr, nullptr, &launch_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, false, 0, false, true, false, true>, \
+     reinterpret_cast<const void *>(                                                                              \
+         &conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, false, 0, false, true, false, true>)}
 #define QCONV_PROJ_INST(B, WP, WK, FP, FK, CK, EXT)                                                               \
     {3, 3, &launch_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, EXT, 0, false, false, true>,                \
      reinterpret_cast<const void *>(&conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, EXT, 0, false, false, true>), \
