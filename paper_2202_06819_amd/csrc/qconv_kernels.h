@@ -311,6 +311,7 @@ __device__ __forceinline__ void transpose4x4(uint32_t a0, uint32_t a1, uint32_t 
 }
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) void lds_void;
 constexpr uint32_t kRsrcWord3 = 0x00020000u;   // raw buffer, dword data format (gfx9 family)
 
@@ -656,6 +657,58 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         // load instruction read one contiguous run (rows up to band_rows, the
         // most any tile's band has; this tile's extra ones are skipped)
         const int nwq = (a.w + 3) >> 2;
+        if ((a.w & 7) == 0) {
+            // rows of whole pixel octets: an item is 8 channels x 8 pixels, one
+            // 8-byte load per channel (half the load instructions of quads)
+            const int nwo = a.w >> 3;
+            const int items8 = NCO * a.band_rows * nwo;
+            const int hw = a.h * a.w;
+            for (int base = 0; base < items8; base += NT) {
+                const int it = base + tid;
+                const int t = (int)fdiv((uint32_t)(2 * it), a.div_wq);   // it / nwo (nwq = 2 nwo)
+                const int wo = it - t * nwo;
+                const int co = (int)fdiv((uint32_t)t, a.div_brows), rowl = t - co * a.band_rows;
+                const bool in_band = it < items8 && rowl < nrows;
+                const int vrow = vlo + rowl;
+                const int img = (int)fdiv((uint32_t)vrow, a.div_vh);
+                const int hh = vrow - img * a.vh - a.ph;
+                const bool row_ok = in_band && img < a.n && hh >= 0 && hh < a.h;
+                const int ww0 = wo * 8;
+                const int ch0 = c * CK + co * 8;
+                const int off0 = row_ok && ch0 < a.c ? (((img * a.c + ch0) * a.h + hh) * a.w) + ww0 : (int)kOutOfRange;
+                u32x2 L[8];
+#pragma unroll
+                for (int k = 0; k < 8; ++k) L[k] = __builtin_amdgcn_raw_buffer_load_b64(rsx, off0, k * hw, 0);
+                if (base == 0) issued();
+                if (!in_band) continue;
+                uint32_t any = 0u;
+#pragma unroll
+                for (int k = 0; k < 8; ++k) any |= L[k][0] | L[k][1];
+                if (BITS == 8 || XS || (any & 0xF0F0F0F0u) != 0u) {
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) {
+                        L[k][0] = saturate_operand<BITS, XS>(L[k][0]);
+                        L[k][1] = saturate_operand<BITS, XS>(L[k][1]);
+                    }
+                }
+                uint8_t *dst = bb + (size_t)(co >> 1) * a.pstride_b + (rowl * a.ncols + a.pw + ww0) * 16 + (co & 1) * 8;
+#pragma unroll
+                for (int hf = 0; hf < 2; ++hf) {
+                    uint32_t d0[4], d1[4];
+                    if constexpr (BITS == 4) {
+                        transpose4x4(L[0][hf], L[2][hf], L[4][hf], L[6][hf], d0);
+                        transpose4x4(L[1][hf], L[3][hf], L[5][hf], L[7][hf], d1);
+                    } else {
+                        transpose4x4(L[0][hf], L[1][hf], L[2][hf], L[3][hf], d0);
+                        transpose4x4(L[4][hf], L[5][hf], L[6][hf], L[7][hf], d1);
+                    }
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        *reinterpret_cast<uint2 *>(dst + (hf * 4 + e) * 16) = uint2{d0[e], d1[e]};
+                }
+            }
+            return;
+        }
         const int items = NCO * a.band_rows * nwq;
         const bool dwords = (a.w & 3) == 0;
         for (int base = 0; base < items; base += NT * IB) {

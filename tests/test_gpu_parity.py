@@ -705,6 +705,7 @@ FUSED_CASES = [
     ("b4_stride2", 4, 28, 28, 64, 128, 2, 4, (0, 15)),
     ("b4_persistent_n32", 32, 56, 56, 64, 64, 1, 4, (0, 15)),    # several tiles per workgroup
     ("b8_28x28_64", 4, 28, 28, 64, 64, 1, 8, (-128, 127)),
+    ("b8_24x32_64_octets", 3, 24, 32, 64, 64, 1, 8, (-128, 127)),   # 8-pixel loads, 8-bit
 ]
 
 
