@@ -785,13 +785,14 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     // tile owns -- from its band's first row up to the next tile's -- and this
     // chunk's channels: each (pixel, granule) read back from the band and
     // repacked (the inverse of the widening).
-    auto nchw_write_packed = [&](int ti, int c, int buf) {
+    // (threads first, first + step, ... of the workgroup take the units)
+    auto nchw_write_packed = [&](int ti, int c, int buf, int first, int step) {
         const uint8_t *bb = smem + (buf ? a.off_b1 : a.off_b0);
         int vlo, nrows, vend_own;
         band_rows_of(ti, vlo, nrows, vend_own);
         constexpr int NG = CK / 16;
         const int units = (vend_own - vlo) * a.w * NG;
-        for (int e = tid; e < units; e += NT) {
+        for (int e = first; e < units; e += step) {
             const int g = e % NG, t = e / NG;
             const int rowl = (int)fdiv((uint32_t)t, a.div_w), ww = t - rowl * a.w;
             const int vrow = vlo + rowl;
@@ -1095,6 +1096,13 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         }
 
         // ---- MFMA loop: int8 fragments straight from LDS, one step of lookahead
+        if constexpr (NCHW && SINGLE) {
+            // a single stage writes the packed copy before its MFMAs, from the
+            // upper half of the waves only: each shares its SIMD with a
+            // lower-half wave, whose MFMAs run meanwhile
+            constexpr int WH = NW > 1 ? NW / 2 : 0;
+            if (a.xpk && wave >= WH) nchw_write_packed(ti, c, cur, tid - WH * 64, NT - WH * 64);
+        }
         const uint8_t *bb = smem + (cur ? a.off_b1 : a.off_b0);
         const uint8_t *wb = smem + ((c_end - c_begin > 1 && cur) ? a.off_w1 : a.off_w0) + lane_a;
         auto offs = [&](int it, int &ao, int &bo) {
@@ -1255,8 +1263,8 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         // the packed copy of this stage's band rows: before the next stage is
         // staged when that reuses the one band buffer, else after it (its
         // loads are then waited for without these stores)
-        if constexpr (NCHW)
-            if (a.xpk && a.off_b1 == a.off_b0) nchw_write_packed(ti, c, cur);
+        if constexpr (NCHW && !SINGLE)
+            if (a.xpk && a.off_b1 == a.off_b0) nchw_write_packed(ti, c, cur, tid, NT);
 
         // The next stage's operands (in flight during the MFMAs) are waited for
         // and staged before this stage's epilogue issues its stores: the wait
@@ -1280,8 +1288,8 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                 }
             }
         }
-        if constexpr (NCHW)
-            if (a.xpk && a.off_b1 != a.off_b0) nchw_write_packed(ti, c, cur);
+        if constexpr (NCHW && !SINGLE)
+            if (a.xpk && a.off_b1 != a.off_b0) nchw_write_packed(ti, c, cur, tid, NT);
         if (c == c_end - 1) {
             if (a.splits > 1) {
                 // split-K: publish this split's partial sums; the last split of the
