@@ -662,16 +662,20 @@ def batch_table(dev, reps: int, batches=(16, 32, 64, 128, 256)) -> list[dict]:
     return rows
 
 
-def fused_step_time(L, x, xp_ref, wp, mult, y_ref, dev, reps: int) -> dict:
+def fused_step_time(L, x, xp_ref, wp, mult, y_ref, dev, reps: int, tile_name: str):
     """The benchmark step as one launch: qconv2d_packing, the pack fused into
-    the convolution, writing the packed input too.  The fastest tile of a
-    short sweep; its output and packed copy are checked against the
-    two-launch step's."""
+    the convolution, writing the packed input too.  Every tile with the fused
+    instance is timed (reported as a table) and checked against the two-launch
+    step's output and packed input; the step runs `tile_name` (the layer's
+    tuned tile) when it has the instance, so that the choice does not depend on
+    a short timing, else the fastest."""
     import torch
     from paper_2202_06819_amd import qconv
     e = L.epilogue
     d = L.desc()
     best = None
+    chosen = None
+    sweep_rows = []
     for t in qconv.tiles():
         if t["variant"] != 2 or qconv.tile_status(d, t["id"]) != 0:
             continue
@@ -688,12 +692,17 @@ def fused_step_time(L, x, xp_ref, wp, mult, y_ref, dev, reps: int) -> dict:
             raise RuntimeError(f"fused pack + conv on {t['name']} differs from the two-launch step")
         g, _ = captured(lambda st: [make(st)], 20)
         us = time_graph(g, 3) * 1000.0 / 60
+        sweep_rows.append({"tile": t["name"], "us": round(us, 3)})
         if best is None or us < best[0]:
             best = (us, t["name"], make)
-    g, _ = captured(lambda st: [best[2](st)], reps)
+        if t["name"] == tile_name:
+            chosen = (us, t["name"], make)
+    if chosen is None:
+        chosen = best
+    g, _ = captured(lambda st: [chosen[2](st)], reps)
     us = time_graph(g, 5) * 1000.0 / (5 * reps)
-    return {"us": round(us, 3), "tops": round(L.ops / (us * 1e-6) / 1e12, 2), "tile": best[1],
-            "entry": "qconv2d_packing", "packed_copy": True}
+    return {"us": round(us, 3), "tops": round(L.ops / (us * 1e-6) / 1e12, 2), "tile": chosen[1],
+            "entry": "qconv2d_packing", "packed_copy": True, "tiles": sweep_rows}, chosen[2]
 
 
 def cpu_baseline(L, seconds: float, threads: int | None = None) -> dict:
@@ -855,44 +864,99 @@ def main() -> int:
     big_p = torch.empty((n_cp,) + tuple(xp.shape), dtype=xp.dtype, device=dev)
     pack_cold_us = cold_time([qconv.PackCall(big_x[i], L.bits, L.x_signed, out=big_p[i]) for i in range(n_cp)])
     del big_x, big_p
-    fused = fused_step_time(L, x, xp, wp, mult, ref_out, dev, reps)
+    fused, fused_make = fused_step_time(L, x, xp, wp, mult, ref_out, dev, reps, tile_name)
     log(f"the step as one launch (pack fused into the conv, packed copy written): {fused['us']:.2f} us = "
         f"{fused['tops']:.1f} TOP/s, tile {fused['tile']}")
+    # the same timed region for the one-launch form of the step
+    g_one, one_calls = captured(lambda s: [fused_make(s)], G)
+    for _ in range(max(1, args.warmup // G)):
+        g_one.replay()
+    torch.cuda.synchronize()
+    one_calls[0].out.zero_()
+    one_calls[0].x_packed.zero_()
+    t_wall_one = time.perf_counter()
+    ms_total_one = time_graph(g_one, args.steps // G)
+    t_wall_one = time.perf_counter() - t_wall_one
+    if not (torch.equal(one_calls[0].out, ref_out) and torch.equal(one_calls[0].x_packed, xp)):
+        raise RuntimeError("the one-launch step's graph replay differs from the two-launch step's output")
+    ms_per_step_one = ms_total_one / args.steps
+    log(f"one-launch step: {ms_per_step_one * 1000:.2f} us ({L.ops / (ms_per_step_one * 1e-3) / 1e12:.1f} TOP/s) "
+        f"from {args.steps // G} replays of a {G}-step graph, wall {t_wall_one:.3f} s")
+    one_form = ms_per_step_one < ms_per_step   # the step's faster form is the one reported
+    forms = {"two_launches": {"ms_per_step": round(ms_per_step, 6), "tile": tile_name,
+                              "value": round(value, 3)},
+             "one_launch": {"ms_per_step": round(ms_per_step_one, 6), "tile": fused["tile"],
+                            "value": round(L.ops / (ms_per_step_one * 1e-3) / 1e12, 3)}}
     probe = mfma_probe(dev)
     log(f"pack kernel cold ({n_cp} copies): {pack_cold_us:.2f} us = {pack_bytes / (pack_cold_us * 1e-6) / 1e9:.0f} GB/s; "
         f"MFMA-only probe {probe['tops']:.0f} TOP/s at {probe['clock_ghz']:.2f} GHz")
 
     workload = (f"conv2d n{L.n} {L.h}x{L.w} {L.c}->{L.k} {L.r}x{L.s} stride {L.stride} pad {L.pad}, "
                 f"{L.bits}-bit, fused requant+repack")
+    workload_one = workload + ", pack fused in (int8 NCHW input, packed copy written)"
     traffic = measured_traffic(workload, tile_name)
     stats = profile_values("kernel_stats", workload, tile_name)
+    traffic_one = measured_traffic(workload_one, fused["tile"] + ":fused")
+    stats_one = profile_values("kernel_stats", workload_one, fused["tile"] + ":fused")
     conv()
     geo = qconv.last_launch()
     torch.cuda.synchronize()
     floor = launch_floor(dev, [(geo["grid"], geo["threads"], 0)])[0]
+    conv_roofline = {"bound": "mfma", "achieved": round(conv_tops, 3), "peak": INT8_PEAK_TOPS, "unit": "TOP/s",
+                     "frac": round(conv_tops / INT8_PEAK_TOPS, 5), "traffic": traffic,
+                     "kernel": "conv_wide" if tile_name.startswith("wide") else "conv_staged",
+                     "avg_us": round(conv_us, 3), "algorithmic_ops_per_launch": L.ops,
+                     "algorithmic_bytes_per_launch": conv_bytes, "kernel_digest": kernel_digest(tile_name),
+                     "frac_of_mfma_probe": round(conv_tops / probe["tops"], 5)}
+    if stats:
+        # the committed kernel-trace summary of this kernel (same sources and tile): its
+        # average over the dispatches that started back to back (< 1 us after the
+        # previous one ended, as in the timed graph), and over all of them (the
+        # tracer's own gaps between dispatches slow the kernel that follows)
+        pavg = float(stats["conv_avg_ns_back_to_back"]) / 1000.0
+        conv_roofline.update({"profile_avg_us": round(pavg, 3),
+                              "profile_frac": round(L.ops / (pavg * 1e-6) / 1e12 / INT8_PEAK_TOPS, 5),
+                              "profile_avg_us_all_dispatches": round(float(stats["conv_avg_ns"]) / 1000.0, 3),
+                              "profile": stats["file"]})
+    # the one-launch kernel reads the int8 input and writes its packed copy too
+    one_bytes = conv_bytes + L.n * L.c * L.h * L.w
+    one_tops = L.ops / (fused["us"] * 1e-6) / 1e12
+    one_roofline = {"bound": "mfma", "achieved": round(one_tops, 3), "peak": INT8_PEAK_TOPS, "unit": "TOP/s",
+                    "frac": round(one_tops / INT8_PEAK_TOPS, 5), "traffic": traffic_one,
+                    "kernel": "conv_wide (int8 NCHW input: the pack fused in)", "avg_us": fused["us"],
+                    "algorithmic_ops_per_launch": L.ops, "algorithmic_bytes_per_launch": one_bytes,
+                    "kernel_digest": kernel_digest(fused["tile"] + ":fused"),
+                    "frac_of_mfma_probe": round(one_tops / probe["tops"], 5),
+                    "hbm_frac": round(one_bytes / (fused["us"] * 1e-6) / 1e9 / HBM_PEAK_GBS, 5)}
+    if stats_one:
+        pavg = float(stats_one["conv_avg_ns_back_to_back"]) / 1000.0
+        one_roofline.update({"profile_avg_us": round(pavg, 3),
+                             "profile_frac": round(L.ops / (pavg * 1e-6) / 1e12 / INT8_PEAK_TOPS, 5),
+                             "profile_avg_us_all_dispatches": round(float(stats_one["conv_avg_ns"]) / 1000.0, 3),
+                             "profile": stats_one["file"]})
     result = {
         "metric": METRIC,
-        "value": round(value, 3),
+        "value": round(L.ops / (ms_per_step_one * 1e-3) / 1e12 if one_form else value, 3),
         "unit": "TOP/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 6),
+        "ms_per_step": round(ms_per_step_one if one_form else ms_per_step, 6),
         "eager_ms_per_step": round(eager_ms, 6),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "int4",
         "data": "synthetic",
-        "config": {"workload": workload, "step": "qconv_pack (int8 NCHW -> packed 4-bit NHWC) + qconv2d",
+        "config": {"workload": workload,
+                   "step": ("qconv2d_packing: int8 NCHW activations packed while the convolution stages them, "
+                            "packed copy written (one launch)") if one_form else
+                           "qconv_pack (int8 NCHW -> packed 4-bit NHWC) + qconv2d (two launches)",
                    "n": L.n, "h": L.h, "w": L.w, "c": L.c, "k": L.k, "r": L.r, "s": L.s, "stride": L.stride,
-                   "pad": L.pad, "bits": L.bits, "ops_per_step": L.ops, "tile": tile_name},
-        "roofline": {"bound": "mfma", "achieved": round(conv_tops, 3), "peak": INT8_PEAK_TOPS, "unit": "TOP/s",
-                     "frac": round(conv_tops / INT8_PEAK_TOPS, 5), "traffic": traffic,
-                     "kernel": "conv_wide" if tile_name.startswith("wide") else "conv_staged",
-                     "avg_us": round(conv_us, 3), "algorithmic_ops_per_launch": L.ops,
-                     "algorithmic_bytes_per_launch": conv_bytes, "kernel_digest": kernel_digest(tile_name),
-                     "frac_of_mfma_probe": round(conv_tops / probe["tops"], 5)},
+                   "pad": L.pad, "bits": L.bits, "ops_per_step": L.ops,
+                   "tile": fused["tile"] if one_form else tile_name, "step_forms": forms},
+        "roofline": one_roofline if one_form else conv_roofline,
+        "roofline_packed_input_conv": conv_roofline,
         "kernels": {"conv_us": round(conv_us, 3), "pack_us": round(pack_us, 3),
                     "pack_gbs": round(pack_gbs, 1), "pack_frac_hbm": round(pack_gbs / HBM_PEAK_GBS, 4),
                     "pack_algorithmic_bytes": pack_bytes, "pack_cold_us": round(pack_cold_us, 3),
@@ -902,16 +966,6 @@ def main() -> int:
         "launch_floor": {"grid": floor, "note": "empty kernel over the conv kernel's grid (qconv_probe_launch)"},
         "build": {"source_digest": hip_build.source_digest(), "library_digest": qconv.build_digest()},
     }
-    if stats:
-        # the committed kernel-trace summary of this kernel (same sources and tile): its
-        # average over the dispatches that started back to back (< 1 us after the
-        # previous one ended, as in the timed graph), and over all of them (the
-        # tracer's own gaps between dispatches slow the kernel that follows)
-        pavg = float(stats["conv_avg_ns_back_to_back"]) / 1000.0
-        result["roofline"].update({"profile_avg_us": round(pavg, 3),
-                                   "profile_frac": round(L.ops / (pavg * 1e-6) / 1e12 / INT8_PEAK_TOPS, 5),
-                                   "profile_avg_us_all_dispatches": round(float(stats["conv_avg_ns"]) / 1000.0, 3),
-                                   "profile": stats["file"]})
 
     tables = [] if args.tables == "none" else [int(v) for v in args.tables.split(",") if v]
     for cfg in tables:
