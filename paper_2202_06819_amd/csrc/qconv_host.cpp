@@ -618,6 +618,10 @@ void fill_args(ConvArgs &a, const qconv_desc *d, const qconv_layout_info &li, co
     a.mtiles = (int32_t)pl.mtiles;
     a.splits = (int32_t)pl.splits;
     a.cps = (int32_t)(pl.cps > 0 ? pl.cps : (d->c + te.info.chunk_c - 1) / te.info.chunk_c);
+    a.gpk = (int32_t)(pl.splits > 1 ? pl.mtiles : std::max<int64_t>(pl.grid / std::max<int64_t>(pl.ktiles, 1), 1));
+    a.div_splits = make_fastdiv((uint32_t)std::max<int64_t>(pl.splits, 1));
+    a.div_ktiles = make_fastdiv((uint32_t)std::max<int64_t>(pl.ktiles, 1));
+    a.div_gpk = make_fastdiv((uint32_t)a.gpk);
     a.div_pq = make_fastdiv((uint32_t)(li.p * li.q));
     a.div_q = make_fastdiv((uint32_t)li.q);
     a.div_vh = make_fastdiv((uint32_t)a.vh);

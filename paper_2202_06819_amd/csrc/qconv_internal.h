@@ -64,6 +64,8 @@ struct ConvArgs {
     int32_t mtiles;         // workgroup tiles along output pixels
     int32_t splits;         // split-K factor over channel chunks (1: none)
     int32_t cps;            // channel chunks per split
+    int32_t gpk;            // wide kernel: workgroups per channel tile (mtiles with a split, grid / ktiles without)
+    FastDiv div_splits, div_ktiles, div_gpk;   // by splits, ktiles and gpk
     int32_t xcd_order;      // 1, 2: renumber workgroups so consecutive tiles share an XCD (wide kernel);
                             // 2: consecutive tiles share a channel tile rather than pixels
     int32_t *ws_part;       // split-K partial sums (splits > 1)

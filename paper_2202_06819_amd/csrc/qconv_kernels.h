@@ -472,14 +472,15 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     // consecutive workgroups share pixels, so an XCD reads its share of the
     // input and every channel tile's filters) or pixel tile fastest
     // (xcd_order 2: an XCD takes one channel tile's filters and the pixels).
+    // (the divisions by launch constants use the host's multiply-shift divisors)
     const int lb = a.xcd_order ? xcd_block(blockIdx.x, gridDim.x) : (int)blockIdx.x;
-    const int sp = a.splits > 1 ? lb % a.splits : 0;
-    const int lt = a.splits > 1 ? lb / a.splits : lb;
-    const int per_kt = a.splits > 1 ? a.mtiles : (int)gridDim.x / a.ktiles;   // logical tiles per channel tile
-    const int kt = a.xcd_order == 2 ? lt / per_kt : lt % a.ktiles;
-    const int j0 = a.xcd_order == 2 ? lt - kt * per_kt : lt / a.ktiles;
-    const int gpk = a.splits > 1 ? a.mtiles : gridDim.x / a.ktiles;   // workgroups sharing this channel tile
-    const int my_tiles = (a.mtiles - j0 + gpk - 1) / gpk;              // tiles j0, j0 + gpk, ...
+    const int lt = (int)fdiv((uint32_t)lb, a.div_splits);   // lb / splits
+    const int sp = lb - lt * a.splits;
+    const int gpk = a.gpk;   // logical tiles per channel tile: workgroups sharing this channel tile
+    const int ltk = (int)fdiv((uint32_t)lt, a.div_ktiles);   // lt / ktiles
+    const int kt = a.xcd_order == 2 ? (int)fdiv((uint32_t)lt, a.div_gpk) : lt - ltk * a.ktiles;
+    const int j0 = a.xcd_order == 2 ? lt - kt * gpk : ltk;
+    const int my_tiles = (int)fdiv((uint32_t)(a.mtiles - j0 + gpk - 1), a.div_gpk);   // tiles j0, j0 + gpk, ...
     const int c_begin = sp * a.cps;                                     // chunks [c_begin, c_end)
     const int c_end = min(a.nchunks, c_begin + a.cps);
     const int nst = my_tiles * (c_end - c_begin);
