@@ -81,8 +81,8 @@ __global__ void __launch_bounds__(WP * WK * 64) conv_staged(ConvArgs a) {
     const int l16 = lane & 15;
     const int gq = lane >> 4;
 
-    const int kt = blockIdx.x % a.ktiles;
-    const int mt = blockIdx.x / a.ktiles;
+    const int mt = (int)fdiv(blockIdx.x, a.div_ktiles);   // blockIdx.x / ktiles
+    const int kt = (int)blockIdx.x - mt * a.ktiles;
     const int m0 = mt * TP;
     const int k0 = kt * TK;
     const int rs = a.r * a.s;

@@ -40,26 +40,28 @@ __device__ __forceinline__ uint32_t gather_byte(const uint32_t (&t)[4], int j) {
     return byte_of(t[0], j) | (byte_of(t[1], j) << 8) | (byte_of(t[2], j) << 16) | (byte_of(t[3], j) << 24);
 }
 
+// (ptiles, ctiles, nb: the divisors of the block and image decompositions)
 template <int BITS, bool SIGNED>
 __global__ void __launch_bounds__(PK_THREADS)
-    pack_nchw(const int8_t *__restrict__ src, uint8_t *__restrict__ dst, int c, int hw, int ptiles, int ctiles,
-              int nb) {
+    pack_nchw(const int8_t *__restrict__ src, uint8_t *__restrict__ dst, int c, int hw, FastDiv ptiles,
+              FastDiv ctiles, FastDiv nb) {
     constexpr int LO = SIGNED ? -(1 << (BITS - 1)) : 0;
     constexpr int HI = SIGNED ? (1 << (BITS - 1)) - 1 : (1 << BITS) - 1;
     __shared__ __attribute__((aligned(16))) uint8_t tile[PK_C * PK_PITCH];
     const int tid = threadIdx.x;
     int bid = pack_xcd_block(blockIdx.x, gridDim.x);
-    const int pt = bid % ptiles;
-    bid /= ptiles;
-    const int ct = bid % ctiles;
-    const int img = bid / ctiles;
+    const int rest = (int)fdiv((uint32_t)bid, ptiles);
+    const int pt = bid - rest * (int)ptiles.d;
+    const int img = (int)fdiv((uint32_t)rest, ctiles);
+    const int ct = rest - img * (int)ctiles.d;
     const int c0 = ct * PK_C;
     const int p0 = pt * PK_P;
     const int8_t *plane = src + (size_t)img * c * hw;
     // destination pixel of (img, pix): nb images interleaved per pixel
     // (nb = 1: plain N x H x W x C)
-    const size_t obase = (size_t)(img / nb) * hw * nb + img % nb;
-    auto out_pixel = [&](int px) { return obase + (size_t)px * nb; };
+    const int ig = (int)fdiv((uint32_t)img, nb);
+    const size_t obase = (size_t)ig * hw * nb.d + (img - ig * (int)nb.d);
+    auto out_pixel = [&](int px) { return obase + (size_t)px * nb.d; };
 
     // ---- phase 1: 64 channel rows x 64 pixels; a lane reads 32 consecutive
     // pixels of one row, saturates them and parks them in LDS
@@ -152,12 +154,14 @@ hipError_t launch_pack(const int8_t *src, void *dst, int32_t n, int32_t c, int32
     const long long blocks = (long long)n * ptiles * ctiles;
     uint8_t *d = static_cast<uint8_t *>(dst);
     const dim3 grid((unsigned)blocks), block(PK_THREADS);
+    const FastDiv dp = make_fastdiv((uint32_t)ptiles), dc = make_fastdiv((uint32_t)ctiles),
+                  dn = make_fastdiv((uint32_t)(nb > 0 ? nb : 1));
     if (bits == 4 && is_signed)
-        hipLaunchKernelGGL((pack_nchw<4, true>), grid, block, 0, stream, src, d, c, hw, ptiles, ctiles, nb);
+        hipLaunchKernelGGL((pack_nchw<4, true>), grid, block, 0, stream, src, d, c, hw, dp, dc, dn);
     else if (bits == 4)
-        hipLaunchKernelGGL((pack_nchw<4, false>), grid, block, 0, stream, src, d, c, hw, ptiles, ctiles, nb);
+        hipLaunchKernelGGL((pack_nchw<4, false>), grid, block, 0, stream, src, d, c, hw, dp, dc, dn);
     else
-        hipLaunchKernelGGL((pack_nchw<8, true>), grid, block, 0, stream, src, d, c, hw, ptiles, ctiles, nb);
+        hipLaunchKernelGGL((pack_nchw<8, true>), grid, block, 0, stream, src, d, c, hw, dp, dc, dn);
     return hipGetLastError();
 }
 
