@@ -103,6 +103,34 @@ def launch_floor(dev, grids, reps: int = 200) -> list[dict]:
     return rows
 
 
+def grid_meeting(dev, blocks_list, rounds: int = 64, reps: int = 50) -> list[dict]:
+    """Cost of one device-wide meeting inside a launch (qconv_probe_grid_meet:
+    agent-scope release, one atomic arrival, poll until the whole grid is
+    there, agent-scope acquire): the per-launch time of a grid meeting `rounds`
+    times minus that of the same grid meeting none, over `rounds`, both back to
+    back in replayed graphs (median of five replays).  Compare with the launch
+    floor: a persistent launch running several layers pays a meeting at each
+    layer boundary where launches pay a launch."""
+    import torch
+    from paper_2202_06819_amd import qconv
+    rows = []
+    for blocks in blocks_list:
+        for two in (False, True):
+            state = torch.zeros(qconv.ProbeGridMeetCall.STATE_ELEMS, dtype=torch.int32, device=dev)
+            per = {}
+            for r in (0, rounds):
+                g, calls = captured(lambda s: [qconv.ProbeGridMeetCall(blocks, r, state, two, s)], reps)
+                per[r] = sorted(time_graph(g, 1) * 1000.0 / reps for _ in range(5))[2]
+                del g
+            torch.cuda.synchronize()
+            ok = int(state[144].item()) == 0
+            rows.append({"blocks": blocks, "threads": 256, "counting": "two-level (per XCD)" if two else "flat",
+                         "rounds": rounds, "launch_us_no_meeting": round(per[0], 3), "launch_us": round(per[rounds], 3),
+                         "us_per_meeting": round((per[rounds] - per[0]) / rounds, 3) if ok else None,
+                         "all_arrived": ok})
+    return rows
+
+
 def copy_calibration(mib: int, reps: int) -> int:
     """A plain one-to-one copy kernel over `mib` MiB of int32 (read once,
     written once): the reference that scales FETCH_SIZE / WRITE_SIZE to bytes."""
@@ -902,6 +930,9 @@ def main() -> int:
     geo = qconv.last_launch()
     torch.cuda.synchronize()
     floor = launch_floor(dev, [(geo["grid"], geo["threads"], 0)])[0]
+    meeting = grid_meeting(dev, [geo["grid"], 256])
+    log(f"launch floor {floor['graph_us']} us; device-wide meeting inside a launch: "
+        + ", ".join(f"{m['blocks']} workgroups {m['counting']} {m['us_per_meeting']} us" for m in meeting))
     conv_roofline = {"bound": "mfma", "achieved": round(conv_tops, 3), "peak": INT8_PEAK_TOPS, "unit": "TOP/s",
                      "frac": round(conv_tops / INT8_PEAK_TOPS, 5), "traffic": traffic,
                      "kernel": "conv_wide" if tile_name.startswith("wide") else "conv_staged",
@@ -963,7 +994,10 @@ def main() -> int:
                     "pack_cold_gbs": round(pack_bytes / (pack_cold_us * 1e-6) / 1e9, 1), "pack_cold_copies": n_cp,
                     "fused_step": fused},
         "mfma_probe": probe,
-        "launch_floor": {"grid": floor, "note": "empty kernel over the conv kernel's grid (qconv_probe_launch)"},
+        "launch_floor": {"grid": floor, "note": "empty kernel over the conv kernel's grid (qconv_probe_launch)",
+                         "grid_meeting": meeting,
+                         "grid_meeting_note": "one device-wide meeting inside a launch (qconv_probe_grid_meet): what "
+                                              "a persistent multi-layer launch pays per layer boundary"},
         "build": {"source_digest": hip_build.source_digest(), "library_digest": qconv.build_digest()},
     }
 

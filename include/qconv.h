@@ -541,6 +541,35 @@ int qconv_last_launch(int64_t *grid, int64_t *threads, int64_t *lds_bytes);
 int qconv_probe_launch(int32_t blocks, int32_t threads, int32_t lds_bytes, void *stream);
 
 /*
+ * qconv_probe_grid_meet -- measurement aid, not part of the convolution: the
+ * cost of a device-wide meeting inside one launch, the alternative to a launch
+ * per layer when a chain of layers (Sec. 3.3: each layer's packed output is
+ * the next one's input) runs as one persistent grid.  Enqueues a one-wave
+ * kernel that zeroes the counters, then `blocks` workgroups of 256 threads
+ * that meet `rounds` times: each workgroup releases its writes at device
+ * scope, counts itself in, waits until the whole grid has arrived, then
+ * acquires.  The time per launch at rounds R minus that at rounds 0, over R,
+ * is the cost of one meeting.
+ *   blocks    1 .. the device's CU count (the grid must be resident at once)
+ *   rounds    0 .. 4096
+ *   two_level 0: every workgroup adds 1 to one counter; 1: each adds 1 to its
+ *             XCD group's counter (blockIdx mod 8) and the last of a group
+ *             adds 1 to the top counter
+ *   arrivals  device uint32[144], 4-byte aligned, owned by the caller: the top
+ *             counter at [0], group g's at [16 (g + 1)]; on return (after the
+ *             stream drains) [0] holds rounds x blocks (flat) or rounds x
+ *             min(blocks, 8) (two-level)
+ *   err       device int32, 4-byte aligned: left alone unless a workgroup gave
+ *             up waiting (2^17 polls, a fraction of a second), which writes 1;
+ *             the caller zeroes it first
+ * QCONV_EINVAL for out-of-range arguments or NULL/misaligned pointers;
+ * QCONV_EHIP if the device cannot be queried or a launch is rejected.
+ * Asynchronous on `stream`; calls that overlap on one set of counters race.
+ */
+int qconv_probe_grid_meet(int32_t blocks, int32_t rounds, int32_t two_level, uint32_t *arrivals, int32_t *err,
+                          void *stream);
+
+/*
  * Host-only self-check of the index arithmetic the kernels use (run-time
  * constant division); touches no device.  Returns 0 when it holds.
  */

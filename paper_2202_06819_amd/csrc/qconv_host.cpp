@@ -631,6 +631,7 @@ void fill_args(ConvArgs &a, const qconv_desc *d, const qconv_layout_info &li, co
     a.div_w = make_fastdiv((uint32_t)d->w);
     a.div_wq = make_fastdiv((uint32_t)((d->w + 3) / 4));
     a.div_brows = make_fastdiv((uint32_t)std::max<int64_t>(pl.rows, 1));
+    a.div_pad2 = make_fastdiv((uint32_t)std::max<int64_t>(2 * (int64_t)d->pad_w, 1));
     a.x_signed = d->x_signed;
     a.w_signed = d->w_signed;
     // widening: unsigned nibble -> low half of a byte; signed nibble -> high half (value * 16)
@@ -1256,6 +1257,28 @@ int qconv_probe_launch(int32_t blocks, int32_t threads, int32_t lds_bytes, void 
                     (long long)kLdsBytes);
     hipError_t e = launch_empty_probe(blocks, threads, lds_bytes, (hipStream_t)stream);
     if (e != hipSuccess) return fail(QCONV_EHIP, "empty probe launch: %s", hipGetErrorString(e));
+    return QCONV_OK;
+}
+
+int qconv_probe_grid_meet(int32_t blocks, int32_t rounds, int32_t two_level, uint32_t *arrivals, int32_t *err,
+                          void *stream) {
+    g_err[0] = 0;
+    if (blocks < 1 || rounds < 0 || rounds > 4096 || (two_level != 0 && two_level != 1))
+        return fail(QCONV_EINVAL, "blocks must be positive, rounds in [0, 4096] and two_level 0 or 1 (got %d, %d, %d)",
+                    blocks, rounds, two_level);
+    if (!arrivals || !err || ((uintptr_t)arrivals & 3u) != 0 || ((uintptr_t)err & 3u) != 0)
+        return fail(QCONV_EINVAL, "arrivals and err must be 4-byte aligned device pointers");
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return fail(QCONV_EHIP, "no device to query");
+    // one 256-thread workgroup per CU at most: the whole grid is resident at once
+    if (blocks > cus) return fail(QCONV_EINVAL, "blocks must be at most %d (the CUs), got %d", cus, blocks);
+    // a fraction of a second of polling (each poll is a device-scope load)
+    // before a workgroup gives up
+    constexpr int kSpinLimit = 1 << 17;
+    hipError_t e = launch_meet_probe(blocks, rounds, two_level, kSpinLimit, arrivals, err, (hipStream_t)stream);
+    if (e != hipSuccess) return fail(QCONV_EHIP, "meeting probe launch: %s", hipGetErrorString(e));
     return QCONV_OK;
 }
 

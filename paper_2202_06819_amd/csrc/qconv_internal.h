@@ -89,6 +89,7 @@ struct ConvArgs {
     uint8_t *xpk;           // packed copy of the input written on the way, or null
     FastDiv div_w, div_wq;  // by w and by its column quads
     FastDiv div_brows;      // by band_rows
+    FastDiv div_pad2;       // by 2 pw, a band row's padding columns (1 if none)
     // a 1x1 projection at the same stride fused into a 3x3 launch (PROJ
     // instances): its filters are tap r*s of the prepared image, its input the
     // centre tap's pixels, its output and epilogue its own
@@ -187,5 +188,11 @@ hipError_t launch_unroll(const int8_t *src, int8_t *dst, const UnrollArgs &a, hi
 int64_t mfma_probe_ops(int blocks, int iters);
 hipError_t launch_mfma_probe(int blocks, int iters, int32_t *sink, uint64_t *stamps, hipStream_t stream);
 hipError_t launch_empty_probe(int blocks, int threads, int lds_bytes, hipStream_t stream);
+// the meeting probe's counters: the top one, then one per XCD group, each on
+// its own 64-byte line (uint32 elements kMeetStride apart)
+constexpr int kMeetCounters = 9;
+constexpr int kMeetStride = 16;
+hipError_t launch_meet_probe(int blocks, int rounds, int two_level, int spin_limit, uint32_t *arrivals, int32_t *err,
+                             hipStream_t stream);
 
 }  // namespace qconv

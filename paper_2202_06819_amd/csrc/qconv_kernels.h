@@ -643,14 +643,19 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         uint8_t *bb = smem + (buf ? a.off_b1 : a.off_b0);
         int vlo, nrows, vend_own;
         band_rows_of(ti, vlo, nrows, vend_own);
-        constexpr int NG = CK / 16;   // granule planes of a chunk
-        const int npad = nrows * 2 * a.pw;
-        for (int e = tid; e < npad * NG; e += NT) {
-            const int g = e % NG, q = e / NG;
-            const int rowl = q / (2 * a.pw), side = q - rowl * 2 * a.pw;
-            const int col = side < a.pw ? side : a.w + side;
-            *reinterpret_cast<uint4 *>(bb + (size_t)g * a.pstride_b + (rowl * a.ncols + col) * 16) = uint4{0u, 0u, 0u, 0u};
-        }
+        // the band rows' padding columns are zeros (stored while the first
+        // round of loads is in flight)
+        auto pad_zero = [&] {
+            constexpr int NG = CK / 16;   // granule planes of a chunk
+            const int npad = nrows * 2 * a.pw;
+            for (int e = tid; e < npad * NG; e += NT) {
+                const int g = e % NG, q = e / NG;
+                const int rowl = (int)fdiv((uint32_t)q, a.div_pad2), side = q - rowl * 2 * a.pw;
+                const int col = side < a.pw ? side : a.w + side;
+                *reinterpret_cast<uint4 *>(bb + (size_t)g * a.pstride_b + (rowl * a.ncols + col) * 16) =
+                    uint4{0u, 0u, 0u, 0u};
+            }
+        };
         constexpr int NCO = CK / 8;   // channel octets of a chunk
         constexpr int IB = 2;         // items a thread has in flight at once
         // items run column quad fastest, then band row, then channel octet:
@@ -680,7 +685,10 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                 u32x2 L[8];
 #pragma unroll
                 for (int k = 0; k < 8; ++k) L[k] = __builtin_amdgcn_raw_buffer_load_b64(rsx, off0, k * hw, 0);
-                if (base == 0) issued();
+                if (base == 0) {
+                    issued();
+                    pad_zero();
+                }
                 if (!in_band) continue;
                 uint32_t any = 0u;
 #pragma unroll
@@ -754,7 +762,10 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
                     }
                 }
             }
-            if (base == 0) issued();
+            if (base == 0) {
+                issued();
+                pad_zero();
+            }
 #pragma unroll
             for (int u = 0; u < IB; ++u) {
                 if (pix0[u] < 0) continue;

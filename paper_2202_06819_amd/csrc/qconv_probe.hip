@@ -56,6 +56,63 @@ __global__ void __launch_bounds__(256) mfma_i8_probe(int iters, int32_t *sink, u
 // shape (and dynamic LDS size) and of waiting for it to drain.
 __global__ void __launch_bounds__(1024) empty_probe() {}
 
+// One wave: the arrival counters of the meeting probe start each launch at 0
+// (a kernel rather than a memset, so the pair can also sit in a graph).
+__global__ void __launch_bounds__(64) zero_counters(uint32_t *arrivals) {
+    if (threadIdx.x < kMeetCounters) __hip_atomic_store(arrivals + threadIdx.x * kMeetStride, 0u, __ATOMIC_RELAXED,
+                                                        __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// A grid that meets `rounds` times inside one launch.  At each meeting every
+// workgroup makes its earlier writes visible to the whole device (agent-scope
+// release), counts itself in, polls until the whole grid has arrived at this
+// meeting, and acquires (agent scope) before it goes on -- what a network run
+// as one persistent launch would pay at each layer boundary instead of a
+// kernel launch.  Counting in: flat, one atomic add per workgroup on one
+// counter; two-level, one add on its group's counter (workgroups are dealt to
+// the eight XCDs round robin, so a group is the workgroups of one XCD) and the
+// last of each group adds the group's arrival to the top counter.  The grid
+// must be co-resident (the host allows at most one workgroup per CU).  The
+// wait is bounded: after `spin_limit` polls a workgroup writes 1 to *err and
+// leaves, so every workgroup ends even if some never arrive.
+__global__ void __launch_bounds__(256) grid_meet_probe(int rounds, int two_level, int spin_limit, uint32_t *arrivals,
+                                                       int32_t *err) {
+    __shared__ int gave_up;
+    const uint32_t ngroups = gridDim.x < 8 ? gridDim.x : 8u;
+    const uint32_t grp = blockIdx.x & 7u;
+    const uint32_t gsize = (gridDim.x - grp + 7u) / 8u;   // workgroups of this group
+    for (int r = 0; r < rounds; ++r) {
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+            uint32_t target;
+            if (two_level) {
+                const uint32_t old = __hip_atomic_fetch_add(arrivals + (1u + grp) * kMeetStride, 1u, __ATOMIC_RELAXED,
+                                                            __HIP_MEMORY_SCOPE_AGENT);
+                if (old == (uint32_t)(r + 1) * gsize - 1u)   // the group's last arrival
+                    __hip_atomic_fetch_add(arrivals, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                target = (uint32_t)(r + 1) * ngroups;
+            } else {
+                __hip_atomic_fetch_add(arrivals, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                target = (uint32_t)(r + 1) * gridDim.x;
+            }
+            bool here = false;
+            for (int polls = 0; polls < spin_limit; ++polls) {
+                if (__hip_atomic_load(arrivals, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= target) {
+                    here = true;
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
+            }
+            if (!here) __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            gave_up = here ? 0 : 1;
+        }
+        __syncthreads();
+        if (gave_up) return;   // uniform over the workgroup
+    }
+}
+
 }  // namespace
 
 hipError_t launch_empty_probe(int blocks, int threads, int lds_bytes, hipStream_t stream) {
@@ -65,6 +122,16 @@ hipError_t launch_empty_probe(int blocks, int threads, int lds_bytes, hipStream_
         if (e != hipSuccess) return e;
     }
     hipLaunchKernelGGL(empty_probe, dim3((unsigned)blocks), dim3((unsigned)threads), (size_t)lds_bytes, stream);
+    return hipGetLastError();
+}
+
+hipError_t launch_meet_probe(int blocks, int rounds, int two_level, int spin_limit, uint32_t *arrivals, int32_t *err,
+                             hipStream_t stream) {
+    hipLaunchKernelGGL(zero_counters, dim3(1), dim3(64), 0, stream, arrivals);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(grid_meet_probe, dim3((unsigned)blocks), dim3(256), 0, stream, rounds, two_level, spin_limit,
+                       arrivals, err);
     return hipGetLastError();
 }
 

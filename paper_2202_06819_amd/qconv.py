@@ -122,6 +122,7 @@ def lib() -> ctypes.CDLL:
                                                _i32, _i32, _vp]
         L.qconv_noalloc_limits.argtypes = [P(_i64), P(_i64)]
         L.qconv_probe_launch.argtypes = [_i32, _i32, _i32, _vp]
+        L.qconv_probe_grid_meet.argtypes = [_i32, _i32, _i32, _vp, _vp, _vp]
         L.qconv_last_launch.argtypes = [P(_i64), P(_i64), P(_i64)]
         L.qconv_proj_default_tile.argtypes = [P(QConvDesc)]
         L.qconv_proj_tile_check.argtypes = [P(QConvDesc), _i32]
@@ -134,6 +135,7 @@ def lib() -> ctypes.CDLL:
                   "qconv_default_tile", "qconv_selftest", "qconv_prepared_filter_bytes", "qconv_prepare_filters",
                   "qconv2d_prepared", "qconv_workspace_bytes", "qconv_max_splits", "qconv_probe_mfma_i8", "qconv_schedule_check", "qconv2d_scheduled", "qconv_unroll", "qconv_pack_interleaved",
                   "qconv2d_packing", "qconv2d_prepared_noalloc", "qconv_noalloc_limits", "qconv_probe_launch",
+                  "qconv_probe_grid_meet",
                   "qconv_last_launch", "qconv_proj_default_tile", "qconv_proj_tile_check",
                   "qconv_prepared_proj_filter_bytes", "qconv_prepare_filters_proj", "qconv_proj_workspace_bytes",
                   "qconv2d_proj"):
@@ -270,6 +272,27 @@ def last_launch() -> dict:
     g, t, l = _i64(0), _i64(0), _i64(0)
     _check(lib().qconv_last_launch(ctypes.byref(g), ctypes.byref(t), ctypes.byref(l)), "qconv_last_launch")
     return {"grid": int(g.value), "threads": int(t.value), "lds_bytes": int(l.value)}
+
+
+class ProbeGridMeetCall:
+    """The device-wide meeting probe (a measurement aid): ``()`` enqueues one
+    launch of `blocks` workgroups that meet `rounds` times (flat, or counted in
+    per XCD group with `two_level`) on the int32 device tensor `state`:
+    elements 0..143 the arrival counters (element 0 the top one), element 144
+    the give-up flag, which the caller zeroes."""
+
+    STATE_ELEMS = 145
+
+    def __init__(self, blocks: int, rounds: int, state: torch.Tensor, two_level: bool = False, stream=None):
+        if state.dtype != torch.int32 or state.numel() < self.STATE_ELEMS or not state.is_cuda:
+            raise ValueError(f"state must be a device int32 tensor of at least {self.STATE_ELEMS} elements")
+        base = _dev_ptr(state, "state", 4 * self.STATE_ELEMS)
+        self._args = (int(blocks), int(rounds), int(bool(two_level)), _vp(base), _vp(base + 4 * 144),
+                      _vp(_stream(stream)))
+        self._fn = lib().qconv_probe_grid_meet
+
+    def __call__(self) -> None:
+        _check(self._fn(*self._args), "qconv_probe_grid_meet")
 
 
 class ProbeLaunchCall:

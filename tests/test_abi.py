@@ -307,6 +307,19 @@ def test_split_k_errors(q):
     assert L.qconv2d_prepared(*args, 0, None, 0, None) == -2
 
 
+def test_grid_meet_probe_argument_errors(q):
+    # rejected before any device is queried or anything is enqueued
+    L = q.lib()
+    a, e = 1 << 32, (1 << 32) + 4 * 144
+    assert L.qconv_probe_grid_meet(0, 1, 0, a, e, None) == -1
+    assert L.qconv_probe_grid_meet(1, -1, 0, a, e, None) == -1
+    assert L.qconv_probe_grid_meet(1, 4097, 0, a, e, None) == -1
+    assert L.qconv_probe_grid_meet(1, 1, 2, a, e, None) == -1
+    assert L.qconv_probe_grid_meet(1, 1, 0, None, e, None) == -1
+    assert L.qconv_probe_grid_meet(1, 1, 0, a + 2, e, None) == -1
+    assert L.qconv_probe_grid_meet(1, 1, 1, a, None, None) == -1
+
+
 def test_mfma_probe_argument_errors(q):
     L = q.lib()
     ops = ctypes.c_int64(0)
@@ -523,13 +536,13 @@ def test_projection_entry_points_validate_on_the_host(q):
     rq.mode, rq.mult, rq.shift, rq.relu, rq.clamp_lo, rq.clamp_hi = q.OUT_REQUANT, 1 << 20, 20, 1, 0, 15
     args = (ctypes.byref(desc), 1 << 20, 2 << 20, 1 << 30)
     assert q.lib().qconv2d_proj(*args, ctypes.byref(raw), 3 << 20, ctypes.byref(rq), 4 << 20, t, 1, None, 0,
-                                None) == q.EINVAL
+                                None) == -1
     rq2 = q.QConvEpilogue.from_buffer_copy(rq)
     rq2.residual = 5 << 20
     assert q.lib().qconv2d_proj(*args, ctypes.byref(rq), 3 << 20, ctypes.byref(rq2), 4 << 20, t, 1, None, 0,
                                 None) == q.EUNSUPPORTED
     assert q.lib().qconv2d_proj(*args, ctypes.byref(rq), 3 << 20, ctypes.byref(rq), None, t, 1, None, 0,
-                                None) == q.EINVAL
+                                None) == -1
     # split-K (over 64-channel chunks): the projection's partial sums double the
     # workspace; a missing one is refused
     d2 = D(n=2, h=9, w=9, c=256, stride_h=2, stride_w=2)
