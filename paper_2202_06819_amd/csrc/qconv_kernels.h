@@ -803,29 +803,37 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         int vlo, nrows, vend_own;
         band_rows_of(ti, vlo, nrows, vend_own);
         constexpr int NG = CK / 16;
-        const int units = (vend_own - vlo) * a.w * NG;
-        for (int e = first; e < units; e += step) {
-            const int g = e % NG, t = e / NG;
+        // a unit is one pixel's granules of this chunk: the lanes of a wave read
+        // consecutive pixels of one plane (256 contiguous bytes per 16 lanes, no
+        // bank conflicts) and write consecutive pixels' packed runs
+        const int units = (vend_own - vlo) * a.w;
+        const int ng = min(NG, (a.c - c * CK + 15) / 16);   // granules of this chunk inside c
+        for (int t = first; t < units; t += step) {
             const int rowl = (int)fdiv((uint32_t)t, a.div_w), ww = t - rowl * a.w;
             const int vrow = vlo + rowl;
             const int img = (int)fdiv((uint32_t)vrow, a.div_vh);
             const int hh = vrow - img * a.vh - a.ph;
-            const int ch0 = c * CK + g * 16;
-            if (img >= a.n || hh < 0 || hh >= a.h || ch0 >= a.c) continue;
-            const uint4 v = *reinterpret_cast<const uint4 *>(bb + (size_t)g * a.pstride_b + (rowl * a.ncols + a.pw + ww) * 16);
+            if (img >= a.n || hh < 0 || hh >= a.h) continue;
+            const uint8_t *src = bb + (rowl * a.ncols + a.pw + ww) * 16;
             const size_t pix = ((size_t)img * a.h + hh) * a.w + ww;
-            if constexpr (BITS == 4) {
-                uint2 w;
-                if constexpr (XS) {
-                    w.x = ((v.x >> 4) & 0x0F0F0F0Fu) | (v.y & 0xF0F0F0F0u);
-                    w.y = ((v.z >> 4) & 0x0F0F0F0Fu) | (v.w & 0xF0F0F0F0u);
+#pragma unroll
+            for (int g = 0; g < NG; ++g) {
+                if (g >= ng) break;
+                const uint4 v = *reinterpret_cast<const uint4 *>(src + (size_t)g * a.pstride_b);
+                const int ch0 = c * CK + g * 16;
+                if constexpr (BITS == 4) {
+                    uint2 w;
+                    if constexpr (XS) {
+                        w.x = ((v.x >> 4) & 0x0F0F0F0Fu) | (v.y & 0xF0F0F0F0u);
+                        w.y = ((v.z >> 4) & 0x0F0F0F0Fu) | (v.w & 0xF0F0F0F0u);
+                    } else {
+                        w.x = (v.x & 0x0F0F0F0Fu) | ((v.y & 0x0F0F0F0Fu) << 4);
+                        w.y = (v.z & 0x0F0F0F0Fu) | ((v.w & 0x0F0F0F0Fu) << 4);
+                    }
+                    *reinterpret_cast<uint2 *>(a.xpk + pix * (a.c / 2) + ch0 / 2) = w;
                 } else {
-                    w.x = (v.x & 0x0F0F0F0Fu) | ((v.y & 0x0F0F0F0Fu) << 4);
-                    w.y = (v.z & 0x0F0F0F0Fu) | ((v.w & 0x0F0F0F0Fu) << 4);
+                    *reinterpret_cast<uint4 *>(a.xpk + pix * a.c + ch0) = v;
                 }
-                *reinterpret_cast<uint2 *>(a.xpk + pix * (a.c / 2) + ch0 / 2) = w;
-            } else {
-                *reinterpret_cast<uint4 *>(a.xpk + pix * a.c + ch0) = v;
             }
         }
     };
