@@ -632,6 +632,7 @@ void fill_args(ConvArgs &a, const qconv_desc *d, const qconv_layout_info &li, co
     a.div_wq = make_fastdiv((uint32_t)((d->w + 3) / 4));
     a.div_brows = make_fastdiv((uint32_t)std::max<int64_t>(pl.rows, 1));
     a.div_pad2 = make_fastdiv((uint32_t)std::max<int64_t>(2 * (int64_t)d->pad_w, 1));
+    a.div_rb4 = make_fastdiv((uint32_t)((std::max<int64_t>(pl.rows, 1) + 3) & ~int64_t(3)));
     a.x_signed = d->x_signed;
     a.w_signed = d->w_signed;
     // widening: unsigned nibble -> low half of a byte; signed nibble -> high half (value * 16)

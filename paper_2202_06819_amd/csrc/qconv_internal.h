@@ -90,6 +90,7 @@ struct ConvArgs {
     FastDiv div_w, div_wq;  // by w and by its column quads
     FastDiv div_brows;      // by band_rows
     FastDiv div_pad2;       // by 2 pw, a band row's padding columns (1 if none)
+    FastDiv div_rb4;        // by band_rows rounded up to a multiple of 4
     // a 1x1 projection at the same stride fused into a 3x3 launch (PROJ
     // instances): its filters are tap r*s of the prepared image, its input the
     // centre tap's pixels, its output and epilogue its own

@@ -665,15 +665,23 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         const int nwq = (a.w + 3) >> 2;
         if ((a.w & 7) == 0) {
             // rows of whole pixel octets: an item is 8 channels x 8 pixels, one
-            // 8-byte load per channel (half the load instructions of quads)
+            // 8-byte load per channel (half the load instructions of quads).
+            // Items run channel-octet parity fastest, then band row (rows
+            // rounded up to 4), then column octet, then octet pair: an item's
+            // eight pixel stores lie 128 bytes apart per lane, so lanes that
+            // differ in row and octet parity are what spreads one store
+            // instruction over the LDS banks
             const int nwo = a.w >> 3;
-            const int items8 = NCO * a.band_rows * nwo;
+            const int rb4 = (a.band_rows + 3) & ~3;
+            const int items8 = NCO * rb4 * nwo;
             const int hw = a.h * a.w;
             for (int base = 0; base < items8; base += NT) {
                 const int it = base + tid;
-                const int t = (int)fdiv((uint32_t)(2 * it), a.div_wq);   // it / nwo (nwq = 2 nwo)
-                const int wo = it - t * nwo;
-                const int co = (int)fdiv((uint32_t)t, a.div_brows), rowl = t - co * a.band_rows;
+                const int q = it >> 1;
+                const int rest = (int)fdiv((uint32_t)q, a.div_rb4), rowl = q - rest * rb4;
+                const int cp = (int)fdiv((uint32_t)(2 * rest), a.div_wq);   // rest / nwo (nwq = 2 nwo)
+                const int wo = rest - cp * nwo;
+                const int co = 2 * cp + (it & 1);
                 const bool in_band = it < items8 && rowl < nrows;
                 const int vrow = vlo + rowl;
                 const int img = (int)fdiv((uint32_t)vrow, a.div_vh);
