@@ -1477,7 +1477,8 @@ __global__ void __launch_bounds__(256) build_filter_image(ConvArgs a, int TK, in
 template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC, bool EXT, int ABL = 0,
           bool MC = false, bool NCHW = false, bool PROJ = false, bool ONE = false>
 __global__ void __launch_bounds__(WP * WK * 64) __attribute__((amdgpu_waves_per_eu(2))) conv_wide(ConvArgs a) {
-    wide_body<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC, EXT, ABL, MC, NCHW, PROJ, ONE>(a);
+    const ConvArgs args = warm_kernarg_lines(a);
+    wide_body<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC, EXT, ABL, MC, NCHW, PROJ, ONE>(args);
 }
 
 // ============================================================== tile registry
