@@ -9,8 +9,10 @@
 
 #include <algorithm>
 #include <initializer_list>
+#include <map>
 #include <mutex>
 #include <string>
+#include <tuple>
 #include <set>
 #include <unordered_map>
 
@@ -421,6 +423,8 @@ int pick_proj_default(const qconv_desc *d, const qconv_layout_info &li) {
 struct DevAttrCache {
     std::mutex mu;
     std::set<std::pair<int, const void *>> done;   // (device, kernel) whose max LDS attribute is set
+    // resident workgroups per CU the runtime reports, per (device, kernel, threads, LDS bytes)
+    std::map<std::tuple<int, const void *, int, int64_t>, int> occupancy;
 };
 DevAttrCache g_attr;
 
@@ -646,6 +650,25 @@ void fill_args(ConvArgs &a, const qconv_desc *d, const qconv_layout_info &li, co
 }
 
 // Kernels that stage more than 64 KiB of LDS must opt in, once per device.
+// Workgroups of `kernel` (threads, dynamic LDS bytes) that fit one CU, as the
+// runtime reports them; 0 if it cannot say.  Asked once per device and shape:
+// eager launches of persistent plans would otherwise query it every call.
+int occupancy_per_cu(const void *kernel, int threads, int64_t lds) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    const auto key = std::make_tuple(dev, kernel, threads, lds);
+    {
+        std::lock_guard<std::mutex> g(g_attr.mu);
+        const auto it = g_attr.occupancy.find(key);
+        if (it != g_attr.occupancy.end()) return it->second;
+    }
+    int occ = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, threads, (size_t)lds) != hipSuccess) return 0;
+    std::lock_guard<std::mutex> g(g_attr.mu);
+    g_attr.occupancy[key] = occ;
+    return occ;
+}
+
 int ensure_lds_attribute(const void *kernel, int64_t lds) {
     if (lds <= 64 * 1024) return QCONV_OK;
     int dev = 0;
@@ -848,19 +871,14 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
         // persistent grid: size it by the occupancy the runtime reports for this kernel
         rc = ensure_lds_attribute(kernel, pl.lds);
         if (rc) return rc;
-        int occ = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, te.info.threads, (size_t)pl.lds) != hipSuccess)
-            occ = 0;
+        const int occ = occupancy_per_cu(kernel, te.info.threads, pl.lds);
         // a single-chunk layer whose second band buffer is what keeps another
         // workgroup off the CU runs with one band buffer instead (automatic
         // choice; band_buffers forces either)
         Plan one;
-        int occ1 = 0;
         const bool one_ok =
             plan_tile(d, li, te.info, &one, 0, 1, true, ablation, proj) == QCONV_OK && one.lds < pl.lds;
-        if (one_ok &&
-            hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ1, kernel, te.info.threads, (size_t)one.lds) != hipSuccess)
-            occ1 = 0;
+        const int occ1 = one_ok ? occupancy_per_cu(kernel, te.info.threads, one.lds) : 0;
         const bool use_one = band_buffers == 1 ? one_ok : (band_buffers == 2 ? false : one_ok && occ > 0 && occ1 > occ);
         const int pc = wg_per_cu > 0 ? wg_per_cu : (use_one ? occ1 : occ);
         if (pc > 0 || use_one) {
