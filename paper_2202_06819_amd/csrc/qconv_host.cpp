@@ -438,7 +438,7 @@ DevAttrCache g_attr;
 // hipGetSymbolAddress gives for the current device, never the name itself.
 constexpr int64_t kScratchBytes = 16ll << 20;
 constexpr int64_t kScratchCounterBytes = 64ll << 10;   // up to 16384 output tiles
-__device__ __align__(256) uint8_t scratch[kScratchBytes];
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
 
 __global__ void __launch_bounds__(256) clear_words(uint32_t *p, int32_t n) {
     const int32_t i = (int32_t)(blockIdx.x * 256 + threadIdx.x);
