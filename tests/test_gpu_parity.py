@@ -706,6 +706,8 @@ FUSED_CASES = [
     ("b4_persistent_n32", 32, 56, 56, 64, 64, 1, 4, (0, 15)),    # several tiles per workgroup
     ("b8_28x28_64", 4, 28, 28, 64, 64, 1, 8, (-128, 127)),
     ("b8_24x32_64_octets", 3, 24, 32, 64, 64, 1, 8, (-128, 127)),   # 8-pixel loads, 8-bit
+    ("b4_octets_c128_16x16", 2, 16, 16, 128, 64, 1, 4, (-20, 30)),   # 8-pixel loads over two chunks, saturation
+    ("b8_octets_stride2_32x32", 2, 32, 32, 64, 64, 2, 8, (-128, 127)),   # 8-pixel loads, strided band rows
 ]
 
 
