@@ -196,22 +196,24 @@ def time_graph(g, replays: int) -> float:
     return e0.elapsed_time(e1)
 
 
-def mfma_probe(dev, blocks: int = 2048, iters: int = 2048, launches: int = 5) -> dict:
-    """The int8 rate of a kernel that issues nothing but MFMAs (all CUs, eight
-    waves per SIMD, eight independent accumulator chains per wave), timed with
-    HIP events; the shader clock it ran at from its own counters."""
+def mfma_probe(dev, blocks: int = 2048, iters: int = 2048, launches: int = 5, shape: int = 0) -> dict:
+    """The int8 rate of a kernel that issues nothing but MFMAs (all CUs; with
+    the default 2048 workgroups eight waves per SIMD; eight independent chains
+    of v_mfma_i32_16x16x64_i8 per wave, or with shape 1 four of
+    v_mfma_i32_32x32x32_i8), timed with HIP events; the shader clock it ran
+    at from its own counters."""
     import statistics
     import torch
     from paper_2202_06819_amd import qconv
     sink = torch.empty(blocks * 256, dtype=torch.int32, device=dev)
     stamps = torch.zeros(blocks * 4, dtype=torch.int64, device=dev)
-    qconv.probe_mfma_i8(blocks, 16, sink, stamps)
+    qconv.probe_mfma_i8(blocks, 16, sink, stamps, shape=shape)
     torch.cuda.synchronize()
     best, ops = None, 0
     for _ in range(launches):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
-        ops = qconv.probe_mfma_i8(blocks, iters, sink, stamps)
+        ops = qconv.probe_mfma_i8(blocks, iters, sink, stamps, shape=shape)
         e1.record()
         torch.cuda.synchronize()
         ms = e0.elapsed_time(e1)
@@ -223,6 +225,21 @@ def mfma_probe(dev, blocks: int = 2048, iters: int = 2048, launches: int = 5) ->
     return {"tops": round(tops, 1), "clock_ghz": round(ghz, 3), "nominal_tops_at_clock": round(nominal, 1),
             "frac_of_nominal_peak": round(tops / INT8_PEAK_TOPS, 4), "ms": round(best, 4), "ops": ops,
             "blocks": blocks, "iters": iters}
+
+
+def mfma_shapes(dev) -> list[dict]:
+    """The MFMA probe at one and two waves per SIMD (256 and 512 workgroups of
+    four waves, the occupancy of the convolution kernels) for both int8
+    instruction shapes: what fraction of the matrix cores' rate at the
+    measured clock each sustains there."""
+    rows = []
+    for blocks in (256, 512):
+        for shape, name in ((0, "v_mfma_i32_16x16x64_i8"), (1, "v_mfma_i32_32x32x32_i8")):
+            r = mfma_probe(dev, blocks=blocks, iters=8192, launches=3, shape=shape)
+            rows.append({"instruction": name, "waves_per_simd": blocks // 256, "tops": r["tops"],
+                         "clock_ghz": r["clock_ghz"],
+                         "frac_of_rate_at_clock": round(r["tops"] / r["nominal_tops_at_clock"], 4)})
+    return rows
 
 
 def layer_bytes(L) -> int:
@@ -916,6 +933,9 @@ def main() -> int:
              "one_launch": {"ms_per_step": round(ms_per_step_one, 6), "tile": fused["tile"],
                             "value": round(L.ops / (ms_per_step_one * 1e-3) / 1e12, 3)}}
     probe = mfma_probe(dev)
+    shapes = mfma_shapes(dev)
+    log("MFMA rate at 1 and 2 waves per SIMD (fraction of the matrix cores' rate at the measured clock): "
+        + ", ".join(f"{r['instruction'][7:]} x{r['waves_per_simd']} {r['frac_of_rate_at_clock']:.3f}" for r in shapes))
     log(f"pack kernel cold ({n_cp} copies): {pack_cold_us:.2f} us = {pack_bytes / (pack_cold_us * 1e-6) / 1e9:.0f} GB/s; "
         f"MFMA-only probe {probe['tops']:.0f} TOP/s at {probe['clock_ghz']:.2f} GHz")
 
@@ -994,6 +1014,7 @@ def main() -> int:
                     "pack_cold_gbs": round(pack_bytes / (pack_cold_us * 1e-6) / 1e9, 1), "pack_cold_copies": n_cp,
                     "fused_step": fused},
         "mfma_probe": probe,
+        "mfma_shapes": shapes,
         "launch_floor": {"grid": floor, "note": "empty kernel over the conv kernel's grid (qconv_probe_launch)",
                          "grid_meeting": meeting,
                          "grid_meeting_note": "one device-wide meeting inside a launch (qconv_probe_grid_meet): what "

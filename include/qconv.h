@@ -521,6 +521,19 @@ int qconv_probe_mfma_i8(int32_t blocks, int32_t iters, int32_t *sink, uint64_t *
                         void *stream);
 
 /*
+ * qconv_probe_mfma_i8_shape -- the same probe with the MFMA shape chosen:
+ * shape 0 is qconv_probe_mfma_i8 (eight chains of v_mfma_i32_16x16x64_i8 per
+ * wave), shape 1 runs four chains of v_mfma_i32_32x32x32_i8 per wave -- the
+ * same int8 operations per round, so *ops has the same closed form.  With
+ * blocks = 256 or 512 (one or two waves per SIMD, the occupancy of the
+ * convolution kernels) the two rates show what the instruction shape itself
+ * costs.  Arguments, errors and asynchrony as for qconv_probe_mfma_i8;
+ * QCONV_EINVAL also for a shape other than 0 or 1.
+ */
+int qconv_probe_mfma_i8_shape(int32_t shape, int32_t blocks, int32_t iters, int32_t *sink, uint64_t *stamps,
+                              int64_t *ops, void *stream);
+
+/*
  * qconv_last_launch -- host only: the grid (workgroups), workgroup size
  * (threads) and dynamic LDS bytes of the calling thread's most recent
  * convolution launch (any qconv2d* entry point that returned QCONV_OK); any

@@ -1248,17 +1248,23 @@ int qconv_unroll(const int8_t *src, int8_t *dst, int32_t n, int32_t c, int32_t h
     return QCONV_OK;
 }
 
-int qconv_probe_mfma_i8(int32_t blocks, int32_t iters, int32_t *sink, uint64_t *stamps, int64_t *ops, void *stream) {
+int qconv_probe_mfma_i8_shape(int32_t shape, int32_t blocks, int32_t iters, int32_t *sink, uint64_t *stamps, int64_t *ops,
+                              void *stream) {
     g_err[0] = 0;
+    if (shape != 0 && shape != 1) return fail(QCONV_EINVAL, "shape must be 0 (16x16x64) or 1 (32x32x32), got %d", shape);
     if (blocks < 1 || blocks > (1 << 20) || iters < 1 || iters > (1 << 24))
         return fail(QCONV_EINVAL, "blocks must be in [1, 2^20] and iters in [1, 2^24] (got %d, %d)", blocks, iters);
     if (!sink || !stamps) return fail(QCONV_EINVAL, "sink and stamps must be device pointers");
     if (((uintptr_t)stamps & 7u) != 0 || ((uintptr_t)sink & 3u) != 0)
         return fail(QCONV_EINVAL, "stamps must be 8-byte and sink 4-byte aligned");
     if (ops) *ops = mfma_probe_ops(blocks, iters);
-    hipError_t e = launch_mfma_probe(blocks, iters, sink, stamps, (hipStream_t)stream);
+    hipError_t e = launch_mfma_probe(blocks, iters, shape == 1, sink, stamps, (hipStream_t)stream);
     if (e != hipSuccess) return fail(QCONV_EHIP, "probe launch: %s", hipGetErrorString(e));
     return QCONV_OK;
+}
+
+int qconv_probe_mfma_i8(int32_t blocks, int32_t iters, int32_t *sink, uint64_t *stamps, int64_t *ops, void *stream) {
+    return qconv_probe_mfma_i8_shape(0, blocks, iters, sink, stamps, ops, stream);
 }
 
 int qconv_last_launch(int64_t *grid, int64_t *threads, int64_t *lds_bytes) {

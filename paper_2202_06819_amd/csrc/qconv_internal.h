@@ -187,7 +187,7 @@ hipError_t launch_unroll(const int8_t *src, int8_t *dst, const UnrollArgs &a, hi
 
 // Defined in qconv_probe.hip (measurement aid).
 int64_t mfma_probe_ops(int blocks, int iters);
-hipError_t launch_mfma_probe(int blocks, int iters, int32_t *sink, uint64_t *stamps, hipStream_t stream);
+hipError_t launch_mfma_probe(int blocks, int iters, bool wide, int32_t *sink, uint64_t *stamps, hipStream_t stream);
 hipError_t launch_empty_probe(int blocks, int threads, int lds_bytes, hipStream_t stream);
 // the meeting probe's counters: the top one, then one per XCD group, each on
 // its own 64-byte line (uint32 elements kMeetStride apart)

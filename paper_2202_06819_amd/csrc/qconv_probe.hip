@@ -6,6 +6,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "qconv_internal.h"
 
 namespace qconv {
@@ -17,31 +19,45 @@ typedef int v4i_p __attribute__((ext_vector_type(4)));
 constexpr int kProbeChains = 8;   // independent accumulators per wave: covers the MFMA's dependent-issue latency
 
 // Four waves per workgroup (one per SIMD when a CU holds one workgroup); each
-// wave runs `iters` rounds of kProbeChains independent 16x16x64 int8 MFMAs.
+// wave runs `iters` rounds of independent int8 MFMAs: eight chains of
+// v_mfma_i32_16x16x64_i8 (WIDE = false) or four of v_mfma_i32_32x32x32_i8
+// (WIDE = true) -- the same int8 operations per round either way.
 // Wave 0 of every workgroup records the shader-clock counter and the 100 MHz
 // constant counter around its loop.
+typedef int v16i_p __attribute__((ext_vector_type(16)));
+template <bool WIDE>
 __global__ void __launch_bounds__(256) mfma_i8_probe(int iters, int32_t *sink, uint64_t *stamps) {
     const int tid = threadIdx.x;
     const v4i_p a = {tid, tid * 7 + 1, tid ^ 0x55, tid + 0x01010101};
     const v4i_p b = {tid * 3, tid + 5, ~tid, tid << 8};
-    v4i_p acc[kProbeChains];
+    constexpr int kChains = WIDE ? kProbeChains / 2 : kProbeChains;
+    typedef typename std::conditional<WIDE, v16i_p, v4i_p>::type Acc;
+    Acc acc[kChains];
 #pragma unroll
-    for (int j = 0; j < kProbeChains; ++j) acc[j] = a + j;
+    for (int j = 0; j < kChains; ++j)
+#pragma unroll
+        for (int e = 0; e < (WIDE ? 16 : 4); ++e) acc[j][e] = tid + j + e;
     const uint64_t c0 = clock64();
     const uint64_t r0 = wall_clock64();
     for (int i = 0; i < iters; ++i) {
         // tied operands keep each accumulator in place (no copies between rounds)
 #pragma unroll
-        for (int j = 0; j < kProbeChains; ++j)
-            asm volatile("v_mfma_i32_16x16x64_i8 %0, %1, %2, %0" : "+v"(acc[j]) : "v"(a), "v"(b));
+        for (int j = 0; j < kChains; ++j) {
+            if constexpr (WIDE)
+                asm volatile("v_mfma_i32_32x32x32_i8 %0, %1, %2, %0" : "+v"(acc[j]) : "v"(a), "v"(b));
+            else
+                asm volatile("v_mfma_i32_16x16x64_i8 %0, %1, %2, %0" : "+v"(acc[j]) : "v"(a), "v"(b));
+        }
     }
     // the accumulators are read by VALU below: let the last MFMAs retire first
-    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
     const uint64_t c1 = clock64();
     const uint64_t r1 = wall_clock64();
     int32_t s = 0;
 #pragma unroll
-    for (int j = 0; j < kProbeChains; ++j) s += acc[j][0] + acc[j][1] + acc[j][2] + acc[j][3];
+    for (int j = 0; j < kChains; ++j)
+#pragma unroll
+        for (int e = 0; e < (WIDE ? 16 : 4); ++e) s += acc[j][e];
     sink[(size_t)blockIdx.x * 256 + tid] = s;
     if (tid == 0) {
         uint64_t *st = stamps + (size_t)blockIdx.x * 4;
@@ -139,8 +155,11 @@ int64_t mfma_probe_ops(int blocks, int iters) {
     return (int64_t)blocks * 4 * iters * kProbeChains * (2 * 16 * 16 * 64);
 }
 
-hipError_t launch_mfma_probe(int blocks, int iters, int32_t *sink, uint64_t *stamps, hipStream_t stream) {
-    hipLaunchKernelGGL(mfma_i8_probe, dim3((unsigned)blocks), dim3(256), 0, stream, iters, sink, stamps);
+hipError_t launch_mfma_probe(int blocks, int iters, bool wide, int32_t *sink, uint64_t *stamps, hipStream_t stream) {
+    if (wide)
+        hipLaunchKernelGGL(mfma_i8_probe<true>, dim3((unsigned)blocks), dim3(256), 0, stream, iters, sink, stamps);
+    else
+        hipLaunchKernelGGL(mfma_i8_probe<false>, dim3((unsigned)blocks), dim3(256), 0, stream, iters, sink, stamps);
     return hipGetLastError();
 }
 

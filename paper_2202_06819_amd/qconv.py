@@ -111,6 +111,7 @@ def lib() -> ctypes.CDLL:
         L.qconv_workspace_bytes.argtypes = [P(QConvDesc), _i32, _i32, P(ctypes.c_size_t)]
         L.qconv_max_splits.argtypes = [P(QConvDesc), _i32]
         L.qconv_probe_mfma_i8.argtypes = [_i32, _i32, _vp, _vp, P(_i64), _vp]
+        L.qconv_probe_mfma_i8_shape.argtypes = [_i32, _i32, _i32, _vp, _vp, P(_i64), _vp]
         L.qconv_schedule_check.argtypes = [P(QConvDesc), P(QConvSchedule)]
         L.qconv_unroll.argtypes = [_vp, _vp] + [_i32] * 12 + [_vp]
         L.qconv_pack_interleaved.argtypes = [_vp, _vp] + [_i32] * 7 + [_vp]
@@ -135,7 +136,7 @@ def lib() -> ctypes.CDLL:
                   "qconv_default_tile", "qconv_selftest", "qconv_prepared_filter_bytes", "qconv_prepare_filters",
                   "qconv2d_prepared", "qconv_workspace_bytes", "qconv_max_splits", "qconv_probe_mfma_i8", "qconv_schedule_check", "qconv2d_scheduled", "qconv_unroll", "qconv_pack_interleaved",
                   "qconv2d_packing", "qconv2d_prepared_noalloc", "qconv_noalloc_limits", "qconv_probe_launch",
-                  "qconv_probe_grid_meet",
+                  "qconv_probe_grid_meet", "qconv_probe_mfma_i8_shape",
                   "qconv_last_launch", "qconv_proj_default_tile", "qconv_proj_tile_check",
                   "qconv_prepared_proj_filter_bytes", "qconv_prepare_filters_proj", "qconv_proj_workspace_bytes",
                   "qconv2d_proj"):
@@ -252,18 +253,20 @@ def prepare_filters(d: dict, w_packed: torch.Tensor, tile: int = -1, out: torch.
     return out
 
 
-def probe_mfma_i8(blocks: int, iters: int, sink: torch.Tensor, stamps: torch.Tensor, stream=None) -> int:
+def probe_mfma_i8(blocks: int, iters: int, sink: torch.Tensor, stamps: torch.Tensor, stream=None,
+                  shape: int = 0) -> int:
     """Launch the MFMA-only rate probe (a measurement aid); returns the int8
     operations the launch performs.  `sink` is int32 [blocks*256] and `stamps`
     int64 [blocks*4] on the device (shader-clock start/end, 100 MHz start/end
-    per workgroup)."""
+    per workgroup).  shape 0: v_mfma_i32_16x16x64_i8; 1: v_mfma_i32_32x32x32_i8."""
     if sink.dtype != torch.int32 or stamps.dtype != torch.int64:
         raise QConvError(EINVAL, "sink must be int32 and stamps int64")
     ops = _i64(0)
-    rc = lib().qconv_probe_mfma_i8(int(blocks), int(iters), _dev_ptr(sink, "sink", 4 * 256 * int(blocks)),
-                                   _dev_ptr(stamps, "stamps", 8 * 4 * int(blocks)), ctypes.byref(ops),
-                                   _vp(_stream(stream)))
-    _check(rc, "qconv_probe_mfma_i8")
+    rc = lib().qconv_probe_mfma_i8_shape(int(shape), int(blocks), int(iters),
+                                         _dev_ptr(sink, "sink", 4 * 256 * int(blocks)),
+                                         _dev_ptr(stamps, "stamps", 8 * 4 * int(blocks)), ctypes.byref(ops),
+                                         _vp(_stream(stream)))
+    _check(rc, "qconv_probe_mfma_i8_shape")
     return int(ops.value)
 
 

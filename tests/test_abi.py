@@ -320,6 +320,15 @@ def test_grid_meet_probe_argument_errors(q):
     assert L.qconv_probe_grid_meet(1, 1, 1, a, None, None) == -1
 
 
+def test_mfma_probe_shape_argument_errors(q):
+    L = q.lib()
+    ops = ctypes.c_int64(0)
+    assert L.qconv_probe_mfma_i8_shape(2, 1, 1, 1 << 32, 1 << 33, ctypes.byref(ops), None) == -1
+    assert L.qconv_probe_mfma_i8_shape(-1, 1, 1, 1 << 32, 1 << 33, ctypes.byref(ops), None) == -1
+    assert L.qconv_probe_mfma_i8_shape(1, 0, 1, 1 << 32, 1 << 33, ctypes.byref(ops), None) == -1
+    assert L.qconv_probe_mfma_i8_shape(1, 1, 1, None, 1 << 33, ctypes.byref(ops), None) == -1
+
+
 def test_mfma_probe_argument_errors(q):
     L = q.lib()
     ops = ctypes.c_int64(0)

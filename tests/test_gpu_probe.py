@@ -8,15 +8,16 @@ from _util import announce
 pytestmark = pytest.mark.gpu
 
 
-def test_mfma_probe_runs_and_stamps_a_clock():
+@pytest.mark.parametrize("shape", [0, 1], ids=["16x16x64", "32x32x32"])
+def test_mfma_probe_runs_and_stamps_a_clock(shape):
     import torch
     from paper_2202_06819_amd import qconv
     blocks, iters = 64, 256
-    announce(f"mfma probe blocks={blocks} iters={iters}")
+    announce(f"mfma probe shape={shape} blocks={blocks} iters={iters}")
     dev = torch.device("cuda:0")
     sink = torch.empty(blocks * 256, dtype=torch.int32, device=dev)
     stamps = torch.zeros(blocks * 4, dtype=torch.int64, device=dev)
-    ops = qconv.probe_mfma_i8(blocks, iters, sink, stamps)
+    ops = qconv.probe_mfma_i8(blocks, iters, sink, stamps, shape=shape)
     torch.cuda.synchronize()
     assert ops == blocks * 4 * iters * 8 * 2 * 16 * 16 * 64
     st = stamps.view(blocks, 4).cpu()
