@@ -929,8 +929,9 @@ int run_conv(const qconv_desc *d, const void *x, const void *w, bool prepared, s
     // every workgroup runs one stage (at most one tile, one chunk): the
     // instance's single-stage copy
     if (single && single->launch_one && pl.cps == 1 && (pl.splits > 1 || pl.grid >= pl.mtiles * pl.ktiles)) {
-        launch = single->launch_one;
-        kernel = single->kernel_one;
+        const bool oct = fused && single->launch_one_oct && d->w % 8 == 0;
+        launch = oct ? single->launch_one_oct : single->launch_one;
+        kernel = oct ? single->kernel_one_oct : single->kernel_one;
     }
     rc = ensure_lds_attribute(kernel, pl.lds);
     if (rc) return rc;

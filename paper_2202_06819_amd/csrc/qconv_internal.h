@@ -125,6 +125,8 @@ struct FixedInstance {
     const void *kernel_mc;
     ConvLauncher launch_one;   // variant for plans whose workgroups each run one stage, or null
     const void *kernel_one;
+    ConvLauncher launch_one_oct;   // the same for input rows of whole pixel octets (fused pack), or null
+    const void *kernel_one_oct;
 };
 
 // The kernels of one tile for one epilogue flavour.

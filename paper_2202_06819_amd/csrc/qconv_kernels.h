@@ -428,7 +428,7 @@ __device__ __forceinline__ int xcd_block(int b, int g) {
 // prefetch machinery (a workgroup with more stages still takes the general
 // loop, so the instance is correct for any plan).
 template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC, bool EXT, int ABL = 0,
-          bool MC = false, bool NCHW = false, bool PROJ = false, bool ONE = false>
+          bool MC = false, bool NCHW = false, bool PROJ = false, bool ONE = false, bool OCT = false>
 __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     constexpr bool FIXED = RC > 0 && SC > 0;
     constexpr bool LOWERED = (ABL & 1) != 0;
@@ -440,6 +440,7 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
     static_assert(ABL == 0 || (FIXED && !EXT), "ablation instances are fixed-size, without bias or residual");
     static_assert(!PROJ || (RC == 3 && SC == 3 && ABL == 0 && !MC && !NCHW), "the projection rides on a plain 3x3");
     static_assert(!ONE || (FIXED && !MC), "single-stage copies are made of the fixed-size instances");
+    static_assert(!OCT || (NCHW && ONE), "the octet-rows copy is a single-stage fused-pack instance");
     constexpr int NW = WP * WK;
     constexpr int NT = NW * 64;
     constexpr int TP = WP * FP * 16;
@@ -663,7 +664,9 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
         // load instruction read one contiguous run (rows up to band_rows, the
         // most any tile's band has; this tile's extra ones are skipped)
         const int nwq = (a.w + 3) >> 2;
-        if ((a.w & 7) == 0) {
+        // (OCT instances run only for rows of whole pixel octets, and carry
+        // no code for other widths: the smaller kernel launches faster)
+        if (OCT || (a.w & 7) == 0) {
             // rows of whole pixel octets: an item is 8 channels x 8 pixels, one
             // 8-byte load per channel (half the load instructions of quads).
             // Items run channel-octet parity fastest, then band row (rows
@@ -726,6 +729,7 @@ __device__ __forceinline__ void wide_body(const ConvArgs &a) {
             }
             return;
         }
+        if constexpr (OCT) return;
         const int items = NCO * a.band_rows * nwq;
         const bool dwords = (a.w & 3) == 0;
         for (int base = 0; base < items; base += NT * IB) {
@@ -1475,10 +1479,10 @@ __global__ void __launch_bounds__(256) build_filter_image(ConvArgs a, int TK, in
 // One operand signedness per kernel (the widening is compiled for it); 8-bit
 // operands are always signed.
 template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC, bool EXT, int ABL = 0,
-          bool MC = false, bool NCHW = false, bool PROJ = false, bool ONE = false>
+          bool MC = false, bool NCHW = false, bool PROJ = false, bool ONE = false, bool OCT = false>
 __global__ void __launch_bounds__(WP * WK * 64) __attribute__((amdgpu_waves_per_eu(2))) conv_wide(ConvArgs a) {
     const ConvArgs args = warm_kernarg_lines(a);
-    wide_body<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC, EXT, ABL, MC, NCHW, PROJ, ONE>(args);
+    wide_body<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC, EXT, ABL, MC, NCHW, PROJ, ONE, OCT>(args);
 }
 
 // ============================================================== tile registry
@@ -1490,9 +1494,9 @@ static hipError_t launch_staged(const ConvArgs &a, dim3 grid, size_t lds, hipStr
 }
 
 template <int BITS, int WP, int WK, int FP, int FK, int CK, bool XS, bool WS, int RC, int SC, bool EXT, int ABL = 0,
-          bool MC = false, bool NCHW = false, bool PROJ = false, bool ONE = false>
+          bool MC = false, bool NCHW = false, bool PROJ = false, bool ONE = false, bool OCT = false>
 static hipError_t launch_wide(const ConvArgs &a, dim3 grid, size_t lds, hipStream_t stream) {
-    hipLaunchKernelGGL((conv_wide<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC, EXT, ABL, MC, NCHW, PROJ, ONE>), grid,
+    hipLaunchKernelGGL((conv_wide<BITS, WP, WK, FP, FK, CK, XS, WS, RC, SC, EXT, ABL, MC, NCHW, PROJ, ONE, OCT>), grid,
                        dim3(WP * WK * 64), lds, stream, a);
     return hipGetLastError();
 }
@@ -1585,7 +1589,10 @@ static hipError_t launch_prep(const ConvArgs &a, uint8_t *img, int64_t elems, co
      reinterpret_cast<const void *>(&conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, false, 0, false, true>), \
      nullptr, nullptr, &launch_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, false, 0, false, true, false, true>, \
      reinterpret_cast<const void *>(                                                                              \
-         &conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, false, 0, false, true, false, true>)}
+         &conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, false, 0, false, true, false, true>),             \
+     &launch_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, false, 0, false, true, false, true, true>,          \
+     reinterpret_cast<const void *>(                                                                              \
+         &conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, false, 0, false, true, false, true, true>)}
 #define QCONV_PROJ_INST(B, WP, WK, FP, FK, CK, EXT)                                                               \
     {3, 3, &launch_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, EXT, 0, false, false, true>,                \
      reinterpret_cast<const void *>(&conv_wide<B, WP, WK, FP, FK, CK, (B == 8), true, 3, 3, EXT, 0, false, false, true>), \
