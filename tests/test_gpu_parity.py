@@ -237,6 +237,85 @@ def test_epilogue_spread_and_ties(bits):
     assert_same(got["y"], ref["y_packed"], "ties")
 
 
+# ----------------------------------------------------------------- operands at the accumulator bound
+
+# The requantiser's shift for these cases: with multipliers near 2^14.5 an
+# output is about acc / 2^9.5, so the two-ends 4-bit outputs spread over the
+# clamp range while the constant ones and most 8-bit ones saturate.
+SHIFT_EXTREME = 24
+
+EXTREME_CASES = [
+    # name, n, h, w, c, k, r, stride, pad, bits, x_signed, (x extremes), (w extremes)
+    ("u4_15_by_m8_c256_3x3_ragged", 3, 13, 11, 256, 72, 3, 1, 1, 4, False, (15, 0), (-8, 7)),
+    ("s4_m8_by_m8_c512_3x3", 2, 9, 9, 512, 64, 3, 1, 1, 4, True, (-8, 7), (-8, 7)),
+    ("s8_m128_by_m128_c512_3x3", 2, 9, 9, 512, 64, 3, 1, 1, 8, True, (-128, 127), (-128, 127)),
+    ("s8_m128_by_127_c2048_1x1", 2, 7, 7, 2048, 64, 1, 1, 0, 8, True, (-128, 127), (127, -128)),
+    ("s8_127_by_127_c256_5x5_s2", 2, 11, 11, 256, 32, 5, 2, 2, 8, True, (127, -128), (127, -128)),
+]
+
+
+def _valid_tap_counts(h, w, r, s, stride, pad):
+    """Per output pixel, the number of filter taps that land inside the image."""
+    p = (h + 2 * pad - r) // stride + 1
+    q = (w + 2 * pad - s) // stride + 1
+    rows = np.array([sum(0 <= i * stride - pad + a < h for a in range(r)) for i in range(p)], dtype=np.int64)
+    cols = np.array([sum(0 <= j * stride - pad + b < w for b in range(s)) for j in range(q)], dtype=np.int64)
+    return rows[:, None] * cols[None, :]
+
+
+@pytest.mark.parametrize("case", EXTREME_CASES, ids=[c[0] for c in EXTREME_CASES])
+def test_extreme_operands_every_tile(case):
+    """Sec. 3.2.1: the int32 accumulator must hold C*R*S products of the
+    largest magnitudes.  Constant operands at one extreme give the closed form
+    x*w*C*(valid taps) (checked on the oracle first), then operands drawn from
+    the two ends of their ranges exercise the signs at the same magnitude; every
+    tile that runs the shape (and the wide ones at their largest split) must reproduce
+    the oracle, raw and requantised (the requantiser's product acc*mult exceeds
+    32 bits here)."""
+    torch, q = _torch(), _qconv()
+    name, n, h, w, c, k, r, stride, pad, bits, xs, xe, we = case
+    xr = (min(xe), max(xe)) if bits == 8 or xs else (0, 15)
+    wr = (min(we), max(we))
+    L = qi.Layer(name, n, h, w, c, k, r, r, stride, pad, bits, xs, True, xr, wr)
+    assert q.layout(L.desc())["max_abs_acc"] >= abs(xe[0] * we[0]) * c * r * r
+    g = np.random.default_rng([1234, c, r, bits])
+    mult = g.integers(2 ** 14, 2 ** 15, size=k).astype(np.int32)
+    lo, hi = (-128, 127) if bits == 8 else (-8, 7)
+    const = {"x": np.full((n, c, h, w), xe[0], dtype=np.int8), "w": np.full((k, c, r, r), we[0], dtype=np.int8),
+             "mult": mult}
+    ends = {"x": np.where(g.random((n, c, h, w)) < 0.5, xe[0], xe[1]).astype(np.int8),
+            "w": np.where(g.random((k, c, r, r)) < 0.5, we[0], we[1]).astype(np.int8), "mult": mult}
+    taps = _valid_tap_counts(h, w, r, r, stride, pad)
+    want = (int(xe[0]) * int(we[0]) * c) * taps
+    dev = torch.device("cuda:0")
+    for label, t in (("constant", const), ("two ends", ends)):
+        ref = ref_layer(L, t, requant=True, shift=SHIFT_EXTREME, relu=False, lo=lo, hi=hi)
+        if label == "constant":
+            assert np.array_equal(ref["acc"], np.broadcast_to(want[None, :, :, None], ref["acc"].shape))
+        xp = q.pack(torch.from_numpy(t["x"]).to(dev), bits, xs)
+        wp = q.pack(torch.from_numpy(t["w"]).to(dev), bits, True)
+        m_dev = torch.from_numpy(mult).to(dev)
+        for tid in _valid_tiles(L):
+            announce(f"extreme {name} {label} tile {tid} raw")
+            y = q.conv2d(L.desc(), xp, wp, tile=tid)
+            torch.cuda.synchronize()
+            assert_same(y.cpu().numpy(), ref["acc"], f"{name} {label} tile {tid} raw")
+            announce(f"extreme {name} {label} tile {tid} requant")
+            y = q.conv2d(L.desc(), xp, wp, tile=tid, requant=True, mult=m_dev, shift=SHIFT_EXTREME, relu=False,
+                         clamp=(lo, hi))
+            torch.cuda.synchronize()
+            assert_same(y.cpu().numpy(), ref["y_packed"], f"{name} {label} tile {tid} requant")
+            if q.tiles()[tid]["variant"] != 2 or q.max_splits(L.desc(), tid) < 2:
+                continue
+            splits = q.max_splits(L.desc(), tid)
+            wprep = q.prepare_filters(L.desc(), wp, tid)
+            ws = q.make_workspace(L.desc(), tid, splits, dev)
+            announce(f"extreme {name} {label} tile {tid} splits {splits} raw")
+            y = q.conv2d(L.desc(), xp, wprep, tile=tid, prepared=True, splits=splits, workspace=ws)
+            torch.cuda.synchronize()
+            assert_same(y.cpu().numpy(), ref["acc"], f"{name} {label} tile {tid} splits {splits} raw")
+
+
 # ----------------------------------------------------------------- buffers, determinism, chaining
 
 def test_every_output_written_and_nothing_past_the_end():
