@@ -1,0 +1,124 @@
+"""GPU parity over many random shapes: every tile that runs a shape, from packed
+and from prepared filters, with a random split-K factor on the wide tiles and,
+for 3x3 shapes, the pack fused into the convolution.  Shapes mix ragged pixel
+counts and channel counts, strides 1-3, paddings beyond the filter's half
+width, filters from 1x1 to 7x7 (non-square ones too), signed and unsigned
+operands and both output signednesses; half of them are large enough that
+workgroups walk several output tiles and bands take several staging rounds.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import qconv_inputs as qi
+from _util import announce, assert_same, gpu_layer, oracle_threads, ref_layer, stress_shift
+
+pytestmark = pytest.mark.gpu
+
+BLOCK = 25
+BLOCKS = [(b * BLOCK, False) for b in range(4)] + [(1000 + b * BLOCK, True) for b in range(4)]
+
+
+def _layer(seed: int, big: bool) -> qi.Layer:
+    g = np.random.default_rng([4242, seed])
+    bits = 8 if seed % 3 == 2 else 4
+    r = int(g.choice([1, 1, 3, 3, 3, 5, 7, 2]))
+    s = int(g.choice([r, r, r, 1, 3]))
+    stride = int(g.choice([1, 1, 1, 2, 2, 3]))
+    pad = int(g.integers(0, max(r, s) // 2 + 2))
+    h = int(g.integers(max(1, r - 2 * pad), 61 if big else 40))
+    w = int(g.integers(max(1, s - 2 * pad), 61 if big else 40))
+    n = int(g.integers(1, 25 if big else 6))
+    if bits == 4:
+        c, k = 8 * int(g.integers(1, 48)), 8 * int(g.integers(1, 40))
+        xs, ws = bool(g.random() < 0.2), bool(g.random() < 0.85)
+        signed_out = bool(g.random() < 0.4)
+        epi = qi.Epilogue(relu=bool(g.random() < 0.5), lo=-8 if signed_out else 0, hi=7 if signed_out else 15)
+        return qi.Layer(f"rand{seed}", n, h, w, c, k, r, s, stride, pad, 4, xs, ws, qi.S4 if xs else qi.U4,
+                        qi.S4 if ws else qi.U4, epi)
+    c, k = 4 * int(g.integers(1, 96)), 4 * int(g.integers(1, 80))
+    epi = qi.Epilogue(relu=bool(g.random() < 0.5), lo=-128, hi=127)
+    return qi.Layer(f"rand{seed}", n, h, w, c, k, r, s, stride, pad, 8, True, True, qi.S8, qi.S8, epi)
+
+
+def _fused(q, torch, L, t, sh, g, dev):
+    """The pack fused in: int8 NCHW input over the whole int8 range (the oracle
+    packs it with saturation); the packed copy too where the bands cover every
+    input row (the library refuses the copy otherwise)."""
+    d, e = L.desc(), L.epilogue
+    tiles = [tt for tt in q.tiles() if tt["variant"] == 2 and q.tile_status(d, tt["id"]) == 0]
+    if not tiles:
+        return
+    x8 = g.integers(-128, 128, size=(L.n, L.c, L.h, L.w)).astype(np.int8)
+    ref = oracle.qconv_layer(x8, t["w"], bits=L.bits, x_signed=L.x_signed, w_signed=L.w_signed,
+                             stride=(L.stride, L.stride), pad=(L.pad, L.pad), mult=t["mult"], shift=sh, relu=e.relu,
+                             lo=e.lo, hi=e.hi, threads=oracle_threads())
+    x_dev = torch.from_numpy(x8).to(dev)
+    wp = q.pack(torch.from_numpy(t["w"]).to(dev), L.bits, L.w_signed)
+    mult = torch.from_numpy(t["mult"]).to(dev)
+    for tt in tiles:
+        wprep = q.prepare_filters(d, wp, tt["id"])
+        announce(f"{L.name} fused tile {tt['name']}")
+        call = q.PackingConv2dCall(d, x_dev, wprep, tile=tt["id"], mult=mult, shift=sh, relu=e.relu,
+                                   clamp=(e.lo, e.hi), x_packed=True)
+        try:
+            y = call()
+            copy = True
+        except q.QConvError as ex:
+            assert "no packed copy" in str(ex), str(ex)
+            y = q.PackingConv2dCall(d, x_dev, wprep, tile=tt["id"], mult=mult, shift=sh, relu=e.relu,
+                                    clamp=(e.lo, e.hi))()
+            copy = False
+        torch.cuda.synchronize()
+        assert_same(y.cpu().numpy(), ref["y_packed"], f"{L.name} fused {tt['name']}")
+        if copy:
+            assert_same(call.x_packed.cpu().numpy(), ref["x_packed"], f"{L.name} fused {tt['name']} packed copy")
+
+
+@pytest.mark.parametrize("block", BLOCKS, ids=lambda b: f"{'large' if b[1] else 'small'}_{b[0]}")
+def test_random_shapes_every_tile(block):
+    import torch
+    from paper_2202_06819_amd import qconv as q
+
+    first, big = block
+    dev = torch.device("cuda:0")
+    tiles_all = q.tiles()
+    ran = 0
+    for seed in range(first, first + BLOCK):
+        L = _layer(seed, big)
+        if L.h + 2 * L.pad < L.r or L.w + 2 * L.pad < L.s:
+            continue
+        tiles = [tt["id"] for tt in tiles_all if q.tile_status(L.desc(), tt["id"]) == 0]
+        assert tiles, f"no tile runs {L.desc()}"
+        t = qi.layer_tensors(4242, seed, L)
+        sh = stress_shift(L, L.x_range, L.w_range)
+        ref = ref_layer(L, t, requant=True, shift=sh)
+        g = np.random.default_rng([77, seed])
+        e = L.epilogue
+        for tid in tiles:
+            announce(f"{L.name} {L.desc()} tile {tid}")
+            assert_same(gpu_layer(L, t, requant=False, tile=tid)["y"], ref["acc"], f"{L.name} tile {tid} raw")
+            assert_same(gpu_layer(L, t, requant=True, tile=tid, shift=sh)["y"], ref["y_packed"],
+                        f"{L.name} tile {tid} requant")
+            ran += 1
+            if tiles_all[tid]["variant"] != 2:
+                continue
+            got = gpu_layer(L, t, requant=True, tile=tid, shift=sh, prepared=True)
+            assert_same(got["y"], ref["y_packed"], f"{L.name} tile {tid} prepared")
+            most = q.max_splits(L.desc(), tid)
+            if most < 2:
+                continue
+            splits = int(g.integers(2, most + 1))
+            wp = q.pack(torch.from_numpy(t["w"]).to(dev), L.bits, L.w_signed)
+            wprep = q.prepare_filters(L.desc(), wp, tid)
+            xp = q.pack(torch.from_numpy(t["x"]).to(dev), L.bits, L.x_signed)
+            ws = q.make_workspace(L.desc(), tid, splits, dev)
+            for rep in range(2):
+                announce(f"{L.name} tile {tid} splits {splits} rep {rep}")
+                y = q.conv2d(L.desc(), xp, wprep, tile=tid, prepared=True, splits=splits, workspace=ws, requant=True,
+                             mult=torch.from_numpy(t["mult"]).to(dev), shift=sh, relu=e.relu, clamp=(e.lo, e.hi))
+                torch.cuda.synchronize()
+                assert_same(y.cpu().numpy(), ref["y_packed"], f"{L.name} tile {tid} splits {splits} rep {rep}")
+        if L.r == 3 and L.s == 3:
+            _fused(q, torch, L, t, sh, g, dev)
+    assert ran > 0
