@@ -116,6 +116,33 @@ def test_proj_every_tile_small(lid):
         _check_layer(L, t, tile, [(s3, s1)], "small", splits=sorted({1, 2, chunks} & set(range(1, chunks + 1))))
 
 
+@pytest.mark.parametrize("first", [0, 20, 40])
+def test_proj_random_shapes(first):
+    """Random shapes (batch 1-12, 2-40 pixels a side, stride 1 or 2, 32-320
+    input and 8-320 output channels, 4-bit and 8-bit) on every tile with a
+    projection instance, without a split and with a random one."""
+    from paper_2202_06819_amd import qconv
+    ran = 0
+    for seed in range(first, first + 20):
+        g = np.random.default_rng([5151, seed])
+        bits = 8 if seed % 3 == 2 else 4
+        stride = int(g.choice([1, 2, 2]))
+        n, h, w = int(g.integers(1, 13)), int(g.integers(2, 41)), int(g.integers(2, 41))
+        c, k = 32 * int(g.integers(1, 11)), 8 * int(g.integers(1, 41))
+        L = _layer(f"pr{seed}", n, h, w, c, k, stride, bits)
+        tiles = [tt["id"] for tt in qconv.tiles() if qconv.proj_tile_status(L.desc(), tt["id"]) == 0]
+        assert tiles, f"no projection tile fits {L.desc()}"
+        t = _tensors(5151, seed, L)
+        s3 = stress_shift(L, L.x_range, L.w_range)
+        s1 = stress_shift(qi.Layer("p", L.n, L.h, L.w, L.c, L.k, 1, 1, bits=L.bits), L.x_range, L.w_range)
+        for tile in tiles:
+            chunks = qconv.max_splits(L.desc(), tile)
+            splits = sorted({1} | ({int(g.integers(2, chunks + 1))} if chunks >= 2 else set()))
+            _check_layer(L, t, tile, [(s3, s1)], "random", splits=splits)
+            ran += 1
+    assert ran > 0
+
+
 def _stage_entries(cfg):
     """(3x3 stride-2 layer, its 1x1 projection, their workload layer ids) of a ResNet-18 stack."""
     layers = qi.WORKLOADS[cfg]()
