@@ -5,6 +5,8 @@ counts and channel counts, strides 1-3, paddings beyond the filter's half
 width, filters from 1x1 to 7x7 (non-square ones too), signed and unsigned
 operands and both output signednesses; half of them are large enough that
 workgroups walk several output tiles and bands take several staging rounds.
+A second set adds a bias and a residual to the requantiser, also through the
+no-alloc entry.
 """
 import numpy as np
 import pytest
@@ -121,4 +123,74 @@ def test_random_shapes_every_tile(block):
                 assert_same(y.cpu().numpy(), ref["y_packed"], f"{L.name} tile {tid} splits {splits} rep {rep}")
         if L.r == 3 and L.s == 3:
             _fused(q, torch, L, t, sh, g, dev)
+    assert ran > 0
+
+
+@pytest.mark.parametrize("block", [(2000, False), (2025, False), (3000, True), (3025, True)],
+                         ids=lambda b: f"{'large' if b[1] else 'small'}_{b[0]}")
+def test_random_shapes_bias_residual(block):
+    """The requantiser with a per-channel bias and a packed residual (of the
+    output's signedness) on random shapes: every tile from packed filters; on
+    the wide tiles also prepared, in place (y over the residual), with a random
+    split through a caller workspace and through the no-alloc entry."""
+    import torch
+    from paper_2202_06819_amd import qconv as q
+
+    first, big = block
+    dev = torch.device("cuda:0")
+    tiles_all = q.tiles()
+    scratch = q.noalloc_limits()["scratch_bytes"]
+    ran = 0
+    for seed in range(first, first + BLOCK):
+        L = _layer(seed, big)
+        if L.h + 2 * L.pad < L.r or L.w + 2 * L.pad < L.s:
+            continue
+        d, e = L.desc(), L.epilogue
+        t = qi.layer_tensors(6161, seed, L)
+        g = np.random.default_rng([6161, seed])
+        sh = stress_shift(L, L.x_range, L.w_range)
+        acc_mag = int(np.sqrt(L.c * L.r * L.s) * 8 * (8 if L.bits == 4 else 80))
+        bias = g.integers(-acc_mag, acc_mag + 1, size=L.k).astype(np.int32)
+        rsig = e.lo < 0
+        rlo, rhi = (-(2 ** (L.bits - 1)), 2 ** (L.bits - 1) - 1) if rsig else (0, 2 ** L.bits - 1)
+        res_vals = g.integers(rlo, rhi + 1, size=(L.n, L.p, L.q, L.k)).astype(np.int32)
+        want = oracle.qconv_layer(t["x"], t["w"], bits=L.bits, x_signed=L.x_signed, w_signed=L.w_signed,
+                                  stride=(L.stride, L.stride), pad=(L.pad, L.pad), mult=t["mult"], shift=sh,
+                                  relu=e.relu, lo=e.lo, hi=e.hi, bias=bias, residual=res_vals,
+                                  threads=oracle_threads())["y_packed"]
+        xp = q.pack(torch.from_numpy(t["x"]).to(dev), L.bits, L.x_signed)
+        wp = q.pack(torch.from_numpy(t["w"]).to(dev), L.bits, L.w_signed)
+        res = torch.from_numpy(np.ascontiguousarray(oracle.pack_output(res_vals, L.bits, rsig))).to(dev)
+        kw = dict(requant=True, mult=torch.from_numpy(t["mult"]).to(dev), shift=sh, relu=e.relu,
+                  clamp=(e.lo, e.hi), bias=torch.from_numpy(bias).to(dev), residual=res, residual_signed=rsig)
+        for tid in [tt["id"] for tt in tiles_all if q.tile_status(d, tt["id"]) == 0]:
+            announce(f"{L.name} {d} tile {tid} bias+residual")
+            y = q.conv2d(d, xp, wp, tile=tid, **kw)
+            torch.cuda.synchronize()
+            assert_same(y.cpu().numpy(), want, f"{L.name} tile {tid}")
+            ran += 1
+            if tiles_all[tid]["variant"] != 2:
+                continue
+            wprep = q.prepare_filters(d, wp, tid)
+            y = q.conv2d(d, xp, wprep, tile=tid, prepared=True, **kw)
+            torch.cuda.synchronize()
+            assert_same(y.cpu().numpy(), want, f"{L.name} tile {tid} prepared")
+            yy = res.clone()
+            q.conv2d(d, xp, wprep, tile=tid, prepared=True, out=yy, **dict(kw, residual=yy))
+            torch.cuda.synchronize()
+            assert_same(yy.cpu().numpy(), want, f"{L.name} tile {tid} in place")
+            most = q.max_splits(d, tid)
+            if most < 2:
+                continue
+            splits = int(g.integers(2, most + 1))
+            ws = q.make_workspace(d, tid, splits, dev)
+            announce(f"{L.name} tile {tid} bias+residual splits {splits}")
+            y = q.conv2d(d, xp, wprep, tile=tid, prepared=True, splits=splits, workspace=ws, **kw)
+            torch.cuda.synchronize()
+            assert_same(y.cpu().numpy(), want, f"{L.name} tile {tid} splits {splits}")
+            if q.workspace_bytes(d, tid, splits) <= scratch:
+                announce(f"{L.name} tile {tid} bias+residual splits {splits} no-alloc")
+                y = q.conv2d(d, xp, wprep, tile=tid, prepared=True, splits=splits, noalloc=True, **kw)
+                torch.cuda.synchronize()
+                assert_same(y.cpu().numpy(), want, f"{L.name} tile {tid} splits {splits} no-alloc")
     assert ran > 0
