@@ -6,7 +6,7 @@ width, filters from 1x1 to 7x7 (non-square ones too), signed and unsigned
 operands and both output signednesses; half of them are large enough that
 workgroups walk several output tiles and bands take several staging rounds.
 A second set adds a bias and a residual to the requantiser, also through the
-no-alloc entry.
+no-alloc entry; a third chains random residual networks.
 """
 import numpy as np
 import pytest
@@ -194,3 +194,81 @@ def test_random_shapes_bias_residual(block):
                 torch.cuda.synchronize()
                 assert_same(y.cpu().numpy(), want, f"{L.name} tile {tid} splits {splits} no-alloc")
     assert ran > 0
+
+
+def _residual_net(seed: int):
+    """A random residual network: 1-3 blocks of (3x3 with bias, 3x3 with bias
+    plus the shortcut), the shortcut a 1x1 projection where the stride or the
+    channel count changes; 4-bit or 8-bit, ReLU on or off per layer."""
+    g = np.random.default_rng([8181, seed])
+    bits = 8 if seed % 3 == 2 else 4
+    n, h, c0 = int(g.integers(1, 9)), int(g.integers(6, 40)), 32 * int(g.integers(1, 5))
+    spec, cur, ch = [], -1, c0    # (name, c, k, r, stride, pad, src, residual_src)
+    for b in range(int(g.integers(1, 4))):
+        stride = int(g.choice([1, 2]))
+        k = ch * (2 if stride == 2 else 1) if g.random() < 0.7 else 32 * int(g.integers(1, 9))
+        base = len(spec)
+        spec.append((f"b{b}c1", ch, k, 3, stride, 1, cur, None))
+        short = cur
+        if stride != 1 or k != ch:
+            spec.append((f"b{b}ds", ch, k, 1, stride, 0, cur, None))
+            short = base + 1
+        spec.append((f"b{b}c2", k, k, 3, 1, 1, base, short))
+        cur, ch = len(spec) - 1, k
+    return g, bits, n, h, c0, spec
+
+
+@pytest.mark.parametrize("first", [0, 10])
+def test_random_residual_chains(first):
+    """Random residual networks chained with no relayout (projections fused
+    into their strided 3x3, or on a second stream): eager and three graph
+    replays, each against the oracle layer by layer."""
+    import torch
+    from paper_2202_06819_amd import nets
+    from paper_2202_06819_amd import qconv as q
+
+    dev = torch.device("cuda:0")
+    for seed in range(first, first + 10):
+        g, bits, n, h, c0, spec = _residual_net(seed)
+        xs = bits == 8
+        lo, hi = (-128, 127) if xs else (0, 15)
+        x = g.integers(-128 if xs else 0, 128 if xs else 16, size=(n, c0, h, h)).astype(np.int8)
+        xp_ref = oracle.relayout_pack(x, bits, xs)
+        in_vals = oracle.unpack_tensor(xp_ref, c0, bits, xs)
+        refs, specs = [], []
+        for i, (name, c, k, r, stride, pad, src, rsrc) in enumerate(spec):
+            hin = h if src < 0 else refs[src]["y"].shape[1]
+            L = qi.Layer(name, n, hin, hin, c, k, r, r, stride, pad, bits, xs, True, qi.S8 if xs else qi.U4,
+                         qi.S8 if xs else (-7, 7))
+            t = qi.layer_tensors(8181, seed * 100 + i, L)
+            sh = stress_shift(L, L.x_range, L.w_range)
+            bias = g.integers(-400, 400, size=k).astype(np.int32)
+            relu = bool(g.random() < 0.7)
+            res = None if rsrc is None else (in_vals if rsrc < 0 else refs[rsrc]["y"])
+            refs.append(oracle.qconv_layer(None, t["w"], bits=bits, x_signed=xs, w_signed=True,
+                                           stride=(stride, stride), pad=(pad, pad), mult=t["mult"], shift=sh,
+                                           relu=relu, lo=lo, hi=hi, bias=bias, residual=res,
+                                           packed_x=xp_ref if src < 0 else refs[src]["y_packed"],
+                                           threads=oracle_threads()))
+            specs.append(nets.LayerSpec(L.desc(), q.pack(torch.from_numpy(t["w"]).to(dev), bits, True),
+                                        torch.from_numpy(t["mult"]).to(dev), sh, relu, (lo, hi), src=src,
+                                        bias=torch.from_numpy(bias).to(dev), residual_src=rsrc, residual_signed=xs))
+        xp = q.pack(torch.from_numpy(x).to(dev), bits, xs)
+        for branches in (False, True):
+            chain = nets.Chain(specs, xp, branches=branches)
+            announce(f"net {seed} {[s[0] for s in spec]} n={n} h={h} bits={bits} branches={branches} eager")
+            outs = [o.clone() for o in chain.forward()]
+            torch.cuda.synchronize()
+            for (name, *_), o, ref in zip(spec, outs, refs):
+                assert_same(o.cpu().numpy(), ref["y_packed"], f"net {seed} eager {name}")
+            chain.capture()
+            for rep in range(3):
+                for o in chain.outputs:
+                    o.zero_()
+                announce(f"net {seed} replay {rep} branches={branches}")
+                got = chain.replay()
+                torch.cuda.synchronize()
+                for (name, *_), o, ref in zip(spec, got, refs):
+                    assert_same(o.cpu().numpy(), ref["y_packed"], f"net {seed} replay {rep} {name}")
+                chain.forward()
+                torch.cuda.synchronize()
