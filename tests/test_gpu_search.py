@@ -1,5 +1,6 @@
 """Schedules on the GPU: every launch knob of qconv2d_scheduled against the
-oracle, and a short live search whose measured schedules are all checked."""
+oracle, random schedules on random shapes, and a short live search whose
+measured schedules are all checked."""
 import random
 
 import pytest
@@ -59,3 +60,44 @@ def test_live_search_checks_every_schedule():
     res = search.search(meas.space, meas, trials=24, batch=8, diversity=True, seed=0, n_iter=60)
     assert len(res.trials) == 24
     assert all(t.us > 0 for t in res.trials)
+
+
+@pytest.mark.parametrize("block", [(0, False), (5000, True)], ids=["small", "large"])
+def test_random_shapes_random_schedules(block):
+    """Random shapes (the generator of the random-shape parity tests), each
+    with up to 30 schedules drawn from its whole space: tile, split-K,
+    workgroups per CU, band buffers, block order and grid size."""
+    import torch
+    from paper_2202_06819_amd import qconv, search
+    from test_gpu_random import _layer
+    first, big = block
+    dev = torch.device("cuda:0")
+    ran = 0
+    for seed in range(first, first + 25):
+        L = _layer(seed, big)
+        if L.h + 2 * L.pad < L.r or L.w + 2 * L.pad < L.s:
+            continue
+        d, e = L.desc(), L.epilogue
+        space = search.ScheduleSpace.for_shape(d)
+        assert len(space) > 0, f"empty schedule space for {d}"
+        t = qi.layer_tensors(9191, seed, L)
+        sh = stress_shift(L, L.x_range, L.w_range)
+        ref = ref_layer(L, t, requant=True, shift=sh)
+        xp = qconv.pack(torch.from_numpy(t["x"]).to(dev), L.bits, L.x_signed)
+        wp = qconv.pack(torch.from_numpy(t["w"]).to(dev), L.bits, L.w_signed)
+        mult = torch.from_numpy(t["mult"]).to(dev)
+        prepared = {}
+        for cfg in random.Random(seed).sample(space.configs, min(30, len(space))):
+            sch = space.schedule(cfg)
+            tid = sch["tile_id"]
+            if tid not in prepared:
+                prepared[tid] = qconv.prepare_filters(d, wp, tid)
+            ws = qconv.make_workspace(d, tid, sch["splits"], dev)
+            announce(f"{L.name} {d} schedule {sch}")
+            for rep in range(2 if sch["splits"] > 1 else 1):
+                y = qconv.Conv2dCall(d, xp, prepared[tid], schedule=sch, workspace=ws, requant=True, mult=mult,
+                                     shift=sh, relu=e.relu, clamp=(e.lo, e.hi))()
+                torch.cuda.synchronize()
+                assert_same(y.cpu().numpy(), ref["y_packed"], f"{L.name} {sch} rep {rep}")
+                ran += 1
+    assert ran > 0
