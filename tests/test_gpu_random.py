@@ -6,7 +6,8 @@ width, filters from 1x1 to 7x7 (non-square ones too), signed and unsigned
 operands and both output signednesses; half of them are large enough that
 workgroups walk several output tiles and bands take several staging rounds.
 A second set adds a bias and a residual to the requantiser, also through the
-no-alloc entry; a third chains random residual networks.
+no-alloc entry; a third chains random residual networks; a fourth runs
+few-channel layers by patch unrolling.
 """
 import numpy as np
 import pytest
@@ -272,3 +273,51 @@ def test_random_residual_chains(first):
                     assert_same(o.cpu().numpy(), ref["y_packed"], f"net {seed} replay {rep} {name}")
                 chain.forward()
                 torch.cuda.synchronize()
+
+
+def test_random_few_channel_layers_by_unrolling():
+    """Random 8-bit layers with 1-4 input channels and 3x3 to 7x7 filters
+    (square or not, stride 1 or 2): input and filters patch-unrolled on the GPU
+    with either fold (checked against the unroll's definition), then the folded
+    convolution on every tile that takes it, against the oracle's direct
+    convolution of the original tensors."""
+    import torch
+    from paper_2202_06819_amd import qconv as q
+    from _util import unroll_def
+
+    dev = torch.device("cuda:0")
+    ran = 0
+    for seed in range(30):
+        g = np.random.default_rng([3131, seed])
+        c, r = int(g.integers(1, 5)), int(g.choice([3, 5, 7]))
+        s = int(g.choice([r, r, 3]))
+        stride, pad = int(g.choice([1, 2, 2])), int(g.integers(0, r // 2 + 1))
+        h, w, n, k = int(g.integers(r, 65)), int(g.integers(s, 65)), int(g.integers(1, 5)), 8 * int(g.integers(1, 13))
+        L = qi.Layer(f"u{seed}", n, h, w, c, k, r, s, stride, pad, bits=8, x_signed=True, w_signed=True,
+                     x_range=qi.S8, w_range=qi.S8, epilogue=qi.Epilogue(relu=True, lo=-128, hi=127))
+        t = qi.layer_tensors(3131, seed, L)
+        sh = stress_shift(L, L.x_range, L.w_range)
+        ref = oracle.qconv_layer(t["x"], t["w"], bits=8, x_signed=True, w_signed=True, stride=(stride, stride),
+                                 pad=(pad, pad), mult=t["mult"], shift=sh, relu=True, lo=-128, hi=127,
+                                 threads=oracle_threads())
+        mult = torch.from_numpy(t["mult"]).to(dev)
+        for fold in ("rows", "all"):
+            c_out = -(-((stride if fold == "rows" else r) * s * c) // 64) * 64
+            plan = q.few_channel_plan(L.desc(), c_out, fold)
+            announce(f"{L.name} {L.desc()} fold {fold} into {c_out} channels")
+            xu = q.unroll(torch.from_numpy(t["x"]).to(dev), c_out, **plan["x"])
+            wu = q.unroll(torch.from_numpy(t["w"]).to(dev), c_out, **plan["w"])
+            torch.cuda.synchronize()
+            assert np.array_equal(xu.cpu().numpy(), unroll_def(t["x"], c_out, **plan["x"])), f"{L.name} x"
+            assert np.array_equal(wu.cpu().numpy(), unroll_def(t["w"], c_out, **plan["w"])), f"{L.name} w"
+            d = plan["desc"]
+            for tt in q.tiles():
+                if q.tile_status(d, tt["id"]) != 0:
+                    continue
+                announce(f"{L.name} fold {fold} tile {tt['name']}")
+                y = q.conv2d(d, xu, wu, tile=tt["id"], requant=True, mult=mult, shift=sh, relu=True,
+                             clamp=(-128, 127))
+                torch.cuda.synchronize()
+                assert_same(y.cpu().numpy(), ref["y_packed"], f"{L.name} {fold} {tt['name']}")
+                ran += 1
+    assert ran > 0
