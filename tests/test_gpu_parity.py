@@ -708,6 +708,42 @@ def test_interleaved_layout(case):
     and prepared filters, raw and requantised, with a bias and a residual, and
     split over channel chunks where there are several; every result equals
     the oracle's plain-layout result put in the interleaved order."""
+    ran = _check_interleaved(case)
+    assert ran >= 2, f"{case[0]}: only {ran} tiles read the interleaved layout"
+
+
+def _random_interleaved_case(seed: int):
+    g = np.random.default_rng([7171, seed])
+    bits = 8 if seed % 3 == 2 else 4
+    nb = int(g.choice([2, 4, 8, 16]))
+    n = nb * int(g.integers(1, 4))
+    r = int(g.choice([1, 3, 3, 5]))
+    pad = int(g.integers(0, r // 2 + 2))
+    h, w = int(g.integers(max(1, r - 2 * pad), 30)), int(g.integers(max(1, r - 2 * pad), 30))
+    strides = (int(g.choice([1, 1, 2])), int(g.choice([1, 1, 2])))
+    c, k = (32 if bits == 4 else 16) * int(g.integers(1, 9)), 8 * int(g.integers(1, 33))
+    return (f"ir{seed}", n, h, w, c, k, r, strides, pad, bits, nb)
+
+
+@pytest.mark.parametrize("first", [0, 40])
+def test_interleaved_layout_random_shapes(first):
+    """The same checks on random shapes (interleave factors 2-16, 1x1 to 5x5,
+    strides 1-2 per axis, ragged sizes); shapes no tile reads are skipped."""
+    q = _qconv()
+    ran = 0
+    for seed in range(first, first + 40):
+        case = _random_interleaved_case(seed)
+        _, n, h, w, c, k, r, (sh_, sw_), pad, bits, nb = case
+        d = dict(n=n, h=h, w=w, c=c, k=k, r=r, s=r, stride_h=sh_, stride_w=sw_, pad_h=pad, pad_w=pad, bits=bits,
+                 x_signed=int(bits == 8), w_signed=1, nb=nb)
+        if any(q.tile_status(d, t["id"]) == 0 for t in q.tiles()):
+            ran += _check_interleaved(case)
+    assert ran > 0
+
+
+def _check_interleaved(case) -> int:
+    """Run one interleaved-layout case on every tile that reads it; returns
+    the number of tiles run."""
     torch, q = _torch(), _qconv()
     name, n, h, w, c, k, r, (sh_, sw_), pad, bits, nb = case
     signed8 = bits == 8
@@ -770,7 +806,7 @@ def test_interleaved_layout(case):
                          workspace=q.make_workspace(d, tid, 2, dev), **rq)
             torch.cuda.synchronize()
             assert_same(y.cpu().numpy(), want_y, f"{name} {t['name']} split 2")
-    assert ran >= 2, f"{name}: only {ran} tiles read the interleaved layout"
+    return ran
 
 
 # ------------------------------------------------ the pack fused into the conv
