@@ -189,9 +189,11 @@ int64_t vrow_of(const qconv_desc *d, int64_t p, int64_t q, int64_t m) {
 int64_t band_rows(const qconv_desc *d, int64_t p, int64_t q, int64_t tile_p) {
     static std::mutex mu;
     static std::unordered_map<std::string, int64_t> cache;
-    char key[160];
-    snprintf(key, sizeof(key), "%d,%d,%d,%d,%d,%d,%d,%lld", d->n, d->h, d->w, d->r, d->s, d->stride_h, d->pad_h,
-             (long long)tile_p);
+    // keyed by everything the result depends on: the output extent (p, q)
+    // follows from both axes' strides and paddings
+    char key[192];
+    snprintf(key, sizeof(key), "%d,%d,%d,%d,%d,%d,%d,%d,%d,%lld,%lld,%lld", d->n, d->h, d->w, d->r, d->s, d->stride_h,
+             d->stride_w, d->pad_h, d->pad_w, (long long)p, (long long)q, (long long)tile_p);
     {
         std::lock_guard<std::mutex> g(mu);
         auto it = cache.find(key);

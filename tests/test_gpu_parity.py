@@ -316,6 +316,37 @@ def test_extreme_operands_every_tile(case):
             assert_same(y.cpu().numpy(), ref["acc"], f"{name} {label} tile {tid} splits {splits} raw")
 
 
+# ----------------------------------------------------------------- plans of shapes that differ in one axis
+
+def test_shapes_differing_only_in_width_stride_or_padding():
+    """Layers equal in every field but the horizontal stride or padding have
+    different output widths, so a workgroup's band spans a different number of
+    input rows; run one after another in one process (narrow bands first),
+    each must get its own plan and equal the oracle on every wide tile."""
+    torch, q = _torch(), _qconv()
+    n, h, w, c, k = 2, 11, 24, 64, 64
+    variants = [(1, 1), (2, 1), (3, 1), (1, 0), (1, 2)]   # (stride_w, pad_w); stride_h = pad_h = 1
+    base = dict(n=n, h=h, w=w, c=c, k=k, r=3, s=3, stride_h=1, pad_h=1, bits=4, x_signed=0, w_signed=1)
+    tiles = [t["id"] for t in q.tiles() if t["variant"] == 2 and
+             all(q.tile_status(dict(base, stride_w=sw, pad_w=pw), t["id"]) == 0 for sw, pw in variants)]
+    assert tiles
+    g = np.random.default_rng(2024)
+    x = g.integers(0, 16, size=(n, c, h, w)).astype(np.int8)
+    f = g.integers(-7, 8, size=(k, c, 3, 3)).astype(np.int8)
+    dev = torch.device("cuda:0")
+    xp = q.pack(torch.from_numpy(x).to(dev), 4, False)
+    wp = q.pack(torch.from_numpy(f).to(dev), 4, True)
+    for sw, pw in variants:
+        d = dict(base, stride_w=sw, pad_w=pw)
+        ref = oracle.qconv_layer(x, f, bits=4, x_signed=False, w_signed=True, stride=(1, sw), pad=(1, pw),
+                                 threads=oracle_threads())
+        for tid in tiles:
+            announce(f"stride_w {sw} pad_w {pw} tile {tid}")
+            y = q.conv2d(d, xp, wp, tile=tid)
+            torch.cuda.synchronize()
+            assert_same(y.cpu().numpy(), ref["acc"], f"stride_w {sw} pad_w {pw} tile {tid}")
+
+
 # ----------------------------------------------------------------- buffers, determinism, chaining
 
 def test_every_output_written_and_nothing_past_the_end():
