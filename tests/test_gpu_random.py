@@ -7,7 +7,8 @@ operands and both output signednesses; half of them are large enough that
 workgroups walk several output tiles and bands take several staging rounds.
 A second set adds a bias and a residual to the requantiser, also through the
 no-alloc entry; a third chains random residual networks; a fourth runs
-few-channel layers by patch unrolling.
+few-channel layers by patch unrolling; a fifth varies stride and padding per
+axis.
 """
 import numpy as np
 import pytest
@@ -320,4 +321,68 @@ def test_random_few_channel_layers_by_unrolling():
                 torch.cuda.synchronize()
                 assert_same(y.cpu().numpy(), ref["y_packed"], f"{L.name} {fold} {tt['name']}")
                 ran += 1
+    assert ran > 0
+
+
+def test_random_shapes_per_axis_strides_and_paddings():
+    """Independent strides (1-3) and paddings per axis and non-square filters,
+    all in one process (so layers that differ in one axis only follow each
+    other): every tile raw and requantised, the wide tiles also from prepared
+    filters and with a random split."""
+    import torch
+    from paper_2202_06819_amd import qconv as q
+
+    dev = torch.device("cuda:0")
+    tiles_all = q.tiles()
+    ran = 0
+    for seed in range(100):
+        g = np.random.default_rng([6262, seed])
+        bits = 8 if seed % 3 == 2 else 4
+        r = int(g.choice([1, 3, 3, 5, 2]))
+        s = int(g.choice([r, r, 1, 3]))
+        sh, sw = int(g.choice([1, 1, 2, 3])), int(g.choice([1, 1, 2, 3]))
+        ph, pw = int(g.integers(0, r // 2 + 2)), int(g.integers(0, s // 2 + 2))
+        h, w = int(g.integers(max(1, r - 2 * ph), 40)), int(g.integers(max(1, s - 2 * pw), 40))
+        n = int(g.integers(1, 9))
+        c, k = (8 if bits == 4 else 4) * int(g.integers(1, 40)), 8 * int(g.integers(1, 30))
+        xs = bits == 8 or bool(g.random() < 0.2)
+        xr = qi.S8 if bits == 8 else (qi.S4 if xs else qi.U4)
+        wr = qi.S8 if bits == 8 else qi.S4
+        d = dict(n=n, h=h, w=w, c=c, k=k, r=r, s=s, stride_h=sh, stride_w=sw, pad_h=ph, pad_w=pw, bits=bits,
+                 x_signed=int(xs), w_signed=1)
+        tiles = [t["id"] for t in tiles_all if q.tile_status(d, t["id"]) == 0]
+        if not tiles:
+            continue
+        x = g.integers(xr[0], xr[1] + 1, size=(n, c, h, w)).astype(np.int8)
+        f = g.integers(wr[0], wr[1] + 1, size=(k, c, r, s)).astype(np.int8)
+        mult = g.integers(2 ** 14, 2 ** 15, size=k).astype(np.int32)
+        shift = stress_shift(qi.Layer("a", n, h, w, c, k, r, s, 1, 0, bits, xs, True, xr, wr), xr, wr)
+        lo, hi = (-128, 127) if bits == 8 else (0, 15)
+        ref = oracle.qconv_layer(x, f, bits=bits, x_signed=xs, w_signed=True, stride=(sh, sw), pad=(ph, pw),
+                                 mult=mult, shift=shift, relu=True, lo=lo, hi=hi, threads=oracle_threads())
+        xp = q.pack(torch.from_numpy(x).to(dev), bits, xs)
+        wp = q.pack(torch.from_numpy(f).to(dev), bits, True)
+        m_dev = torch.from_numpy(mult).to(dev)
+        for tid in tiles:
+            announce(f"per-axis {d} tile {tid}")
+            y = q.conv2d(d, xp, wp, tile=tid)
+            torch.cuda.synchronize()
+            assert_same(y.cpu().numpy(), ref["acc"], f"{d} tile {tid} raw")
+            y = q.conv2d(d, xp, wp, tile=tid, requant=True, mult=m_dev, shift=shift, relu=True, clamp=(lo, hi))
+            torch.cuda.synchronize()
+            assert_same(y.cpu().numpy(), ref["y_packed"], f"{d} tile {tid} requant")
+            ran += 1
+            if tiles_all[tid]["variant"] != 2:
+                continue
+            wprep = q.prepare_filters(d, wp, tid)
+            y = q.conv2d(d, xp, wprep, tile=tid, prepared=True)
+            torch.cuda.synchronize()
+            assert_same(y.cpu().numpy(), ref["acc"], f"{d} tile {tid} prepared")
+            most = q.max_splits(d, tid)
+            if most > 1:
+                splits = int(g.integers(2, most + 1))
+                y = q.conv2d(d, xp, wprep, tile=tid, prepared=True, splits=splits,
+                             workspace=q.make_workspace(d, tid, splits, dev))
+                torch.cuda.synchronize()
+                assert_same(y.cpu().numpy(), ref["acc"], f"{d} tile {tid} splits {splits}")
     assert ran > 0
