@@ -8,7 +8,7 @@ workgroups walk several output tiles and bands take several staging rounds.
 A second set adds a bias and a residual to the requantiser, also through the
 no-alloc entry; a third chains random residual networks; a fourth runs
 few-channel layers by patch unrolling; a fifth varies stride and padding per
-axis.
+axis, also for the fused pack.
 """
 import numpy as np
 import pytest
@@ -385,4 +385,65 @@ def test_random_shapes_per_axis_strides_and_paddings():
                              workspace=q.make_workspace(d, tid, splits, dev))
                 torch.cuda.synchronize()
                 assert_same(y.cpu().numpy(), ref["acc"], f"{d} tile {tid} splits {splits}")
+    assert ran > 0
+
+
+def test_random_fused_pack_per_axis_strides():
+    """The pack fused into 3x3 convolutions with independent strides per axis,
+    widths with and without whole pixel octets and 1-4 channel chunks, from
+    int8 input over the whole int8 range: requantised (with the packed copy
+    where the bands cover every input row) and raw, on every wide tile."""
+    import torch
+    from paper_2202_06819_amd import qconv as q
+
+    dev = torch.device("cuda:0")
+    ran = 0
+    for seed in range(40):
+        g = np.random.default_rng([7373, seed])
+        bits = 8 if seed % 3 == 2 else 4
+        sh, sw = int(g.choice([1, 1, 2])), int(g.choice([1, 1, 2]))
+        h = int(g.integers(1, 48))
+        w = int(8 * g.integers(1, 7)) if g.random() < 0.5 else int(g.integers(1, 48))
+        n = int(g.integers(1, 9))
+        c = 64 * int(g.integers(1, 4)) if bits == 4 else 32 * int(g.integers(1, 5))
+        k = 8 * int(g.integers(1, 24))
+        signed = bits == 8
+        d = dict(n=n, h=h, w=w, c=c, k=k, r=3, s=3, stride_h=sh, stride_w=sw, pad_h=1, pad_w=1, bits=bits,
+                 x_signed=int(signed), w_signed=1)
+        tiles = [t for t in q.tiles() if t["variant"] == 2 and q.tile_status(d, t["id"]) == 0]
+        if not tiles:
+            continue
+        x = g.integers(-128, 128, size=(n, c, h, w)).astype(np.int8)
+        wr = qi.S8 if signed else (-7, 7)
+        f = g.integers(wr[0], wr[1] + 1, size=(k, c, 3, 3)).astype(np.int8)
+        mult = g.integers(2 ** 14, 2 ** 15, size=k).astype(np.int32)
+        L = qi.Layer("f", n, h, w, c, k, 3, 3, 1, 1, bits, signed, True, qi.S8 if signed else (0, 15), wr)
+        shift = stress_shift(L, L.x_range, wr)
+        lo, hi, relu = (-128, 127, False) if signed else (0, 15, True)
+        ref = oracle.qconv_layer(x, f, bits=bits, x_signed=signed, w_signed=True, stride=(sh, sw), pad=(1, 1),
+                                 mult=mult, shift=shift, relu=relu, lo=lo, hi=hi, threads=oracle_threads())
+        x_dev = torch.from_numpy(x).to(dev)
+        wp = q.pack(torch.from_numpy(f).to(dev), bits, True)
+        m_dev = torch.from_numpy(mult).to(dev)
+        for t in tiles:
+            wprep = q.prepare_filters(d, wp, t["id"])
+            announce(f"fused per-axis {d} tile {t['name']}")
+            call = q.PackingConv2dCall(d, x_dev, wprep, tile=t["id"], mult=m_dev, shift=shift, relu=relu,
+                                       clamp=(lo, hi), x_packed=True)
+            try:
+                y = call()
+                copy = True
+            except q.QConvError as ex:
+                assert "no packed copy" in str(ex), str(ex)
+                y = q.PackingConv2dCall(d, x_dev, wprep, tile=t["id"], mult=m_dev, shift=shift, relu=relu,
+                                        clamp=(lo, hi))()
+                copy = False
+            torch.cuda.synchronize()
+            assert_same(y.cpu().numpy(), ref["y_packed"], f"{d} {t['name']}")
+            if copy:
+                assert_same(call.x_packed.cpu().numpy(), ref["x_packed"], f"{d} {t['name']} packed copy")
+            y = q.PackingConv2dCall(d, x_dev, wprep, tile=t["id"], requant=False)()
+            torch.cuda.synchronize()
+            assert_same(y.cpu().numpy(), ref["acc"], f"{d} {t['name']} raw")
+            ran += 1
     assert ran > 0
