@@ -108,3 +108,29 @@ def unroll_def(src, c_out, taps_h, stride_h, pad_h, out_h, taps_w, stride_w, pad
             block = src[:, :, y[uu]][:, :, :, col[qq]]
             dst[:, uu[:, None], qq[None, :], base:base + c] = block.transpose(0, 2, 3, 1)
     return dst
+
+
+def random_layer(seed: int, big: bool) -> qi.Layer:
+    """A random layer of the random-shape parity tests: ragged sizes, strides
+    1-3, paddings beyond the filter's half width, 1x1 to 7x7 filters (some
+    non-square), 4-bit or 8-bit operands of either signedness; `big` allows
+    batches up to 24 and 60 pixels a side."""
+    g = np.random.default_rng([4242, seed])
+    bits = 8 if seed % 3 == 2 else 4
+    r = int(g.choice([1, 1, 3, 3, 3, 5, 7, 2]))
+    s = int(g.choice([r, r, r, 1, 3]))
+    stride = int(g.choice([1, 1, 1, 2, 2, 3]))
+    pad = int(g.integers(0, max(r, s) // 2 + 2))
+    h = int(g.integers(max(1, r - 2 * pad), 61 if big else 40))
+    w = int(g.integers(max(1, s - 2 * pad), 61 if big else 40))
+    n = int(g.integers(1, 25 if big else 6))
+    if bits == 4:
+        c, k = 8 * int(g.integers(1, 48)), 8 * int(g.integers(1, 40))
+        xs, ws = bool(g.random() < 0.2), bool(g.random() < 0.85)
+        signed_out = bool(g.random() < 0.4)
+        epi = qi.Epilogue(relu=bool(g.random() < 0.5), lo=-8 if signed_out else 0, hi=7 if signed_out else 15)
+        return qi.Layer(f"rand{seed}", n, h, w, c, k, r, s, stride, pad, 4, xs, ws, qi.S4 if xs else qi.U4,
+                        qi.S4 if ws else qi.U4, epi)
+    c, k = 4 * int(g.integers(1, 96)), 4 * int(g.integers(1, 80))
+    epi = qi.Epilogue(relu=bool(g.random() < 0.5), lo=-128, hi=127)
+    return qi.Layer(f"rand{seed}", n, h, w, c, k, r, s, stride, pad, 8, True, True, qi.S8, qi.S8, epi)

@@ -15,34 +15,12 @@ import pytest
 
 import oracle
 import qconv_inputs as qi
-from _util import announce, assert_same, gpu_layer, oracle_threads, ref_layer, stress_shift
+from _util import announce, assert_same, gpu_layer, oracle_threads, random_layer, ref_layer, stress_shift
 
 pytestmark = pytest.mark.gpu
 
 BLOCK = 25
 BLOCKS = [(b * BLOCK, False) for b in range(4)] + [(1000 + b * BLOCK, True) for b in range(4)]
-
-
-def _layer(seed: int, big: bool) -> qi.Layer:
-    g = np.random.default_rng([4242, seed])
-    bits = 8 if seed % 3 == 2 else 4
-    r = int(g.choice([1, 1, 3, 3, 3, 5, 7, 2]))
-    s = int(g.choice([r, r, r, 1, 3]))
-    stride = int(g.choice([1, 1, 1, 2, 2, 3]))
-    pad = int(g.integers(0, max(r, s) // 2 + 2))
-    h = int(g.integers(max(1, r - 2 * pad), 61 if big else 40))
-    w = int(g.integers(max(1, s - 2 * pad), 61 if big else 40))
-    n = int(g.integers(1, 25 if big else 6))
-    if bits == 4:
-        c, k = 8 * int(g.integers(1, 48)), 8 * int(g.integers(1, 40))
-        xs, ws = bool(g.random() < 0.2), bool(g.random() < 0.85)
-        signed_out = bool(g.random() < 0.4)
-        epi = qi.Epilogue(relu=bool(g.random() < 0.5), lo=-8 if signed_out else 0, hi=7 if signed_out else 15)
-        return qi.Layer(f"rand{seed}", n, h, w, c, k, r, s, stride, pad, 4, xs, ws, qi.S4 if xs else qi.U4,
-                        qi.S4 if ws else qi.U4, epi)
-    c, k = 4 * int(g.integers(1, 96)), 4 * int(g.integers(1, 80))
-    epi = qi.Epilogue(relu=bool(g.random() < 0.5), lo=-128, hi=127)
-    return qi.Layer(f"rand{seed}", n, h, w, c, k, r, s, stride, pad, 8, True, True, qi.S8, qi.S8, epi)
 
 
 def _fused(q, torch, L, t, sh, g, dev):
@@ -89,7 +67,7 @@ def test_random_shapes_every_tile(block):
     tiles_all = q.tiles()
     ran = 0
     for seed in range(first, first + BLOCK):
-        L = _layer(seed, big)
+        L = random_layer(seed, big)
         if L.h + 2 * L.pad < L.r or L.w + 2 * L.pad < L.s:
             continue
         tiles = [tt["id"] for tt in tiles_all if q.tile_status(L.desc(), tt["id"]) == 0]
@@ -144,7 +122,7 @@ def test_random_shapes_bias_residual(block):
     scratch = q.noalloc_limits()["scratch_bytes"]
     ran = 0
     for seed in range(first, first + BLOCK):
-        L = _layer(seed, big)
+        L = random_layer(seed, big)
         if L.h + 2 * L.pad < L.r or L.w + 2 * L.pad < L.s:
             continue
         d, e = L.desc(), L.epilogue

@@ -6,7 +6,7 @@ import random
 import pytest
 
 import qconv_inputs as qi
-from _util import announce, assert_same, ref_layer, stress_shift
+from _util import announce, assert_same, random_layer, ref_layer, stress_shift
 
 pytestmark = pytest.mark.gpu
 
@@ -69,12 +69,11 @@ def test_random_shapes_random_schedules(block):
     workgroups per CU, band buffers, block order and grid size."""
     import torch
     from paper_2202_06819_amd import qconv, search
-    from test_gpu_random import _layer
     first, big = block
     dev = torch.device("cuda:0")
     ran = 0
     for seed in range(first, first + 25):
-        L = _layer(seed, big)
+        L = random_layer(seed, big)
         if L.h + 2 * L.pad < L.r or L.w + 2 * L.pad < L.s:
             continue
         d, e = L.desc(), L.epilogue
