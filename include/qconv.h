@@ -24,9 +24,13 @@
  *   - Return value: QCONV_OK or a negative status; qconv_strerror() names it
  *     and qconv_last_error() gives the detail of the calling thread's most
  *     recent failure.
- *   - The library holds no mutable global state besides a per-thread error
- *     message and a per-device attribute cache; calls on distinct streams may
- *     run concurrently from any threads.
+ *   - Mutable global state: per thread, the last error message and the
+ *     last launch's geometry; per device, caches of kernel attributes and
+ *     occupancy; a cache of band heights keyed by every shape field they
+ *     depend on; and the no-alloc entry's scratch array.  The caches are
+ *     locked, so calls on distinct streams may run concurrently from any
+ *     threads, except that no-alloc calls that overlap on one device race
+ *     on its scratch.
  *
  * Packed layouts (b = bits)
  *   activations  N x H x W x C, channels innermost
