@@ -567,3 +567,55 @@ def test_projection_entry_points_validate_on_the_host(q):
                                 None) == q.EWORKSPACE
     with pytest.raises(q.QConvError):
         q.proj_workspace_bytes(d2, t2, 5)
+
+
+def test_validation_fuzz(q):
+    """Random and extreme descriptor fields, tile ids, split factors and
+    schedule knobs into every host-side query: each returns a status (no
+    crash), and for shapes a tile runs, the split-K queries are consistent
+    (at least one chunk, no workspace without a split)."""
+    import random
+    L = q.lib()
+    fields = [f for f, _ in q.QConvDesc._fields_]
+    knobs = [f for f, _ in q.QConvSchedule._fields_]
+    extreme = [-(1 << 31), -(1 << 30), -7, -1, 0, 1, 2, 3, 4, 7, 8, 9, 15, 16, 31, 32, 63, 64, 65, 128, 1000, 4096,
+               1 << 16, 1 << 20, 1 << 30, (1 << 31) - 1]
+    base = dict(n=2, h=14, w=14, c=64, k=64, r=3, s=3, stride_h=1, stride_w=1, pad_h=1, pad_w=1, bits=4, x_signed=0,
+                w_signed=1, nb=0)
+    nt = L.qconv_tile_count()
+    rng = random.Random(11)
+    valid = running = 0
+    for _ in range(3000):
+        d = dict(base)
+        for f in fields:
+            u = rng.random()
+            if u < 0.15:
+                d[f] = rng.choice(extreme)
+            elif u < 0.3:
+                d[f] = rng.randint(-3, 300)
+        desc = q.QConvDesc(**d)
+        info = q.QConvLayoutInfo()
+        rc = L.qconv_layout(ctypes.byref(desc), ctypes.byref(info))
+        assert rc <= 0
+        valid += rc == 0
+        n = ctypes.c_size_t(0)
+        for tile in (rng.choice([-7, -1, 0, nt - 1, nt, 1 << 20]), rng.randrange(nt)):
+            st = L.qconv_tile_check(ctypes.byref(desc), tile)
+            ms = L.qconv_max_splits(ctypes.byref(desc), tile)
+            assert st <= 0
+            if st == 0:
+                running += 1
+                assert rc == 0 and ms >= 1
+                assert L.qconv_workspace_bytes(ctypes.byref(desc), tile, 1, ctypes.byref(n)) == 0 and n.value == 0
+            assert L.qconv_workspace_bytes(ctypes.byref(desc), tile, rng.choice([-1, 0, 2, 3, 64, 1 << 20]),
+                                           ctypes.byref(n)) <= 0
+            assert L.qconv_prepared_filter_bytes(ctypes.byref(desc), tile, ctypes.byref(n)) <= 0
+            assert L.qconv_proj_tile_check(ctypes.byref(desc), tile) <= 0
+            assert L.qconv_proj_workspace_bytes(ctypes.byref(desc), tile, rng.choice([-1, 0, 1, 2, 7]),
+                                                ctypes.byref(n)) <= 0
+            sch = q.QConvSchedule(**{k: rng.choice([-(1 << 31), -1, 0, 1, 2, 3, 4, 8, 1 << 20, (1 << 31) - 1, tile])
+                                     for k in knobs})
+            assert L.qconv_schedule_check(ctypes.byref(desc), ctypes.byref(sch)) <= 0
+        L.qconv_default_tile(ctypes.byref(desc))
+        L.qconv_proj_default_tile(ctypes.byref(desc))
+    assert valid > 100 and running > 50
